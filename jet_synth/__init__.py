@@ -1,0 +1,369 @@
+"""Seeded synthetic inputs for candidate scoring: model files and workloads.
+
+This module is the one piece shared by the fp64 oracle and the GPU path. It
+holds no arithmetic of the scoring method: it draws random numbers, rounds
+them to the storage dtype, writes/reads the model file format, and builds the
+CSR arrays that describe questions and candidates.
+
+Model file format (little endian)::
+
+    bytes 0..7    magic  b"JETMDL01"
+    bytes 8..15   uint64 length H of the JSON header
+    bytes 16..    JSON header (utf-8), then zero padding
+    tensors       each at a 4096-byte aligned absolute offset given in the header
+
+Header keys: ``arch`` ("dense" | "hybrid"), ``dtype`` ("bf16" | "f32", the
+storage type of every matrix), ``d_model``, ``n_layers``, ``n_heads``,
+``n_kv_heads``, ``head_dim``, ``ffn``, ``vocab``, ``rms_eps``, ``rope_theta``,
+``layer_types`` (list of "attn" | "gdn"), ``gdn_heads``, ``gdn_dk``, ``gdn_dv``,
+``conv_kernel``, ``max_ctx``, ``seed``, ``init_std``, ``zero``, and ``tensors``:
+a list of ``{name, dtype, shape, offset, nbytes}``. Matrices use the
+``[out_features, in_features]`` convention. Norm gains, ``A_log`` and
+``dt_bias`` are stored as f32 whatever the matrix dtype is.
+
+Random numbers: every tensor is split into fixed chunks of ``CHUNK`` elements;
+chunk ``j`` of tensor ``name`` is drawn from a Philox-4x64 counter-based
+stream keyed on ``(seed, crc32(name) << 32 | j)`` as standard normals in
+float32, scaled by ``init_std`` in float32 and rounded to nearest-even into
+bfloat16 (or kept as float32). The result therefore does not depend on the
+number of threads used to write the file.
+"""
+from __future__ import annotations
+
+import json
+import os
+import struct
+import zlib
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
+
+import numpy as np
+
+MAGIC = b"JETMDL01"
+ALIGN = 4096
+CHUNK = 1 << 22
+# Sampling seed of the paper's experimental protocol (Appendix A); reused here
+# as the master seed of every synthetic input.
+MASTER_SEED = 20260921
+
+# --------------------------------------------------------------------------
+# model shapes
+# --------------------------------------------------------------------------
+
+MODEL_SPECS: dict[str, dict] = {
+    # 2 layers, d=128, 4 heads of 32 (MHA), SwiGLU 512, vocab 1024, fp32.
+    "tiny_dense_fp32": dict(arch="dense", dtype="f32", d_model=128, n_layers=2,
+                            n_heads=4, n_kv_heads=4, head_dim=32, ffn=512,
+                            vocab=1024, max_ctx=4096),
+    # Same shape stored in bf16 (used for bf16-path parity at tiny size).
+    "tiny_dense_bf16": dict(arch="dense", dtype="bf16", d_model=128, n_layers=2,
+                            n_heads=4, n_kv_heads=4, head_dim=32, ffn=512,
+                            vocab=1024, max_ctx=4096),
+    # Small GQA model with the production head size (hd=128), bf16.
+    "small_gqa_bf16": dict(arch="dense", dtype="bf16", d_model=256, n_layers=2,
+                           n_heads=6, n_kv_heads=2, head_dim=128, ffn=768,
+                           vocab=3000, max_ctx=8192),
+    "small_gqa_fp32": dict(arch="dense", dtype="f32", d_model=256, n_layers=2,
+                           n_heads=6, n_kv_heads=2, head_dim=128, ffn=768,
+                           vocab=3000, max_ctx=8192),
+    # 1.5B-shape dense decoder: 28 layers, d=1536, GQA 12/2 (hd 128), FFN 8960.
+    "dense_1p5b": dict(arch="dense", dtype="bf16", d_model=1536, n_layers=28,
+                       n_heads=12, n_kv_heads=2, head_dim=128, ffn=8960,
+                       vocab=151936, max_ctx=8192),
+    # 27B-shape dense decoder: 64 layers, d=5120, GQA 40/8 (hd 128), FFN 17408.
+    "dense_27b": dict(arch="dense", dtype="bf16", d_model=5120, n_layers=64,
+                      n_heads=40, n_kv_heads=8, head_dim=128, ffn=17408,
+                      vocab=151936, max_ctx=8192),
+    # 4B-shape hybrid: 8 x [3 gated delta-rule layers + 1 GQA attention layer].
+    "hybrid_4b": dict(arch="hybrid", dtype="bf16", d_model=2560, n_layers=32,
+                      n_heads=16, n_kv_heads=4, head_dim=128, ffn=9728,
+                      vocab=151936, gdn_heads=16, gdn_dk=128, gdn_dv=128,
+                      conv_kernel=4, max_ctx=8192),
+    # Small hybrid with production head sizes (for GPU parity at small size).
+    "small_hybrid_bf16": dict(arch="hybrid", dtype="bf16", d_model=256, n_layers=4,
+                              n_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                              vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
+                              conv_kernel=4, max_ctx=8192),
+    "small_hybrid_fp32": dict(arch="hybrid", dtype="f32", d_model=256, n_layers=4,
+                              n_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                              vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
+                              conv_kernel=4, max_ctx=8192),
+    # Micro hybrid for oracle self-checks on the CPU: L=4, d=64.
+    "micro_hybrid_fp32": dict(arch="hybrid", dtype="f32", d_model=64, n_layers=4,
+                              n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
+                              vocab=512, gdn_heads=2, gdn_dk=16, gdn_dv=16,
+                              conv_kernel=4, max_ctx=4096),
+}
+
+DEFAULTS = dict(rms_eps=1e-6, rope_theta=1.0e6, init_std=0.02)
+
+
+def full_spec(spec: dict | str) -> dict:
+    s = dict(MODEL_SPECS[spec]) if isinstance(spec, str) else dict(spec)
+    for k, v in DEFAULTS.items():
+        s.setdefault(k, v)
+    if s["arch"] == "hybrid":
+        s.setdefault("layer_types", ["gdn", "gdn", "gdn", "attn"] * (s["n_layers"] // 4))
+    else:
+        s.setdefault("layer_types", ["attn"] * s["n_layers"])
+    assert len(s["layer_types"]) == s["n_layers"]
+    return s
+
+
+def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
+    """(name, storage dtype, shape, init) for every tensor, in file order.
+
+    init is "normal" (i.i.d. N(0, init_std^2)), "ones" or "zeros".
+    """
+    s = full_spec(spec)
+    d, V, F = s["d_model"], s["vocab"], s["ffn"]
+    mt = s["dtype"]
+    out = [("tok_embed", mt, (V, d), "normal")]
+    for i, lt in enumerate(s["layer_types"]):
+        p = f"blk.{i}."
+        out.append((p + "attn_norm", "f32", (d,), "ones"))
+        if lt == "attn":
+            hq, hkv, hd = s["n_heads"], s["n_kv_heads"], s["head_dim"]
+            out += [(p + "wq", mt, (hq * hd, d), "normal"),
+                    (p + "wk", mt, (hkv * hd, d), "normal"),
+                    (p + "wv", mt, (hkv * hd, d), "normal"),
+                    (p + "wo", mt, (d, hq * hd), "normal")]
+        else:
+            H, dk, dv, kc = s["gdn_heads"], s["gdn_dk"], s["gdn_dv"], s["conv_kernel"]
+            out += [(p + "gdn_wq", mt, (H * dk, d), "normal"),
+                    (p + "gdn_wk", mt, (H * dk, d), "normal"),
+                    (p + "gdn_wv", mt, (H * dv, d), "normal"),
+                    (p + "gdn_wz", mt, (H * dv, d), "normal"),
+                    (p + "gdn_wb", mt, (H, d), "normal"),
+                    (p + "gdn_wa", mt, (H, d), "normal"),
+                    (p + "gdn_conv", mt, (2 * H * dk + H * dv, kc), "normal"),
+                    (p + "gdn_A_log", "f32", (H,), "zeros"),
+                    (p + "gdn_dt_bias", "f32", (H,), "zeros"),
+                    (p + "gdn_norm", "f32", (dv,), "ones"),
+                    (p + "gdn_wo", mt, (d, H * dv), "normal")]
+        out += [(p + "ffn_norm", "f32", (d,), "ones"),
+                (p + "w_gate", mt, (F, d), "normal"),
+                (p + "w_up", mt, (F, d), "normal"),
+                (p + "w_down", mt, (d, F), "normal")]
+    out += [("final_norm", "f32", (d,), "ones"), ("lm_head", mt, (V, d), "normal")]
+    return out
+
+
+def n_params(spec) -> int:
+    return int(sum(np.prod(sh) for _, _, sh, _ in tensor_list(spec)))
+
+
+# --------------------------------------------------------------------------
+# writing / reading model files
+# --------------------------------------------------------------------------
+
+def _f32_to_bf16_rne(x: np.ndarray, out: np.ndarray) -> None:
+    """Round float32 to bfloat16 bits (round to nearest, ties to even)."""
+    u = x.view(np.uint32)
+    t = u >> 16
+    t &= 1
+    t += 0x7FFF
+    t += u
+    t >>= 16
+    out[:] = t
+
+
+def _fill_chunk(seed: int, name: str, j: int, std: float, init: str,
+                dst: np.ndarray, dtype: str, zero: bool) -> None:
+    n = dst.size
+    if init == "ones":
+        val = np.ones(n, np.float32)
+    elif init == "zeros" or zero:
+        val = np.zeros(n, np.float32)
+    else:
+        key = (zlib.crc32(name.encode()) << 32) | j
+        g = np.random.Generator(np.random.Philox(key=[seed, key]))
+        val = np.empty(n, np.float32)
+        g.standard_normal(out=val, dtype=np.float32)
+        val *= np.float32(std)
+    if dtype == "bf16":
+        _f32_to_bf16_rne(val, dst)
+    else:
+        dst[:] = val
+
+
+def _np_storage(dtype: str):
+    return np.uint16 if dtype == "bf16" else np.float32
+
+
+def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
+                zero: bool = False, threads: int | None = None) -> dict:
+    """Write a seeded synthetic model file; returns its header."""
+    s = full_spec(spec)
+    tensors = []
+    # header is written last; reserve generous room for it
+    hdr_room = 1 << 20
+    off = ALIGN * ((16 + hdr_room + ALIGN - 1) // ALIGN)
+    for name, dt, shape, init in tensor_list(s):
+        nbytes = int(np.prod(shape)) * (2 if dt == "bf16" else 4)
+        tensors.append(dict(name=name, dtype=dt, shape=list(shape), offset=off,
+                            nbytes=nbytes, init=init))
+        off += ALIGN * ((nbytes + ALIGN - 1) // ALIGN)
+    header = dict(format=1, **{k: v for k, v in s.items()}, seed=int(seed), zero=bool(zero),
+                  tensors=[{k: t[k] for k in ("name", "dtype", "shape", "offset", "nbytes")}
+                           for t in tensors])
+    hjson = json.dumps(header).encode()
+    assert len(hjson) <= hdr_room
+    tmp = path + ".tmp"
+    with open(tmp, "wb") as f:
+        f.truncate(off)
+        f.seek(0)
+        f.write(MAGIC + struct.pack("<Q", len(hjson)) + hjson)
+    mm = np.memmap(tmp, dtype=np.uint8, mode="r+")
+    jobs = []
+    for t in tensors:
+        n = t["nbytes"] // (2 if t["dtype"] == "bf16" else 4)
+        arr = mm[t["offset"]:t["offset"] + t["nbytes"]].view(_np_storage(t["dtype"]))
+        for j in range(0, (n + CHUNK - 1) // CHUNK):
+            jobs.append((t["name"], j, t["init"], arr[j * CHUNK:(j + 1) * CHUNK], t["dtype"]))
+    nthr = threads or max(1, min(32, len(os.sched_getaffinity(0))))
+    std = s["init_std"]
+    with ThreadPoolExecutor(nthr) as ex:
+        list(ex.map(lambda a: _fill_chunk(seed, a[0], a[1], std, a[2], a[3], a[4], zero), jobs))
+    mm.flush()
+    del mm
+    os.replace(tmp, path)
+    return header
+
+
+def read_header(path: str) -> dict:
+    with open(path, "rb") as f:
+        head = f.read(16)
+        if head[:8] != MAGIC:
+            raise ValueError(f"{path}: not a model file")
+        (n,) = struct.unpack("<Q", head[8:16])
+        return json.loads(f.read(n))
+
+
+def tensor_raw(path: str, name: str, header: dict | None = None) -> np.ndarray:
+    """Memory-mapped raw storage of one tensor (uint16 bf16 bits or float32)."""
+    h = header or read_header(path)
+    for t in h["tensors"]:
+        if t["name"] == name:
+            return np.memmap(path, dtype=_np_storage(t["dtype"]), mode="r",
+                             offset=t["offset"], shape=tuple(t["shape"]))
+    raise KeyError(name)
+
+
+def model_cache_dir() -> str:
+    d = os.environ.get("JET_MODEL_CACHE") or os.path.join("/tmp", "jet_models")
+    os.makedirs(d, exist_ok=True)
+    return d
+
+
+def ensure_model(spec_name: str, seed: int = MASTER_SEED, zero: bool = False,
+                 cache_dir: str | None = None) -> str:
+    """Path of the model file for a named spec, writing it if absent."""
+    d = cache_dir or model_cache_dir()
+    path = os.path.join(d, f"{spec_name}_s{seed}{'_zero' if zero else ''}.jetm")
+    if not os.path.exists(path):
+        write_model(path, spec_name, seed=seed, zero=zero)
+    return path
+
+
+# --------------------------------------------------------------------------
+# workloads
+# --------------------------------------------------------------------------
+
+@dataclass
+class Workload:
+    """Questions and candidates as CSR arrays (the layout the C ABI takes)."""
+    prefix_offsets: np.ndarray   # int64 [Q+1]
+    prefix_tokens: np.ndarray    # int32 [sum P]
+    q_cand_offsets: np.ndarray   # int64 [Q+1]
+    cand_tok_offsets: np.ndarray  # int64 [N+1]
+    cand_tokens: np.ndarray      # int32 [sum m]
+
+    @property
+    def n_questions(self) -> int:
+        return len(self.prefix_offsets) - 1
+
+    @property
+    def n_candidates(self) -> int:
+        return len(self.cand_tok_offsets) - 1
+
+    def prefix(self, q: int) -> np.ndarray:
+        return self.prefix_tokens[self.prefix_offsets[q]:self.prefix_offsets[q + 1]]
+
+    def candidates(self, q: int) -> list[np.ndarray]:
+        return [self.cand_tokens[self.cand_tok_offsets[c]:self.cand_tok_offsets[c + 1]]
+                for c in range(self.q_cand_offsets[q], self.q_cand_offsets[q + 1])]
+
+    def subset(self, qs) -> "Workload":
+        """The questions ``qs`` (in that order) with their candidates."""
+        pre, cands = [], []
+        for q in qs:
+            pre.append(self.prefix(q))
+            cands.append(self.candidates(q))
+        return from_lists(pre, cands)
+
+
+def from_lists(prefixes: list, cands: list[list]) -> Workload:
+    """Build the CSR arrays from per-question prefix and candidate token lists."""
+    po = np.zeros(len(prefixes) + 1, np.int64)
+    po[1:] = np.cumsum([len(p) for p in prefixes])
+    qo = np.zeros(len(cands) + 1, np.int64)
+    qo[1:] = np.cumsum([len(c) for c in cands])
+    flat = [np.asarray(y, np.int32) for cs in cands for y in cs]
+    co = np.zeros(len(flat) + 1, np.int64)
+    co[1:] = np.cumsum([len(y) for y in flat])
+    pt = np.concatenate([np.asarray(p, np.int32) for p in prefixes]) if prefixes else np.zeros(0, np.int32)
+    ct = np.concatenate(flat) if flat else np.zeros(0, np.int32)
+    return Workload(po, pt.astype(np.int32), qo, co, ct.astype(np.int32))
+
+
+# Workload recipes. Lengths are discrete uniform, inclusive. "zipf" ids follow
+# P(id = r) proportional to 1/(r+1) over [0, V); "uniform" ids are uniform.
+WORKLOADS: dict[str, dict] = {
+    "tiny": dict(model="tiny_dense_fp32", Q=16, P=(32, 32), ids="uniform", K=4, m=(1, 4)),
+    "small": dict(model="small_gqa_bf16", Q=12, P=(40, 300), ids="zipf", K=4, m=(1, 24)),
+    "dense_1p5b_k4": dict(model="dense_1p5b", Q=256, P=(150, 900), ids="zipf", K=4, m=(1, 24)),
+    "dense_1p5b_binary": dict(model="dense_1p5b", Q=512, P=(300, 2000), ids="zipf", K=2, m=(1, 1)),
+    "dense_1p5b_ordinal": dict(model="dense_1p5b", Q=512, P=(300, 2000), ids="zipf", K=5, m=(1, 3)),
+    "hybrid_4b_k4": dict(model="hybrid_4b", Q=128, P=(200, 1500), ids="zipf", K=4, m=(1, 24)),
+    "dense_27b_k10": dict(model="dense_27b", Q=64, P=(1024, 4096), ids="zipf", K=10, m=(8, 40)),
+    "small_hybrid": dict(model="small_hybrid_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
+    "micro_hybrid": dict(model="micro_hybrid_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
+}
+
+
+def _stream(seed: int, label: str) -> np.random.Generator:
+    return np.random.Generator(np.random.Philox(key=[seed, zlib.crc32(label.encode())]))
+
+
+def zipf_ids(g: np.random.Generator, n: int, V: int) -> np.ndarray:
+    w = 1.0 / np.arange(1, V + 1, dtype=np.float64)
+    cdf = np.cumsum(w)
+    cdf /= cdf[-1]
+    u = g.random(n)
+    return np.minimum(np.searchsorted(cdf, u, side="right"), V - 1).astype(np.int32)
+
+
+def make_workload(name: str, seed: int = MASTER_SEED, n_questions: int | None = None,
+                  vocab: int | None = None, **over) -> Workload:
+    """Generate the seeded workload ``name`` (see WORKLOADS)."""
+    r = dict(WORKLOADS[name])
+    r.update(over)
+    V = vocab or full_spec(r["model"])["vocab"]
+    Q = r["Q"] if n_questions is None else n_questions
+    g_plen = _stream(seed, name + "/prefix_len")
+    g_pid = _stream(seed, name + "/prefix_ids")
+    g_mlen = _stream(seed, name + "/cand_len")
+    g_cid = _stream(seed, name + "/cand_ids")
+    plen = g_plen.integers(r["P"][0], r["P"][1] + 1, size=Q)
+    prefixes = []
+    for q in range(Q):
+        if r["ids"] == "zipf":
+            prefixes.append(zipf_ids(g_pid, int(plen[q]), V))
+        else:
+            prefixes.append(g_pid.integers(0, V, size=int(plen[q])).astype(np.int32))
+    cands = []
+    for q in range(Q):
+        ml = g_mlen.integers(r["m"][0], r["m"][1] + 1, size=r["K"])
+        cands.append([g_cid.integers(0, V, size=int(m)).astype(np.int32) for m in ml])
+    return from_lists(prefixes, cands)

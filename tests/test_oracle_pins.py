@@ -1,0 +1,417 @@
+"""Pins of the fp64 oracle against values fixed by the paper and by mathematics.
+
+Each check is independent of the oracle's own formulas: the paper's worked
+example, closed forms, invariants, brute force, and independent library
+implementations of the same network blocks (transformers' Qwen2 decoder and
+Qwen3-Next gated delta-rule layer, evaluated on the same weights).
+"""
+import copy
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import jet_synth
+import oracle
+from oracle import model as om
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _spec(name, **over):
+    s = dict(jet_synth.MODEL_SPECS[name])
+    s.update(over)
+    return s
+
+
+@pytest.fixture(scope="module")
+def tiny_path(model_dir):
+    return jet_synth.ensure_model("tiny_dense_fp32", cache_dir=model_dir)
+
+
+@pytest.fixture(scope="module")
+def micro_hybrid_path(model_dir):
+    return jet_synth.ensure_model("micro_hybrid_fp32", cache_dir=model_dir)
+
+
+@pytest.fixture(scope="module")
+def pin_dense_path(model_dir):
+    # larger init so every term of every block moves the result visibly
+    p = os.path.join(model_dir, "pin_dense.jetm")
+    if not os.path.exists(p):
+        jet_synth.write_model(p, _spec("tiny_dense_fp32", n_heads=4, n_kv_heads=2,
+                                       init_std=0.08, vocab=300))
+    return p
+
+
+@pytest.fixture(scope="module")
+def pin_hybrid_path(model_dir):
+    p = os.path.join(model_dir, "pin_hybrid.jetm")
+    if not os.path.exists(p):
+        jet_synth.write_model(p, _spec("micro_hybrid_fp32", init_std=0.15))
+    return p
+
+
+# --------------------------------------------------------------------------
+# Section 3.1-3.3: log-probabilities, sums, normalisation, decisions
+# --------------------------------------------------------------------------
+
+def test_worked_example_normalisation():
+    g = json.load(open(os.path.join(GOLDEN, "worked_example.json")))
+    s = np.log(np.array(g["likelihoods"]))
+    q = oracle.normalize(s)
+    np.testing.assert_allclose(q, g["normalized"], rtol=0, atol=1e-15)
+    assert oracle.decide_choice(s) == 0
+
+
+def test_log_softmax_brute_force_sums_to_one():
+    rng = np.random.default_rng(1)
+    z = rng.normal(0, 3.0, size=(6, 1024))
+    V = z.shape[1]
+    for r in range(z.shape[0]):
+        ell = oracle.log_softmax_rows(np.repeat(z[r:r + 1], V, axis=0), np.arange(V))
+        assert abs(np.sum(np.exp(ell)) - 1.0) < 1e-12
+        # the unshifted textbook form agrees for moderate logits
+        naive = z[r] - np.log(np.sum(np.exp(z[r])))
+        np.testing.assert_allclose(ell, naive, atol=1e-13, rtol=0)
+        np.testing.assert_allclose(ell, z[r] - scipy.special.logsumexp(z[r]), atol=1e-13, rtol=0)
+
+
+def test_log_softmax_large_logits_stay_finite():
+    z = np.array([[1000.0, 999.0, -1000.0]])
+    ell = oracle.log_softmax_rows(np.repeat(z, 3, 0), np.arange(3))
+    assert np.all(np.isfinite(ell[:2]))
+    np.testing.assert_allclose(ell[:2], [-math.log1p(math.exp(-1.0)), -1.0 - math.log1p(math.exp(-1.0))],
+                               atol=1e-12)
+
+
+def test_decisions_closed_forms():
+    s = np.array([-3.2, -1.5])
+    assert oracle.decide_binary(s) == pytest.approx(1.0 / (1.0 + math.exp(-(s[1] - s[0]))), abs=1e-15)
+    s5 = np.array([-4.0, -2.0, -2.5, -7.0, -3.0])
+    q = oracle.normalize(s5)
+    assert oracle.decide_ordinal(s5) == pytest.approx(sum(i * q[i] for i in range(5)), abs=1e-15)
+    # equal scores: lowest index wins; duplicates split the mass
+    assert oracle.decide_choice(np.array([-1.0, -0.5, -0.5])) == 1
+    np.testing.assert_allclose(oracle.normalize(np.array([-2.0, -2.0])), [0.5, 0.5], atol=1e-16)
+    # a constant shift of every score leaves q unchanged (Eq. 4)
+    np.testing.assert_allclose(oracle.normalize(s5 + 123.0), q, atol=1e-15)
+    with pytest.raises(ValueError):
+        oracle.decide_binary(s5)
+
+
+def test_zero_weights_give_uniform_vocabulary(model_dir):
+    g = json.load(open(os.path.join(GOLDEN, "zero_model_logprob.json")))["per_token"]
+    for spec, wname in (("tiny_dense_fp32", "tiny"), ("micro_hybrid_fp32", "micro_hybrid")):
+        p = jet_synth.ensure_model(spec, zero=True, cache_dir=model_dir)
+        V = jet_synth.read_header(p)["vocab"]
+        wl = jet_synth.make_workload(wname)
+        tok, sums = oracle.score_unshared(p, wl)
+        assert np.all(tok == g[str(V)]), (spec, np.unique(tok))
+        m = np.diff(wl.cand_tok_offsets)
+        np.testing.assert_allclose(sums, m * g[str(V)], rtol=1e-15, atol=0)
+
+
+# --------------------------------------------------------------------------
+# network blocks: closed forms and special cases
+# --------------------------------------------------------------------------
+
+def test_rope_identity_and_relative_position():
+    rng = np.random.default_rng(2)
+    x = rng.normal(size=(1, 3, 32))
+    np.testing.assert_array_equal(om.rope(x, np.array([0]), 1e6), x)
+    q = rng.normal(size=(1, 1, 32)); k = rng.normal(size=(1, 1, 32))
+    for th in (1e4, 1e6):
+        d1 = np.sum(om.rope(q, np.array([7]), th) * om.rope(k, np.array([3]), th))
+        d2 = np.sum(om.rope(q, np.array([4007]), th) * om.rope(k, np.array([4003]), th))
+        assert abs(d1 - d2) < 1e-9
+        # norms are preserved
+        assert abs(np.linalg.norm(om.rope(q, np.array([123]), th)) - np.linalg.norm(q)) < 1e-12
+    # the pairs are (i, i + hd/2): a vector living only in dim 0 rotates into dim 16
+    e0 = np.zeros((1, 1, 32)); e0[0, 0, 0] = 1.0
+    r = om.rope(e0, np.array([1]), 1e6)
+    assert abs(r[0, 0, 0] - math.cos(1.0)) < 1e-15 and abs(r[0, 0, 16] - math.sin(1.0)) < 1e-15
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(3)
+    # a single visible key returns its value exactly
+    q = rng.normal(size=(1, 4, 16)); k = rng.normal(size=(1, 2, 16)); v = rng.normal(size=(1, 2, 16))
+    out = om.attention(q, k, v, np.array([0]), np.array([0]))
+    for h in range(4):
+        np.testing.assert_allclose(out[0, h], v[0, h // 2], atol=1e-15)
+    # zero queries: uniform weights over the visible keys (causal prefix mean)
+    n = 5
+    q = np.zeros((n, 4, 16)); k = rng.normal(size=(n, 2, 16)); v = rng.normal(size=(n, 2, 16))
+    out = om.attention(q, k, v, np.arange(n), np.arange(n))
+    for i in range(n):
+        for h in range(4):
+            np.testing.assert_allclose(out[i, h], v[:i + 1, h // 2].mean(axis=0), atol=1e-14)
+
+
+def test_gated_delta_rule_closed_forms():
+    rng = np.random.default_rng(4)
+    H, dk, dv, n = 2, 8, 6, 5
+    S0 = rng.normal(size=(H, dv, dk))
+    q = rng.normal(size=(n, H, dk)); k = rng.normal(size=(n, H, dk)); v = rng.normal(size=(n, H, dv))
+    # alpha = 1, beta = 0: state unchanged, output is S0 q
+    o, S = om.gdn_recurrence(q, k, v, np.ones((n, H)), np.zeros((n, H)), S0)
+    np.testing.assert_allclose(S, S0, atol=0)
+    np.testing.assert_allclose(o, np.einsum("hvk,nhk->nhv", S0, q), atol=1e-13)
+    # alpha = 1, beta = 1, unit keys: the state maps k_t to v_t exactly afterwards
+    ku = k / np.linalg.norm(k, axis=-1, keepdims=True)
+    S = S0
+    for t in range(n):
+        _, S = om.gdn_recurrence(q[t:t + 1], ku[t:t + 1], v[t:t + 1], np.ones((1, H)), np.ones((1, H)), S)
+        np.testing.assert_allclose(np.einsum("hvk,hk->hv", S, ku[t]), v[t], atol=1e-12)
+    # alpha = 0 forgets everything before the step
+    o0, _ = om.gdn_recurrence(q[:1], k[:1], v[:1], np.zeros((1, H)), np.full((1, H), 0.7), S0)
+    o1, _ = om.gdn_recurrence(q[:1], k[:1], v[:1], np.zeros((1, H)), np.full((1, H), 0.7), np.zeros_like(S0))
+    np.testing.assert_allclose(o0, o1, atol=1e-15)
+
+
+def test_causal_conv_matches_direct_sum():
+    rng = np.random.default_rng(5)
+    x = rng.normal(size=(7, 3)); w = rng.normal(size=(3, 4))
+    out, tail = om.causal_conv(x, np.zeros((3, 3)), w)
+    for t in range(7):
+        ref = sum(w[:, j] * (x[t - 3 + j] if t - 3 + j >= 0 else 0.0) for j in range(4))
+        np.testing.assert_allclose(out[t], ref, atol=1e-14)
+    np.testing.assert_array_equal(tail, x[-3:])
+    # splitting the sequence and carrying the tail gives the same output
+    o1, t1 = om.causal_conv(x[:2], np.zeros((3, 3)), w)
+    o2, _ = om.causal_conv(x[2:], t1, w)
+    np.testing.assert_allclose(np.concatenate([o1, o2]), out, atol=1e-15)
+
+
+# --------------------------------------------------------------------------
+# independent library implementations of the same blocks
+# --------------------------------------------------------------------------
+
+def _hf_qwen2(path):
+    import torch
+    from transformers import Qwen2Config, Qwen2ForCausalLM
+    m = oracle.Model(path)
+    h = m.h
+    cfg = Qwen2Config(vocab_size=h["vocab"], hidden_size=h["d_model"], intermediate_size=h["ffn"],
+                      num_hidden_layers=h["n_layers"], num_attention_heads=h["n_heads"],
+                      num_key_value_heads=h["n_kv_heads"], head_dim=h["head_dim"],
+                      rms_norm_eps=h["rms_eps"], rope_theta=h["rope_theta"],
+                      max_position_embeddings=4096, tie_word_embeddings=False,
+                      attn_implementation="eager")
+    net = Qwen2ForCausalLM(cfg).double().eval()
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))
+    with torch.no_grad():
+        net.model.embed_tokens.weight.copy_(T(m.w("tok_embed")))
+        for i, layer in enumerate(net.model.layers):
+            W = m.layer(i)
+            layer.input_layernorm.weight.copy_(T(W["attn_norm"]))
+            layer.post_attention_layernorm.weight.copy_(T(W["ffn_norm"]))
+            at = layer.self_attn
+            at.q_proj.weight.copy_(T(W["wq"])); at.q_proj.bias.zero_()
+            at.k_proj.weight.copy_(T(W["wk"])); at.k_proj.bias.zero_()
+            at.v_proj.weight.copy_(T(W["wv"])); at.v_proj.bias.zero_()
+            at.o_proj.weight.copy_(T(W["wo"]))
+            layer.mlp.gate_proj.weight.copy_(T(W["w_gate"]))
+            layer.mlp.up_proj.weight.copy_(T(W["w_up"]))
+            layer.mlp.down_proj.weight.copy_(T(W["w_down"]))
+        net.model.norm.weight.copy_(T(m.w("final_norm")))
+        net.lm_head.weight.copy_(T(m.w("lm_head")))
+    return net
+
+
+def test_dense_scores_match_transformers_qwen2(pin_dense_path):
+    """End-to-end: logits of an independent decoder implementation on the same
+    weights give the same per-token log-probabilities (covers the projection
+    orientation, RoPE pairing, GQA head mapping, causal mask, SwiGLU order and
+    the one-position shift between a token and the row that predicts it)."""
+    import torch
+    net = _hf_qwen2(pin_dense_path)
+    V = jet_synth.read_header(pin_dense_path)["vocab"]
+    wl = jet_synth.make_workload("tiny", n_questions=3, vocab=V, P=(9, 30), m=(1, 6))
+    tok, sums = oracle.score_unshared(pin_dense_path, wl)
+    ref = np.zeros_like(tok)
+    for q in range(wl.n_questions):
+        x = wl.prefix(q)
+        for j, y in enumerate(wl.candidates(q)):
+            c = wl.q_cand_offsets[q] + j
+            seq = np.concatenate([x, y]).astype(np.int64)
+            with torch.no_grad():
+                logits = net(torch.from_numpy(seq)[None]).logits[0].numpy()
+            lp = logits - scipy.special.logsumexp(logits, axis=1, keepdims=True)
+            P = len(x)
+            ref[wl.cand_tok_offsets[c]:wl.cand_tok_offsets[c + 1]] = [lp[P - 1 + t, y[t]] for t in range(len(y))]
+    # transformers normalises in float32 internally, so agreement is ~1e-6
+    np.testing.assert_allclose(tok, ref, atol=2e-5, rtol=0)
+    assert np.std(tok) > 0.05  # the pin model is far from uniform
+
+
+def test_dense_pin_detects_planted_mistakes(pin_dense_path, monkeypatch):
+    """The transformers pin is sensitive: a wrong RoPE pairing or a wrong GQA
+    head mapping planted in the oracle moves the scores well past the pin's
+    tolerance."""
+    V = jet_synth.read_header(pin_dense_path)["vocab"]
+    wl = jet_synth.make_workload("tiny", n_questions=2, vocab=V, P=(9, 30), m=(1, 6))
+    good, _ = oracle.score_unshared(pin_dense_path, wl)
+
+    def rope_interleaved(x, pos, theta):
+        hd = x.shape[-1]
+        c, s = om.rope_angles(pos, hd, theta)
+        c, s = c[:, None, :], s[:, None, :]
+        x1, x2 = x[..., 0::2], x[..., 1::2]
+        out = np.empty_like(x)
+        out[..., 0::2] = x1 * c - x2 * s
+        out[..., 1::2] = x2 * c + x1 * s
+        return out
+
+    monkeypatch.setattr(om, "rope", rope_interleaved)
+    bad, _ = oracle.score_unshared(pin_dense_path, wl)
+    assert np.max(np.abs(bad - good)) > 1e-3
+    monkeypatch.undo()
+
+    real_attention = om.attention
+
+    def attention_wrong_group(q, k, v, qp, kp):
+        return real_attention(q, k[:, ::-1], v[:, ::-1], qp, kp)
+
+    monkeypatch.setattr(om, "attention", attention_wrong_group)
+    bad, _ = oracle.score_unshared(pin_dense_path, wl)
+    assert np.max(np.abs(bad - good)) > 1e-3
+
+
+def _hf_gdn(m, layer):
+    import torch
+    from transformers.models.qwen3_next.configuration_qwen3_next import Qwen3NextConfig
+    from transformers.models.qwen3_next.modeling_qwen3_next import Qwen3NextGatedDeltaNet
+    h = m.h
+    H, dk, dv = h["gdn_heads"], h["gdn_dk"], h["gdn_dv"]
+    cfg = Qwen3NextConfig(hidden_size=h["d_model"], linear_num_value_heads=H, linear_num_key_heads=H,
+                          linear_key_head_dim=dk, linear_value_head_dim=dv,
+                          linear_conv_kernel_dim=h["conv_kernel"], hidden_act="silu",
+                          rms_norm_eps=h["rms_eps"], num_hidden_layers=4,
+                          layer_types=["linear_attention"] * 4)
+    net = Qwen3NextGatedDeltaNet(cfg, layer).double().eval()
+    W = m.layer(layer)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))
+    qkvz = []
+    for hh in range(H):
+        qkvz += [W["gdn_wq"][hh * dk:(hh + 1) * dk], W["gdn_wk"][hh * dk:(hh + 1) * dk],
+                 W["gdn_wv"][hh * dv:(hh + 1) * dv], W["gdn_wz"][hh * dv:(hh + 1) * dv]]
+    ba = []
+    for hh in range(H):
+        ba += [W["gdn_wb"][hh:hh + 1], W["gdn_wa"][hh:hh + 1]]
+    with torch.no_grad():
+        net.in_proj_qkvz.weight.copy_(T(np.concatenate(qkvz)))
+        net.in_proj_ba.weight.copy_(T(np.concatenate(ba)))
+        net.conv1d.weight.copy_(T(W["gdn_conv"][:, None, :]))
+        net.A_log.copy_(T(W["gdn_A_log"]))
+        net.dt_bias.copy_(T(W["gdn_dt_bias"]))
+        net.norm.weight.copy_(T(W["gdn_norm"]))
+        net.out_proj.weight.copy_(T(W["gdn_wo"]))
+    return net, W
+
+
+def test_gdn_layer_matches_transformers_qwen3next(pin_hybrid_path):
+    """The gated delta-rule layer (projections, causal conv + SiLU, l2 norms,
+    beta / decay gates, recurrence, gated output norm, output projection)
+    against transformers' Qwen3-Next implementation (its chunked form)."""
+    import torch
+    m = oracle.Model(pin_hybrid_path)
+    rng = np.random.default_rng(6)
+    n = 23
+    a = rng.normal(size=(n, m.d))
+    for layer in (0, 2):
+        net, W = _hf_gdn(m, layer)
+        with torch.no_grad():
+            ref = net(torch.from_numpy(a)[None]).numpy()[0]
+        got, _ = om._gdn_layer(m.h, W, a, [slice(0, n)], [None], layer, False, m.eps)
+        # transformers runs the recurrence in float32
+        np.testing.assert_allclose(got, ref, atol=2e-5 * np.abs(ref).max(), rtol=0)
+        assert np.abs(ref).max() > 1e-2
+
+
+def test_gdn_recurrence_matches_transformers_recurrent_form():
+    import torch
+    from transformers.models.qwen3_next.modeling_qwen3_next import torch_recurrent_gated_delta_rule
+    rng = np.random.default_rng(7)
+    n, H, dk, dv = 9, 3, 8, 5
+    q = rng.normal(size=(n, H, dk)); k = rng.normal(size=(n, H, dk)); v = rng.normal(size=(n, H, dv))
+    g = -np.abs(rng.normal(size=(n, H))); beta = 1 / (1 + np.exp(-rng.normal(size=(n, H))))
+    S0 = rng.normal(size=(H, dv, dk))
+    qn = om.l2norm(q); kn = om.l2norm(k)
+    o, S = om.gdn_recurrence(qn / np.sqrt(dk), kn, v, np.exp(g), beta, S0)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))[None]
+    ref_o, ref_S = torch_recurrent_gated_delta_rule(T(q), T(k), T(v), T(g), T(beta),
+                                                    initial_state=T(np.transpose(S0, (0, 2, 1)))[0][None],
+                                                    output_final_state=True, use_qk_l2norm_in_kernel=True)
+    np.testing.assert_allclose(o, ref_o[0].double().numpy(), atol=1e-5)
+    # transformers keeps the state as [dk, dv]
+    np.testing.assert_allclose(S, np.transpose(ref_S[0].double().numpy(), (0, 2, 1)), atol=1e-5)
+
+
+# --------------------------------------------------------------------------
+# invariants of the scoring method (Section 4.1, Section 5.6)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("which", ["dense", "hybrid"])
+def test_prefix_sharing_equals_unshared(which, pin_dense_path, pin_hybrid_path):
+    path = pin_dense_path if which == "dense" else pin_hybrid_path
+    V = jet_synth.read_header(path)["vocab"]
+    wl = jet_synth.make_workload("micro_hybrid", vocab=V, Q=3, P=(4, 17), K=4, m=(1, 6))
+    a, sa = oracle.score_unshared(path, wl)
+    b, sb = oracle.score_incremental(path, wl)
+    np.testing.assert_allclose(a, b, atol=1e-10, rtol=0)
+    np.testing.assert_allclose(sa, sb, atol=1e-10, rtol=0)
+
+
+@pytest.mark.parametrize("which", ["dense", "hybrid"])
+def test_isolation_and_planted_leak(which, pin_dense_path, pin_hybrid_path):
+    """Scoring a candidate after its siblings equals scoring it alone; the
+    planted leak (state not restored between candidates) is detected."""
+    path = pin_dense_path if which == "dense" else pin_hybrid_path
+    V = jet_synth.read_header(path)["vocab"]
+    wl = jet_synth.make_workload("micro_hybrid", vocab=V, Q=2, P=(6, 12), K=4, m=(2, 6))
+    full, _ = oracle.score_incremental(path, wl)
+    for q in range(wl.n_questions):
+        x = wl.prefix(q)
+        for j, y in enumerate(wl.candidates(q)):
+            alone = jet_synth.from_lists([x], [[y]])
+            t, _ = oracle.score_incremental(path, alone)
+            c = wl.q_cand_offsets[q] + j
+            np.testing.assert_array_equal(t, full[wl.cand_tok_offsets[c]:wl.cand_tok_offsets[c + 1]])
+    leaky, _ = oracle.score_incremental(path, wl, leak=True)
+    assert np.max(np.abs(leaky - full)) > 1e-3
+
+
+def test_candidate_permutation_invariance(pin_dense_path):
+    V = jet_synth.read_header(pin_dense_path)["vocab"]
+    wl = jet_synth.make_workload("tiny", n_questions=3, vocab=V, P=(5, 20), m=(1, 5))
+    _, s = oracle.score_unshared(pin_dense_path, wl)
+    rng = np.random.default_rng(8)
+    pre, cands, perm_all = [], [], []
+    for q in range(wl.n_questions):
+        cs = wl.candidates(q)
+        perm = rng.permutation(len(cs))
+        pre.append(wl.prefix(q)); cands.append([cs[i] for i in perm])
+        perm_all += [wl.q_cand_offsets[q] + i for i in perm]
+    _, s2 = oracle.score_unshared(pin_dense_path, jet_synth.from_lists(pre, cands))
+    np.testing.assert_allclose(s2, s[perm_all], atol=1e-12, rtol=0)
+
+
+def test_duplicates_and_causality(pin_dense_path):
+    """Equal answer text gives equal likelihood (Section 3.3), and a token's
+    log-probability depends only on the tokens before it (Eq. 3 chain rule)."""
+    V = jet_synth.read_header(pin_dense_path)["vocab"]
+    x = np.array([5, 9, 2, 77, 31, 8], np.int32)
+    y = np.array([10, 20, 30, 40], np.int32)
+    y2 = y.copy(); y2[-1] = 41
+    wl = jet_synth.from_lists([x], [[y, y.copy(), y2, y[:2]]])
+    tok, s = oracle.score_unshared(pin_dense_path, wl)
+    assert abs(s[0] - s[1]) < 1e-12
+    assert oracle.decide_choice(np.array([s[0], s[1]])) == 0
+    np.testing.assert_allclose(tok[8:11], tok[0:3], atol=1e-12)   # y2 shares its first 3 tokens
+    assert abs(tok[11] - tok[3]) > 1e-6
+    np.testing.assert_allclose(tok[12:14], tok[0:2], atol=1e-12)  # the 2-token prefix of y
