@@ -1,0 +1,220 @@
+/*
+ * jet.h - C ABI of the MI355X (gfx950) candidate-scoring library.
+ *
+ * The library scores a finite set of candidate answers against one shared
+ * question context by teacher forcing (JET, arXiv 2609.33874):
+ *
+ *   p(y_{c,t} | x, y_{c,<t}) is normalised over the full vocabulary with no
+ *   temperature and no top-k/top-p filtering (Section 3.1, Eq. 1), its log is
+ *   taken in the max-shifted form of Eq. 2, summed per candidate (Section 3.2,
+ *   Eq. 3), normalised over the candidate set (Eq. 4) and turned into a choice,
+ *   a binary probability or an ordinal expectation (Section 3.3, Eq. 5).
+ *
+ * The question prefix is evaluated once and its attention cache / recurrent
+ * state is retained (Section 4.1); every candidate then runs against that
+ * retained state in batches, isolated from its siblings. Only the
+ * log-probabilities of the supplied tokens leave the device (Section 4.2).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Return value: JET_OK (0) or one of the JET_E_* codes. On error no output
+ *   buffer is written, every `out` handle is set to NULL, and jet_last_error()
+ *   returns a message for the calling thread (Figure 1: invalid requests
+ *   produce errors).
+ * Ownership: the caller owns every array passed in or out; the library reads
+ *   and writes them only during the call and keeps no pointer to them. The
+ *   library owns the opaque handles; a jet_prefix borrows its jet_model and
+ *   must be freed before it.
+ * Memory kinds: arrays documented as "host" must be host memory. Arrays
+ *   documented as "host or device" may be host memory or device memory of
+ *   the model's GPU (the kind is queried with hipPointerGetAttributes).
+ * Blocking: every call has finished its GPU work and its outputs are in place
+ *   when it returns (it synchronises the model's stream).
+ * Concurrency: calls on one model must be serialised by the caller.
+ * Token ids: int32 in [0, vocab). Offsets: int64 CSR arrays, first element 0,
+ *   non-decreasing.
+ */
+#ifndef JET_H
+#define JET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  JET_OK = 0,
+  JET_E_INVALID = 1,   /* malformed arguments, ids out of range, empty sequences */
+  JET_E_CAPACITY = 2,  /* a sequence P + m - 1 exceeds max_ctx (never truncated) */
+  JET_E_OOM = 3,       /* device allocation failed or max_device_bytes exceeded */
+  JET_E_DEVICE = 4,    /* a HIP runtime error */
+  JET_E_IO = 5         /* model file missing or malformed */
+};
+
+enum { JET_BF16 = 0, JET_FP32 = 1 };                  /* compute dtype */
+enum { JET_CHOICE = 0, JET_BINARY = 1, JET_ORDINAL = 2 }; /* decision rule */
+
+/* flags for jet_load_opts.flags */
+enum {
+  JET_FLAG_KERNEL_TIMING = 1 /* time every launch with HIP events (jet_stats) */
+};
+
+typedef struct jet_model jet_model;
+typedef struct jet_prefix jet_prefix;
+
+typedef struct {
+  int32_t dtype;                /* JET_BF16 (bf16 operands, fp32 accumulation) or
+                                   JET_FP32 (fp32 everywhere; validation mode) */
+  int32_t device;               /* HIP device ordinal */
+  int64_t max_ctx;              /* max positions per sequence; 0 = the file's value */
+  int64_t prefill_token_budget; /* max prefix tokens per prefill wave; 0 = no limit.
+                                   Waves hold whole questions. */
+  int64_t wave_token_budget;    /* max candidate body tokens per scoring wave;
+                                   0 = no limit. Waves hold whole candidates. */
+  int64_t max_device_bytes;     /* cap on the library's device allocations; 0 = none */
+  void *hip_stream;             /* hipStream_t to run on; NULL = the null stream */
+  int32_t flags;                /* JET_FLAG_* */
+  int32_t reserved;
+} jet_load_opts;
+
+/* Kernel classes reported by jet_stats (index into jet_stats.kernel_*). */
+enum {
+  JET_K_GEMM_QKV = 0,   /* attention / delta-rule input projections */
+  JET_K_GEMM_O = 1,     /* output projection + residual add */
+  JET_K_GEMM_GATEUP = 2,/* FFN gate/up projection + SwiGLU */
+  JET_K_GEMM_DOWN = 3,  /* FFN down projection + residual add */
+  JET_K_LMHEAD = 4,     /* LM head + online log-sum-exp */
+  JET_K_ATTN_PREFIX = 5,/* causal attention over the prefix */
+  JET_K_ATTN_CAND = 6,  /* candidate attention over shared prefix + own suffix */
+  JET_K_GDN = 7,        /* gated delta-rule recurrence (prefix and candidates) */
+  JET_K_OTHER = 8,      /* norms, RoPE, gathers, reductions, ... */
+  JET_K_COUNT = 9
+};
+
+typedef struct {
+  int64_t prefix_tokens;     /* prefix tokens evaluated (sum of P over prefill calls) */
+  int64_t prefix_evals;      /* prefixes evaluated (questions over prefill calls) */
+  int64_t cand_body_tokens;  /* candidate tokens run through the network (sum of m-1) */
+  int64_t scored_tokens;     /* candidate tokens scored (sum of m) */
+  int64_t lm_rows;           /* rows through the LM head */
+  int64_t prefill_waves;
+  int64_t score_waves;
+  int64_t kernel_launches[JET_K_COUNT];
+  double kernel_ms[JET_K_COUNT];       /* only with JET_FLAG_KERNEL_TIMING */
+  double kernel_flops[JET_K_COUNT];    /* algorithmic FLOPs launched per class */
+  double kernel_bytes[JET_K_COUNT];    /* algorithmic HBM bytes launched per class */
+} jet_stats;
+
+/*
+ * jet_model_load - read a model file and upload its weights.
+ *   model_path: host string, path of a model file (JSON header + raw tensors).
+ *   opts: host, may be NULL (defaults: JET_BF16, device 0, no limits, null stream).
+ *   out: host, receives the model handle.
+ * Errors: JET_E_IO (file), JET_E_INVALID (unsupported shape or dtype
+ *   combination: an f32 file cannot be run in JET_BF16), JET_E_OOM, JET_E_DEVICE.
+ */
+int jet_model_load(const char *model_path, const jet_load_opts *opts, jet_model **out);
+
+/*
+ * jet_prefill_prefix - evaluate every question prefix once and retain its
+ * state (Section 4.1; Figure 1, shared-prefix prefill).
+ *   n_q: number of questions (>= 1).
+ *   prefix_offsets: host, int64[n_q + 1]; question q owns
+ *     prefix_tokens[prefix_offsets[q] .. prefix_offsets[q+1]); every P >= 1.
+ *   prefix_tokens: host or device, int32[prefix_offsets[n_q]].
+ *   out: host, receives the prefix handle. It holds the attention cache of
+ *     every attention layer, the recurrent state and convolution tail of every
+ *     delta-rule layer, and the final hidden row and log-sum-exp of each
+ *     prefix's last position (which predicts every candidate's first token,
+ *     Section 4.1). It is immutable and may serve many jet_score_candidates
+ *     calls.
+ * Errors: JET_E_INVALID (offsets, ids, P = 0), JET_E_CAPACITY (P > max_ctx),
+ *   JET_E_OOM, JET_E_DEVICE.
+ */
+int jet_prefill_prefix(jet_model *model, int32_t n_q, const int64_t *prefix_offsets,
+                       const int32_t *prefix_tokens, jet_prefix **out);
+
+/*
+ * jet_score_candidates - teacher-forced log-likelihood of every candidate
+ * (Section 3.1 Eq. 1-2, Section 3.2 Eq. 3).
+ *   q_cand_offsets: host, int64[n_q + 1] (n_q of the prefix); candidate j
+ *     belongs to question q iff q_cand_offsets[q] <= j < q_cand_offsets[q+1].
+ *     A question may have zero candidates.
+ *   cand_tok_offsets: host, int64[N + 1], N = q_cand_offsets[n_q]; candidate j
+ *     is cand_tokens[cand_tok_offsets[j] .. cand_tok_offsets[j+1]); m >= 1.
+ *   cand_tokens: host or device, int32[cand_tok_offsets[N]].
+ *   out_token_logprob: host or device, float[cand_tok_offsets[N]] or NULL;
+ *     element i is log p of cand_tokens[i] given the prefix and the
+ *     candidate's earlier tokens (same CSR indexing as cand_tokens).
+ *   out_cand_sum: host or device, float[N]; s_j, summed in ascending t.
+ * Token y_{c,t} sits at position P + t - 1. Candidates never see each other.
+ * Errors: JET_E_INVALID (offsets, ids, m = 0, prefix of another model),
+ *   JET_E_CAPACITY (P + m - 1 > max_ctx), JET_E_OOM, JET_E_DEVICE.
+ */
+int jet_score_candidates(jet_model *model, const jet_prefix *prefix,
+                         const int64_t *q_cand_offsets, const int64_t *cand_tok_offsets,
+                         const int32_t *cand_tokens, float *out_token_logprob,
+                         float *out_cand_sum);
+
+/*
+ * jet_decide - turn candidate scores into decisions (Section 3.2 Eq. 4,
+ * Section 3.3 Eq. 5). Pure host function in fp64; touches no device.
+ *   mode: JET_CHOICE, JET_BINARY (every question has exactly 2 candidates,
+ *     index 0 = false, 1 = true) or JET_ORDINAL (>= 2 candidates, zero-based
+ *     levels in the supplied order).
+ *   q_cand_offsets: host, int64[n_q + 1]; each question needs >= 1 candidate.
+ *   cand_sum: host, float[N].
+ *   out_q: host, double[N] or NULL: q(c) = exp(s_c - M) / sum_d exp(s_d - M).
+ *   out_choice: host, int32[n_q] or NULL: argmax s, lowest index on ties.
+ *   out_value: host, double[n_q] or NULL: q(true) (JET_BINARY) or
+ *     sum_i i q(i) (JET_ORDINAL); ignored for JET_CHOICE.
+ * Errors: JET_E_INVALID.
+ */
+int jet_decide(int32_t mode, int32_t n_q, const int64_t *q_cand_offsets,
+               const float *cand_sum, double *out_q, int32_t *out_choice,
+               double *out_value);
+
+/*
+ * jet_candidate_layout - the integer row layout that jet_score_candidates
+ * builds (host only; exported so that it can be checked on its own).
+ *   prefix_offsets / q_cand_offsets / cand_tok_offsets: host, as above.
+ *   max_ctx: capacity check, P + m - 1 <= max_ctx (0 = no check).
+ *   cap_rows: capacity of the row_* arrays.
+ *   out_n_rows: host, receives the number of body rows R = sum_c (m_c - 1).
+ *   row_pos / row_q / row_c / row_tok: host, int32[cap_rows] or NULL. Body row
+ *     r carries token cand_tokens[row_tok[r]] = y_{c,t} (t <= m_c - 1) of
+ *     candidate row_c[r] of question row_q[r], at position
+ *     row_pos[r] = P_q + t - 1. Rows are ordered by candidate, then t.
+ *   out_lm_row: host, int32[cand_tok_offsets[N]] or NULL: the row whose
+ *     output distribution predicts token i: -(q + 1) for a first token
+ *     (the last prefix position of question q), else the body row holding
+ *     y_{c,t-1}.
+ * Errors: JET_E_INVALID, JET_E_CAPACITY (also when R > cap_rows).
+ */
+int jet_candidate_layout(int32_t n_q, const int64_t *prefix_offsets,
+                         const int64_t *q_cand_offsets, const int64_t *cand_tok_offsets,
+                         int64_t max_ctx, int64_t cap_rows, int64_t *out_n_rows,
+                         int32_t *row_pos, int32_t *row_q, int32_t *row_c,
+                         int32_t *row_tok, int32_t *out_lm_row);
+
+/* jet_stats - counters and per-kernel-class timings accumulated since load
+ * (or since the last jet_stats_reset). out: host. */
+int jet_stats_get(const jet_model *model, jet_stats *out);
+int jet_stats_reset(jet_model *model);
+
+/* Model facts: vocabulary size, layer count, max_ctx, compute dtype. */
+int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n_layers,
+                   int64_t *max_ctx, int32_t *dtype);
+
+void jet_prefix_free(jet_prefix *prefix);
+void jet_model_free(jet_model *model);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *jet_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* JET_H */

@@ -1,0 +1,230 @@
+// Row-wise and gather kernels of the scoring path: embedding gather, RMSNorm,
+// RoPE + KV-cache scatter, log-sum-exp merge, target log-probability gather
+// (Section 3.1 Eq. 2), per-candidate sums (Section 3.2 Eq. 3), id checks.
+// All are memory-bound; each reads its rows once with 16-byte accesses where
+// the layout allows.
+#include "device.h"
+#include "kernels.h"
+
+namespace jetk {
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const T *__restrict__ E, const int32_t *__restrict__ ids,
+                                                     const int32_t *__restrict__ idx, int d,
+                                                     float *__restrict__ resid) {
+  const int r = blockIdx.x;
+  const int64_t tok = ids[idx ? idx[r] : r];
+  const T *src = E + tok * d;
+  float *dst = resid + (int64_t)r * d;
+  for (int i = threadIdx.x; i < d; i += 256) dst[i] = to_f<T>(src[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ x, const int32_t *__restrict__ map,
+                                                       const float *__restrict__ g, int d, float eps,
+                                                       T *__restrict__ out) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const int64_t src = map ? map[r] : r;
+  const float *xr = x + src * d;
+  float ss = 0.0f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = xr[i];
+    ss += v * v;
+  }
+  ss = warp_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = rsqrtf(tot / (float)d + eps);
+  T *o = out + (int64_t)r * d;
+  for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f<T>(xr[i] * inv * g[i]);
+}
+
+// One block per row; thread t handles rotation pairs (i, i + hd/2).
+template <typename T>
+__global__ __launch_bounds__(256) void rope_scatter_kernel(const float *__restrict__ qkv, const int32_t *__restrict__ pos,
+                                                            const float *__restrict__ cos_t,
+                                                            const float *__restrict__ sin_t, int Hq, int Hkv,
+                                                            int hd, T *__restrict__ q_out, T *__restrict__ kc,
+                                                            T *__restrict__ vc, int64_t S, int64_t slot0) {
+  const int r = blockIdx.x;
+  const int half = hd / 2;
+  const int W = (Hq + 2 * Hkv) * hd;
+  const float *src = qkv + (int64_t)r * W;
+  const int64_t p = pos[r];
+  const float *cs = cos_t + p * half, *sn = sin_t + p * half;
+  const int64_t slot = slot0 + r;
+  for (int t = threadIdx.x; t < (Hq + Hkv) * half; t += 256) {
+    const int h = t / half, i = t % half;
+    const float x1 = src[h * hd + i], x2 = src[h * hd + i + half];
+    const float c = cs[i], s = sn[i];
+    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    if (h < Hq) {
+      T *o = q_out + ((int64_t)r * Hq + h) * hd;
+      o[i] = from_f<T>(y1);
+      o[i + half] = from_f<T>(y2);
+    } else {
+      T *o = kc + ((int64_t)(h - Hq) * S + slot) * hd;
+      o[i] = from_f<T>(y1);
+      o[i + half] = from_f<T>(y2);
+    }
+  }
+  for (int t = threadIdx.x; t < Hkv * hd; t += 256) {
+    const int h = t / hd, i = t % hd;
+    vc[((int64_t)h * S + slot) * hd + i] = from_f<T>(src[(Hq + Hkv) * hd + t]);
+  }
+}
+
+__global__ __launch_bounds__(256) void lse_merge_kernel(const float *__restrict__ pm, const float *__restrict__ ps,
+                                                         int nsplit, int R, float *__restrict__ lse) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= R) return;
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pm[(int64_t)s * R + r]);
+  float S = 0.0f;
+  for (int s = 0; s < nsplit; ++s) S += ps[(int64_t)s * R + r] * exp2f(pm[(int64_t)s * R + r] - M);
+  lse[r] = (M + log2f(S)) * kLn2;
+}
+
+// One wave per scored token: ell = <f_row, W[y]> - lse_row.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__restrict__ tokens,
+                                                              const int32_t *__restrict__ lm_row, int n_out,
+                                                              int row_base, const T *__restrict__ f_body,
+                                                              const float *__restrict__ lse_body,
+                                                              const T *__restrict__ f_last,
+                                                              const float *__restrict__ lse_last,
+                                                              const T *__restrict__ W, int d,
+                                                              float *__restrict__ ell) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= n_out) return;
+  const int r = lm_row[i];
+  const T *f;
+  float lse;
+  if (r < 0) {
+    f = f_last + (int64_t)(-r - 1) * d;
+    lse = lse_last[-r - 1];
+  } else {
+    f = f_body + (int64_t)(r - row_base) * d;
+    lse = lse_body[r - row_base];
+  }
+  const T *w = W + (int64_t)tokens[i] * d;
+  float acc = 0.0f;
+  for (int k = lane; k < d; k += 64) acc += to_f<T>(f[k]) * to_f<T>(w[k]);
+  acc = warp_sum(acc);
+  if (lane == 0) ell[i] = acc - lse;
+}
+
+__global__ __launch_bounds__(256) void segment_sum_kernel(const float *__restrict__ ell, const int64_t *__restrict__ off,
+                                                           int n, float *__restrict__ s) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= n) return;
+  const int64_t b = off[0];
+  float acc = 0.0f;
+  for (int64_t i = off[c]; i < off[c + 1]; ++i) acc += ell[i - b];
+  s[c] = acc;
+}
+
+__global__ __launch_bounds__(256) void count_bad_ids_kernel(const int32_t *__restrict__ ids, int64_t n, int V,
+                                                             int *__restrict__ bad) {
+  int cnt = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    cnt += (ids[i] < 0 || ids[i] >= V) ? 1 : 0;
+  cnt = (int)warp_sum((float)cnt);
+  if ((threadIdx.x & 63) == 0 && cnt) atomicAdd(bad, cnt);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void convert_f32_kernel(const float *__restrict__ src, int64_t n, T *__restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = from_f<T>(src[i]);
+}
+
+__global__ __launch_bounds__(256) void bf16_to_f32_kernel(const uint16_t *__restrict__ src, int64_t n,
+                                                           float *__restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = bf2f(src[i]);
+}
+
+// ---------------------------------------------------------------------------
+
+hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int32_t *idx, int R, int d,
+                        float *resid, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0) hipLaunchKernelGGL(embed_kernel<bf16>, dim3(R), dim3(256), 0, st, (const bf16 *)E, ids, idx, d, resid);
+  else hipLaunchKernelGGL(embed_kernel<float>, dim3(R), dim3(256), 0, st, (const float *)E, ids, idx, d, resid);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, const float *x, const int32_t *map, const float *g, int R, int d, float eps,
+                          void *out, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0) hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
+  else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(R), dim3(256), 0, st, x, map, g, d, eps, (float *)out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_scatter(int dtype, const float *qkv, const int32_t *pos, const float *cos_t,
+                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, void *k_cache,
+                               void *v_cache, int64_t S, int64_t slot0, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0)
+    hipLaunchKernelGGL(rope_scatter_kernel<bf16>, dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq, Hkv, hd,
+                       (bf16 *)q_out, (bf16 *)k_cache, (bf16 *)v_cache, S, slot0);
+  else
+    hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq, Hkv, hd,
+                       (float *)q_out, (float *)k_cache, (float *)v_cache, S, slot0);
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_merge(const float *pm, const float *ps, int nsplit, int R, float *lse, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3((R + 255) / 256), dim3(256), 0, st, pm, ps, nsplit, R, lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_logprob(int dtype, const int32_t *tokens, const int32_t *lm_row, int n_out, int row_base,
+                                 const void *f_body, const float *lse_body, const void *f_last,
+                                 const float *lse_last, const void *W, int d, float *ell, hipStream_t st) {
+  if (n_out <= 0) return hipSuccess;
+  dim3 grid((n_out + 3) / 4);
+  if (dtype == 0)
+    hipLaunchKernelGGL(gather_logprob_kernel<bf16>, grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
+                       (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d, ell);
+  else
+    hipLaunchKernelGGL(gather_logprob_kernel<float>, grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
+                       (const float *)f_body, lse_body, (const float *)f_last, lse_last, (const float *)W, d, ell);
+  return hipGetLastError();
+}
+
+hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n, float *s, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(segment_sum_kernel, dim3((n + 255) / 256), dim3(256), 0, st, ell, off, n, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_bad_ids(const int32_t *ids, int64_t n, int V, int *bad, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 1024);
+  hipLaunchKernelGGL(count_bad_ids_kernel, dim3(blocks), dim3(256), 0, st, ids, n, V, bad);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
+  if (dtype == 0) hipLaunchKernelGGL(convert_f32_kernel<bf16>, dim3(blocks), dim3(256), 0, st, src, n, (bf16 *)dst);
+  else hipLaunchKernelGGL(convert_f32_kernel<float>, dim3(blocks), dim3(256), 0, st, src, n, (float *)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(blocks), dim3(256), 0, st, src, n, dst);
+  return hipGetLastError();
+}
+
+}  // namespace jetk

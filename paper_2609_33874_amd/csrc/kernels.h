@@ -1,0 +1,85 @@
+// Host-side launchers of the HIP kernels (internal to the library).
+// dtype: 0 = bf16 operands, 1 = fp32 operands. Every launcher returns the
+// launch status and enqueues work on `st` only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jetk {
+
+enum { EPI_STORE_F32 = 0, EPI_RESID_ADD = 1, EPI_SWIGLU = 2, EPI_STORE_T = 3 };
+
+// C[M x N] (epilogue) A[M x K] * B[N x K]^T. K must be a multiple of
+// gemm_k_step(dtype). EPI_SWIGLU expects B rows interleaved in blocks of 32
+// gate rows then 32 up rows and writes silu(gate) * up to out[M x N/2] (T).
+int gemm_k_step(int dtype);
+hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
+                       int N, int K, void *out, int64_t ldo, hipStream_t st);
+
+// LM head + online log-sum-exp: partial (max, sum) in base 2 per (split, row).
+int lmhead_num_splits(int V, int tiles_per_split);
+hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K,
+                             int tiles_per_split, float *part_m, float *part_s, hipStream_t st);
+// lse[r] = ln(sum over splits) from the partials.
+hipError_t launch_lse_merge(const float *part_m, const float *part_s, int nsplit, int R, float *lse,
+                            hipStream_t st);
+
+// Attention work item: one (question, kv head, block of <= 64 query slots).
+struct AttnItem {
+  int32_t q, kvh, slot0, nslots, nkeys_pre;
+};
+// Per question of a call (device arrays indexed by the item's q).
+struct AttnQuestions {
+  const int32_t *qrow0;    // first query row of the question in Q / O
+  const int32_t *nrows;    // query rows of the question
+  const int64_t *pre_slot0;  // first prefix key slot in the prefix cache
+  const int32_t *pre_len;  // prefix keys
+  const int32_t *suf_row0; // first own-suffix key row in the call's K/V (candidate mode)
+  const int32_t *suf_len;
+};
+// mode 0: causal prefix attention (query i of a question sees prefix keys 0..i).
+// mode 1: candidate attention: every prefix key, plus the suffix keys j with
+//         row_c[j] == row_c[i] and row_t[j] <= row_t[i].
+struct AttnArgs {
+  int mode;
+  const void *Q;        // [rows][Hq][hd]
+  void *O;              // [rows][Hq][hd]
+  const void *Kp, *Vp;  // prefix cache [Hkv][S_pre][hd]
+  int64_t s_pre;
+  const void *Ks, *Vs;  // own-suffix keys of the call [Hkv][S_suf][hd]
+  int64_t s_suf;
+  const int32_t *row_c, *row_t;  // per call row (candidate mode)
+  AttnQuestions qs;
+  const AttnItem *items;
+  int n_items;
+  int Hq, Hkv, hd;
+  float scale;
+};
+hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st);
+
+// resid[r][:] = E[ids[idx ? idx[r] : r]][:] (as fp32).
+hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int32_t *idx, int R, int d,
+                        float *resid, hipStream_t st);
+// out[r][:] = x[src][:] / sqrt(mean(x[src]^2) + eps) * g, src = map ? map[r] : r; out in T.
+hipError_t launch_rmsnorm(int dtype, const float *x, const int32_t *map, const float *g, int R, int d,
+                          float eps, void *out, hipStream_t st);
+// qkv fp32 [R][(Hq + 2 Hkv) hd] -> q (T) [R][Hq][hd] with RoPE, K (RoPE) and V
+// into the cache [Hkv][S][hd] at slot slot0 + r, angles from pos[r].
+hipError_t launch_rope_scatter(int dtype, const float *qkv, const int32_t *pos, const float *cos_t,
+                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, void *k_cache,
+                               void *v_cache, int64_t S, int64_t slot0, hipStream_t st);
+// ell[i] = dot(f_row, W[y_i]) - lse_row for output i; the row is f_body[lm_row[i] - row_base]
+// or, when lm_row[i] < 0, f_last[-lm_row[i] - 1].
+hipError_t launch_gather_logprob(int dtype, const int32_t *tokens, const int32_t *lm_row, int n_out,
+                                 int row_base, const void *f_body, const float *lse_body, const void *f_last,
+                                 const float *lse_last, const void *W, int d, float *ell, hipStream_t st);
+// s[c] = sum of ell[off[c] - off[0] .. off[c+1] - off[0]) in ascending order.
+hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n_cand, float *s, hipStream_t st);
+// Counts ids outside [0, V) into *bad (int, must be zeroed by the caller).
+hipError_t launch_count_bad_ids(const int32_t *ids, int64_t n, int V, int *bad, hipStream_t st);
+// dst[i] = src[i] with fp32 -> T conversion (weights upload helpers).
+hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst, hipStream_t st);
+hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst, hipStream_t st);
+
+}  // namespace jetk

@@ -1,0 +1,847 @@
+// Scoring runtime: weight upload, shared-prefix prefill, batched candidate
+// scoring, and the C ABI entry points of jet.h.
+//
+// Flow (Section 4.1, Figure 1): jet_prefill_prefix runs every question prefix
+// once, keeps its attention cache / recurrent state and the final hidden row
+// of its last position; jet_score_candidates runs all candidate tokens of a
+// wave as one batch against that retained state, computes full-vocabulary
+// log-sum-exps without writing logits (Section 4.2) and sums each candidate's
+// log-probabilities (Eq. 3).
+#include "runtime.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+using namespace jet;
+
+#define HIPC(x)                                                                                      \
+  do {                                                                                               \
+    hipError_t e_ = (x);                                                                             \
+    if (e_ != hipSuccess)                                                                            \
+      return Status::err(e_ == hipErrorOutOfMemory ? JET_E_OOM : JET_E_DEVICE,                       \
+                         std::string(#x) + ": " + hipGetErrorString(e_));                           \
+  } while (0)
+
+#define TRY(x)                 \
+  do {                         \
+    Status s_ = (x);           \
+    if (!s_) return s_;        \
+  } while (0)
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// device memory with an optional byte budget
+// ---------------------------------------------------------------------------
+
+Status dmalloc(jet_model *m, size_t bytes, void **p) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  if (m->max_bytes > 0 && m->bytes_used + bytes > (size_t)m->max_bytes)
+    return Status::err(JET_E_OOM, "device byte budget exceeded (" + std::to_string(m->bytes_used + bytes) +
+                                      " > " + std::to_string(m->max_bytes) + ")");
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return Status::err(JET_E_OOM, "hipMalloc(" + std::to_string(bytes) + "): " + hipGetErrorString(e));
+  }
+  m->bytes_used += bytes;
+  return Status::ok();
+}
+
+void dfree(jet_model *m, void *p, size_t bytes) {
+  if (!p) return;
+  (void)hipFree(p);
+  m->bytes_used -= std::min(m->bytes_used, bytes == 0 ? (size_t)256 : bytes);
+}
+
+// Grow-only named workspace buffer.
+Status ws(jet_model *m, const char *name, size_t bytes, void **p) {
+  DevBuf &b = m->ws[name];
+  if (b.bytes < bytes) {
+    dfree(m, b.p, b.bytes);
+    b = DevBuf{};
+    size_t want = bytes + bytes / 8;
+    TRY(dmalloc(m, want, &b.p));
+    b.bytes = want;
+  }
+  *p = b.p;
+  return Status::ok();
+}
+
+template <typename T>
+Status ws_t(jet_model *m, const char *name, size_t n, T **p) {
+  void *v;
+  TRY(ws(m, name, n * sizeof(T), &v));
+  *p = (T *)v;
+  return Status::ok();
+}
+
+template <typename T>
+Status upload(jet_model *m, const char *name, const std::vector<T> &v, T **p) {
+  TRY(ws_t<T>(m, name, std::max<size_t>(v.size(), 1), p));
+  if (!v.empty()) HIPC(hipMemcpyAsync(*p, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice, m->st));
+  return Status::ok();
+}
+
+bool is_device_ptr(const void *p) {
+  if (!p) return false;
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged;
+}
+
+// ---------------------------------------------------------------------------
+// kernel timing (HIP events around each launch when JET_FLAG_KERNEL_TIMING)
+// ---------------------------------------------------------------------------
+
+struct KTimer {
+  jet_model *m;
+  int cls;
+  hipEvent_t a = nullptr, b = nullptr;
+  KTimer(jet_model *m_, int cls_, double flops, double bytes) : m(m_), cls(cls_) {
+    m->stats.kernel_launches[cls]++;
+    m->stats.kernel_flops[cls] += flops;
+    m->stats.kernel_bytes[cls] += bytes;
+    if (m->flags & JET_FLAG_KERNEL_TIMING) {
+      a = get();
+      b = get();
+      (void)hipEventRecord(a, m->st);
+    }
+  }
+  hipEvent_t get() {
+    if (!m->event_pool.empty()) {
+      hipEvent_t e = m->event_pool.back();
+      m->event_pool.pop_back();
+      return e;
+    }
+    hipEvent_t e;
+    (void)hipEventCreate(&e);
+    return e;
+  }
+  ~KTimer() {
+    if (a) {
+      (void)hipEventRecord(b, m->st);
+      m->pending.push_back({cls, a, b});
+    }
+  }
+};
+
+void drain_timers(jet_model *m) {
+  for (auto &p : m->pending) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) m->stats.kernel_ms[p.cls] += ms;
+    else (void)hipGetLastError();
+    m->event_pool.push_back(p.a);
+    m->event_pool.push_back(p.b);
+  }
+  m->pending.clear();
+}
+
+Status sync(jet_model *m) {
+  HIPC(hipStreamSynchronize(m->st));
+  drain_timers(m);
+  return Status::ok();
+}
+
+#define LAUNCH(x) HIPC(x)
+
+// ---------------------------------------------------------------------------
+// model loading
+// ---------------------------------------------------------------------------
+
+struct Loader {
+  jet_model *m;
+  std::vector<char> host;
+
+  Status read(const std::string &name, const TensorInfo **ti) {
+    auto it = m->h.tensors.find(name);
+    if (it == m->h.tensors.end()) return Status::err(JET_E_IO, "model file lacks tensor " + name);
+    *ti = &it->second;
+    host.resize((size_t)it->second.nbytes);
+    return read_tensor_bytes(m->path, it->second, host.data());
+  }
+
+  // Uploads host bytes of `n` elements stored as bf16 (src_bf16) or f32 into a
+  // new device array of the compute dtype.
+  Status put_matrix(const void *src, int64_t n, bool src_bf16, void **out) {
+    const size_t dst_bytes = (size_t)n * m->esz;
+    TRY(dmalloc(m, dst_bytes, out));
+    m->weight_allocs.push_back(*out);
+    if ((m->dtype == JET_BF16) == src_bf16) {
+      HIPC(hipMemcpy(*out, src, dst_bytes, hipMemcpyHostToDevice));
+      return Status::ok();
+    }
+    // bf16 file in fp32 mode: upload bits, widen exactly on the device
+    void *tmp;
+    TRY(dmalloc(m, (size_t)n * 2, &tmp));
+    hipError_t e = hipMemcpy(tmp, src, (size_t)n * 2, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = jetk::launch_convert_bf16_to_f32((const uint16_t *)tmp, n, (float *)*out, m->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->st);
+    dfree(m, tmp, (size_t)n * 2);
+    HIPC(e);
+    return Status::ok();
+  }
+
+  Status matrix(const std::string &name, void **out) {
+    const TensorInfo *ti;
+    TRY(read(name, &ti));
+    return put_matrix(host.data(), ti->numel(), ti->bf16, out);
+  }
+
+  Status vec_f32(const std::string &name, float **out, int64_t expect) {
+    const TensorInfo *ti;
+    TRY(read(name, &ti));
+    if (ti->bf16 || ti->numel() != expect) return Status::err(JET_E_IO, name + ": expected f32[" + std::to_string(expect) + "]");
+    TRY(dmalloc(m, (size_t)expect * 4, (void **)out));
+    m->weight_allocs.push_back(*out);
+    HIPC(hipMemcpy(*out, host.data(), (size_t)expect * 4, hipMemcpyHostToDevice));
+    return Status::ok();
+  }
+
+  // Concatenates matrices row-wise (all [rows_i][d]) and pads to `pad_rows`.
+  Status concat(const std::vector<std::string> &names, int64_t d, int64_t pad_rows, void **out, int64_t *rows_out) {
+    std::vector<char> all;
+    bool bf = m->h.bf16;
+    const size_t es = bf ? 2 : 4;
+    int64_t rows = 0;
+    for (auto &nm : names) {
+      const TensorInfo *ti;
+      TRY(read(nm, &ti));
+      if (ti->shape.size() != 2 || ti->shape[1] != d) return Status::err(JET_E_IO, nm + ": bad shape");
+      all.insert(all.end(), host.begin(), host.end());
+      rows += ti->shape[0];
+    }
+    if (pad_rows > rows) {
+      all.resize((size_t)pad_rows * d * es, 0);
+      rows = pad_rows;
+    }
+    if (rows_out) *rows_out = rows;
+    return put_matrix(all.data(), rows * d, bf, out);
+  }
+
+  // gate/up interleaved in blocks of 32 rows: [g0..g31, u0..u31, g32.., u32.., ...]
+  Status gate_up(const std::string &g, const std::string &u, int64_t F, int64_t d, void **out) {
+    const bool bf = m->h.bf16;
+    const size_t es = bf ? 2 : 4, row = (size_t)d * es;
+    const TensorInfo *ti;
+    TRY(read(g, &ti));
+    std::vector<char> gate = host;
+    TRY(read(u, &ti));
+    std::vector<char> all((size_t)2 * F * row);
+    for (int64_t b = 0; b < F / 32; ++b) {
+      std::memcpy(&all[(size_t)(2 * b) * 32 * row], &gate[(size_t)b * 32 * row], 32 * row);
+      std::memcpy(&all[(size_t)(2 * b + 1) * 32 * row], &host[(size_t)b * 32 * row], 32 * row);
+    }
+    return put_matrix(all.data(), 2 * F * d, bf, out);
+  }
+};
+
+Status check_shapes(const ModelHeader &h, int dtype) {
+  const int64_t bk = dtype == JET_BF16 ? 64 : 32;
+  if (dtype == JET_BF16 && !h.bf16)
+    return Status::err(JET_E_INVALID, "an f32 model file cannot run in JET_BF16 (its weights are not bf16 values)");
+  if (h.head_dim != 32 && h.head_dim != 64 && h.head_dim != 128)
+    return Status::err(JET_E_INVALID, "head_dim must be 32, 64 or 128");
+  if (h.n_kv_heads < 1 || h.n_heads % h.n_kv_heads != 0) return Status::err(JET_E_INVALID, "n_heads % n_kv_heads != 0");
+  if (h.d % bk || (h.n_heads * h.head_dim) % bk || h.ffn % bk)
+    return Status::err(JET_E_INVALID, "d_model, n_heads*head_dim and ffn must be multiples of " + std::to_string(bk));
+  if (h.ffn % 32) return Status::err(JET_E_INVALID, "ffn must be a multiple of 32");
+  if (h.hybrid) return Status::err(JET_E_INVALID, "hybrid (gated delta-rule) models are not supported by this build");
+  return Status::ok();
+}
+
+Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
+  m->path = path;
+  TRY(read_model_header(m->path, &m->h));
+  const ModelHeader &h = m->h;
+  TRY(check_shapes(h, m->dtype));
+  m->esz = m->dtype == JET_BF16 ? 2 : 4;
+  m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
+  HIPC(hipSetDevice(m->device));
+  Loader L{m, {}};
+  TRY(L.matrix("tok_embed", &m->embed));
+  TRY(L.matrix("lm_head", &m->lm_head));
+  TRY(L.vec_f32("final_norm", &m->final_norm, h.d));
+  m->layers.resize((size_t)h.n_layers);
+  for (int64_t i = 0; i < h.n_layers; ++i) {
+    Layer &ly = m->layers[(size_t)i];
+    const std::string p = "blk." + std::to_string(i) + ".";
+    ly.gdn = h.layer_is_gdn[(size_t)i] != 0;
+    TRY(L.vec_f32(p + "attn_norm", &ly.attn_norm, h.d));
+    TRY(L.vec_f32(p + "ffn_norm", &ly.ffn_norm, h.d));
+    if (!ly.gdn) {
+      TRY(L.concat({p + "wq", p + "wk", p + "wv"}, h.d, 0, &ly.w_qkv, nullptr));
+      TRY(L.matrix(p + "wo", &ly.w_o));
+    }
+    TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu));
+    TRY(L.matrix(p + "w_down", &ly.w_down));
+  }
+  // RoPE tables: angles in fp64 on the host, stored as fp32 [max_ctx][hd/2]
+  const int64_t half = h.head_dim / 2;
+  std::vector<float> c((size_t)(m->max_ctx * half)), s((size_t)(m->max_ctx * half));
+  for (int64_t p = 0; p < m->max_ctx; ++p)
+    for (int64_t i = 0; i < half; ++i) {
+      const double inv = std::pow(h.rope_theta, -(2.0 * (double)i) / (double)h.head_dim);
+      const double a = (double)p * inv;
+      c[(size_t)(p * half + i)] = (float)std::cos(a);
+      s[(size_t)(p * half + i)] = (float)std::sin(a);
+    }
+  TRY(dmalloc(m, c.size() * 4, (void **)&m->rope_cos));
+  m->weight_allocs.push_back(m->rope_cos);
+  TRY(dmalloc(m, s.size() * 4, (void **)&m->rope_sin));
+  m->weight_allocs.push_back(m->rope_sin);
+  HIPC(hipMemcpy(m->rope_cos, c.data(), c.size() * 4, hipMemcpyHostToDevice));
+  HIPC(hipMemcpy(m->rope_sin, s.data(), s.size() * 4, hipMemcpyHostToDevice));
+  return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
+// shared pieces of the forward pass
+// ---------------------------------------------------------------------------
+
+double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (double)N * (double)K; }
+
+Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t M,
+                int64_t N, int64_t K, void *out, int64_t ldo) {
+  const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 : N) *
+                           (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
+                           (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
+  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K + N * K) * (double)m->esz + out_bytes);
+  LAUNCH(jetk::launch_gemm(m->dtype == JET_BF16 ? 0 : 1, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, out, ldo, m->st));
+  return Status::ok();
+}
+
+// LM head + online LSE over R rows of F (compute dtype) -> lse[R] (fp32).
+Status run_lmhead(jet_model *m, const void *F, int64_t R, float *lse) {
+  if (R <= 0) return Status::ok();
+  const int64_t V = m->h.vocab, d = m->h.d;
+  const int64_t ntiles = (V + 127) / 128, rtiles = (R + 127) / 128;
+  int64_t tps = std::max<int64_t>(1, (ntiles * rtiles + 4095) / 4096);
+  const int nsplit = jetk::lmhead_num_splits((int)V, (int)tps);
+  float *pm, *ps;
+  TRY(ws_t<float>(m, "lm_pm", (size_t)(nsplit * R), &pm));
+  TRY(ws_t<float>(m, "lm_ps", (size_t)(nsplit * R), &ps));
+  {
+    KTimer t(m, JET_K_LMHEAD, gemm_flops(R, V, d), (double)(V * d + R * d) * (double)m->esz);
+    LAUNCH(jetk::launch_lmhead_lse(m->dtype == JET_BF16 ? 0 : 1, m->lm_head, F, (int)V, (int)R, (int)d, (int)tps,
+                                   pm, ps, m->st));
+  }
+  KTimer t2(m, JET_K_OTHER, 0, 0);
+  LAUNCH(jetk::launch_lse_merge(pm, ps, nsplit, (int)R, lse, m->st));
+  m->stats.lm_rows += R;
+  return Status::ok();
+}
+
+struct QDesc {
+  std::vector<int32_t> qrow0, nrows, pre_len, suf_row0, suf_len;
+  std::vector<int64_t> pre_slot0;
+};
+
+// Work items: per (question, kv head), blocks of 64 (head, row) slots.
+void build_items(const QDesc &qd, int G, int Hkv, bool causal, std::vector<jetk::AttnItem> *items,
+                 double *flops_pairs) {
+  items->clear();
+  double pairs = 0;
+  for (size_t q = 0; q < qd.nrows.size(); ++q) {
+    const int n = qd.nrows[q];
+    if (n <= 0) continue;
+    const int total = G * n;
+    for (int kvh = 0; kvh < Hkv; ++kvh)
+      for (int s0 = 0; s0 < total; s0 += 64) {
+        const int ns = std::min(64, total - s0);
+        int maxq;
+        if (s0 / n != (s0 + ns - 1) / n) maxq = n - 1;
+        else maxq = (s0 + ns - 1) % n;
+        items->push_back({(int32_t)q, kvh, s0, ns, maxq + 1});
+      }
+    if (causal) pairs += (double)G * Hkv * (double)n * (double)(n + 1) / 2.0;
+    else pairs += (double)G * Hkv * (double)n * (double)(qd.pre_len[q] + qd.suf_len[q]);
+  }
+  *flops_pairs = pairs;
+}
+
+// Attention launch plan of one wave: work items and per-question descriptors
+// uploaded once, reused by every attention layer of the wave.
+struct AttnPlan {
+  jetk::AttnArgs a{};
+  double flops = 0, bytes = 0;
+};
+
+Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, AttnPlan *pl) {
+  const ModelHeader &h = m->h;
+  const int G = (int)(h.n_heads / h.n_kv_heads);
+  std::vector<jetk::AttnItem> items;
+  double pairs = 0;
+  build_items(qd, G, (int)h.n_kv_heads, mode == 0, &items, &pairs);
+  jetk::AttnItem *d_items;
+  int32_t *d_qrow0, *d_nrows, *d_prelen, *d_sufrow0, *d_suflen;
+  int64_t *d_preslot;
+  const std::string t(tag);
+  TRY(upload(m, (t + "items").c_str(), items, &d_items));
+  TRY(upload(m, (t + "qrow0").c_str(), qd.qrow0, &d_qrow0));
+  TRY(upload(m, (t + "nrows").c_str(), qd.nrows, &d_nrows));
+  TRY(upload(m, (t + "prelen").c_str(), qd.pre_len, &d_prelen));
+  TRY(upload(m, (t + "sufrow0").c_str(), qd.suf_row0, &d_sufrow0));
+  TRY(upload(m, (t + "suflen").c_str(), qd.suf_len, &d_suflen));
+  TRY(upload(m, (t + "preslot").c_str(), qd.pre_slot0, &d_preslot));
+  jetk::AttnArgs &a = pl->a;
+  a.mode = mode;
+  a.qs = {d_qrow0, d_nrows, d_preslot, d_prelen, d_sufrow0, d_suflen};
+  a.items = d_items;
+  a.n_items = (int)items.size();
+  a.Hq = (int)h.n_heads;
+  a.Hkv = (int)h.n_kv_heads;
+  a.hd = (int)h.head_dim;
+  a.scale = (float)(1.0 / std::sqrt((double)h.head_dim));
+  // algorithmic bytes: every K/V row of the prefix (and suffix) read once per
+  // kv head, Q read and O written once
+  double kv_rows = 0, qo_rows = 0;
+  for (size_t q = 0; q < qd.nrows.size(); ++q)
+    if (qd.nrows[q] > 0) kv_rows += (double)qd.pre_len[q] + (double)qd.suf_len[q];
+  for (auto n : qd.nrows) qo_rows += n;
+  pl->bytes = (double)m->esz * (kv_rows * 2.0 * (double)h.n_kv_heads * (double)h.head_dim +
+                                qo_rows * 2.0 * (double)h.n_heads * (double)h.head_dim);
+  pl->flops = 4.0 * pairs * (double)h.head_dim;
+  return Status::ok();
+}
+
+Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, void *O, const void *Kp, const void *Vp,
+                     int64_t s_pre, const void *Ks, const void *Vs, int64_t s_suf, const int32_t *row_c,
+                     const int32_t *row_t) {
+  if (pl.a.n_items == 0) return Status::ok();
+  jetk::AttnArgs a = pl.a;
+  a.Q = Q;
+  a.O = O;
+  a.Kp = Kp;
+  a.Vp = Vp;
+  a.s_pre = s_pre;
+  a.Ks = Ks;
+  a.Vs = Vs;
+  a.s_suf = s_suf;
+  a.row_c = row_c;
+  a.row_t = row_t;
+  KTimer t(m, a.mode == 0 ? JET_K_ATTN_PREFIX : JET_K_ATTN_CAND, pl.flops, pl.bytes);
+  LAUNCH(jetk::launch_attention(m->dtype == JET_BF16 ? 0 : 1, a, m->st));
+  return Status::ok();
+}
+
+// Buffers of one forward wave over R rows.
+struct WaveBufs {
+  float *resid = nullptr, *qkv = nullptr;
+  void *xn = nullptr, *q = nullptr, *att = nullptr, *act = nullptr;
+};
+
+Status wave_bufs(jet_model *m, int64_t R, WaveBufs *b) {
+  const ModelHeader &h = m->h;
+  const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
+  TRY(ws_t<float>(m, "resid", (size_t)(R * h.d), &b->resid));
+  TRY(ws_t<float>(m, "qkv", (size_t)(R * nqkv), &b->qkv));
+  TRY(ws(m, "xn", (size_t)(R * h.d) * m->esz, &b->xn));
+  TRY(ws(m, "q", (size_t)(R * h.n_heads * h.head_dim) * m->esz, &b->q));
+  TRY(ws(m, "att", (size_t)(R * h.n_heads * h.head_dim) * m->esz, &b->att));
+  TRY(ws(m, "act", (size_t)(R * h.ffn) * m->esz, &b->act));
+  return Status::ok();
+}
+
+// The FFN sublayer: resid += down(silu(gate(x)) * up(x)), x = RMSNorm(resid).
+Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
+  const ModelHeader &h = m->h;
+  {
+    KTimer t(m, JET_K_OTHER, 0, 0);
+    LAUNCH(jetk::launch_rmsnorm(m->dtype == JET_BF16 ? 0 : 1, b.resid, nullptr, ly.ffn_norm, (int)R, (int)h.d,
+                                (float)h.rms_eps, b.xn, m->st));
+  }
+  TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, h.d, ly.w_gu, h.d, R, 2 * h.ffn, h.d, b.act, h.ffn));
+  TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, h.ffn, ly.w_down, h.ffn, R, h.d, h.ffn, b.resid, h.d));
+  return Status::ok();
+}
+
+// Attention sublayer up to the attention kernel: x = RMSNorm(resid); qkv;
+// RoPE; K/V written to (kc, vc) at slot0 + r of an [Hkv][S][hd] cache.
+Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, const int32_t *d_pos, void *kc, void *vc,
+               int64_t S, int64_t slot0) {
+  const ModelHeader &h = m->h;
+  const int dt = m->dtype == JET_BF16 ? 0 : 1;
+  const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
+  {
+    KTimer t(m, JET_K_OTHER, 0, 0);
+    LAUNCH(jetk::launch_rmsnorm(dt, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps, b.xn, m->st));
+  }
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv));
+  KTimer t(m, JET_K_OTHER, 0, 0);
+  LAUNCH(jetk::launch_rope_scatter(dt, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
+                                   (int)h.n_kv_heads, (int)h.head_dim, b.q, kc, vc, S, slot0, m->st));
+  return Status::ok();
+}
+
+Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
+  const ModelHeader &h = m->h;
+  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, h.n_heads * h.head_dim, ly.w_o,
+                  h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d);
+}
+
+// Token ids: validated on the host (host memory) or by a device count.
+Status check_ids(jet_model *m, const int32_t *ids, int64_t n, bool on_device, const char *what) {
+  if (n == 0) return Status::ok();
+  if (!ids) return Status::err(JET_E_INVALID, std::string(what) + " is NULL");
+  if (!on_device) return check_ids_host(ids, n, m->h.vocab, what);
+  int *bad;
+  TRY(ws_t<int>(m, "badids", 1, &bad));
+  HIPC(hipMemsetAsync(bad, 0, sizeof(int), m->st));
+  LAUNCH(jetk::launch_count_bad_ids(ids, n, (int)m->h.vocab, bad, m->st));
+  int hb = 0;
+  HIPC(hipMemcpyAsync(&hb, bad, sizeof(int), hipMemcpyDeviceToHost, m->st));
+  TRY(sync(m));
+  if (hb) return Status::err(JET_E_INVALID, std::string(what) + ": " + std::to_string(hb) + " ids outside [0, vocab)");
+  return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
+// prefill
+// ---------------------------------------------------------------------------
+
+void free_prefix(jet_prefix *p) {
+  if (!p) return;
+  for (void *a : p->allocs) (void)hipFree(a);
+  if (p->m) {
+    p->m->bytes_used -= std::min(p->m->bytes_used, p->bytes);
+    p->m->n_prefixes--;
+  }
+  delete p;
+}
+
+Status palloc(jet_prefix *p, size_t bytes, void **out) {
+  TRY(dmalloc(p->m, bytes, out));
+  p->allocs.push_back(*out);
+  p->bytes += bytes == 0 ? 256 : bytes;
+  return Status::ok();
+}
+
+Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *tokens, jet_prefix *p) {
+  const ModelHeader &h = m->h;
+  TRY(check_offsets(offs, n_q, 1, "prefix_offsets"));
+  for (int32_t q = 0; q < n_q; ++q)
+    if (offs[q + 1] - offs[q] > m->max_ctx)
+      return Status::err(JET_E_CAPACITY, "prefix " + std::to_string(q) + " longer than max_ctx");
+  const int64_t T = offs[n_q];
+  const bool tok_dev = is_device_ptr(tokens);
+  TRY(check_ids(m, tokens, T, tok_dev, "prefix_tokens"));
+  p->n_q = n_q;
+  p->prefix_offsets.assign(offs, offs + n_q + 1);
+  p->T = T;
+  const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz;
+  p->kcache.assign((size_t)h.n_layers, nullptr);
+  p->vcache.assign((size_t)h.n_layers, nullptr);
+  for (int64_t l = 0; l < h.n_layers; ++l) {
+    if (m->layers[(size_t)l].gdn) continue;
+    TRY(palloc(p, kv_bytes, &p->kcache[(size_t)l]));
+    TRY(palloc(p, kv_bytes, &p->vcache[(size_t)l]));
+  }
+  TRY(palloc(p, (size_t)(n_q * h.d) * m->esz, &p->f_last));
+  TRY(palloc(p, (size_t)n_q * 4, (void **)&p->lse_last));
+
+  const int32_t *d_tok = tokens;
+  if (!tok_dev) {
+    int32_t *dt;
+    TRY(ws_t<int32_t>(m, "pre_tok", (size_t)std::max<int64_t>(T, 1), &dt));
+    HIPC(hipMemcpyAsync(dt, tokens, (size_t)T * 4, hipMemcpyHostToDevice, m->st));
+    d_tok = dt;
+  }
+  const int dt = m->dtype == JET_BF16 ? 0 : 1;
+  // waves of whole questions under the prefill token budget
+  int32_t q0 = 0;
+  while (q0 < n_q) {
+    int32_t q1 = q0 + 1;
+    while (q1 < n_q && (m->prefill_budget <= 0 || offs[q1 + 1] - offs[q0] <= m->prefill_budget)) ++q1;
+    const int64_t t0 = offs[q0], R = offs[q1] - offs[q0];
+    std::vector<int32_t> pos((size_t)R), last((size_t)(q1 - q0));
+    QDesc qd;
+    for (int32_t q = q0; q < q1; ++q) {
+      const int64_t P = offs[q + 1] - offs[q];
+      for (int64_t i = 0; i < P; ++i) pos[(size_t)(offs[q] - t0 + i)] = (int32_t)i;
+      last[(size_t)(q - q0)] = (int32_t)(offs[q] - t0 + P - 1);
+      qd.qrow0.push_back((int32_t)(offs[q] - t0));
+      qd.nrows.push_back((int32_t)P);
+      qd.pre_slot0.push_back(offs[q]);
+      qd.pre_len.push_back((int32_t)P);
+      qd.suf_row0.push_back(0);
+      qd.suf_len.push_back(0);
+    }
+    int32_t *d_pos, *d_last;
+    TRY(upload(m, "pre_pos", pos, &d_pos));
+    TRY(upload(m, "pre_last", last, &d_last));
+    AttnPlan plan;
+    TRY(plan_attention(m, 0, qd, "pre_at_", &plan));
+    WaveBufs b;
+    TRY(wave_bufs(m, R, &b));
+    {
+      KTimer t(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_embed(dt, m->embed, d_tok + t0, nullptr, (int)R, (int)h.d, b.resid, m->st));
+    }
+    for (int64_t l = 0; l < h.n_layers; ++l) {
+      const Layer &ly = m->layers[(size_t)l];
+      TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
+      TRY(run_attention(m, plan, b.q, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr, 0,
+                        nullptr, nullptr));
+      TRY(attn_out(m, ly, b, R));
+      TRY(ffn(m, ly, b, R));
+    }
+    {
+      KTimer t(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_rmsnorm(dt, b.resid, d_last, m->final_norm, (int)(q1 - q0), (int)h.d, (float)h.rms_eps,
+                                  (char *)p->f_last + (size_t)(q0 * h.d) * m->esz, m->st));
+    }
+    m->stats.prefill_waves++;
+    q0 = q1;
+  }
+  TRY(run_lmhead(m, p->f_last, n_q, p->lse_last));
+  TRY(sync(m));
+  m->stats.prefix_tokens += T;
+  m->stats.prefix_evals += n_q;
+  return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
+// candidate scoring
+// ---------------------------------------------------------------------------
+
+Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_t *cto, const int32_t *tokens,
+             float *out_tok, float *out_sum) {
+  const ModelHeader &h = m->h;
+  if (p->m != m) return Status::err(JET_E_INVALID, "prefix belongs to another model");
+  if (!out_sum) return Status::err(JET_E_INVALID, "out_cand_sum is NULL");
+  CandLayout L;
+  TRY(build_cand_layout(p->n_q, p->prefix_offsets.data(), qco, cto, m->max_ctx, &L));
+  const int64_t N = L.n_cand, NT = L.n_tok;
+  if (N == 0) return Status::ok();
+  const bool tok_dev = is_device_ptr(tokens);
+  TRY(check_ids(m, tokens, NT, tok_dev, "cand_tokens"));
+  const int dt = m->dtype == JET_BF16 ? 0 : 1;
+
+  const int32_t *d_tok = tokens;
+  if (!tok_dev) {
+    int32_t *d;
+    TRY(ws_t<int32_t>(m, "cand_tok", (size_t)NT, &d));
+    HIPC(hipMemcpyAsync(d, tokens, (size_t)NT * 4, hipMemcpyHostToDevice, m->st));
+    d_tok = d;
+  }
+  int32_t *d_rpos, *d_rtok, *d_rc, *d_rt, *d_lm;
+  int64_t *d_cto;
+  TRY(upload(m, "row_pos", L.row_pos, &d_rpos));
+  TRY(upload(m, "row_tok", L.row_tok, &d_rtok));
+  TRY(upload(m, "row_c", L.row_c, &d_rc));
+  TRY(upload(m, "row_t", L.row_t, &d_rt));
+  TRY(upload(m, "lm_row", L.lm_row, &d_lm));
+  std::vector<int64_t> cto_v(cto, cto + N + 1);
+  TRY(upload(m, "cto", cto_v, &d_cto));
+  float *d_ell, *d_sum;
+  TRY(ws_t<float>(m, "ell", (size_t)NT, &d_ell));
+  TRY(ws_t<float>(m, "csum", (size_t)N, &d_sum));
+
+  // question of each candidate
+  std::vector<int32_t> cand_q((size_t)N);
+  for (int32_t q = 0; q < p->n_q; ++q)
+    for (int64_t c = qco[q]; c < qco[q + 1]; ++c) cand_q[(size_t)c] = q;
+  auto row0 = [&](int64_t c) { return c < N ? (int64_t)L.cand_row0[(size_t)c] : L.n_rows; };
+
+  int64_t c0 = 0;
+  while (c0 < N) {
+    int64_t c1 = c0 + 1;
+    while (c1 < N && (m->wave_budget <= 0 || row0(c1 + 1) - row0(c0) <= m->wave_budget)) ++c1;
+    const int64_t r0 = row0(c0), r1 = row0(c1), R = r1 - r0;
+    const int64_t t0 = cto[c0], t1 = cto[c1];
+    void *f_body = nullptr;
+    float *lse_body = nullptr;
+    if (R > 0) {
+      QDesc qd;
+      int64_t c = c0;
+      while (c < c1) {
+        const int32_t q = cand_q[(size_t)c];
+        int64_t ce = c;
+        while (ce < c1 && cand_q[(size_t)ce] == q) ++ce;
+        const int64_t a = row0(c) - r0, e = row0(ce) - r0;
+        qd.qrow0.push_back((int32_t)a);
+        qd.nrows.push_back((int32_t)(e - a));
+        qd.pre_slot0.push_back(p->prefix_offsets[(size_t)q]);
+        qd.pre_len.push_back((int32_t)(p->prefix_offsets[(size_t)q + 1] - p->prefix_offsets[(size_t)q]));
+        qd.suf_row0.push_back((int32_t)a);
+        qd.suf_len.push_back((int32_t)(e - a));
+        c = ce;
+      }
+      AttnPlan plan;
+      TRY(plan_attention(m, 1, qd, "cand_at_", &plan));
+      WaveBufs b;
+      TRY(wave_bufs(m, R, &b));
+      void *kc, *vc;
+      const size_t kvb = (size_t)(h.n_kv_heads * R * h.head_dim) * m->esz;
+      TRY(ws(m, "cand_k", kvb, &kc));
+      TRY(ws(m, "cand_v", kvb, &vc));
+      {
+        KTimer t(m, JET_K_OTHER, 0, 0);
+        LAUNCH(jetk::launch_embed(dt, m->embed, d_tok, d_rtok + r0, (int)R, (int)h.d, b.resid, m->st));
+      }
+      for (int64_t l = 0; l < h.n_layers; ++l) {
+        const Layer &ly = m->layers[(size_t)l];
+        TRY(attn_in(m, ly, b, R, d_rpos + r0, kc, vc, R, 0));
+        TRY(run_attention(m, plan, b.q, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], p->T, kc, vc, R,
+                          d_rc + r0, d_rt + r0));
+        TRY(attn_out(m, ly, b, R));
+        TRY(ffn(m, ly, b, R));
+      }
+      TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz, &f_body));
+      TRY(ws_t<float>(m, "lse_body", (size_t)R, &lse_body));
+      {
+        KTimer t(m, JET_K_OTHER, 0, 0);
+        LAUNCH(jetk::launch_rmsnorm(dt, b.resid, nullptr, m->final_norm, (int)R, (int)h.d, (float)h.rms_eps, f_body,
+                                    m->st));
+      }
+      TRY(run_lmhead(m, f_body, R, lse_body));
+    }
+    {
+      KTimer t(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_gather_logprob(dt, d_tok + t0, d_lm + t0, (int)(t1 - t0), (int)r0, f_body, lse_body,
+                                         p->f_last, p->lse_last, m->lm_head, (int)h.d, d_ell + t0, m->st));
+      LAUNCH(jetk::launch_segment_sum(d_ell + t0, d_cto + c0, (int)(c1 - c0), d_sum + c0, m->st));
+    }
+    m->stats.score_waves++;
+    c0 = c1;
+  }
+  const hipMemcpyKind k_sum = is_device_ptr(out_sum) ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+  HIPC(hipMemcpyAsync(out_sum, d_sum, (size_t)N * 4, k_sum, m->st));
+  if (out_tok) {
+    const hipMemcpyKind k_tok = is_device_ptr(out_tok) ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    HIPC(hipMemcpyAsync(out_tok, d_ell, (size_t)NT * 4, k_tok, m->st));
+  }
+  TRY(sync(m));
+  m->stats.cand_body_tokens += L.n_rows;
+  m->stats.scored_tokens += NT;
+  return Status::ok();
+}
+
+void free_model(jet_model *m) {
+  if (!m) return;
+  (void)hipSetDevice(m->device);
+  if (m->st) (void)hipStreamSynchronize(m->st);
+  for (auto &kv : m->ws) (void)hipFree(kv.second.p);
+  for (void *a : m->weight_allocs) (void)hipFree(a);
+  for (auto &p : m->pending) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  for (auto e : m->event_pool) (void)hipEventDestroy(e);
+  delete m;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" int jet_model_load(const char *model_path, const jet_load_opts *opts, jet_model **out) {
+  clear_error();
+  if (!out) return fail(Status::err(JET_E_INVALID, "out is NULL"));
+  *out = nullptr;
+  if (!model_path) return fail(Status::err(JET_E_INVALID, "model_path is NULL"));
+  jet_model *m = new jet_model();
+  if (opts) {
+    if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32) {
+      delete m;
+      return fail(Status::err(JET_E_INVALID, "unknown dtype"));
+    }
+    if (opts->max_ctx < 0 || opts->prefill_token_budget < 0 || opts->wave_token_budget < 0 ||
+        opts->max_device_bytes < 0) {
+      delete m;
+      return fail(Status::err(JET_E_INVALID, "negative option"));
+    }
+    m->dtype = opts->dtype;
+    m->device = opts->device;
+    m->prefill_budget = opts->prefill_token_budget;
+    m->wave_budget = opts->wave_token_budget;
+    m->max_bytes = opts->max_device_bytes;
+    m->st = (hipStream_t)opts->hip_stream;
+    m->flags = opts->flags;
+  }
+  Status s = load_model(m, model_path, opts);
+  if (!s) {
+    free_model(m);
+    return fail(s);
+  }
+  *out = m;
+  return JET_OK;
+}
+
+extern "C" int jet_prefill_prefix(jet_model *model, int32_t n_q, const int64_t *prefix_offsets,
+                                  const int32_t *prefix_tokens, jet_prefix **out) {
+  clear_error();
+  if (!out) return fail(Status::err(JET_E_INVALID, "out is NULL"));
+  *out = nullptr;
+  if (!model) return fail(Status::err(JET_E_INVALID, "model is NULL"));
+  if (n_q < 1) return fail(Status::err(JET_E_INVALID, "n_q must be >= 1"));
+  if (hipSetDevice(model->device) != hipSuccess) return fail(Status::err(JET_E_DEVICE, "hipSetDevice failed"));
+  jet_prefix *p = new jet_prefix();
+  p->m = model;
+  model->n_prefixes++;
+  Status s = prefill(model, n_q, prefix_offsets, prefix_tokens, p);
+  if (!s) {
+    (void)hipStreamSynchronize(model->st);
+    drain_timers(model);
+    free_prefix(p);
+    return fail(s);
+  }
+  *out = p;
+  return JET_OK;
+}
+
+extern "C" int jet_score_candidates(jet_model *model, const jet_prefix *prefix, const int64_t *q_cand_offsets,
+                                    const int64_t *cand_tok_offsets, const int32_t *cand_tokens,
+                                    float *out_token_logprob, float *out_cand_sum) {
+  clear_error();
+  if (!model || !prefix) return fail(Status::err(JET_E_INVALID, "model or prefix is NULL"));
+  if (hipSetDevice(model->device) != hipSuccess) return fail(Status::err(JET_E_DEVICE, "hipSetDevice failed"));
+  Status s = score(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens, out_token_logprob, out_cand_sum);
+  if (!s) {
+    (void)hipStreamSynchronize(model->st);
+    drain_timers(model);
+    return fail(s);
+  }
+  return JET_OK;
+}
+
+extern "C" int jet_stats_get(const jet_model *model, jet_stats *out) {
+  clear_error();
+  if (!model || !out) return fail(Status::err(JET_E_INVALID, "NULL argument"));
+  *out = model->stats;
+  return JET_OK;
+}
+
+extern "C" int jet_stats_reset(jet_model *model) {
+  clear_error();
+  if (!model) return fail(Status::err(JET_E_INVALID, "NULL argument"));
+  model->stats = jet_stats{};
+  return JET_OK;
+}
+
+extern "C" int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n_layers, int64_t *max_ctx,
+                              int32_t *dtype) {
+  clear_error();
+  if (!model) return fail(Status::err(JET_E_INVALID, "NULL model"));
+  if (vocab) *vocab = model->h.vocab;
+  if (n_layers) *n_layers = model->h.n_layers;
+  if (max_ctx) *max_ctx = model->max_ctx;
+  if (dtype) *dtype = model->dtype;
+  return JET_OK;
+}
+
+extern "C" void jet_prefix_free(jet_prefix *prefix) {
+  if (prefix && prefix->m) (void)hipSetDevice(prefix->m->device);
+  free_prefix(prefix);
+}
+
+extern "C" void jet_model_free(jet_model *model) { free_model(model); }

@@ -1,0 +1,78 @@
+// Internal runtime state of the scoring library (opaque behind jet.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <string>
+#include <vector>
+
+#include "host.h"
+#include "kernels.h"
+#include "model_file.h"
+
+struct jet_model;
+
+namespace jet {
+
+struct Layer {
+  bool gdn = false;
+  float *attn_norm = nullptr, *ffn_norm = nullptr;
+  void *w_qkv = nullptr;   // attention: [Hq hd + 2 Hkv hd][d] (q rows, k rows, v rows)
+  void *w_o = nullptr;     // [d][Hq hd] (attention) or [d][H dv] (delta rule)
+  void *w_gu = nullptr;    // [2F][d], blocks of 32 gate rows then 32 up rows
+  void *w_down = nullptr;  // [d][F]
+  // gated delta-rule layers
+  void *w_in = nullptr;    // [n_in][d]: q, k, v (conv channels), z, b, a, zero pad
+  int64_t n_in = 0;
+  float *conv_w = nullptr; // [C][kc], C = 2 H dk + H dv
+  float *A_log = nullptr, *dt_bias = nullptr, *gdn_norm = nullptr;
+};
+
+struct DevBuf {
+  void *p = nullptr;
+  size_t bytes = 0;
+};
+
+struct PendingTimer {
+  int cls;
+  hipEvent_t a, b;
+};
+
+}  // namespace jet
+
+struct jet_model {
+  jet::ModelHeader h;
+  std::string path;
+  int dtype = JET_BF16;
+  int device = 0;
+  hipStream_t st = nullptr;
+  int64_t max_ctx = 0, prefill_budget = 0, wave_budget = 0, max_bytes = 0;
+  int flags = 0;
+  size_t esz = 2;  // bytes per compute element
+  size_t bytes_used = 0;
+  void *embed = nullptr, *lm_head = nullptr;
+  float *final_norm = nullptr;
+  std::vector<jet::Layer> layers;
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  std::map<std::string, jet::DevBuf> ws;
+  std::vector<jet::PendingTimer> pending;
+  std::vector<hipEvent_t> event_pool;
+  std::vector<void *> weight_allocs;
+  jet_stats stats{};
+  int n_prefixes = 0;
+};
+
+struct jet_prefix {
+  jet_model *m = nullptr;
+  int32_t n_q = 0;
+  std::vector<int64_t> prefix_offsets;
+  int64_t T = 0;                     // total prefix tokens
+  std::vector<void *> kcache, vcache;  // per layer (attention layers only), [Hkv][T][hd]
+  std::vector<float *> S_pre;        // per layer (delta-rule only), [n_q][H][dv][dk]
+  std::vector<float *> conv_tail;    // per layer (delta-rule only), [n_q][kc-1][C]
+  void *f_last = nullptr;            // [n_q][d] final-normed last prefix rows (compute dtype)
+  float *lse_last = nullptr;         // [n_q]
+  std::vector<void *> allocs;
+  size_t bytes = 0;
+};

@@ -1,0 +1,212 @@
+"""GPU parity: the HIP scoring path, called through the C ABI, against the
+fp64 oracle on the same seeded inputs.
+
+Tolerances: per-token |d ell| <= 1e-4 and per-candidate |d s| <= m * 1e-4 in
+the fp32 mode; per-token <= 2e-2 and per-candidate <= 5e-2 in bf16; identical
+argmax wherever the oracle's margin exceeds 0.1 nats; integer layout bit-exact.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import jet_synth
+import oracle
+from paper_2609_33874_amd import jet as J
+
+pytestmark = pytest.mark.gpu
+
+TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2)}
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def check_parity(wl, tok, sums, ref_tok, ref_sums, dtype):
+    t_tol, s_tol = TOL[dtype]
+    m = np.diff(wl.cand_tok_offsets)
+    dt = np.abs(tok.astype(np.float64) - ref_tok)
+    ds = np.abs(sums.astype(np.float64) - ref_sums)
+    s_lim = m * t_tol if dtype == J.JET_FP32 else np.full(len(m), s_tol)
+    assert dt.max() <= t_tol, f"per-token max |d| = {dt.max():.3e} at {dt.argmax()}"
+    assert np.all(ds <= s_lim), f"per-candidate max |d| = {ds.max():.3e}"
+    # decisions agree wherever the oracle margin exceeds 0.1 nats
+    for q in range(wl.n_questions):
+        a, b = wl.q_cand_offsets[q], wl.q_cand_offsets[q + 1]
+        if b - a < 2:
+            continue
+        r = np.sort(ref_sums[a:b])
+        if r[-1] - r[-2] > 0.1:
+            assert np.argmax(sums[a:b]) == np.argmax(ref_sums[a:b])
+    return dt.max(), ds.max()
+
+
+def run_gpu(path, wl, dtype, **kw):
+    m = J.jet_model_load(path, dtype=dtype, **kw)
+    try:
+        p = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+        try:
+            tok, sums = J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+            stats = J.jet_stats_get(m)
+        finally:
+            J.jet_prefix_free(p)
+    finally:
+        J.jet_model_free(m)
+    return tok, sums, stats
+
+
+_ORACLE_CACHE = {}
+
+
+def oracle_scores(path, name, wl):
+    key = (path, name)
+    if key not in _ORACLE_CACHE:
+        _ORACLE_CACHE[key] = oracle.score_unshared(path, wl)
+    return _ORACLE_CACHE[key]
+
+
+CASES = [
+    # (model spec, workload, dtype)
+    ("tiny_dense_fp32", "tiny", J.JET_FP32),
+    ("tiny_dense_bf16", "tiny", J.JET_BF16),
+    ("small_gqa_bf16", "small", J.JET_BF16),
+    ("small_gqa_bf16", "small", J.JET_FP32),
+]
+
+
+@pytest.mark.parametrize("spec,wname,dtype", CASES)
+def test_scores_match_oracle(spec, wname, dtype, model_dir):
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
+    wl = jet_synth.make_workload(wname)
+    log(f"[parity] {spec} {wname} dtype={dtype} Q={wl.n_questions} N={wl.n_candidates}")
+    ref_tok, ref_sums = oracle_scores(path, wname, wl)
+    tok, sums, stats = run_gpu(path, wl, dtype)
+    dt, ds = check_parity(wl, tok, sums, ref_tok, ref_sums, dtype)
+    log(f"[parity] max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    # work counters follow the closed forms of shared-prefix evaluation (Section 4.1)
+    P = np.diff(wl.prefix_offsets)
+    m = np.diff(wl.cand_tok_offsets)
+    assert stats["prefix_tokens"] == P.sum()
+    assert stats["prefix_evals"] == wl.n_questions
+    assert stats["cand_body_tokens"] == (m - 1).sum()
+    assert stats["lm_rows"] == wl.n_questions + (m - 1).sum()
+
+
+def test_prefix_sharing_matches_unshared_on_gpu(model_dir):
+    """Unshared evaluation (each candidate with its own copy of the prefix,
+    K P prefix tokens) gives the same scores as shared evaluation (P tokens)."""
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    wl = jet_synth.make_workload("small", n_questions=6)
+    tok_s, sum_s, st_s = run_gpu(path, wl, J.JET_FP32)
+    pre, cands = [], []
+    for q in range(wl.n_questions):
+        for y in wl.candidates(q):
+            pre.append(wl.prefix(q)); cands.append([y])
+    un = jet_synth.from_lists(pre, cands)
+    tok_u, sum_u, st_u = run_gpu(path, un, J.JET_FP32)
+    np.testing.assert_allclose(tok_u, tok_s, atol=2e-5, rtol=0)
+    K = np.diff(wl.q_cand_offsets)
+    P = np.diff(wl.prefix_offsets)
+    assert st_s["prefix_tokens"] == P.sum()
+    assert st_u["prefix_tokens"] == (K * P).sum()
+
+
+def test_waves_and_budgets_do_not_change_scores(model_dir):
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    wl = jet_synth.make_workload("small", n_questions=8)
+    a_tok, a_sum, _ = run_gpu(path, wl, J.JET_FP32)
+    b_tok, b_sum, st = run_gpu(path, wl, J.JET_FP32, prefill_token_budget=300, wave_token_budget=20)
+    assert st["prefill_waves"] > 1 and st["score_waves"] > 1
+    np.testing.assert_allclose(b_tok, a_tok, atol=1e-5, rtol=0)
+
+
+def test_duplicates_permutation_and_determinism(model_dir):
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    base = jet_synth.make_workload("small", n_questions=4)
+    pre, cands, perm_idx = [], [], []
+    rng = np.random.default_rng(3)
+    for q in range(base.n_questions):
+        cs = base.candidates(q)
+        cs = cs + [cs[0].copy()]                  # a duplicate of the first candidate
+        perm = rng.permutation(len(cs))
+        pre.append(base.prefix(q)); cands.append([cs[i] for i in perm])
+        perm_idx.append(perm)
+    wl = jet_synth.from_lists(pre, cands)
+    t1, s1, _ = run_gpu(path, wl, J.JET_BF16)
+    t2, s2, _ = run_gpu(path, wl, J.JET_BF16)
+    np.testing.assert_array_equal(t1, t2)        # run to run: bitwise
+    np.testing.assert_array_equal(s1, s2)
+    _, s0, _ = run_gpu(path, base, J.JET_BF16)
+    for q in range(base.n_questions):
+        a = wl.q_cand_offsets[q]
+        perm = perm_idx[q]
+        got = s1[a:a + len(perm)]
+        orig = np.concatenate([s0[base.q_cand_offsets[q]:base.q_cand_offsets[q + 1]],
+                               s0[base.q_cand_offsets[q]:base.q_cand_offsets[q] + 1]])
+        np.testing.assert_allclose(got, orig[perm], atol=5e-2, rtol=0)
+        # the two copies of the duplicated candidate score identically
+        dup = [i for i, p in enumerate(perm) if p in (0, len(perm) - 1)]
+        assert got[dup[0]] == got[dup[1]]
+
+
+def test_device_resident_inputs_and_outputs(model_dir):
+    import torch
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    wl = jet_synth.make_workload("small", n_questions=5)
+    h_tok, h_sum, _ = run_gpu(path, wl, J.JET_BF16)
+    dev = torch.device("cuda:0")
+    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    try:
+        pt = torch.from_numpy(wl.prefix_tokens).to(dev)
+        ct = torch.from_numpy(wl.cand_tokens).to(dev)
+        p = J.jet_prefill_prefix(m, wl.prefix_offsets, pt)
+        o_tok = torch.empty(len(wl.cand_tokens), dtype=torch.float32, device=dev)
+        o_sum = torch.empty(wl.n_candidates, dtype=torch.float32, device=dev)
+        J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, ct, o_tok, o_sum)
+        np.testing.assert_array_equal(o_tok.cpu().numpy(), h_tok)
+        np.testing.assert_array_equal(o_sum.cpu().numpy(), h_sum)
+        bad = ct.clone()
+        bad[3] = 10 ** 6
+        before = o_sum.clone()
+        with pytest.raises(J.JetError) as e:
+            J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, bad, o_tok, o_sum)
+        assert e.value.code == J.JET_E_INVALID
+        assert torch.equal(before, o_sum)  # outputs untouched on error
+        J.jet_prefix_free(p)
+    finally:
+        J.jet_model_free(m)
+
+
+def test_error_paths_on_gpu(model_dir):
+    path = jet_synth.ensure_model("tiny_dense_fp32", cache_dir=model_dir)
+    with pytest.raises(J.JetError) as e:
+        J.jet_model_load(path, dtype=J.JET_BF16)  # f32 weights are not bf16 values
+    assert e.value.code == J.JET_E_INVALID
+    m = J.jet_model_load(path, dtype=J.JET_FP32, max_ctx=40)
+    try:
+        with pytest.raises(J.JetError) as e:
+            J.jet_prefill_prefix(m, [0, 3], np.array([1, 2, 5000], np.int32))
+        assert e.value.code == J.JET_E_INVALID
+        with pytest.raises(J.JetError) as e:
+            J.jet_prefill_prefix(m, [0, 41], np.zeros(41, np.int32))
+        assert e.value.code == J.JET_E_CAPACITY
+        p = J.jet_prefill_prefix(m, [0, 38], np.zeros(38, np.int32))
+        out = np.full(1, 7.0, np.float32)
+        with pytest.raises(J.JetError) as e:  # 38 + 4 - 1 > 40
+            J.jet_score_candidates(m, p, [0, 1], [0, 4], np.ones(4, np.int32), None, out)
+        assert e.value.code == J.JET_E_CAPACITY
+        assert out[0] == 7.0
+        J.jet_score_candidates(m, p, [0, 1], [0, 3], np.ones(3, np.int32), None, out)
+        J.jet_prefix_free(p)
+    finally:
+        J.jet_model_free(m)
+
+
+def test_device_budget_oom(model_dir):
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    with pytest.raises(J.JetError) as e:
+        J.jet_model_load(path, dtype=J.JET_BF16, max_device_bytes=1 << 16)
+    assert e.value.code == J.JET_E_OOM

@@ -1,0 +1,130 @@
+"""C ABI checks that need no GPU: exports, decisions (Eq. 4-5), the integer
+row layout (bit-exact) and request validation."""
+import json
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import jet_synth
+import oracle
+from paper_2609_33874_amd import jet as J
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "jet.h")).read()
+    declared = set(re.findall(r"^(?:int|void|const char \*)\s*(jet_[a-z_]+)\s*\(", hdr, re.M))
+    assert declared == set(J.EXPORTS)
+    L = J.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_decide_worked_example():
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "worked_example.json")))
+    s = np.log(np.array(g["likelihoods"], np.float32))
+    q, choice, _ = J.jet_decide(J.JET_CHOICE, [0, 2], s)
+    # float32 inputs: ln 0.06 and ln 0.02 are rounded once to float32
+    np.testing.assert_allclose(q, g["normalized"], atol=1e-7)
+    assert choice[0] == 0
+
+
+def test_decide_matches_oracle_rules():
+    rng = np.random.default_rng(0)
+    qco = np.array([0, 2, 4, 9, 12], np.int64)
+    s = rng.normal(-10, 3, size=12).astype(np.float32)
+    s[10] = s[11] = s[9] + 1.0  # tie in the last question: lowest index wins
+    q, ch, _ = J.jet_decide(J.JET_CHOICE, qco, s)
+    oq, och, _ = oracle.decide("choice", qco, s.astype(np.float64))
+    np.testing.assert_allclose(q, oq, rtol=0, atol=1e-15)
+    np.testing.assert_array_equal(ch, och)
+    assert ch[3] == 1
+    qb = np.array([0, 2, 4], np.int64)
+    _, _, v = J.jet_decide(J.JET_BINARY, qb, s[:4])
+    for i in range(2):
+        a, b = float(s[2 * i]), float(s[2 * i + 1])
+        assert v[i] == pytest.approx(1 / (1 + math.exp(a - b)), abs=1e-15)
+    qo = np.array([0, 5, 12], np.int64)
+    _, _, v = J.jet_decide(J.JET_ORDINAL, qo, s)
+    for i in range(2):
+        assert v[i] == pytest.approx(oracle.decide_ordinal(s[qo[i]:qo[i + 1]].astype(np.float64)), abs=1e-13)
+
+
+def test_decide_rejects_bad_requests():
+    with pytest.raises(J.JetError) as e:
+        J.jet_decide(J.JET_BINARY, [0, 3], np.zeros(3, np.float32))
+    assert e.value.code == J.JET_E_INVALID
+    with pytest.raises(J.JetError):
+        J.jet_decide(J.JET_ORDINAL, [0, 1], np.zeros(1, np.float32))
+    with pytest.raises(J.JetError):
+        J.jet_decide(J.JET_CHOICE, [0, 2, 1], np.zeros(2, np.float32))
+    with pytest.raises(J.JetError):
+        J.jet_decide(J.JET_CHOICE, [0, 0], np.zeros(0, np.float32))
+    with pytest.raises(J.JetError):
+        J.jet_decide(J.JET_CHOICE, [0, 2], np.array([0.0, np.nan], np.float32))
+    with pytest.raises(J.JetError):
+        J.jet_decide(7, [0, 2], np.zeros(2, np.float32))
+
+
+def _expected_layout(wl):
+    """Definition: y_{c,t} sits at position P + t - 1 and is predicted by the
+    row holding y_{c,t-1}; y_{c,1} by the last prefix position."""
+    pos, qq, cc, tok, lm = [], [], [], [], np.zeros(len(wl.cand_tokens), np.int32)
+    for q in range(wl.n_questions):
+        P = wl.prefix_offsets[q + 1] - wl.prefix_offsets[q]
+        for c in range(wl.q_cand_offsets[q], wl.q_cand_offsets[q + 1]):
+            t0, t1 = wl.cand_tok_offsets[c], wl.cand_tok_offsets[c + 1]
+            lm[t0] = -(q + 1)
+            for t in range(1, t1 - t0):
+                lm[t0 + t] = len(pos)
+                pos.append(P + t - 1); qq.append(q); cc.append(c); tok.append(t0 + t - 1)
+    return dict(row_pos=pos, row_q=qq, row_c=cc, row_tok=tok, lm_row=lm)
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "dense_1p5b_k4", "dense_1p5b_binary", "dense_27b_k10"])
+def test_candidate_layout_bit_exact(name):
+    wl = jet_synth.make_workload(name, n_questions=min(40, jet_synth.WORKLOADS[name]["Q"]))
+    got = J.jet_candidate_layout(wl.prefix_offsets, wl.q_cand_offsets, wl.cand_tok_offsets)
+    exp = _expected_layout(wl)
+    for k, v in exp.items():
+        np.testing.assert_array_equal(got[k], np.asarray(v, np.int32), err_msg=k)
+
+
+def test_layout_edge_cases():
+    # questions without candidates, single-token candidates only, one long candidate
+    wl = jet_synth.from_lists([[1, 2, 3], [4], [5, 6]], [[], [[7], [8]], [[9, 10, 11, 12]]])
+    got = J.jet_candidate_layout(wl.prefix_offsets, wl.q_cand_offsets, wl.cand_tok_offsets)
+    np.testing.assert_array_equal(got["row_pos"], [2, 3, 4])
+    np.testing.assert_array_equal(got["lm_row"], [-2, -2, -3, 0, 1, 2])
+
+
+def test_layout_validation_errors():
+    po = np.array([0, 3], np.int64)
+    with pytest.raises(J.JetError) as e:  # empty candidate
+        J.jet_candidate_layout(po, [0, 2], [0, 2, 2])
+    assert e.value.code == J.JET_E_INVALID
+    with pytest.raises(J.JetError):  # empty prefix
+        J.jet_candidate_layout([0, 0], [0, 1], [0, 2])
+    with pytest.raises(J.JetError):  # decreasing offsets
+        J.jet_candidate_layout(po, [0, 2], [0, 3, 1])
+    with pytest.raises(J.JetError):  # first offset not zero
+        J.jet_candidate_layout(po, [1, 2], [0, 1, 2])
+    with pytest.raises(J.JetError) as e:  # P + m - 1 beyond capacity: rejected, never truncated
+        J.jet_candidate_layout(po, [0, 1], [0, 5], max_ctx=6)
+    assert e.value.code == J.JET_E_CAPACITY
+    J.jet_candidate_layout(po, [0, 1], [0, 4], max_ctx=6)  # exactly at capacity is fine
+
+
+def test_model_load_reports_io_errors(tmp_path):
+    with pytest.raises(J.JetError) as e:
+        J.jet_model_load(str(tmp_path / "missing.jetm"))
+    assert e.value.code in (J.JET_E_IO, J.JET_E_DEVICE)
+    bad = tmp_path / "bad.jetm"
+    bad.write_bytes(b"NOTAMODEL" * 10)
+    with pytest.raises(J.JetError) as e:
+        J.jet_model_load(str(bad))
+    assert e.value.code in (J.JET_E_IO, J.JET_E_DEVICE)
