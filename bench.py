@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Throughput of teacher-forced candidate scoring on one MI355X.
+
+A step is one pass of the whole hot path over one batch: prefill every
+question prefix once (retaining its attention cache), score every candidate
+against it (batched candidate bodies, fused LM head + full-vocabulary
+log-sum-exp, per-candidate sums), copy the sums to the host and decide.
+Inputs (token ids) are resident in HBM before the timed region starts.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 (matrix and vector)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+MODE_OF = {"dense_1p5b_binary": "binary", "dense_1p5b_ordinal": "ordinal"}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def describe(wname: str) -> dict:
+    import jet_synth
+    r = jet_synth.WORKLOADS[wname]
+    s = jet_synth.full_spec(r["model"])
+    return {"workload": wname,
+            "model": (f"{s['arch']} {s['n_layers']}L d={s['d_model']} heads {s['n_heads']}/{s['n_kv_heads']} "
+                      f"hd={s['head_dim']} ffn={s['ffn']} vocab={s['vocab']} {s['dtype']} random N(0,0.02)"),
+            "questions": r["Q"], "prefix_len": list(r["P"]), "prefix_ids": r["ids"],
+            "candidates_per_question": r["K"], "candidate_len": list(r["m"])}
+
+
+def cpu_baseline(path: str, wl, seconds_hint: float = 30.0) -> dict:
+    """The fp64 oracle (independent full forward per candidate) on question 0."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    sub = wl.subset([0])
+    P = int(sub.prefix_offsets[-1])
+    m = np.diff(sub.cand_tok_offsets)
+    t0 = time.perf_counter()
+    oracle.score_unshared(path, sub)
+    dt = time.perf_counter() - t0
+    return {"value": 1.0 / dt, "unit": "questions/s", "cores": int(threads), "kind": "oracle",
+            "seconds": dt,
+            "sample": (f"question 0 of the workload: prefix {P} tokens, {len(m)} candidates, "
+                       f"{int(m.sum())} scored tokens; every candidate an independent fp64 forward")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="dense_1p5b_k4")
+    ap.add_argument("--unshared-steps", type=int, default=2,
+                    help="steps of unshared (per-candidate prefix) evaluation for the reuse speedup; 0 = skip")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-timing", action="store_true", help="do not time kernels with HIP events")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the scoring path has no "
+              "multi-GPU mode in this build", file=sys.stderr)
+        return 2
+
+    import torch
+    import jet_synth
+    from paper_2609_33874_amd import jet as J
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    wname = args.workload
+    spec = jet_synth.WORKLOADS[wname]["model"]
+    t = time.perf_counter()
+    path = jet_synth.ensure_model(spec)
+    log(f"model file {path} ready in {time.perf_counter() - t:.1f}s")
+    wl = jet_synth.make_workload(wname)
+    mode = {"binary": J.JET_BINARY, "ordinal": J.JET_ORDINAL}.get(MODE_OF.get(wname, ""), J.JET_CHOICE)
+    Q, N = wl.n_questions, wl.n_candidates
+    T_p = int(wl.prefix_offsets[-1])
+    T_c = int(wl.cand_tok_offsets[-1])
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    flags = 0 if args.no_timing else J.JET_FLAG_KERNEL_TIMING
+    t = time.perf_counter()
+    model = J.jet_model_load(path, dtype=J.JET_BF16, device=0, hip_stream=stream.cuda_stream, flags=flags)
+    log(f"model loaded in {time.perf_counter() - t:.1f}s")
+
+    def make_inputs(w):
+        return (torch.from_numpy(w.prefix_tokens).to(dev), torch.from_numpy(w.cand_tokens).to(dev),
+                torch.empty(int(w.cand_tok_offsets[-1]), dtype=torch.float32, device=dev),
+                torch.empty(w.n_candidates, dtype=torch.float32, device=dev))
+
+    phase = {"prefill": 0.0, "score": 0.0, "decide": 0.0}
+
+    def step(w, inp):
+        d_pre, d_cand, o_tok, o_sum = inp
+        a = time.perf_counter()
+        p = J.jet_prefill_prefix(model, w.prefix_offsets, d_pre)
+        b = time.perf_counter()
+        J.jet_score_candidates(model, p, w.q_cand_offsets, w.cand_tok_offsets, d_cand, o_tok, o_sum)
+        c = time.perf_counter()
+        sums = o_sum.cpu().numpy()
+        J.jet_decide(mode, w.q_cand_offsets, sums)
+        d = time.perf_counter()
+        J.jet_prefix_free(p)
+        phase["prefill"] += b - a
+        phase["score"] += c - b
+        phase["decide"] += d - c
+
+    inp = make_inputs(wl)
+    for i in range(args.warmup):
+        step(wl, inp)
+        log(f"warmup step {i + 1}/{args.warmup} done")
+    J.jet_stats_reset(model)
+    for k in phase:
+        phase[k] = 0.0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(wl, inp)
+        log(f"step {i + 1}/{args.steps} done")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stats = J.jet_stats_get(model)
+    ms_step = 1e3 * elapsed / args.steps
+    qps = Q * args.steps / elapsed
+
+    # per-kernel-class rates from the HIP events around every launch
+    kernels = {}
+    for cls in J.KERNEL_CLASSES:
+        n = stats["kernel_launches"][cls]
+        ms = stats["kernel_ms"][cls]
+        if n == 0:
+            continue
+        fl, by = stats["kernel_flops"][cls], stats["kernel_bytes"][cls]
+        kernels[cls] = {"launches": n, "ms_total": round(ms, 3), "ms_per_launch": round(ms / n, 4),
+                        "tflops": round(fl / (ms * 1e9), 2) if ms > 0 and fl > 0 else None,
+                        "gbs": round(by / (ms * 1e6), 1) if ms > 0 and by > 0 else None}
+    roofline = None
+    if kernels and not args.no_timing:
+        dom = max((c for c in kernels if c != "other"), key=lambda c: kernels[c]["ms_total"])
+        n = stats["kernel_launches"][dom]
+        ms_avg = stats["kernel_ms"][dom] / n
+        if dom.startswith("attn"):
+            ach = stats["kernel_bytes"][dom] / n / (ms_avg * 1e6)
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+        else:
+            ach = stats["kernel_flops"][dom] / n / (ms_avg * 1e9)
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None}
+        roofline["launches"] = n
+        roofline["ms_per_launch"] = round(ms_avg, 4)
+        roofline["flops_per_launch"] = stats["kernel_flops"][dom] / n
+    gemm_cls = ["gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "lmhead"]
+    g_ms = sum(stats["kernel_ms"][c] for c in gemm_cls)
+    g_fl = sum(stats["kernel_flops"][c] for c in gemm_cls)
+    gemm_lm_frac = (g_fl / (g_ms * 1e9)) / PEAK_BF16_TFLOPS if g_ms > 0 else None
+
+    result = {
+        "metric": "questions/sec & scored tokens/sec on 1 MI355X; LM-head+GEMM % MFMA peak",
+        "value": round(qps, 3), "unit": "questions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": describe(wname),
+        "scored_tokens_per_s": round(T_c * args.steps / elapsed, 1),
+        "prefix_tokens_per_s": round(T_p * args.steps / phase["prefill"], 1),
+        "phase_ms_per_step": {k: round(1e3 * v / args.steps, 2) for k, v in phase.items()},
+        "gemm_lmhead_mfma_frac": round(gemm_lm_frac, 4) if gemm_lm_frac else None,
+        "roofline": roofline, "kernels": kernels,
+    }
+
+    if args.unshared_steps > 0:
+        pre, cands = [], []
+        for q in range(Q):
+            for y in wl.candidates(q):
+                pre.append(wl.prefix(q))
+                cands.append([y])
+        un = jet_synth.from_lists(pre, cands)
+        uinp = make_inputs(un)
+        step(un, uinp)  # warm-up (workspace growth)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for i in range(args.unshared_steps):
+            step(un, uinp)
+            log(f"unshared step {i + 1}/{args.unshared_steps} done")
+        torch.cuda.synchronize()
+        ms_un = 1e3 * (time.perf_counter() - t1) / args.unshared_steps
+        result["unshared_ms_per_step"] = round(ms_un, 3)
+        result["prefix_reuse_speedup"] = round(ms_un / ms_step, 3)
+        del uinp
+
+    J.jet_model_free(model)
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the CPU")
+        result["cpu_baseline"] = cpu_baseline(path, wl)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
