@@ -53,7 +53,13 @@ enum {
   JET_E_IO = 5         /* model file missing or malformed */
 };
 
-enum { JET_BF16 = 0, JET_FP32 = 1 };                  /* compute dtype */
+/* Compute modes. JET_BF16: bf16 weights and bf16 matrix-core products; the
+ * activations, attention caches and probabilities are carried as (hi, lo)
+ * bf16 pairs (value = hi + lo) so that rounding does not accumulate through
+ * deep stacks (fp32 accumulation throughout). JET_FP32: fp32 everything
+ * (validation mode). JET_BF16_SINGLE: single bf16 activations and caches;
+ * faster, with rounding that grows with depth. */
+enum { JET_BF16 = 0, JET_FP32 = 1, JET_BF16_SINGLE = 2 };
 enum { JET_CHOICE = 0, JET_BINARY = 1, JET_ORDINAL = 2 }; /* decision rule */
 
 /* flags for jet_load_opts.flags */
@@ -65,8 +71,7 @@ typedef struct jet_model jet_model;
 typedef struct jet_prefix jet_prefix;
 
 typedef struct {
-  int32_t dtype;                /* JET_BF16 (bf16 operands, fp32 accumulation) or
-                                   JET_FP32 (fp32 everywhere; validation mode) */
+  int32_t dtype;                /* JET_BF16, JET_FP32 or JET_BF16_SINGLE (see above) */
   int32_t device;               /* HIP device ordinal */
   int64_t max_ctx;              /* max positions per sequence; 0 = the file's value */
   int64_t prefill_token_budget; /* max prefix tokens per prefill wave; 0 = no limit.
@@ -113,7 +118,7 @@ typedef struct {
  *   opts: host, may be NULL (defaults: JET_BF16, device 0, no limits, null stream).
  *   out: host, receives the model handle.
  * Errors: JET_E_IO (file), JET_E_INVALID (unsupported shape or dtype
- *   combination: an f32 file cannot be run in JET_BF16), JET_E_OOM, JET_E_DEVICE.
+ *   combination: an f32 file cannot be run in a bf16 mode), JET_E_OOM, JET_E_DEVICE.
  */
 int jet_model_load(const char *model_path, const jet_load_opts *opts, jet_model **out);
 

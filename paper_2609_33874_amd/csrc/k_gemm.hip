@@ -3,136 +3,41 @@
 // needs fused in (fp32 store, residual add, SwiGLU), and the LM head with a
 // full-vocabulary online log-sum-exp epilogue that never writes logits.
 //
-// Tiling: BM x BN output tile per workgroup, K step of 128 bytes per row
-// (64 bf16 / 32 fp32), WM x WN per wave built from 32x32 MFMA blocks.
-// Global -> registers -> LDS with double buffering (one barrier per K step);
-// LDS rows are 8 chunks of 16 B, chunk c of row r stored at c ^ (r & 7) so
-// that the MFMA operand reads of 8 consecutive rows hit distinct banks.
-#include "device.h"
+// Large problems use 256x256 tiles (8 waves of 128x64, register-staged LDS
+// double buffering); problems with too few such tiles to fill the 256 CUs use
+// 128x128 tiles (4 waves of 64x64, direct global->LDS loads). Tiles are
+// ordered so that each XCD works on a contiguous band (see tile_coords).
+#include <algorithm>
+
+#include "gemm_core.h"
 #include "kernels.h"
 
 namespace jetk {
-
-template <typename T, int BM_, int BN_, int WM_, int WN_>
-struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
-  static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
-  static constexpr int NT = WAVES_M * WAVES_N * 64;
-  static constexpr int MI = WM / 32, NI = WN / 32;
-  static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
-  static constexpr int BK = 8 * EPC;                // elements per K step (128 B)
-  static constexpr int A_PT = BM * 8 / NT, B_PT = BN * 8 / NT;
-  static constexpr int BUF = (BM + BN) * 8;         // chunks per LDS buffer
-  static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile/thread mismatch");
-};
-
-template <typename T>
-__device__ __forceinline__ void lds_frag(Frag<T> &f, const uint4 *row, int c0, int swz);
-template <>
-__device__ __forceinline__ void lds_frag<bf16>(Frag<bf16> &f, const uint4 *row, int c0, int swz) {
-  f.v = __builtin_bit_cast(bf16x8, row[c0 ^ swz]);
-}
-template <>
-__device__ __forceinline__ void lds_frag<float>(Frag<float> &f, const uint4 *row, int c0, int swz) {
-  uint4 a = row[c0 ^ swz], b = row[(c0 + 1) ^ swz];
-  f.v[0] = __uint_as_float(a.x); f.v[1] = __uint_as_float(a.y);
-  f.v[2] = __uint_as_float(a.z); f.v[3] = __uint_as_float(a.w);
-  f.v[4] = __uint_as_float(b.x); f.v[5] = __uint_as_float(b.y);
-  f.v[6] = __uint_as_float(b.z); f.v[7] = __uint_as_float(b.w);
-}
-
-// One output tile: acc = A[m0:m0+BM, :] * B[n0:n0+BN, :]^T. Rows beyond M / N
-// read as zero. K must be a multiple of C::BK. Ends with a barrier.
-template <typename T, class C>
-__device__ __forceinline__ void gemm_tile(const T *__restrict__ A, int64_t lda, const T *__restrict__ B,
-                                          int64_t ldb, int M, int N, int K, int m0, int n0, uint4 *lds,
-                                          f32x16 (&acc)[C::MI][C::NI]) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int j = 0; j < C::NI; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-  uint4 ra[C::A_PT], rb[C::B_PT];
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < C::A_PT; ++i) {
-      const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7, gm = m0 + r;
-      ra[i] = gm < M ? ld16(A + (int64_t)gm * lda + k0 + c * C::EPC) : zero4;
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_PT; ++i) {
-      const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7, gn = n0 + r;
-      rb[i] = gn < N ? ld16(B + (int64_t)gn * ldb + k0 + c * C::EPC) : zero4;
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint4 *a = lds + buf * C::BUF, *b = a + C::BM * 8;
-#pragma unroll
-    for (int i = 0; i < C::A_PT; ++i) {
-      const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7;
-      a[r * 8 + (c ^ (r & 7))] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_PT; ++i) {
-      const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7;
-      b[r * 8 + (c ^ (r & 7))] = rb[i];
-    }
-  };
-
-  const int nk = K / C::BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * C::BK);
-    const uint4 *a = lds + (kt & 1) * C::BUF, *b = a + C::BM * 8;
-#pragma unroll
-    for (int kk = 0; kk < C::BK / 16; ++kk) {
-      const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
-      Frag<T> fa[C::MI], fb[C::NI];
-#pragma unroll
-      for (int i = 0; i < C::MI; ++i) {
-        const int r = wm * C::WM + i * 32 + (lane & 31);
-        lds_frag<T>(fa[i], a + r * 8, c0, r & 7);
-      }
-#pragma unroll
-      for (int j = 0; j < C::NI; ++j) {
-        const int r = wn * C::WN + j * 32 + (lane & 31);
-        lds_frag<T>(fb[j], b + r * 8, c0, r & 7);
-      }
-#pragma unroll
-      for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-        for (int j = 0; j < C::NI; ++j) mma32(acc[i][j], fa[i], fb[j]);
-    }
-    if (kt + 1 < nk) lstore((kt + 1) & 1);
-    __syncthreads();
-  }
-}
 
 template <typename T>
 struct GemmArgs {
   const T *A;
   const T *B;
   int64_t lda, ldb;
-  int M, N, K;
+  int M, N;
+  int K, KA, KB;  // K steps over K columns; A column k mod KA, B column k mod KB
   void *out;
   int64_t ldo;
+  int pair_out;   // SwiGLU: write (hi, lo) bf16 pairs, hi at column f, lo at N/2 + f
 };
 
 // EPI: 0 = store fp32, 1 = fp32 residual add, 2 = SwiGLU into T (B rows
 // interleaved in blocks of 32 gate rows / 32 up rows), 3 = store T.
-template <typename T, class C, int EPI>
-__global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<T> g) {
+template <class C, int EPI>
+__global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> g) {
+  using T = typename C::type;
   extern __shared__ uint4 lds[];
-  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const int nt_m = (g.M + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
+  int tm, tn;
+  tile_coords<8>(nt_m, nt_n, &tm, &tn);
+  const int m0 = tm * C::BM, n0 = tn * C::BN;
   f32x16 acc[C::MI][C::NI];
-  gemm_tile<T, C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, m0, n0, lds, acc);
+  gemm_tile<C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   if constexpr (EPI == 2) {
@@ -142,14 +47,16 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<T> g) {
 #pragma unroll
       for (int jp = 0; jp < C::NI / 2; ++jp) {
         const int gcol = n0 + wn * C::WN + jp * 64;  // first column of the gate block
-        if (gcol >= g.N) continue;
         const int f = (gcol >> 6) * 32 + (lane & 31);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          if (row < g.M) {
+          if (row < g.M && gcol < g.N) {
             const float gt = acc[i][2 * jp][e], up = acc[i][2 * jp + 1][e];
-            out[(int64_t)row * g.ldo + f] = from_f<T>(gt / (1.0f + __expf(-gt)) * up);
+            const float v = gt / (1.0f + __expf(-gt)) * up;
+            const T hi = from_f<T>(v);
+            out[(int64_t)row * g.ldo + f] = hi;
+            if (g.pair_out) out[(int64_t)row * g.ldo + (g.N >> 1) + f] = from_f<T>(v - to_f<T>(hi));
           }
         }
       }
@@ -159,11 +66,10 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<T> g) {
 #pragma unroll
       for (int j = 0; j < C::NI; ++j) {
         const int col = n0 + wn * C::WN + j * 32 + (lane & 31);
-        if (col >= g.N) continue;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          if (row >= g.M) continue;
+          if (row >= g.M || col >= g.N) continue;
           const int64_t o = (int64_t)row * g.ldo + col;
           if constexpr (EPI == 0) ((float *)g.out)[o] = acc[i][j][e];
           else if constexpr (EPI == 1) ((float *)g.out)[o] += acc[i][j][e];
@@ -177,9 +83,12 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<T> g) {
 // tiles): logits^T = W[V x K] * F[R x K]^T tile by tile; each lane keeps a
 // running (max, sum of exp) in base 2 for its rows of F; one partial per
 // (row, vocabulary split) is written. The logits stay in registers.
-template <typename T, class C>
-__global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__ W, const T *__restrict__ F,
-                                                          int V, int R, int K, int tiles_per_split,
+// F holds R rows of K columns: the final hidden rows, or (hi, lo) pairs of
+// them when K = 2 KW (W rows are then read twice).
+template <class C>
+__global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::type *__restrict__ W,
+                                                          const typename C::type *__restrict__ F, int V, int R,
+                                                          int KW, int K, int tiles_per_split,
                                                           float *__restrict__ part_m, float *__restrict__ part_s) {
   extern __shared__ uint4 lds[];
   const int n0 = blockIdx.x * C::BN, split = blockIdx.y;
@@ -189,11 +98,14 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   float rm[C::NI], rs[C::NI];
 #pragma unroll
-  for (int j = 0; j < C::NI; ++j) { rm[j] = -INFINITY; rs[j] = 0.0f; }
+  for (int j = 0; j < C::NI; ++j) {
+    rm[j] = -INFINITY;
+    rs[j] = 0.0f;
+  }
   f32x16 acc[C::MI][C::NI];
   for (int vt = vt0; vt < vt1; ++vt) {
     const int m0 = vt * C::BM;
-    gemm_tile<T, C>(W, K, F, K, V, R, K, m0, n0, lds, acc);
+    gemm_tile<C>(W, KW, F, K, V, R, K, KW, K, m0, n0, lds, acc);
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
       float mx = -INFINITY;
@@ -217,7 +129,8 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__
       rs[j] = s;
     }
   }
-  // merge the two lane halves that hold the same column
+  // merge the two lane halves that hold the same column, then the waves
+  // along the vocabulary dimension through LDS
   float *sm = reinterpret_cast<float *>(lds);  // [WAVES_M][BN] maxima, then sums
 #pragma unroll
   for (int j = 0; j < C::NI; ++j) {
@@ -225,8 +138,6 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__
     const float nm = fmaxf(rm[j], om);
     float s = 0.0f;
     if (nm != -INFINITY) s = rs[j] * exp2f(rm[j] - nm) + os * exp2f(om - nm);
-    rm[j] = nm;
-    rs[j] = s;
     if (lane < 32) {
       const int cl = wn * C::WN + j * 32 + lane;
       sm[wm * C::BN + cl] = nm;
@@ -241,7 +152,8 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__
     for (int w = 0; w < C::WAVES_M; ++w) M = fmaxf(M, sm[w * C::BN + cl]);
     float S = 0.0f;
     if (M != -INFINITY)
-      for (int w = 0; w < C::WAVES_M; ++w) S += sm[C::WAVES_M * C::BN + w * C::BN + cl] * exp2f(sm[w * C::BN + cl] - M);
+      for (int w = 0; w < C::WAVES_M; ++w)
+        S += sm[C::WAVES_M * C::BN + w * C::BN + cl] * exp2f(sm[w * C::BN + cl] - M);
     part_m[(int64_t)split * R + row] = M;
     part_s[(int64_t)split * R + row] = S;
   }
@@ -251,60 +163,83 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const T *__restrict__
 // launchers
 // ---------------------------------------------------------------------------
 
-using CfgB = Cfg<bf16, 128, 128, 64, 64>;
-using CfgF = Cfg<float, 128, 128, 64, 64>;
+using BigB = GCfg<bf16, 256, 256, 128, 64, 0, 0>;
+using SmallB = GCfg<bf16, 128, 128, 64, 64, 1, 1>;
+using CfgF = GCfg<float, 128, 128, 64, 64, 0, 0>;
+using LmB = GCfg<bf16, 256, 256, 128, 64, 0, 0>;
+using LmF = GCfg<float, 128, 128, 64, 64, 0, 0>;
 
-template <typename T, class C, int EPI>
-static hipError_t run_gemm(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+// Kernels whose LDS exceeds the default 64 KB limit must opt in once.
+template <class C>
+static hipError_t allow_lds(const void *fn) {
+  if (C::LDS_BYTES <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
+}
+
+template <class C, int EPI>
+static hipError_t run_gemm(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K, int pair,
                            void *out, int64_t ldo, hipStream_t st) {
-  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, K, out, ldo};
-  dim3 grid((N + C::BN - 1) / C::BN, (M + C::BM - 1) / C::BM);
-  const size_t lds = sizeof(uint4) * 2 * C::BUF;
-  hipLaunchKernelGGL((gemm_kernel<T, C, EPI>), grid, dim3(C::NT), lds, st, g);
+  using T = typename C::type;
+  static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
+  if (once != hipSuccess) return once;
+  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, pair ? 2 * K : K, pair ? 2 * K : K, K, out, ldo, pair};
+  const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
   return hipGetLastError();
 }
 
-int gemm_k_step(int dtype) { return dtype == 0 ? CfgB::BK : CfgF::BK; }
-int gemm_n_step(int) { return 64; }
+template <class C>
+static hipError_t run_epi(int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+                          int pair, void *out, int64_t ldo, hipStream_t st) {
+  switch (epi) {
+    case EPI_STORE_F32: return run_gemm<C, 0>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    case EPI_RESID_ADD: return run_gemm<C, 1>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    case EPI_SWIGLU: return run_gemm<C, 2>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    default: return run_gemm<C, 3>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+  }
+}
 
-hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
-                       int N, int K, void *out, int64_t ldo, hipStream_t st) {
+int gemm_k_step(int dtype) { return dtype == 0 ? BigB::BK : CfgF::BK; }
+
+hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N,
+                       int K, int pair, void *out, int64_t ldo, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (dtype == 0) {
-    switch (epi) {
-      case EPI_STORE_F32: return run_gemm<bf16, CfgB, 0>(A, lda, B, ldb, M, N, K, out, ldo, st);
-      case EPI_RESID_ADD: return run_gemm<bf16, CfgB, 1>(A, lda, B, ldb, M, N, K, out, ldo, st);
-      case EPI_SWIGLU: return run_gemm<bf16, CfgB, 2>(A, lda, B, ldb, M, N, K, out, ldo, st);
-      default: return run_gemm<bf16, CfgB, 3>(A, lda, B, ldb, M, N, K, out, ldo, st);
-    }
+    // 256x256 tiles when there are enough of them to fill the chip twice over
+    const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+    if (big_tiles >= 512) return run_epi<BigB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    return run_epi<SmallB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
   }
-  switch (epi) {
-    case EPI_STORE_F32: return run_gemm<float, CfgF, 0>(A, lda, B, ldb, M, N, K, out, ldo, st);
-    case EPI_RESID_ADD: return run_gemm<float, CfgF, 1>(A, lda, B, ldb, M, N, K, out, ldo, st);
-    case EPI_SWIGLU: return run_gemm<float, CfgF, 2>(A, lda, B, ldb, M, N, K, out, ldo, st);
-    default: return run_gemm<float, CfgF, 3>(A, lda, B, ldb, M, N, K, out, ldo, st);
-  }
+  return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, st);
 }
 
-int lmhead_tile_rows(int) { return 128; }
-
-int lmhead_num_splits(int V, int tiles_per_split) {
-  const int nt = (V + 127) / 128;
-  return (nt + tiles_per_split - 1) / tiles_per_split;
+void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit) {
+  (void)R;
+  // The split of the vocabulary depends on V only, so that a row's
+  // log-sum-exp is merged in the same order whatever batch it is in; about
+  // 256 splits keep even a one-row-tile launch spread over the CUs.
+  const int bm = dtype == 0 ? LmB::BM : LmF::BM;
+  const int vt = (V + bm - 1) / bm;
+  const int tps = std::max(1, vt / 256);
+  *tiles_per_split = tps;
+  *nsplit = (vt + tps - 1) / tps;
 }
 
-hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int tiles_per_split,
-                             float *part_m, float *part_s, hipStream_t st) {
+hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
+                             int tiles_per_split, float *part_m, float *part_s, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  const int nsplit = lmhead_num_splits(V, tiles_per_split);
   if (dtype == 0) {
-    dim3 grid((R + CfgB::BN - 1) / CfgB::BN, nsplit);
-    hipLaunchKernelGGL((lmhead_lse_kernel<bf16, CfgB>), grid, dim3(CfgB::NT), sizeof(uint4) * 2 * CfgB::BUF, st,
-                       (const bf16 *)W, (const bf16 *)F, V, R, K, tiles_per_split, part_m, part_s);
+    static const hipError_t once = allow_lds<LmB>((const void *)lmhead_lse_kernel<LmB>);
+    if (once != hipSuccess) return once;
+    const int nsplit = ((V + LmB::BM - 1) / LmB::BM + tiles_per_split - 1) / tiles_per_split;
+    dim3 grid((R + LmB::BN - 1) / LmB::BN, nsplit);
+    hipLaunchKernelGGL((lmhead_lse_kernel<LmB>), grid, dim3(LmB::NT), LmB::LDS_BYTES, st, (const bf16 *)W,
+                       (const bf16 *)F, V, R, K, pair ? 2 * K : K, tiles_per_split, part_m, part_s);
   } else {
-    dim3 grid((R + CfgF::BN - 1) / CfgF::BN, nsplit);
-    hipLaunchKernelGGL((lmhead_lse_kernel<float, CfgF>), grid, dim3(CfgF::NT), sizeof(uint4) * 2 * CfgF::BUF, st,
-                       (const float *)W, (const float *)F, V, R, K, tiles_per_split, part_m, part_s);
+    const int nsplit = ((V + LmF::BM - 1) / LmF::BM + tiles_per_split - 1) / tiles_per_split;
+    dim3 grid((R + LmF::BN - 1) / LmF::BN, nsplit);
+    hipLaunchKernelGGL((lmhead_lse_kernel<LmF>), grid, dim3(LmF::NT), LmF::LDS_BYTES, st, (const float *)W,
+                       (const float *)F, V, R, K, K, tiles_per_split, part_m, part_s);
   }
   return hipGetLastError();
 }

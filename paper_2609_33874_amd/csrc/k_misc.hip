@@ -19,7 +19,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const T *__restrict__ E, con
   for (int i = threadIdx.x; i < d; i += 256) dst[i] = to_f<T>(src[i]);
 }
 
-template <typename T>
+template <typename T, bool PAIR>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ x, const int32_t *__restrict__ map,
                                                        const float *__restrict__ g, int d, float eps,
                                                        T *__restrict__ out) {
@@ -37,17 +37,30 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ 
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = rsqrtf(tot / (float)d + eps);
-  T *o = out + (int64_t)r * d;
-  for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f<T>(xr[i] * inv * g[i]);
+  T *o = out + (int64_t)r * d * (PAIR ? 2 : 1);
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = xr[i] * inv * g[i];
+    const T hi = from_f<T>(v);
+    o[i] = hi;
+    if constexpr (PAIR) o[d + i] = from_f<T>(v - to_f<T>(hi));
+  }
 }
 
 // One block per row; thread t handles rotation pairs (i, i + hd/2).
-template <typename T>
+template <typename T, bool PAIR>
+__device__ __forceinline__ void put_val(T *p, int64_t ps, float v) {
+  const T hi = from_f<T>(v);
+  p[0] = hi;
+  if constexpr (PAIR) p[ps] = from_f<T>(v - to_f<T>(hi));
+}
+
+template <typename T, bool PAIR>
 __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *__restrict__ qkv, const int32_t *__restrict__ pos,
                                                             const float *__restrict__ cos_t,
                                                             const float *__restrict__ sin_t, int Hq, int Hkv,
-                                                            int hd, T *__restrict__ q_out, T *__restrict__ kc,
-                                                            T *__restrict__ vc, int64_t S, int64_t slot0) {
+                                                            int hd, T *__restrict__ q_out, int64_t q_ps,
+                                                            T *__restrict__ kc, T *__restrict__ vc, int64_t kv_ps,
+                                                            int64_t S, int64_t slot0) {
   const int r = blockIdx.x;
   const int half = hd / 2;
   const int W = (Hq + 2 * Hkv) * hd;
@@ -62,17 +75,17 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *__restri
     const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
     if (h < Hq) {
       T *o = q_out + ((int64_t)r * Hq + h) * hd;
-      o[i] = from_f<T>(y1);
-      o[i + half] = from_f<T>(y2);
+      put_val<T, PAIR>(o + i, q_ps, y1);
+      put_val<T, PAIR>(o + i + half, q_ps, y2);
     } else {
       T *o = kc + ((int64_t)(h - Hq) * S + slot) * hd;
-      o[i] = from_f<T>(y1);
-      o[i + half] = from_f<T>(y2);
+      put_val<T, PAIR>(o + i, kv_ps, y1);
+      put_val<T, PAIR>(o + i + half, kv_ps, y2);
     }
   }
   for (int t = threadIdx.x; t < Hkv * hd; t += 256) {
     const int h = t / hd, i = t % hd;
-    vc[((int64_t)h * S + slot) * hd + i] = from_f<T>(src[(Hq + Hkv) * hd + t]);
+    put_val<T, PAIR>(vc + ((int64_t)h * S + slot) * hd + i, kv_ps, src[(Hq + Hkv) * hd + t]);
   }
 }
 
@@ -88,7 +101,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const float *__restrict_
 }
 
 // One wave per scored token: ell = <f_row, W[y]> - lse_row.
-template <typename T>
+template <typename T, bool PAIR>
 __global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__restrict__ tokens,
                                                               const int32_t *__restrict__ lm_row, int n_out,
                                                               int row_base, const T *__restrict__ f_body,
@@ -103,16 +116,21 @@ __global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__re
   const int r = lm_row[i];
   const T *f;
   float lse;
+  const int64_t ld = (int64_t)d * (PAIR ? 2 : 1);
   if (r < 0) {
-    f = f_last + (int64_t)(-r - 1) * d;
+    f = f_last + (int64_t)(-r - 1) * ld;
     lse = lse_last[-r - 1];
   } else {
-    f = f_body + (int64_t)(r - row_base) * d;
+    f = f_body + (int64_t)(r - row_base) * ld;
     lse = lse_body[r - row_base];
   }
   const T *w = W + (int64_t)tokens[i] * d;
   float acc = 0.0f;
-  for (int k = lane; k < d; k += 64) acc += to_f<T>(f[k]) * to_f<T>(w[k]);
+  for (int k = lane; k < d; k += 64) {
+    float fv = to_f<T>(f[k]);
+    if constexpr (PAIR) fv += to_f<T>(f[d + k]);
+    acc += fv * to_f<T>(w[k]);
+  }
   acc = warp_sum(acc);
   if (lane == 0) ell[i] = acc - lse;
 }
@@ -158,24 +176,32 @@ hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int3
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(int dtype, const float *x, const int32_t *map, const float *g, int R, int d, float eps,
-                          void *out, hipStream_t st) {
+hipError_t launch_rmsnorm(int dtype, int pair, const float *x, const int32_t *map, const float *g, int R, int d,
+                          float eps, void *out, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  if (dtype == 0) hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
-  else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(R), dim3(256), 0, st, x, map, g, d, eps, (float *)out);
+  if (dtype == 0 && pair)
+    hipLaunchKernelGGL((rmsnorm_kernel<bf16, true>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
+  else if (dtype == 0)
+    hipLaunchKernelGGL((rmsnorm_kernel<bf16, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
+  else
+    hipLaunchKernelGGL((rmsnorm_kernel<float, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (float *)out);
   return hipGetLastError();
 }
 
-hipError_t launch_rope_scatter(int dtype, const float *qkv, const int32_t *pos, const float *cos_t,
-                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, void *k_cache,
-                               void *v_cache, int64_t S, int64_t slot0, hipStream_t st) {
+hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int32_t *pos, const float *cos_t,
+                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, int64_t q_ps,
+                               void *k_cache, void *v_cache, int64_t kv_ps, int64_t S, int64_t slot0,
+                               hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  if (dtype == 0)
-    hipLaunchKernelGGL(rope_scatter_kernel<bf16>, dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq, Hkv, hd,
-                       (bf16 *)q_out, (bf16 *)k_cache, (bf16 *)v_cache, S, slot0);
+  if (dtype == 0 && pair)
+    hipLaunchKernelGGL((rope_scatter_kernel<bf16, true>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
+                       Hkv, hd, (bf16 *)q_out, q_ps, (bf16 *)k_cache, (bf16 *)v_cache, kv_ps, S, slot0);
+  else if (dtype == 0)
+    hipLaunchKernelGGL((rope_scatter_kernel<bf16, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
+                       Hkv, hd, (bf16 *)q_out, q_ps, (bf16 *)k_cache, (bf16 *)v_cache, kv_ps, S, slot0);
   else
-    hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq, Hkv, hd,
-                       (float *)q_out, (float *)k_cache, (float *)v_cache, S, slot0);
+    hipLaunchKernelGGL((rope_scatter_kernel<float, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
+                       Hkv, hd, (float *)q_out, q_ps, (float *)k_cache, (float *)v_cache, kv_ps, S, slot0);
   return hipGetLastError();
 }
 
@@ -185,17 +211,22 @@ hipError_t launch_lse_merge(const float *pm, const float *ps, int nsplit, int R,
   return hipGetLastError();
 }
 
-hipError_t launch_gather_logprob(int dtype, const int32_t *tokens, const int32_t *lm_row, int n_out, int row_base,
-                                 const void *f_body, const float *lse_body, const void *f_last,
+hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
+                                 int row_base, const void *f_body, const float *lse_body, const void *f_last,
                                  const float *lse_last, const void *W, int d, float *ell, hipStream_t st) {
   if (n_out <= 0) return hipSuccess;
   dim3 grid((n_out + 3) / 4);
-  if (dtype == 0)
-    hipLaunchKernelGGL(gather_logprob_kernel<bf16>, grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
+  if (dtype == 0 && pair)
+    hipLaunchKernelGGL((gather_logprob_kernel<bf16, true>), grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
                        (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d, ell);
+  else if (dtype == 0)
+    hipLaunchKernelGGL((gather_logprob_kernel<bf16, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
+                       row_base, (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d,
+                       ell);
   else
-    hipLaunchKernelGGL(gather_logprob_kernel<float>, grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
-                       (const float *)f_body, lse_body, (const float *)f_last, lse_last, (const float *)W, d, ell);
+    hipLaunchKernelGGL((gather_logprob_kernel<float, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
+                       row_base, (const float *)f_body, lse_body, (const float *)f_last, lse_last,
+                       (const float *)W, d, ell);
   return hipGetLastError();
 }
 

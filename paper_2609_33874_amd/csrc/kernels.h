@@ -11,15 +11,20 @@ namespace jetk {
 enum { EPI_STORE_F32 = 0, EPI_RESID_ADD = 1, EPI_SWIGLU = 2, EPI_STORE_T = 3 };
 
 // C[M x N] (epilogue) A[M x K] * B[N x K]^T. K must be a multiple of
-// gemm_k_step(dtype). EPI_SWIGLU expects B rows interleaved in blocks of 32
-// gate rows then 32 up rows and writes silu(gate) * up to out[M x N/2] (T).
+// gemm_k_step(dtype). pair (bf16 only): every A row holds a (hi, lo) bf16
+// pair of the activations, [a_hi (K) | a_lo (K)], and C = (A_hi + A_lo) B^T.
+// EPI_SWIGLU expects B rows interleaved in blocks of 32 gate rows then 32 up
+// rows and writes silu(gate) * up to out[M x N/2] (T), or with pair to
+// out[M x N] as [hi (N/2) | lo (N/2)].
 int gemm_k_step(int dtype);
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
-                       int N, int K, void *out, int64_t ldo, hipStream_t st);
+                       int N, int K, int pair, void *out, int64_t ldo, hipStream_t st);
 
 // LM head + online log-sum-exp: partial (max, sum) in base 2 per (split, row).
-int lmhead_num_splits(int V, int tiles_per_split);
-hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K,
+// lmhead_plan gives the vocabulary tiles per workgroup and the split count.
+void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit);
+// F: [R][K] rows, or [R][2K] (hi, lo) pairs when pair.
+hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
                              int tiles_per_split, float *part_m, float *part_s, hipStream_t st);
 // lse[r] = ln(sum over splits) from the partials.
 hipError_t launch_lse_merge(const float *part_m, const float *part_s, int nsplit, int R, float *lse,
@@ -41,14 +46,19 @@ struct AttnQuestions {
 // mode 0: causal prefix attention (query i of a question sees prefix keys 0..i).
 // mode 1: candidate attention: every prefix key, plus the suffix keys j with
 //         row_c[j] == row_c[i] and row_t[j] <= row_t[i].
+// pair: Q, K, V are (hi, lo) bf16 planes (the lo plane at +q_ps / +kp_ps /
+// +ks_ps elements) and O rows hold [hi (Hq hd) | lo (Hq hd)].
 struct AttnArgs {
   int mode;
-  const void *Q;        // [rows][Hq][hd]
-  void *O;              // [rows][Hq][hd]
-  const void *Kp, *Vp;  // prefix cache [Hkv][S_pre][hd]
-  int64_t s_pre;
-  const void *Ks, *Vs;  // own-suffix keys of the call [Hkv][S_suf][hd]
-  int64_t s_suf;
+  int pair;
+  const void *Q;        // [planes][rows][Hq][hd]
+  int64_t q_ps;
+  void *O;              // [rows][o_ld]: head h, dim d at h * hd + d (lo part at (Hq + h) * hd + d)
+  int64_t o_ld;
+  const void *Kp, *Vp;  // prefix cache [planes][Hkv][S_pre][hd]
+  int64_t s_pre, kp_ps;
+  const void *Ks, *Vs;  // own-suffix keys of the call [planes][Hkv][S_suf][hd]
+  int64_t s_suf, ks_ps;
   const int32_t *row_c, *row_t;  // per call row (candidate mode)
   AttnQuestions qs;
   const AttnItem *items;
@@ -61,17 +71,20 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st);
 // resid[r][:] = E[ids[idx ? idx[r] : r]][:] (as fp32).
 hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int32_t *idx, int R, int d,
                         float *resid, hipStream_t st);
-// out[r][:] = x[src][:] / sqrt(mean(x[src]^2) + eps) * g, src = map ? map[r] : r; out in T.
-hipError_t launch_rmsnorm(int dtype, const float *x, const int32_t *map, const float *g, int R, int d,
+// out[r][:] = x[src][:] / sqrt(mean(x[src]^2) + eps) * g, src = map ? map[r] : r; out in T,
+// as [hi (d) | lo (d)] rows when pair.
+hipError_t launch_rmsnorm(int dtype, int pair, const float *x, const int32_t *map, const float *g, int R, int d,
                           float eps, void *out, hipStream_t st);
 // qkv fp32 [R][(Hq + 2 Hkv) hd] -> q (T) [R][Hq][hd] with RoPE, K (RoPE) and V
-// into the cache [Hkv][S][hd] at slot slot0 + r, angles from pos[r].
-hipError_t launch_rope_scatter(int dtype, const float *qkv, const int32_t *pos, const float *cos_t,
-                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, void *k_cache,
-                               void *v_cache, int64_t S, int64_t slot0, hipStream_t st);
+// into the cache [Hkv][S][hd] at slot slot0 + r, angles from pos[r]. With
+// pair, lo planes follow at +q_ps (q) and +kv_ps (caches) elements.
+hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int32_t *pos, const float *cos_t,
+                               const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, int64_t q_ps,
+                               void *k_cache, void *v_cache, int64_t kv_ps, int64_t S, int64_t slot0,
+                               hipStream_t st);
 // ell[i] = dot(f_row, W[y_i]) - lse_row for output i; the row is f_body[lm_row[i] - row_base]
-// or, when lm_row[i] < 0, f_last[-lm_row[i] - 1].
-hipError_t launch_gather_logprob(int dtype, const int32_t *tokens, const int32_t *lm_row, int n_out,
+// or, when lm_row[i] < 0, f_last[-lm_row[i] - 1]; rows are [hi | lo] pairs when pair.
+hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
                                  int row_base, const void *f_body, const float *lse_body, const void *f_last,
                                  const float *lse_last, const void *W, int d, float *ell, hipStream_t st);
 // s[c] = sum of ell[off[c] - off[0] .. off[c+1] - off[0]) in ascending order.

@@ -173,7 +173,7 @@ struct Loader {
     const size_t dst_bytes = (size_t)n * m->esz;
     TRY(dmalloc(m, dst_bytes, out));
     m->weight_allocs.push_back(*out);
-    if ((m->dtype == JET_BF16) == src_bf16) {
+    if ((m->kdt == 0) == src_bf16) {
       HIPC(hipMemcpy(*out, src, dst_bytes, hipMemcpyHostToDevice));
       return Status::ok();
     }
@@ -244,8 +244,8 @@ struct Loader {
 
 Status check_shapes(const ModelHeader &h, int dtype) {
   const int64_t bk = dtype == JET_BF16 ? 64 : 32;
-  if (dtype == JET_BF16 && !h.bf16)
-    return Status::err(JET_E_INVALID, "an f32 model file cannot run in JET_BF16 (its weights are not bf16 values)");
+  if (dtype != JET_FP32 && !h.bf16)
+    return Status::err(JET_E_INVALID, "an f32 model file cannot run in a bf16 mode (its weights are not bf16 values)");
   if (h.head_dim != 32 && h.head_dim != 64 && h.head_dim != 128)
     return Status::err(JET_E_INVALID, "head_dim must be 32, 64 or 128");
   if (h.n_kv_heads < 1 || h.n_heads % h.n_kv_heads != 0) return Status::err(JET_E_INVALID, "n_heads % n_kv_heads != 0");
@@ -261,7 +261,10 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   TRY(read_model_header(m->path, &m->h));
   const ModelHeader &h = m->h;
   TRY(check_shapes(h, m->dtype));
-  m->esz = m->dtype == JET_BF16 ? 2 : 4;
+  m->kdt = m->dtype == JET_FP32 ? 1 : 0;
+  m->pair = m->dtype == JET_BF16 ? 1 : 0;
+  m->np = m->pair ? 2 : 1;
+  m->esz = m->kdt == 0 ? 2 : 4;
   m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
   HIPC(hipSetDevice(m->device));
   Loader L{m, {}};
@@ -307,13 +310,14 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
 
 double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (double)N * (double)K; }
 
+// A holds activations ([hi | lo] pairs in the pair mode, lda counts both).
 Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t M,
                 int64_t N, int64_t K, void *out, int64_t ldo) {
-  const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 : N) *
+  const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 * m->np : N) *
                            (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
                            (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
-  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K + N * K) * (double)m->esz + out_bytes);
-  LAUNCH(jetk::launch_gemm(m->dtype == JET_BF16 ? 0 : 1, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, out, ldo, m->st));
+  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * m->np + N * K) * (double)m->esz + out_bytes);
+  LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, m->pair, out, ldo, m->st));
   return Status::ok();
 }
 
@@ -321,16 +325,14 @@ Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, cons
 Status run_lmhead(jet_model *m, const void *F, int64_t R, float *lse) {
   if (R <= 0) return Status::ok();
   const int64_t V = m->h.vocab, d = m->h.d;
-  const int64_t ntiles = (V + 127) / 128, rtiles = (R + 127) / 128;
-  int64_t tps = std::max<int64_t>(1, (ntiles * rtiles + 4095) / 4096);
-  const int nsplit = jetk::lmhead_num_splits((int)V, (int)tps);
+  int tps = 1, nsplit = 1;
+  jetk::lmhead_plan(m->kdt, (int)V, (int)R, &tps, &nsplit);
   float *pm, *ps;
   TRY(ws_t<float>(m, "lm_pm", (size_t)(nsplit * R), &pm));
   TRY(ws_t<float>(m, "lm_ps", (size_t)(nsplit * R), &ps));
   {
-    KTimer t(m, JET_K_LMHEAD, gemm_flops(R, V, d), (double)(V * d + R * d) * (double)m->esz);
-    LAUNCH(jetk::launch_lmhead_lse(m->dtype == JET_BF16 ? 0 : 1, m->lm_head, F, (int)V, (int)R, (int)d, (int)tps,
-                                   pm, ps, m->st));
+    KTimer t(m, JET_K_LMHEAD, gemm_flops(R, V, d), (double)(V * d + R * d * m->np) * (double)m->esz);
+    LAUNCH(jetk::launch_lmhead_lse(m->kdt, m->lm_head, F, (int)V, (int)R, (int)d, m->pair, tps, pm, ps, m->st));
   }
   KTimer t2(m, JET_K_OTHER, 0, 0);
   LAUNCH(jetk::launch_lse_merge(pm, ps, nsplit, (int)R, lse, m->st));
@@ -392,6 +394,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   TRY(upload(m, (t + "preslot").c_str(), qd.pre_slot0, &d_preslot));
   jetk::AttnArgs &a = pl->a;
   a.mode = mode;
+  a.pair = m->pair;
   a.qs = {d_qrow0, d_nrows, d_preslot, d_prelen, d_sufrow0, d_suflen};
   a.items = d_items;
   a.n_items = (int)items.size();
@@ -405,29 +408,35 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   for (size_t q = 0; q < qd.nrows.size(); ++q)
     if (qd.nrows[q] > 0) kv_rows += (double)qd.pre_len[q] + (double)qd.suf_len[q];
   for (auto n : qd.nrows) qo_rows += n;
-  pl->bytes = (double)m->esz * (kv_rows * 2.0 * (double)h.n_kv_heads * (double)h.head_dim +
-                                qo_rows * 2.0 * (double)h.n_heads * (double)h.head_dim);
+  pl->bytes = (double)m->esz * m->np * (kv_rows * 2.0 * (double)h.n_kv_heads * (double)h.head_dim +
+                                        qo_rows * 2.0 * (double)h.n_heads * (double)h.head_dim);
   pl->flops = 4.0 * pairs * (double)h.head_dim;
   return Status::ok();
 }
 
-Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, void *O, const void *Kp, const void *Vp,
+// Q: [planes][R][Hq][hd]; O: [R][planes * Hq * hd]; caches [planes][Hkv][S][hd].
+Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void *O, const void *Kp, const void *Vp,
                      int64_t s_pre, const void *Ks, const void *Vs, int64_t s_suf, const int32_t *row_c,
                      const int32_t *row_t) {
   if (pl.a.n_items == 0) return Status::ok();
+  const ModelHeader &h = m->h;
   jetk::AttnArgs a = pl.a;
   a.Q = Q;
+  a.q_ps = R * h.n_heads * h.head_dim;
   a.O = O;
+  a.o_ld = m->np * h.n_heads * h.head_dim;
   a.Kp = Kp;
   a.Vp = Vp;
   a.s_pre = s_pre;
+  a.kp_ps = h.n_kv_heads * s_pre * h.head_dim;
   a.Ks = Ks;
   a.Vs = Vs;
   a.s_suf = s_suf;
+  a.ks_ps = h.n_kv_heads * s_suf * h.head_dim;
   a.row_c = row_c;
   a.row_t = row_t;
   KTimer t(m, a.mode == 0 ? JET_K_ATTN_PREFIX : JET_K_ATTN_CAND, pl.flops, pl.bytes);
-  LAUNCH(jetk::launch_attention(m->dtype == JET_BF16 ? 0 : 1, a, m->st));
+  LAUNCH(jetk::launch_attention(m->kdt, a, m->st));
   return Status::ok();
 }
 
@@ -442,10 +451,11 @@ Status wave_bufs(jet_model *m, int64_t R, WaveBufs *b) {
   const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
   TRY(ws_t<float>(m, "resid", (size_t)(R * h.d), &b->resid));
   TRY(ws_t<float>(m, "qkv", (size_t)(R * nqkv), &b->qkv));
-  TRY(ws(m, "xn", (size_t)(R * h.d) * m->esz, &b->xn));
-  TRY(ws(m, "q", (size_t)(R * h.n_heads * h.head_dim) * m->esz, &b->q));
-  TRY(ws(m, "att", (size_t)(R * h.n_heads * h.head_dim) * m->esz, &b->att));
-  TRY(ws(m, "act", (size_t)(R * h.ffn) * m->esz, &b->act));
+  const size_t pe = (size_t)m->np * m->esz;  // bytes per activation element
+  TRY(ws(m, "xn", (size_t)(R * h.d) * pe, &b->xn));
+  TRY(ws(m, "q", (size_t)(R * h.n_heads * h.head_dim) * pe, &b->q));
+  TRY(ws(m, "att", (size_t)(R * h.n_heads * h.head_dim) * pe, &b->att));
+  TRY(ws(m, "act", (size_t)(R * h.ffn) * pe, &b->act));
   return Status::ok();
 }
 
@@ -454,11 +464,13 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
   {
     KTimer t(m, JET_K_OTHER, 0, 0);
-    LAUNCH(jetk::launch_rmsnorm(m->dtype == JET_BF16 ? 0 : 1, b.resid, nullptr, ly.ffn_norm, (int)R, (int)h.d,
-                                (float)h.rms_eps, b.xn, m->st));
+    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.ffn_norm, (int)R, (int)h.d, (float)h.rms_eps,
+                                b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, h.d, ly.w_gu, h.d, R, 2 * h.ffn, h.d, b.act, h.ffn));
-  TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, h.ffn, ly.w_down, h.ffn, R, h.d, h.ffn, b.resid, h.d));
+  TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, ly.w_gu, h.d, R, 2 * h.ffn, h.d, b.act,
+               m->np * h.ffn));
+  TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, ly.w_down, h.ffn, R, h.d, h.ffn,
+               b.resid, h.d));
   return Status::ok();
 }
 
@@ -467,22 +479,23 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
 Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, const int32_t *d_pos, void *kc, void *vc,
                int64_t S, int64_t slot0) {
   const ModelHeader &h = m->h;
-  const int dt = m->dtype == JET_BF16 ? 0 : 1;
   const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
   {
     KTimer t(m, JET_K_OTHER, 0, 0);
-    LAUNCH(jetk::launch_rmsnorm(dt, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps, b.xn, m->st));
+    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps,
+                                b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv));
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv));
   KTimer t(m, JET_K_OTHER, 0, 0);
-  LAUNCH(jetk::launch_rope_scatter(dt, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
-                                   (int)h.n_kv_heads, (int)h.head_dim, b.q, kc, vc, S, slot0, m->st));
+  LAUNCH(jetk::launch_rope_scatter(m->kdt, m->pair, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
+                                   (int)h.n_kv_heads, (int)h.head_dim, b.q, R * h.n_heads * h.head_dim, kc, vc,
+                                   h.n_kv_heads * S * h.head_dim, S, slot0, m->st));
   return Status::ok();
 }
 
 Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
-  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, h.n_heads * h.head_dim, ly.w_o,
+  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, m->np * h.n_heads * h.head_dim, ly.w_o,
                   h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d);
 }
 
@@ -535,7 +548,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
   p->n_q = n_q;
   p->prefix_offsets.assign(offs, offs + n_q + 1);
   p->T = T;
-  const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz;
+  const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz * m->np;
   p->kcache.assign((size_t)h.n_layers, nullptr);
   p->vcache.assign((size_t)h.n_layers, nullptr);
   for (int64_t l = 0; l < h.n_layers; ++l) {
@@ -543,7 +556,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     TRY(palloc(p, kv_bytes, &p->kcache[(size_t)l]));
     TRY(palloc(p, kv_bytes, &p->vcache[(size_t)l]));
   }
-  TRY(palloc(p, (size_t)(n_q * h.d) * m->esz, &p->f_last));
+  TRY(palloc(p, (size_t)(n_q * h.d) * m->esz * m->np, &p->f_last));
   TRY(palloc(p, (size_t)n_q * 4, (void **)&p->lse_last));
 
   const int32_t *d_tok = tokens;
@@ -553,7 +566,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     HIPC(hipMemcpyAsync(dt, tokens, (size_t)T * 4, hipMemcpyHostToDevice, m->st));
     d_tok = dt;
   }
-  const int dt = m->dtype == JET_BF16 ? 0 : 1;
+  const int dt = m->kdt;
   // waves of whole questions under the prefill token budget
   int32_t q0 = 0;
   while (q0 < n_q) {
@@ -587,15 +600,15 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     for (int64_t l = 0; l < h.n_layers; ++l) {
       const Layer &ly = m->layers[(size_t)l];
       TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
-      TRY(run_attention(m, plan, b.q, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr, 0,
+      TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr, 0,
                         nullptr, nullptr));
       TRY(attn_out(m, ly, b, R));
       TRY(ffn(m, ly, b, R));
     }
     {
       KTimer t(m, JET_K_OTHER, 0, 0);
-      LAUNCH(jetk::launch_rmsnorm(dt, b.resid, d_last, m->final_norm, (int)(q1 - q0), (int)h.d, (float)h.rms_eps,
-                                  (char *)p->f_last + (size_t)(q0 * h.d) * m->esz, m->st));
+      LAUNCH(jetk::launch_rmsnorm(dt, m->pair, b.resid, d_last, m->final_norm, (int)(q1 - q0), (int)h.d,
+                                  (float)h.rms_eps, (char *)p->f_last + (size_t)(q0 * h.d) * m->esz * m->np, m->st));
     }
     m->stats.prefill_waves++;
     q0 = q1;
@@ -622,7 +635,7 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
   if (N == 0) return Status::ok();
   const bool tok_dev = is_device_ptr(tokens);
   TRY(check_ids(m, tokens, NT, tok_dev, "cand_tokens"));
-  const int dt = m->dtype == JET_BF16 ? 0 : 1;
+  const int dt = m->kdt;
 
   const int32_t *d_tok = tokens;
   if (!tok_dev) {
@@ -679,7 +692,7 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       WaveBufs b;
       TRY(wave_bufs(m, R, &b));
       void *kc, *vc;
-      const size_t kvb = (size_t)(h.n_kv_heads * R * h.head_dim) * m->esz;
+      const size_t kvb = (size_t)(h.n_kv_heads * R * h.head_dim) * m->esz * m->np;
       TRY(ws(m, "cand_k", kvb, &kc));
       TRY(ws(m, "cand_v", kvb, &vc));
       {
@@ -689,24 +702,24 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       for (int64_t l = 0; l < h.n_layers; ++l) {
         const Layer &ly = m->layers[(size_t)l];
         TRY(attn_in(m, ly, b, R, d_rpos + r0, kc, vc, R, 0));
-        TRY(run_attention(m, plan, b.q, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], p->T, kc, vc, R,
+        TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], p->T, kc, vc, R,
                           d_rc + r0, d_rt + r0));
         TRY(attn_out(m, ly, b, R));
         TRY(ffn(m, ly, b, R));
       }
-      TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz, &f_body));
+      TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz * m->np, &f_body));
       TRY(ws_t<float>(m, "lse_body", (size_t)R, &lse_body));
       {
         KTimer t(m, JET_K_OTHER, 0, 0);
-        LAUNCH(jetk::launch_rmsnorm(dt, b.resid, nullptr, m->final_norm, (int)R, (int)h.d, (float)h.rms_eps, f_body,
-                                    m->st));
+        LAUNCH(jetk::launch_rmsnorm(dt, m->pair, b.resid, nullptr, m->final_norm, (int)R, (int)h.d,
+                                    (float)h.rms_eps, f_body, m->st));
       }
       TRY(run_lmhead(m, f_body, R, lse_body));
     }
     {
       KTimer t(m, JET_K_OTHER, 0, 0);
-      LAUNCH(jetk::launch_gather_logprob(dt, d_tok + t0, d_lm + t0, (int)(t1 - t0), (int)r0, f_body, lse_body,
-                                         p->f_last, p->lse_last, m->lm_head, (int)h.d, d_ell + t0, m->st));
+      LAUNCH(jetk::launch_gather_logprob(dt, m->pair, d_tok + t0, d_lm + t0, (int)(t1 - t0), (int)r0, f_body,
+                                         lse_body, p->f_last, p->lse_last, m->lm_head, (int)h.d, d_ell + t0, m->st));
       LAUNCH(jetk::launch_segment_sum(d_ell + t0, d_cto + c0, (int)(c1 - c0), d_sum + c0, m->st));
     }
     m->stats.score_waves++;
@@ -751,7 +764,7 @@ extern "C" int jet_model_load(const char *model_path, const jet_load_opts *opts,
   if (!model_path) return fail(Status::err(JET_E_INVALID, "model_path is NULL"));
   jet_model *m = new jet_model();
   if (opts) {
-    if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32) {
+    if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32 && opts->dtype != JET_BF16_SINGLE) {
       delete m;
       return fail(Status::err(JET_E_INVALID, "unknown dtype"));
     }

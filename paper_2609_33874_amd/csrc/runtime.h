@@ -44,7 +44,10 @@ struct PendingTimer {
 struct jet_model {
   jet::ModelHeader h;
   std::string path;
-  int dtype = JET_BF16;
+  int dtype = JET_BF16;  // requested mode
+  int kdt = 0;           // kernel element type: 0 = bf16, 1 = fp32
+  int pair = 1;          // activations and caches as (hi, lo) bf16 pairs
+  int np = 2;            // planes per activation element (2 with pair)
   int device = 0;
   hipStream_t st = nullptr;
   int64_t max_ctx = 0, prefill_budget = 0, wave_budget = 0, max_bytes = 0;
@@ -68,10 +71,10 @@ struct jet_prefix {
   int32_t n_q = 0;
   std::vector<int64_t> prefix_offsets;
   int64_t T = 0;                     // total prefix tokens
-  std::vector<void *> kcache, vcache;  // per layer (attention layers only), [Hkv][T][hd]
+  std::vector<void *> kcache, vcache;  // per layer (attention layers only), [planes][Hkv][T][hd]
   std::vector<float *> S_pre;        // per layer (delta-rule only), [n_q][H][dv][dk]
   std::vector<float *> conv_tail;    // per layer (delta-rule only), [n_q][kc-1][C]
-  void *f_last = nullptr;            // [n_q][d] final-normed last prefix rows (compute dtype)
+  void *f_last = nullptr;            // [n_q][planes * d] final-normed last prefix rows
   float *lse_last = nullptr;         // [n_q]
   std::vector<void *> allocs;
   size_t bytes = 0;

@@ -20,3 +20,13 @@ def model_dir(tmp_path_factory):
         os.makedirs(d, exist_ok=True)
         return d
     return str(tmp_path_factory.mktemp("models"))
+
+
+def record_parity(name, **vals):
+    """Append measured parity errors to $JET_PARITY_LOG (JSON lines), if set."""
+    import json
+    path = os.environ.get("JET_PARITY_LOG")
+    if not path:
+        return
+    with open(path, "a") as f:
+        f.write(json.dumps({"case": name, **{k: float(v) for k, v in vals.items()}}) + "\n")

@@ -1,0 +1,94 @@
+"""Full-size GPU parity: the real workload shapes in the launch configuration
+that bench.py times (every question on the GPU, bf16), checked against the
+fp64 oracle on sampled questions and through properties that hold at any size.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import jet_synth
+import oracle
+from paper_2609_33874_amd import jet as J
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dense_1p5b_path():
+    return jet_synth.ensure_model("dense_1p5b")
+
+
+@pytest.fixture(scope="module")
+def dense_1p5b_model(dense_1p5b_path):
+    m = J.jet_model_load(dense_1p5b_path, dtype=J.JET_BF16)
+    yield m
+    J.jet_model_free(m)
+
+
+def run(model, wl):
+    p = J.jet_prefill_prefix(model, wl.prefix_offsets, wl.prefix_tokens)
+    try:
+        return J.jet_score_candidates(model, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+    finally:
+        J.jet_prefix_free(p)
+
+
+def sampled_parity(path, wl, tok, sums, qs):
+    sub = wl.subset(qs)
+    ref_tok, ref_sum = oracle.score_unshared(path, sub)
+    got_tok = np.concatenate([tok[wl.cand_tok_offsets[wl.q_cand_offsets[q]]:
+                                  wl.cand_tok_offsets[wl.q_cand_offsets[q + 1]]] for q in qs])
+    got_sum = np.concatenate([sums[wl.q_cand_offsets[q]:wl.q_cand_offsets[q + 1]] for q in qs])
+    dt = np.abs(got_tok - ref_tok).max()
+    ds = np.abs(got_sum - ref_sum).max()
+    log(f"[fullsize] questions {qs}: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    from conftest import record_parity
+    record_parity(f"fullsize/{len(wl.cand_tokens)}tok/q{qs}", max_tok=dt, max_sum=ds)
+    assert dt <= 2e-2 and ds <= 5e-2
+    return ref_sum, got_sum
+
+
+def properties(wl, tok, sums):
+    assert np.all(np.isfinite(tok)) and np.all(tok <= 1e-4)
+    # sums are the per-candidate sums of the token log-probs (Eq. 3)
+    s = np.add.reduceat(tok.astype(np.float64), wl.cand_tok_offsets[:-1]) if len(tok) else tok
+    np.testing.assert_allclose(sums, s, atol=1e-3, rtol=1e-5)
+
+
+def test_dense_1p5b_k4_full(dense_1p5b_path, dense_1p5b_model):
+    wl = jet_synth.make_workload("dense_1p5b_k4")
+    log(f"[fullsize] dense_1p5b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    tok, sums = run(dense_1p5b_model, wl)
+    properties(wl, tok, sums)
+    sampled_parity(dense_1p5b_path, wl, tok, sums, [0, 97, 255])
+    st = J.jet_stats_get(dense_1p5b_model)
+    assert st["prefix_tokens"] >= int(wl.prefix_offsets[-1])
+
+
+@pytest.mark.parametrize("name", ["dense_1p5b_binary", "dense_1p5b_ordinal"])
+def test_dense_1p5b_decisions_full(name, dense_1p5b_path, dense_1p5b_model):
+    wl = jet_synth.make_workload(name)
+    log(f"[fullsize] {name}: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    tok, sums = run(dense_1p5b_model, wl)
+    properties(wl, tok, sums)
+    ref_sum, got_sum = sampled_parity(dense_1p5b_path, wl, tok, sums, [0, wl.n_questions - 1])
+    mode = J.JET_BINARY if name.endswith("binary") else J.JET_ORDINAL
+    K = 2 if mode == J.JET_BINARY else 5
+    qo = np.arange(0, len(ref_sum) + 1, K, dtype=np.int64)
+    _, _, v_gpu = J.jet_decide(mode, qo, got_sum.astype(np.float32))
+    qs_o, _, v_ref = oracle.decide("binary" if mode == J.JET_BINARY else "ordinal", qo, ref_sum)
+    # sums within 5e-2 move q(true) / the expected level by at most ~K * 5e-2
+    np.testing.assert_allclose(v_gpu, np.array(v_ref, dtype=np.float64), atol=0.05 * K)
+    _, _, v_all = J.jet_decide(mode, wl.q_cand_offsets, sums)
+    assert np.all(np.isfinite(v_all))
+    if mode == J.JET_BINARY:
+        assert np.all((v_all >= 0) & (v_all <= 1))
+    else:
+        assert np.all((v_all >= 0) & (v_all <= K - 1))

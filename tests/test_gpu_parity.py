@@ -2,7 +2,9 @@
 fp64 oracle on the same seeded inputs.
 
 Tolerances: per-token |d ell| <= 1e-4 and per-candidate |d s| <= m * 1e-4 in
-the fp32 mode; per-token <= 2e-2 and per-candidate <= 5e-2 in bf16; identical
+the fp32 mode; per-token <= 2e-2 and per-candidate <= 5e-2 in the bf16 modes
+(the single-bf16 mode only on these 2-layer models: its rounding grows with
+depth); identical
 argmax wherever the oracle's margin exceeds 0.1 nats; integer layout bit-exact.
 """
 import os
@@ -17,7 +19,7 @@ from paper_2609_33874_amd import jet as J
 
 pytestmark = pytest.mark.gpu
 
-TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2)}
+TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2), J.JET_BF16_SINGLE: (2e-2, 5e-2)}
 
 
 def log(msg):
@@ -74,6 +76,8 @@ CASES = [
     ("tiny_dense_bf16", "tiny", J.JET_BF16),
     ("small_gqa_bf16", "small", J.JET_BF16),
     ("small_gqa_bf16", "small", J.JET_FP32),
+    ("small_gqa_bf16", "small", J.JET_BF16_SINGLE),
+    ("tiny_dense_bf16", "tiny", J.JET_BF16_SINGLE),
 ]
 
 
@@ -86,6 +90,8 @@ def test_scores_match_oracle(spec, wname, dtype, model_dir):
     tok, sums, stats = run_gpu(path, wl, dtype)
     dt, ds = check_parity(wl, tok, sums, ref_tok, ref_sums, dtype)
     log(f"[parity] max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    from conftest import record_parity
+    record_parity(f"{spec}/{wname}/dtype{dtype}", max_tok=dt, max_sum=ds)
     # work counters follow the closed forms of shared-prefix evaluation (Section 4.1)
     P = np.diff(wl.prefix_offsets)
     m = np.diff(wl.cand_tok_offsets)
