@@ -68,6 +68,40 @@ struct AttnArgs {
 };
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st);
 
+// Gated delta-rule layers. Projection output x [R][ldx] = q~ (H dk) | k~ (H dk)
+// | v~ (H dv) | z (H dv) | b (H) | a (H), fp32. hist[3 r + j - 1] names the
+// input j rows earlier: >= 0 a row of x, -1 zero, <= -2 row (-2 - h) of tail
+// [*][C], C = 2 H dk + H dv. tail_slot[r] >= 0 stores row r's pre-convolution
+// channels at tail[tail_slot[r]] (prefix snapshot); tail_slot may be NULL.
+struct GdnConvArgs {
+  const float *x;
+  int64_t ldx;
+  const int32_t *hist, *tail_slot;
+  float *tail;
+  const float *conv_w, *A_log, *dt_bias;  // conv_w [C][4], w[c][3] multiplies the current row
+  int H, dk, dv;
+  float *q, *k, *v, *alpha, *beta;        // [R][H][dk], [R][H][dk], [R][H][dv], [R][H], [R][H]
+};
+hipError_t launch_gdn_conv(const GdnConvArgs &g, int R, hipStream_t st);
+// One recurrence per (sequence, head): rows row0 .. row0 + len - 1; the state
+// starts from S_init[init] (or zero if init < 0) and, if fin >= 0, the final
+// state is written to S_fin[fin]. States are [*][H][dv][dk] fp32; dk = dv = 128.
+struct GdnSeq {
+  int32_t row0, len, init, fin;
+};
+struct GdnRecurArgs {
+  const GdnSeq *seqs;
+  const float *q, *k, *v, *alpha, *beta;
+  int H, dk, dv;
+  const float *S_init;
+  float *S_fin;
+  float *o;  // [R][H][dv]
+};
+hipError_t launch_gdn_recur(const GdnRecurArgs &g, int nseq, hipStream_t st);
+// y [R][H dv] (T; [hi | lo] pairs with pair) = RMSNorm(o) * w * silu(z), z at column zoff of x.
+hipError_t launch_gdn_out(int dtype, int pair, const float *o, const float *x, int64_t ldx, int zoff, const float *w,
+                          float eps, int H, int dv, int R, void *y, hipStream_t st);
+
 // resid[r][:] = E[ids[idx ? idx[r] : r]][:] (as fp32).
 hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int32_t *idx, int R, int d,
                         float *resid, hipStream_t st);

@@ -204,6 +204,27 @@ struct Loader {
     return Status::ok();
   }
 
+  // Any stored tensor as an fp32 device array (bf16 storage widened exactly).
+  Status f32_array(const std::string &name, float **out, int64_t expect) {
+    const TensorInfo *ti;
+    TRY(read(name, &ti));
+    if (ti->numel() != expect) return Status::err(JET_E_IO, name + ": unexpected size");
+    std::vector<float> f((size_t)expect);
+    if (ti->bf16) {
+      const uint16_t *h = reinterpret_cast<const uint16_t *>(host.data());
+      for (int64_t i = 0; i < expect; ++i) {
+        const uint32_t u = (uint32_t)h[i] << 16;
+        std::memcpy(&f[(size_t)i], &u, 4);
+      }
+    } else {
+      std::memcpy(f.data(), host.data(), (size_t)expect * 4);
+    }
+    TRY(dmalloc(m, (size_t)expect * 4, (void **)out));
+    m->weight_allocs.push_back(*out);
+    HIPC(hipMemcpy(*out, f.data(), (size_t)expect * 4, hipMemcpyHostToDevice));
+    return Status::ok();
+  }
+
   // Concatenates matrices row-wise (all [rows_i][d]) and pads to `pad_rows`.
   Status concat(const std::vector<std::string> &names, int64_t d, int64_t pad_rows, void **out, int64_t *rows_out) {
     std::vector<char> all;
@@ -252,7 +273,12 @@ Status check_shapes(const ModelHeader &h, int dtype) {
   if (h.d % bk || (h.n_heads * h.head_dim) % bk || h.ffn % bk)
     return Status::err(JET_E_INVALID, "d_model, n_heads*head_dim and ffn must be multiples of " + std::to_string(bk));
   if (h.ffn % 32) return Status::err(JET_E_INVALID, "ffn must be a multiple of 32");
-  if (h.hybrid) return Status::err(JET_E_INVALID, "hybrid (gated delta-rule) models are not supported by this build");
+  if (h.hybrid) {
+    if (h.gdn_dk != 128 || h.gdn_dv != 128 || h.conv_kernel != 4 || h.gdn_heads < 1)
+      return Status::err(JET_E_INVALID, "delta-rule layers need dk = dv = 128 and a width-4 convolution");
+    if ((h.gdn_heads * h.gdn_dv) % bk)
+      return Status::err(JET_E_INVALID, "gdn_heads * gdn_dv must be a multiple of " + std::to_string(bk));
+  }
   return Status::ok();
 }
 
@@ -281,6 +307,15 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
     if (!ly.gdn) {
       TRY(L.concat({p + "wq", p + "wk", p + "wv"}, h.d, 0, &ly.w_qkv, nullptr));
       TRY(L.matrix(p + "wo", &ly.w_o));
+    } else {
+      const int64_t H = h.gdn_heads, C = 2 * H * h.gdn_dk + H * h.gdn_dv;
+      TRY(L.concat({p + "gdn_wq", p + "gdn_wk", p + "gdn_wv", p + "gdn_wz", p + "gdn_wb", p + "gdn_wa"}, h.d, 0,
+                   &ly.w_in, &ly.n_in));
+      TRY(L.matrix(p + "gdn_wo", &ly.w_o));
+      TRY(L.f32_array(p + "gdn_conv", &ly.conv_w, C * h.conv_kernel));
+      TRY(L.f32_array(p + "gdn_A_log", &ly.A_log, H));
+      TRY(L.f32_array(p + "gdn_dt_bias", &ly.dt_bias, H));
+      TRY(L.f32_array(p + "gdn_norm", &ly.gdn_norm, h.gdn_dv));
     }
     TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu));
     TRY(L.matrix(p + "w_down", &ly.w_down));
@@ -499,6 +534,62 @@ Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
                   h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d);
 }
 
+// Per-wave tables of the delta-rule layers (built on the host, uploaded once).
+struct GdnPlan {
+  int32_t *hist = nullptr, *tail_slot = nullptr;
+  jetk::GdnSeq *seqs = nullptr;
+  int nseq = 0;
+  double tok_heads = 0;
+};
+
+// Gated delta-rule sublayer: resid += W_o y, y = RMSNorm(o) silu(z), o from
+// the recurrence over each sequence of the plan. tail: the layer's [Q][3][C]
+// snapshot buffer; S_init / S_fin: the layer's [Q][H][dv][dk] state snapshots.
+Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, const GdnPlan &gp, float *tail,
+                 const float *S_init, float *S_fin) {
+  const ModelHeader &h = m->h;
+  const int64_t H = h.gdn_heads, dk = h.gdn_dk, dv = h.gdn_dv;
+  const int64_t C = 2 * H * dk + H * dv;
+  float *gx, *gq, *gk, *gv, *ga, *gb, *go;
+  void *gy;
+  TRY(ws_t<float>(m, "gdn_x", (size_t)(R * ly.n_in), &gx));
+  TRY(ws_t<float>(m, "gdn_q", (size_t)(R * H * dk), &gq));
+  TRY(ws_t<float>(m, "gdn_k", (size_t)(R * H * dk), &gk));
+  TRY(ws_t<float>(m, "gdn_v", (size_t)(R * H * dv), &gv));
+  TRY(ws_t<float>(m, "gdn_a", (size_t)(R * H), &ga));
+  TRY(ws_t<float>(m, "gdn_b", (size_t)(R * H), &gb));
+  TRY(ws_t<float>(m, "gdn_o", (size_t)(R * H * dv), &go));
+  TRY(ws(m, "gdn_y", (size_t)(R * H * dv) * m->esz * m->np, &gy));
+  {
+    KTimer t(m, JET_K_OTHER, 0, 0);
+    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps,
+                                b.xn, m->st));
+  }
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_in, h.d, R, ly.n_in, h.d, gx,
+               ly.n_in));
+  {
+    KTimer t(m, JET_K_OTHER, 0, 0);
+    jetk::GdnConvArgs g{gx, ly.n_in, gp.hist, gp.tail_slot, tail, ly.conv_w, ly.A_log, ly.dt_bias,
+                        (int)H, (int)dk, (int)dv, gq, gk, gv, ga, gb};
+    LAUNCH(jetk::launch_gdn_conv(g, (int)R, m->st));
+  }
+  {
+    const double flops = gp.tok_heads * 7.0 * (double)dk * (double)dv;
+    const double bytes = gp.tok_heads * 4.0 * (double)(2 * dk + 2 * dv + 2) +
+                         (double)gp.nseq * (double)H * (double)(dk * dv) * 4.0;
+    KTimer t(m, JET_K_GDN, flops, bytes);
+    jetk::GdnRecurArgs g{gp.seqs, gq, gk, gv, ga, gb, (int)H, (int)dk, (int)dv, S_init, S_fin, go};
+    LAUNCH(jetk::launch_gdn_recur(g, gp.nseq, m->st));
+  }
+  {
+    KTimer t(m, JET_K_OTHER, 0, 0);
+    LAUNCH(jetk::launch_gdn_out(m->kdt, m->pair, go, gx, ly.n_in, (int)C, ly.gdn_norm, (float)h.rms_eps, (int)H,
+                                (int)dv, (int)R, gy, m->st));
+  }
+  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, gy, m->np * H * dv, ly.w_o, H * dv, R, h.d, H * dv,
+                  b.resid, h.d);
+}
+
 // Token ids: validated on the host (host memory) or by a device count.
 Status check_ids(jet_model *m, const int32_t *ids, int64_t n, bool on_device, const char *what) {
   if (n == 0) return Status::ok();
@@ -551,8 +642,17 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
   const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz * m->np;
   p->kcache.assign((size_t)h.n_layers, nullptr);
   p->vcache.assign((size_t)h.n_layers, nullptr);
+  p->S_pre.assign((size_t)h.n_layers, nullptr);
+  p->conv_tail.assign((size_t)h.n_layers, nullptr);
+  const int64_t gH = h.gdn_heads, gC = 2 * h.gdn_heads * h.gdn_dk + h.gdn_heads * h.gdn_dv;
   for (int64_t l = 0; l < h.n_layers; ++l) {
-    if (m->layers[(size_t)l].gdn) continue;
+    if (m->layers[(size_t)l].gdn) {
+      TRY(palloc(p, (size_t)(n_q * gH * h.gdn_dk * h.gdn_dv) * 4, (void **)&p->S_pre[(size_t)l]));
+      const size_t tb = (size_t)(n_q * 3 * gC) * 4;
+      TRY(palloc(p, tb, (void **)&p->conv_tail[(size_t)l]));
+      HIPC(hipMemsetAsync(p->conv_tail[(size_t)l], 0, tb, m->st));
+      continue;
+    }
     TRY(palloc(p, kv_bytes, &p->kcache[(size_t)l]));
     TRY(palloc(p, kv_bytes, &p->vcache[(size_t)l]));
   }
@@ -591,6 +691,24 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     TRY(upload(m, "pre_last", last, &d_last));
     AttnPlan plan;
     TRY(plan_attention(m, 0, qd, "pre_at_", &plan));
+    GdnPlan gp;
+    if (h.hybrid) {
+      std::vector<int32_t> hist((size_t)R * 3), tslot((size_t)R, -1);
+      std::vector<jetk::GdnSeq> seqs;
+      for (int32_t q = q0; q < q1; ++q) {
+        const int64_t P = offs[q + 1] - offs[q], base = offs[q] - t0;
+        for (int64_t i = 0; i < P; ++i) {
+          for (int j = 1; j <= 3; ++j) hist[(size_t)((base + i) * 3 + j - 1)] = i - j >= 0 ? (int32_t)(base + i - j) : -1;
+          if (i >= P - 3) tslot[(size_t)(base + i)] = (int32_t)(q * 3 + (i - (P - 3)));
+        }
+        seqs.push_back({(int32_t)base, (int32_t)P, -1, q});
+      }
+      TRY(upload(m, "pre_ghist", hist, &gp.hist));
+      TRY(upload(m, "pre_gtslot", tslot, &gp.tail_slot));
+      TRY(upload(m, "pre_gseqs", seqs, &gp.seqs));
+      gp.nseq = (int)seqs.size();
+      gp.tok_heads = (double)R * (double)h.gdn_heads;
+    }
     WaveBufs b;
     TRY(wave_bufs(m, R, &b));
     {
@@ -599,10 +717,14 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     }
     for (int64_t l = 0; l < h.n_layers; ++l) {
       const Layer &ly = m->layers[(size_t)l];
-      TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
-      TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr, 0,
-                        nullptr, nullptr));
-      TRY(attn_out(m, ly, b, R));
+      if (ly.gdn) {
+        TRY(gdn_layer(m, ly, b, R, gp, p->conv_tail[(size_t)l], nullptr, p->S_pre[(size_t)l]));
+      } else {
+        TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
+        TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr,
+                          0, nullptr, nullptr));
+        TRY(attn_out(m, ly, b, R));
+      }
       TRY(ffn(m, ly, b, R));
     }
     {
@@ -689,6 +811,25 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       }
       AttnPlan plan;
       TRY(plan_attention(m, 1, qd, "cand_at_", &plan));
+      GdnPlan gp;
+      if (h.hybrid) {
+        // conv history: own earlier rows, then the question's prefix tail
+        std::vector<int32_t> hist((size_t)R * 3);
+        std::vector<jetk::GdnSeq> seqs;
+        for (int64_t r = r0; r < r1; ++r) {
+          const int32_t t = L.row_t[(size_t)r], q = L.row_q[(size_t)r];
+          for (int j = 1; j <= 3; ++j)
+            hist[(size_t)((r - r0) * 3 + j - 1)] = j <= t - 1 ? (int32_t)(r - r0 - j) : -(2 + (q * 3 + (t + 2 - j)));
+        }
+        for (int64_t cc = c0; cc < c1; ++cc) {
+          const int64_t a = row0(cc), e = row0(cc + 1);
+          if (e > a) seqs.push_back({(int32_t)(a - r0), (int32_t)(e - a), cand_q[(size_t)cc], -1});
+        }
+        TRY(upload(m, "cand_ghist", hist, &gp.hist));
+        TRY(upload(m, "cand_gseqs", seqs, &gp.seqs));
+        gp.nseq = (int)seqs.size();
+        gp.tok_heads = (double)R * (double)h.gdn_heads;
+      }
       WaveBufs b;
       TRY(wave_bufs(m, R, &b));
       void *kc, *vc;
@@ -701,10 +842,14 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       }
       for (int64_t l = 0; l < h.n_layers; ++l) {
         const Layer &ly = m->layers[(size_t)l];
-        TRY(attn_in(m, ly, b, R, d_rpos + r0, kc, vc, R, 0));
-        TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], p->T, kc, vc, R,
-                          d_rc + r0, d_rt + r0));
-        TRY(attn_out(m, ly, b, R));
+        if (ly.gdn) {
+          TRY(gdn_layer(m, ly, b, R, gp, p->conv_tail[(size_t)l], p->S_pre[(size_t)l], nullptr));
+        } else {
+          TRY(attn_in(m, ly, b, R, d_rpos + r0, kc, vc, R, 0));
+          TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], p->T, kc, vc, R,
+                            d_rc + r0, d_rt + r0));
+          TRY(attn_out(m, ly, b, R));
+        }
         TRY(ffn(m, ly, b, R));
       }
       TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz * m->np, &f_body));

@@ -92,3 +92,19 @@ def test_dense_1p5b_decisions_full(name, dense_1p5b_path, dense_1p5b_model):
         assert np.all((v_all >= 0) & (v_all <= 1))
     else:
         assert np.all((v_all >= 0) & (v_all <= K - 1))
+
+
+def test_hybrid_4b_k4_full():
+    """4B-shape hybrid (24 delta-rule + 8 attention layers): all 128 questions
+    on the GPU, the shortest-prefix question checked against the oracle."""
+    path = jet_synth.ensure_model("hybrid_4b")
+    wl = jet_synth.make_workload("hybrid_4b_k4")
+    log(f"[fullsize] hybrid_4b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    try:
+        tok, sums = run(m, wl)
+    finally:
+        J.jet_model_free(m)
+    properties(wl, tok, sums)
+    q = int(np.argmin(np.diff(wl.prefix_offsets)))
+    sampled_parity(path, wl, tok, sums, [q])

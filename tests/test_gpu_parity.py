@@ -78,6 +78,9 @@ CASES = [
     ("small_gqa_bf16", "small", J.JET_FP32),
     ("small_gqa_bf16", "small", J.JET_BF16_SINGLE),
     ("tiny_dense_bf16", "tiny", J.JET_BF16_SINGLE),
+    ("small_hybrid_fp32", "small_hybrid", J.JET_FP32),
+    ("small_hybrid_bf16", "small_hybrid", J.JET_BF16),
+    ("small_hybrid_bf16", "small_hybrid", J.JET_FP32),
 ]
 
 
@@ -101,11 +104,12 @@ def test_scores_match_oracle(spec, wname, dtype, model_dir):
     assert stats["lm_rows"] == wl.n_questions + (m - 1).sum()
 
 
-def test_prefix_sharing_matches_unshared_on_gpu(model_dir):
+@pytest.mark.parametrize("spec,wname", [("small_gqa_bf16", "small"), ("small_hybrid_bf16", "small_hybrid")])
+def test_prefix_sharing_matches_unshared_on_gpu(spec, wname, model_dir):
     """Unshared evaluation (each candidate with its own copy of the prefix,
     K P prefix tokens) gives the same scores as shared evaluation (P tokens)."""
-    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
-    wl = jet_synth.make_workload("small", n_questions=6)
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
+    wl = jet_synth.make_workload(wname, n_questions=6)
     tok_s, sum_s, st_s = run_gpu(path, wl, J.JET_FP32)
     pre, cands = [], []
     for q in range(wl.n_questions):
@@ -216,3 +220,27 @@ def test_device_budget_oom(model_dir):
     with pytest.raises(J.JetError) as e:
         J.jet_model_load(path, dtype=J.JET_BF16, max_device_bytes=1 << 16)
     assert e.value.code == J.JET_E_OOM
+
+
+@pytest.mark.parametrize("spec,wname", [("small_hybrid_bf16", "small_hybrid"), ("small_gqa_bf16", "small")])
+def test_candidate_isolation_on_gpu(spec, wname, model_dir):
+    """A candidate scored together with its siblings equals the same candidate
+    scored alone against the same prefix, bitwise: the forked recurrent state
+    and the own-suffix attention never see a sibling (Section 4.1, 5.6)."""
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
+    wl = jet_synth.make_workload(wname, n_questions=3)
+    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    try:
+        p = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+        tok, sums = J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+        for q in range(wl.n_questions):
+            for j, y in enumerate(wl.candidates(q)):
+                c = wl.q_cand_offsets[q] + j
+                qco = np.zeros(wl.n_questions + 1, np.int64)
+                qco[q + 1:] = 1
+                t1, s1 = J.jet_score_candidates(m, p, qco, [0, len(y)], y)
+                np.testing.assert_array_equal(t1, tok[wl.cand_tok_offsets[c]:wl.cand_tok_offsets[c + 1]])
+                assert s1[0] == sums[c]
+        J.jet_prefix_free(p)
+    finally:
+        J.jet_model_free(m)
