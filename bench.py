@@ -71,8 +71,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="dense_1p5b_k4")
-    ap.add_argument("--unshared-steps", type=int, default=2,
-                    help="steps of unshared (per-candidate prefix) evaluation for the reuse speedup; 0 = skip")
+    ap.add_argument("--unshared-steps", type=int, default=None,
+                    help="steps of unshared (per-candidate prefix) evaluation for the reuse speedup; "
+                         "0 = skip; default 2 on dense_1p5b_k4, else 0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with HIP events")
     args = ap.parse_args()
@@ -89,6 +90,8 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     wname = args.workload
+    if args.unshared_steps is None:
+        args.unshared_steps = 2 if wname == "dense_1p5b_k4" else 0
     spec = jet_synth.WORKLOADS[wname]["model"]
     t = time.perf_counter()
     path = jet_synth.ensure_model(spec)

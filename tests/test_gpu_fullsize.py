@@ -108,3 +108,31 @@ def test_hybrid_4b_k4_full():
     properties(wl, tok, sums)
     q = int(np.argmin(np.diff(wl.prefix_offsets)))
     sampled_parity(path, wl, tok, sums, [q])
+
+
+def test_dense_27b_k10_full():
+    """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
+    GPU; one whole candidate sequence (the shortest question's shortest
+    candidate, ~1.1k positions) checked against the oracle, plus properties."""
+    path = jet_synth.ensure_model("dense_27b")
+    wl = jet_synth.make_workload("dense_27b_k10")
+    log(f"[fullsize] dense_27b_k10: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    try:
+        tok, sums = run(m, wl)
+    finally:
+        J.jet_model_free(m)
+    properties(wl, tok, sums)
+    q = int(np.argmin(np.diff(wl.prefix_offsets)))
+    cands = wl.candidates(q)
+    j = int(np.argmin([len(y) for y in cands]))
+    c = wl.q_cand_offsets[q] + j
+    sub = jet_synth.from_lists([wl.prefix(q)], [[cands[j]]])
+    ref_tok, ref_sum = oracle.score_unshared(path, sub)
+    got = tok[wl.cand_tok_offsets[c]:wl.cand_tok_offsets[c + 1]]
+    dt = np.abs(got - ref_tok).max()
+    ds = abs(float(sums[c]) - float(ref_sum[0]))
+    log(f"[fullsize] 27b question {q} candidate {j}: max|d tok|={dt:.3e} |d sum|={ds:.3e}")
+    from conftest import record_parity
+    record_parity(f"fullsize/27b/q{q}c{j}", max_tok=dt, max_sum=ds)
+    assert dt <= 2e-2 and ds <= 5e-2
