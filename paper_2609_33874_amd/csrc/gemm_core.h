@@ -2,40 +2,52 @@
 // with A [M][K] and B [N][K] both K-contiguous, fp32 accumulation in 32x32
 // MFMA blocks.
 //
-// Per K step every row of the A and B tiles contributes 128 bytes (64 bf16 /
-// 32 fp32) = 8 chunks of 16 B. In LDS, chunk c of tile row r is stored at
-// position c ^ swz(r) of that row, so the MFMA operand reads (one row per
-// lane, same logical chunk) spread over all banks. Two LDS buffers alternate.
-// Tiles reach LDS either through registers (global load, then ds_write) or
-// directly (global_load_lds_dwordx4: each wave instruction fills 1 KB = 8
-// tile rows, lane L filling physical chunk L % 8 of row L / 8, so it fetches
-// the logical chunk (L % 8) ^ swz(row)).
+// Per K step every row of the A and B tiles contributes CPR chunks of 16 B
+// (CPR = 8: 64 bf16 / 32 fp32; CPR = 4: half of that). In LDS, chunk c of tile
+// row r is stored at position c ^ swz(r) of that row, so that the 16 lanes
+// the LDS serves per clock (one row each, same logical chunk) hit distinct
+// banks. Tiles reach LDS either through registers (global load, then
+// ds_write; LOAD 0, two stages) or directly (global_load_lds_dwordx4: each
+// wave instruction fills 1 KB = 64 / CPR tile rows, lane L filling physical
+// chunk L % CPR, so it fetches logical chunk (L % CPR) ^ swz(row); LOAD 1 with
+// two stages, LOAD 2 with NSTAGE stages and one barrier per K step).
+// Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
 #include "device.h"
 
 namespace jetk {
 
-template <typename T, int BM_, int BN_, int WM_, int WN_, int LOAD_ = 0, int SWZ_ = 0>
+template <typename T, int BM_, int BN_, int WM_, int WN_, int LOAD_ = 0, int SWZ_ = 0, int NSTAGE_ = 2,
+          int CPR_ = 8>
 struct GCfg {
   using type = T;
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, LOAD = LOAD_, SWZ = SWZ_;
+  static constexpr int NSTAGE = NSTAGE_, CPR = CPR_;
   static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN, NWAVES = WAVES_M * WAVES_N;
   static constexpr int NT = NWAVES * 64;
   static constexpr int MI = WM / 32, NI = WN / 32;
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
-  static constexpr int BK = 8 * EPC;                // elements per K step (128 B per row)
-  static constexpr int A_PT = BM * 8 / NT, B_PT = BN * 8 / NT;  // chunks per thread per K step
-  static constexpr int BUF = (BM + BN) * 8;                      // chunks per LDS buffer
-  static constexpr size_t LDS_BYTES = sizeof(uint4) * 2 * BUF;
-  static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile/thread mismatch");
-  static_assert(BM % (8 * NWAVES) == 0 && BN % (8 * NWAVES) == 0, "direct loads fill 8 rows per wave");
+  static constexpr int BK = CPR * EPC;              // elements per K step
+  static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step
+  static constexpr int BUF = (BM + BN) * CPR;                        // chunks per LDS stage
+  static constexpr size_t LDS_BYTES = sizeof(uint4) * NSTAGE * BUF;
+  static constexpr int RPI = 64 / CPR;  // tile rows per direct-load wave instruction
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
+  static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
+  static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
+  static_assert(LOAD >= 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
+  static_assert(LOAD != 3 || NWAVES == 8, "ping-pong needs two groups of four waves");
 };
 
-template <int SWZ>
+// SWZ 0: c ^ (r mod CPR). SWZ 1 (CPR 8): c ^ ((r >> 1) & 7). SWZ 2 (CPR 4):
+// c ^ ((r >> 2) & 3). With 256-byte LDS lines, 1 and 2 give 16 consecutive
+// rows distinct banks for one logical chunk.
+template <class C>
 __device__ __forceinline__ int lds_swz(int r) {
-  if constexpr (SWZ == 0) return r & 7;
-  else return (r >> 1) & 7;
+  if constexpr (C::SWZ == 0) return r & (C::CPR - 1);
+  else if constexpr (C::SWZ == 1) return (r >> 1) & 7;
+  else return (r >> 2) & 3;
 }
 
 template <typename T>
@@ -59,6 +71,23 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Waits until at most `tiles` K steps of direct loads (PT each) are in flight.
+template <int PT, int MAXT>
+__device__ __forceinline__ void wait_tiles(int tiles) {
+  if constexpr (MAXT >= 3) {
+    if (tiles >= 3) { wait_vmcnt<3 * PT>(); return; }
+  }
+  if constexpr (MAXT >= 2) {
+    if (tiles == 2) { wait_vmcnt<2 * PT>(); return; }
+  }
+  if constexpr (MAXT >= 1) {
+    if (tiles == 1) { wait_vmcnt<PT>(); return; }
+  }
+  wait_vmcnt<0>();
 }
 
 // Tile order: blockIdx.x enumerates tiles; workgroups are dealt round-robin to
@@ -94,7 +123,7 @@ template <class C>
 __device__ __forceinline__ void tile_compute(const uint4 *__restrict__ lds, int buf, int lane, int wm, int wn,
                                              f32x16 (&acc)[C::MI][C::NI]) {
   using T = typename C::type;
-  const uint4 *a = lds + buf * C::BUF, *b = a + C::BM * 8;
+  const uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
 #pragma unroll
   for (int kk = 0; kk < C::BK / 16; ++kk) {
     const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
@@ -102,12 +131,12 @@ __device__ __forceinline__ void tile_compute(const uint4 *__restrict__ lds, int 
 #pragma unroll
     for (int i = 0; i < C::MI; ++i) {
       const int r = wm * C::WM + i * 32 + (lane & 31);
-      lds_frag<T>(fa[i], a + r * 8, c0, lds_swz<C::SWZ>(r));
+      lds_frag<T>(fa[i], a + r * C::CPR, c0, lds_swz<C>(r));
     }
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
       const int r = wn * C::WN + j * 32 + (lane & 31);
-      lds_frag<T>(fb[j], b + r * 8, c0, lds_swz<C::SWZ>(r));
+      lds_frag<T>(fb[j], b + r * C::CPR, c0, lds_swz<C>(r));
     }
 #pragma unroll
     for (int i = 0; i < C::MI; ++i)
@@ -116,22 +145,56 @@ __device__ __forceinline__ void tile_compute(const uint4 *__restrict__ lds, int 
   }
 }
 
+// Fragments of one K step from LDS stage `buf` into registers.
+template <class C>
+__device__ __forceinline__ void tile_frags(const uint4 *__restrict__ lds, int buf, int lane, int wm, int wn,
+                                           Frag<typename C::type> (&fa)[C::BK / 16][C::MI],
+                                           Frag<typename C::type> (&fb)[C::BK / 16][C::NI]) {
+  using T = typename C::type;
+  const uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
+#pragma unroll
+  for (int kk = 0; kk < C::BK / 16; ++kk) {
+    const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i) {
+      const int r = wm * C::WM + i * 32 + (lane & 31);
+      lds_frag<T>(fa[kk][i], a + r * C::CPR, c0, lds_swz<C>(r));
+    }
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const int r = wn * C::WN + j * 32 + (lane & 31);
+      lds_frag<T>(fb[kk][j], b + r * C::CPR, c0, lds_swz<C>(r));
+    }
+  }
+}
+
+template <class C>
+__device__ __forceinline__ void tile_mma(const Frag<typename C::type> (&fa)[C::BK / 16][C::MI],
+                                         const Frag<typename C::type> (&fb)[C::BK / 16][C::NI],
+                                         f32x16 (&acc)[C::MI][C::NI]) {
+#pragma unroll
+  for (int kk = 0; kk < C::BK / 16; ++kk)
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NI; ++j) mma32(acc[i][j], fa[kk][i], fb[kk][j]);
+}
+
 // Register path: global -> registers.
 template <class C>
 __device__ __forceinline__ void tile_gload(const typename C::type *__restrict__ A, int64_t lda,
                                            const typename C::type *__restrict__ B, int64_t ldb, int M, int N,
                                            int m0, int n0, int ka, int kb, int tid, uint4 (&ra)[C::A_PT],
                                            uint4 (&rb)[C::B_PT]) {
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < C::A_PT; ++i) {
-    const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7, gm = m0 + r;
-    ra[i] = gm < M ? ld16(A + (int64_t)gm * lda + ka + c * C::EPC) : zero4;
+    const int ch = tid + i * C::NT, r = ch / C::CPR, c = ch % C::CPR, gm = min(m0 + r, M - 1);
+    ra[i] = ld16(A + (int64_t)gm * lda + ka + c * C::EPC);
   }
 #pragma unroll
   for (int i = 0; i < C::B_PT; ++i) {
-    const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7, gn = n0 + r;
-    rb[i] = gn < N ? ld16(B + (int64_t)gn * ldb + kb + c * C::EPC) : zero4;
+    const int ch = tid + i * C::NT, r = ch / C::CPR, c = ch % C::CPR, gn = min(n0 + r, N - 1);
+    rb[i] = ld16(B + (int64_t)gn * ldb + kb + c * C::EPC);
   }
 }
 
@@ -139,16 +202,16 @@ __device__ __forceinline__ void tile_gload(const typename C::type *__restrict__ 
 template <class C>
 __device__ __forceinline__ void tile_lstore(uint4 *__restrict__ lds, int buf, int tid, const uint4 (&ra)[C::A_PT],
                                             const uint4 (&rb)[C::B_PT]) {
-  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * 8;
+  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
 #pragma unroll
   for (int i = 0; i < C::A_PT; ++i) {
-    const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7;
-    a[r * 8 + (c ^ lds_swz<C::SWZ>(r))] = ra[i];
+    const int ch = tid + i * C::NT, r = ch / C::CPR, c = ch % C::CPR;
+    a[r * C::CPR + (c ^ lds_swz<C>(r))] = ra[i];
   }
 #pragma unroll
   for (int i = 0; i < C::B_PT; ++i) {
-    const int ch = tid + i * C::NT, r = ch >> 3, c = ch & 7;
-    b[r * 8 + (c ^ lds_swz<C::SWZ>(r))] = rb[i];
+    const int ch = tid + i * C::NT, r = ch / C::CPR, c = ch % C::CPR;
+    b[r * C::CPR + (c ^ lds_swz<C>(r))] = rb[i];
   }
 }
 
@@ -159,13 +222,13 @@ __device__ __forceinline__ void tile_issue_direct(const typename C::type *__rest
                                                   const typename C::type *__restrict__ B, int64_t ldb, int M,
                                                   int N, int m0, int n0, int ka, int kb, uint4 *lds, int buf,
                                                   int wave, int lane) {
-  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * 8;
-  const int sub_r = lane >> 3;
+  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
+  const int sub_r = lane / C::CPR, pc = lane % C::CPR;
 #pragma unroll
   for (int i = 0; i < C::A_PT; ++i) {
     const int blk = i * C::NWAVES + wave;
-    const int r = blk * 8 + sub_r;
-    const int c = (lane & 7) ^ lds_swz<C::SWZ>(r);
+    const int r = blk * C::RPI + sub_r;
+    const int c = pc ^ lds_swz<C>(r);
     const int gm = min(m0 + r, M - 1);
     __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)gm * lda + ka + c * C::EPC),
                                      (lds_void *)(a + blk * 64), 16, 0, 0);
@@ -173,8 +236,8 @@ __device__ __forceinline__ void tile_issue_direct(const typename C::type *__rest
 #pragma unroll
   for (int i = 0; i < C::B_PT; ++i) {
     const int blk = i * C::NWAVES + wave;
-    const int r = blk * 8 + sub_r;
-    const int c = (lane & 7) ^ lds_swz<C::SWZ>(r);
+    const int r = blk * C::RPI + sub_r;
+    const int c = pc ^ lds_swz<C>(r);
     const int gn = min(n0 + r, N - 1);
     __builtin_amdgcn_global_load_lds((const void *)(B + (int64_t)gn * ldb + kb + c * C::EPC),
                                      (lds_void *)(b + blk * 64), 16, 0, 0);
@@ -210,6 +273,63 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
       if (more) tile_lstore<C>(lds, (kt + 1) & 1, tid, ra, rb);
       __syncthreads();
     }
+  } else if constexpr (C::LOAD == 2) {
+    // NSTAGE-deep pipeline, one barrier per K step: the barrier of step kt
+    // certifies that every wave's loads of tile kt have landed and that every
+    // wave is done reading the stage that tile kt + NSTAGE - 1 overwrites.
+    constexpr int PT = C::A_PT + C::B_PT, AHEAD = C::NSTAGE - 1;
+#pragma unroll
+    for (int s = 0; s < AHEAD; ++s)
+      if (s < nk)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(s * C::BK, KA), kmod(s * C::BK, KB), lds, s, wave,
+                             lane);
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_tiles<PT, AHEAD - 1>(min(AHEAD - 1, nk - 1 - kt));
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();
+      const int kn = kt + AHEAD;
+      if (kn < nk)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(kn * C::BK, KA), kmod(kn * C::BK, KB), lds,
+                             kn % C::NSTAGE, wave, lane);
+      tile_compute<C>(lds, kt % C::NSTAGE, lane, wm, wn, acc);
+    }
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+  } else if constexpr (C::LOAD == 3) {
+    // Ping-pong: waves 0-3 and 4-7 (one per SIMD in each group) alternate
+    // between a load phase (direct loads of a later tile, LDS -> registers for
+    // this tile) and an MFMA phase, one phase apart, with one barrier per
+    // phase; so on every SIMD one wave feeds the matrix core while the other
+    // loads. Hazards: a wave issues the loads of tile kt + NSTAGE - 1 into the
+    // stage of tile kt - 1 during its load phase of tile kt, after both groups
+    // finished reading tile kt - 1 (each waited for its LDS reads before the
+    // barrier that ended its load phase of kt - 1); every wave waits for its
+    // own loads of tile kt + 1 before its load phase of kt ends, and the
+    // barrier after that phase precedes any read of tile kt + 1.
+    constexpr int PT = C::A_PT + C::B_PT, AHEAD = C::NSTAGE - 1;
+    const int grp = wave >> 2;
+#pragma unroll
+    for (int s = 0; s < AHEAD; ++s)
+      if (s < nk)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(s * C::BK, KA), kmod(s * C::BK, KB), lds, s, wave,
+                             lane);
+    wait_tiles<PT, AHEAD - 1>(min(AHEAD - 1, nk - 1));
+    __builtin_amdgcn_s_barrier();
+    if (grp == 1) __builtin_amdgcn_s_barrier();
+    Frag<typename C::type> fa[C::BK / 16][C::MI], fb[C::BK / 16][C::NI];
+    for (int kt = 0; kt < nk; ++kt) {
+      tile_frags<C>(lds, kt % C::NSTAGE, lane, wm, wn, fa, fb);
+      const int kn = kt + AHEAD;
+      if (kn < nk)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(kn * C::BK, KA), kmod(kn * C::BK, KB), lds,
+                             kn % C::NSTAGE, wave, lane);
+      wait_tiles<PT, AHEAD - 1>(max(0, min(AHEAD - 1, nk - 2 - kt)));
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();
+      tile_mma<C>(fa, fb, acc);
+      __builtin_amdgcn_s_barrier();
+    }
+    if (grp == 0) __builtin_amdgcn_s_barrier();
   } else {
     tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, 0, 0, lds, 0, wave, lane);
     for (int kt = 0; kt < nk; ++kt) {

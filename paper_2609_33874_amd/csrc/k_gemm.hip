@@ -3,10 +3,11 @@
 // needs fused in (fp32 store, residual add, SwiGLU), and the LM head with a
 // full-vocabulary online log-sum-exp epilogue that never writes logits.
 //
-// Large problems use 256x256 tiles (8 waves of 128x64, register-staged LDS
-// double buffering); problems with too few such tiles to fill the 256 CUs use
-// 128x128 tiles (4 waves of 64x64, direct global->LDS loads). Tiles are
-// ordered so that each XCD works on a contiguous band (see tile_coords).
+// Large problems use 256x256 tiles (8 waves of 128x64); problems with too few
+// such tiles to fill the 256 CUs use 256x128 tiles (8 waves of 64x64). Both
+// feed LDS with direct global->LDS loads through a 3-4 stage pipeline with one
+// barrier per K step. Tiles are ordered so that each XCD works on a
+// contiguous band (see tile_coords).
 #include <algorithm>
 
 #include "gemm_core.h"
@@ -163,11 +164,13 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
 // launchers
 // ---------------------------------------------------------------------------
 
-using BigB = GCfg<bf16, 256, 256, 128, 64, 0, 0>;
-using SmallB = GCfg<bf16, 128, 128, 64, 64, 1, 1>;
-using CfgF = GCfg<float, 128, 128, 64, 64, 0, 0>;
-using LmB = GCfg<bf16, 256, 256, 128, 64, 0, 0>;
-using LmF = GCfg<float, 128, 128, 64, 64, 0, 0>;
+// 4-stage direct-load pipelines with bank-conflict-free swizzles (64-byte
+// rows for the 256x256 tiles, 128-byte rows for the smaller ones).
+using BigB = GCfg<bf16, 256, 256, 128, 64, 2, 2, 4, 4>;
+using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
+using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
+using LmB = GCfg<bf16, 256, 256, 128, 64, 2, 2, 4, 4>;
+using LmF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
 template <class C>
