@@ -6,13 +6,18 @@
 // (CPR = 8: 64 bf16 / 32 fp32; CPR = 4: half of that). In LDS, chunk c of tile
 // row r is stored at position c ^ swz(r) of that row, so that the 16 lanes
 // the LDS serves per clock (one row each, same logical chunk) hit distinct
-// banks. Tiles reach LDS either through registers (global load, then
-// ds_write; LOAD 0, two stages) or directly (global_load_lds_dwordx4: each
-// wave instruction fills 1 KB = 64 / CPR tile rows, lane L filling physical
-// chunk L % CPR, so it fetches logical chunk (L % CPR) ^ swz(row); LOAD 1 with
-// two stages, LOAD 2 with NSTAGE stages and one barrier per K step).
+// banks. Tile schedules:
+//   LOAD 0  global -> registers -> ds_write, two stages (any element type);
+//   LOAD 2  global_load_lds_dwordx4 straight into LDS (each wave instruction
+//           fills 1 KB = 64 / CPR tile rows, lane L filling physical chunk
+//           L % CPR, so it fetches logical chunk (L % CPR) ^ swz(row)),
+//           NSTAGE stages, NSTAGE - 1 K steps in flight, one barrier per step;
+//   LOAD 4  as LOAD 2 with the MFMA fragments read one MFMA step ahead into
+//           registers (bf16), all NSTAGE stages in flight.
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
+
+#include <utility>
 
 #include "device.h"
 
@@ -36,8 +41,9 @@ struct GCfg {
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD >= 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
-  static_assert(LOAD != 3 || NWAVES == 8, "ping-pong needs two groups of four waves");
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4, "tile load schedule");
+  static_assert(LOAD == 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
+  static_assert(LOAD != 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
 
 // SWZ 0: c ^ (r mod CPR). SWZ 1 (CPR 8): c ^ ((r >> 1) & 7). SWZ 2 (CPR 4):
@@ -75,6 +81,31 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// LDS reads issued as inline asm, so that their completion is waited for
+// explicitly (wait_frags) instead of by the compiler's conservative
+// lgkmcnt(0) in front of the first use. The offset is an immediate.
+template <int OFF>
+__device__ __forceinline__ void ds_read16(bf16x8 &v, uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
+}
+
+template <int STRIDE, int N, int... I>
+__device__ __forceinline__ void ds_read_rows(Frag<bf16> (&f)[N], uint32_t addr, std::integer_sequence<int, I...>) {
+  (ds_read16<I * STRIDE>(f[I].v, addr), ...);
+}
+
+// Waits until at most N LDS reads are in flight, then ties the fragments to
+// that wait so that no use of them is scheduled above it.
+template <int N, int MI, int NI>
+__device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fb)[NI]) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+#pragma unroll
+  for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v));
+#pragma unroll
+  for (int j = 0; j < NI; ++j) asm volatile("" : "+v"(fb[j].v));
+}
+
 // Waits until at most `tiles` K steps of direct loads (PT each) are in flight.
 template <int PT, int MAXT>
 __device__ __forceinline__ void wait_tiles(int tiles) {
@@ -92,14 +123,20 @@ __device__ __forceinline__ void wait_tiles(int tiles) {
 
 // Tile order: blockIdx.x enumerates tiles; workgroups are dealt round-robin to
 // the 8 XCDs, so tile ids are remapped to give each XCD a contiguous band of
-// tiles (which share A rows in its L2), and inside the band tiles run in
-// groups of GM row-tiles so consecutive tiles also share B columns.
-template <int GM>
+// tiles, and inside the band tiles run in groups of gm row-tiles (row-tile
+// fastest). With the 32 tiles an XCD runs at once spanning all column tiles
+// of their rows (gm = 32 / nt_n), every A row panel is fetched once and
+// shared in L2 by the tiles that read it; with more column tiles, gm = 2
+// keeps the two A panels of a group (2 x 256 rows x K) in L2 while the
+// group sweeps the columns, and B streams from the last-level cache.
+__host__ __device__ __forceinline__ int tile_group_rows(int nt_n) { return nt_n <= 16 ? 32 / nt_n : 2; }
+
 __device__ __forceinline__ void tile_coords(int nt_m, int nt_n, int *tm, int *tn) {
   const int ntiles = nt_m * nt_n;
   int id = blockIdx.x;
   const int per = ntiles / 8;  // tiles per XCD (the remainder keeps its id)
   if (id < per * 8) id = (id & 7) * per + (id >> 3);
+  const int GM = tile_group_rows(nt_n);
   const int group = GM * nt_n;
   const int g = id / group, first_m = g * GM;
   const int gm = min(nt_m - first_m, GM);
@@ -145,39 +182,29 @@ __device__ __forceinline__ void tile_compute(const uint4 *__restrict__ lds, int 
   }
 }
 
-// Fragments of one K step from LDS stage `buf` into registers.
+// Fragments of MFMA step kk of stage `buf`, read as inline asm (bf16): one base
+// address per operand, the 32-row blocks at immediate offsets (the swizzle
+// depends on the row modulo 32 only).
 template <class C>
-__device__ __forceinline__ void tile_frags(const uint4 *__restrict__ lds, int buf, int lane, int wm, int wn,
-                                           Frag<typename C::type> (&fa)[C::BK / 16][C::MI],
-                                           Frag<typename C::type> (&fb)[C::BK / 16][C::NI]) {
-  using T = typename C::type;
-  const uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
-#pragma unroll
-  for (int kk = 0; kk < C::BK / 16; ++kk) {
-    const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
-#pragma unroll
-    for (int i = 0; i < C::MI; ++i) {
-      const int r = wm * C::WM + i * 32 + (lane & 31);
-      lds_frag<T>(fa[kk][i], a + r * C::CPR, c0, lds_swz<C>(r));
-    }
-#pragma unroll
-    for (int j = 0; j < C::NI; ++j) {
-      const int r = wn * C::WN + j * 32 + (lane & 31);
-      lds_frag<T>(fb[kk][j], b + r * C::CPR, c0, lds_swz<C>(r));
-    }
-  }
+__device__ __forceinline__ void kk_frags_asm(uint32_t lds_addr, int buf, int kk, int lane, int wm, int wn,
+                                             Frag<bf16> (&fa)[C::MI], Frag<bf16> (&fb)[C::NI]) {
+  static_assert(sizeof(typename C::type) == 2, "asm fragment reads are bf16 only");
+  const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
+  const int ra = wm * C::WM + (lane & 31), rb = C::BM + wn * C::WN + (lane & 31);
+  const uint32_t stage = lds_addr + (uint32_t)(buf * C::BUF) * 16u;
+  const uint32_t a = stage + (uint32_t)(ra * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
+  const uint32_t b = stage + (uint32_t)(rb * C::CPR + (c0 ^ lds_swz<C>(rb - C::BM))) * 16u;
+  ds_read_rows<32 * C::CPR * 16>(fa, a, std::make_integer_sequence<int, C::MI>{});
+  ds_read_rows<32 * C::CPR * 16>(fb, b, std::make_integer_sequence<int, C::NI>{});
 }
 
 template <class C>
-__device__ __forceinline__ void tile_mma(const Frag<typename C::type> (&fa)[C::BK / 16][C::MI],
-                                         const Frag<typename C::type> (&fb)[C::BK / 16][C::NI],
-                                         f32x16 (&acc)[C::MI][C::NI]) {
+__device__ __forceinline__ void kk_mma(const Frag<typename C::type> (&fa)[C::MI],
+                                       const Frag<typename C::type> (&fb)[C::NI], f32x16 (&acc)[C::MI][C::NI]) {
 #pragma unroll
-  for (int kk = 0; kk < C::BK / 16; ++kk)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
-    for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-      for (int j = 0; j < C::NI; ++j) mma32(acc[i][j], fa[kk][i], fb[kk][j]);
+    for (int j = 0; j < C::NI; ++j) mma32(acc[i][j], fa[i], fb[j]);
 }
 
 // Register path: global -> registers.
@@ -295,56 +322,50 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
     }
     wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
-  } else if constexpr (C::LOAD == 3) {
-    // Ping-pong: waves 0-3 and 4-7 (one per SIMD in each group) alternate
-    // between a load phase (direct loads of a later tile, LDS -> registers for
-    // this tile) and an MFMA phase, one phase apart, with one barrier per
-    // phase; so on every SIMD one wave feeds the matrix core while the other
-    // loads. Hazards: a wave issues the loads of tile kt + NSTAGE - 1 into the
-    // stage of tile kt - 1 during its load phase of tile kt, after both groups
-    // finished reading tile kt - 1 (each waited for its LDS reads before the
-    // barrier that ended its load phase of kt - 1); every wave waits for its
-    // own loads of tile kt + 1 before its load phase of kt ends, and the
-    // barrier after that phase precedes any read of tile kt + 1.
-    constexpr int PT = C::A_PT + C::B_PT, AHEAD = C::NSTAGE - 1;
-    const int grp = wave >> 2;
+  } else if constexpr (C::LOAD == 4) {
+    // As LOAD 2, with the fragments of every MFMA step read into registers
+    // one step ahead: the reads for step kk + 1 (for the last step: the first
+    // step of the next tile, after the barrier) are issued before the MFMAs of
+    // step kk, which wait only for the older reads. When the barrier of tile
+    // kt is passed every wave has its last fragments of tile kt in registers,
+    // so tile kt + NSTAGE is loaded straight into kt's stage: all NSTAGE
+    // stages hold tiles in flight.
+    constexpr int PT = C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = C::MI + C::NI;
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
 #pragma unroll
-    for (int s = 0; s < AHEAD; ++s)
+    for (int s = 0; s < NS; ++s)
       if (s < nk)
         tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(s * C::BK, KA), kmod(s * C::BK, KB), lds, s, wave,
                              lane);
-    wait_tiles<PT, AHEAD - 1>(min(AHEAD - 1, nk - 1));
+    wait_tiles<PT, NS - 1>(min(NS - 1, nk - 1));
     __builtin_amdgcn_s_barrier();
-    if (grp == 1) __builtin_amdgcn_s_barrier();
-    Frag<typename C::type> fa[C::BK / 16][C::MI], fb[C::BK / 16][C::NI];
+    Frag<bf16> fa[2][C::MI], fb[2][C::NI];
+    kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
     for (int kt = 0; kt < nk; ++kt) {
-      tile_frags<C>(lds, kt % C::NSTAGE, lane, wm, wn, fa, fb);
-      const int kn = kt + AHEAD;
-      if (kn < nk)
-        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(kn * C::BK, KA), kmod(kn * C::BK, KB), lds,
-                             kn % C::NSTAGE, wave, lane);
-      wait_tiles<PT, AHEAD - 1>(max(0, min(AHEAD - 1, nk - 2 - kt)));
-      wait_lgkmcnt0();
-      __builtin_amdgcn_s_barrier();
-      tile_mma<C>(fa, fb, acc);
-      __builtin_amdgcn_s_barrier();
-    }
-    if (grp == 0) __builtin_amdgcn_s_barrier();
-  } else {
-    tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, 0, 0, lds, 0, wave, lane);
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) {
-        const int k1 = (kt + 1) * C::BK;
-        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(k1, KA), kmod(k1, KB), lds, (kt + 1) & 1, wave,
-                             lane);
-        wait_vmcnt<C::A_PT + C::B_PT>();
-      } else {
-        wait_vmcnt<0>();
+      const int st = kt % NS;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int cur = kk & 1, nx = cur ^ 1;
+        if (kk + 1 < KK) {
+          kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
+          wait_frags<NR>(fa[cur], fb[cur]);
+        } else if (kt + 1 < nk) {
+          // tiles kt + 2 .. min(kt + NS - 1, nk - 1) may still be in flight
+          wait_tiles<PT, NS - 2>(min(NS - 2, nk - 2 - kt));
+          wait_frags<0>(fa[cur], fb[cur]);
+          __builtin_amdgcn_s_barrier();
+          const int kn = kt + NS;
+          if (kn < nk)
+            tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kmod(kn * C::BK, KA), kmod(kn * C::BK, KB), lds, st,
+                                 wave, lane);
+          kk_frags_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, wn, fa[nx], fb[nx]);
+        } else {
+          wait_frags<0>(fa[cur], fb[cur]);
+        }
+        kk_mma<C>(fa[cur], fb[cur], acc);
       }
-      __syncthreads();
-      tile_compute<C>(lds, kt & 1, lane, wm, wn, acc);
-      __syncthreads();
     }
+    __builtin_amdgcn_s_barrier();
   }
 }
 

@@ -3,11 +3,11 @@
 // needs fused in (fp32 store, residual add, SwiGLU), and the LM head with a
 // full-vocabulary online log-sum-exp epilogue that never writes logits.
 //
-// Large problems use 256x256 tiles (8 waves of 128x64); problems with too few
-// such tiles to fill the 256 CUs use 256x128 tiles (8 waves of 64x64). Both
-// feed LDS with direct global->LDS loads through a 3-4 stage pipeline with one
-// barrier per K step. Tiles are ordered so that each XCD works on a
-// contiguous band (see tile_coords).
+// Large problems use 256x256 tiles (8 waves of 128x64, two LDS stages, MFMA
+// fragments read one step ahead); problems with too few such tiles to fill
+// the 256 CUs use 256x128 tiles (8 waves of 64x64, three stages). Both feed
+// LDS with direct global->LDS loads, one barrier per K step. Tiles are ordered
+// so that each XCD works on a contiguous band (see tile_coords).
 #include <algorithm>
 
 #include "gemm_core.h"
@@ -35,7 +35,7 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
   extern __shared__ uint4 lds[];
   const int nt_m = (g.M + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
   int tm, tn;
-  tile_coords<8>(nt_m, nt_n, &tm, &tn);
+  tile_coords(nt_m, nt_n, &tm, &tn);
   const int m0 = tm * C::BM, n0 = tn * C::BN;
   f32x16 acc[C::MI][C::NI];
   gemm_tile<C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
@@ -164,12 +164,13 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
 // launchers
 // ---------------------------------------------------------------------------
 
-// 4-stage direct-load pipelines with bank-conflict-free swizzles (64-byte
-// rows for the 256x256 tiles, 128-byte rows for the smaller ones).
-using BigB = GCfg<bf16, 256, 256, 128, 64, 2, 2, 4, 4>;
+// Direct-load pipelines with bank-conflict-free swizzles and 128-byte tile
+// rows: the 256x256 tiles with fragments read one MFMA step ahead (two stages
+// of 64 KB), the 256x128 tiles with three stages.
+using BigB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
 using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
-using LmB = GCfg<bf16, 256, 256, 128, 64, 2, 2, 4, 4>;
+using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 using LmF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
