@@ -29,11 +29,7 @@ namespace jetk {
 template <typename T> __device__ __forceinline__ Frag<T> pack8(const float (&x)[8]);
 template <> __device__ __forceinline__ Frag<bf16> pack8<bf16>(const float (&x)[8]) {
   Frag<bf16> f;
-  uint4 u;
-  u.x = (uint32_t)f2bf(x[0]) | ((uint32_t)f2bf(x[1]) << 16);
-  u.y = (uint32_t)f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
-  u.z = (uint32_t)f2bf(x[4]) | ((uint32_t)f2bf(x[5]) << 16);
-  u.w = (uint32_t)f2bf(x[6]) | ((uint32_t)f2bf(x[7]) << 16);
+  const uint4 u = make_uint4(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]), f2bf2(x[4], x[5]), f2bf2(x[6], x[7]));
   f.v = __builtin_bit_cast(bf16x8, u);
   return f;
 }
@@ -42,20 +38,6 @@ template <> __device__ __forceinline__ Frag<float> pack8<float>(const float (&x)
 #pragma unroll
   for (int j = 0; j < 8; ++j) f.v[j] = x[j];
   return f;
-}
-
-// Four consecutive elements from LDS into lanes j0..j0+3 of a fragment.
-__device__ __forceinline__ void frag_put4(Frag<bf16> &f, const bf16 *p, int j0) {
-  const uint2 u = *reinterpret_cast<const uint2 *>(p);
-  bf16x8 v = f.v;
-  const __bf16 *h = reinterpret_cast<const __bf16 *>(&u);
-  v[j0 + 0] = h[0]; v[j0 + 1] = h[1]; v[j0 + 2] = h[2]; v[j0 + 3] = h[3];
-  f.v = v;
-}
-__device__ __forceinline__ void frag_put4(Frag<float> &f, const float *p, int j0) {
-  const uint4 u = *reinterpret_cast<const uint4 *>(p);
-  f.v[j0 + 0] = __uint_as_float(u.x); f.v[j0 + 1] = __uint_as_float(u.y);
-  f.v[j0 + 2] = __uint_as_float(u.z); f.v[j0 + 3] = __uint_as_float(u.w);
 }
 
 template <typename T>
@@ -73,15 +55,67 @@ __device__ __forceinline__ void lds_kfrag<float>(Frag<float> &f, const uint4 *ro
   f.v[6] = __uint_as_float(u1.z); f.v[7] = __uint_as_float(u1.w);
 }
 
+// Transposed V tile: row d holds the KT keys of dim d. Key k = 32 mm + 16 h +
+// 4 g + e (mm, h in {0, 1}, g, e in 0..3) sits at position 32 mm + 8 g + 4 h + e,
+// so the 8 keys one lane of lane group g needs for the PV product (the keys
+// of its probabilities, 32 mm + 4 g + e and 32 mm + 16 + 4 g + e) are one
+// contiguous 16-byte (bf16) or 32-byte (fp32) run; 16-byte units are
+// XOR-swizzled by d so the 16 lanes of a group (16 consecutive d) hit
+// distinct banks.
+__device__ __forceinline__ int vt_unit(const bf16 *, int unit, int d) { return unit ^ ((d >> 1) & 7); }
+__device__ __forceinline__ int vt_unit(const float *, int unit, int d) { return unit ^ (d & 15); }
+
+// Writes 4 keys 4u..4u+3 (rows r[0..3], one 16-byte chunk c of dims each).
+template <int KT>
+__device__ __forceinline__ void v_put_transposed(bf16 *vt, const uint4 (&r)[4], int u, int c) {
+  const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&r[0]), *w1 = reinterpret_cast<const uint32_t *>(&r[1]);
+  const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&r[2]), *w3 = reinterpret_cast<const uint32_t *>(&r[3]);
+  const int unit = 4 * (u >> 3) + (u & 3), half = ((u >> 2) & 1) * 4;  // 8-element unit, 4-key half
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int d = c * 8 + j;
+    const int sh = (j & 1) * 16;
+    const uint32_t e0 = (w0[j >> 1] >> sh) & 0xffffu, e1 = (w1[j >> 1] >> sh) & 0xffffu;
+    const uint32_t e2 = (w2[j >> 1] >> sh) & 0xffffu, e3 = (w3[j >> 1] >> sh) & 0xffffu;
+    *reinterpret_cast<uint2 *>(vt + d * KT + (vt_unit(vt, unit, d) << 3) + half) =
+        make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+  }
+}
+template <int KT>
+__device__ __forceinline__ void v_put_transposed(float *vt, const uint4 (&r)[4], int u, int c) {
+  const int unit = 8 * (u >> 3) + 2 * (u & 3) + ((u >> 2) & 1);  // 4-element unit
+  const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&r[0]), *w1 = reinterpret_cast<const uint32_t *>(&r[1]);
+  const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&r[2]), *w3 = reinterpret_cast<const uint32_t *>(&r[3]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int d = c * 4 + j;
+    *reinterpret_cast<uint4 *>(vt + d * KT + (vt_unit(vt, unit, d) << 2)) = make_uint4(w0[j], w1[j], w2[j], w3[j]);
+  }
+}
+
+// PV operand of lane group g for dim d and key half mm (see the layout above).
+template <int KT>
+__device__ __forceinline__ void v_frag(Frag<bf16> &f, const bf16 *vt, int d, int mm, int g) {
+  f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(vt + d * KT + (vt_unit(vt, 4 * mm + g, d) << 3)));
+}
+template <int KT>
+__device__ __forceinline__ void v_frag(Frag<float> &f, const float *vt, int d, int mm, int g) {
+  const int unit = 8 * mm + 2 * g;
+  const uint4 a = *reinterpret_cast<const uint4 *>(vt + d * KT + (vt_unit(vt, unit, d) << 2));
+  const uint4 b = *reinterpret_cast<const uint4 *>(vt + d * KT + (vt_unit(vt, unit + 1, d) << 2));
+  f.v[0] = __uint_as_float(a.x); f.v[1] = __uint_as_float(a.y); f.v[2] = __uint_as_float(a.z); f.v[3] = __uint_as_float(a.w);
+  f.v[4] = __uint_as_float(b.x); f.v[5] = __uint_as_float(b.y); f.v[6] = __uint_as_float(b.z); f.v[7] = __uint_as_float(b.w);
+}
+
 template <typename T, int HD, int MODE, bool PAIR>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int KT = 64;                        // keys per tile
   constexpr int EPC = 16 / (int)sizeof(T);      // elements per 16-byte chunk
   constexpr int CPR = HD / EPC;                 // chunks per K row
   constexpr int KSW = CPR < 16 ? CPR : 16;      // XOR range of the K-row swizzle
   constexpr int NP = PAIR ? 2 : 1;              // planes: hi (and lo)
   __shared__ uint4 Ks[NP][KT * CPR];
-  __shared__ T Vt[NP][HD * KT];
+  __shared__ __align__(16) T Vt[NP][HD * KT];
 
   const AttnItem it = a.items[blockIdx.x];
   const int G = a.Hq / a.Hkv;
@@ -117,33 +151,76 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int npre = MODE == 0 ? it.nkeys_pre : a.qs.pre_len[it.q];
   const int ntile = (npre + KT - 1) / KT;
 
+  // Tiles are software-pipelined: the global loads of tile t + 1 are issued
+  // into registers before the MFMAs of tile t and written to LDS after them.
+  // Loads always read a valid row (key clamped into the tile); keys beyond
+  // the tile are zeroed when the registers are written to LDS, so no load
+  // sits in a divergent branch or waits early.
+  constexpr int NKC = (KT * CPR + 255) / 256;        // K chunks per thread
+  constexpr int NVB = ((KT / 4) * CPR + 255) / 256;  // V 4-key blocks per thread
+  constexpr bool KFULL = (KT * CPR) % 256 == 0, VFULL = ((KT / 4) * CPR) % 256 == 0;
+  uint4 kreg[NP][NKC], vreg[NP][NVB][4];
+  const int64_t ps = a.kp_ps;
+  const T *kvbase_k = Kp + ((int64_t)it.kvh * a.s_pre + pslot) * HD;
+  const T *kvbase_v = Vp + ((int64_t)it.kvh * a.s_pre + pslot) * HD;
+  auto issue_tile = [&](int kb, int nkt, uint4 (&kr)[NP][NKC], uint4 (&vr)[NP][NVB][4]) {
+#pragma unroll
+    for (int i = 0; i < NKC; ++i) {
+      const int ch = tid + i * 256, key = min(ch / CPR, nkt - 1), c = ch % CPR;
+#pragma unroll
+      for (int p = 0; p < NP; ++p) kr[p][i] = ld16(kvbase_k + p * ps + (int64_t)(kb + key) * HD + c * EPC);
+    }
+#pragma unroll
+    for (int i = 0; i < NVB; ++i) {
+      const int bk = tid + i * 256, u = min(bk / CPR, KT / 4 - 1), c = bk % CPR;
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          vr[p][i][e] = ld16(kvbase_v + p * ps + (int64_t)(kb + min(4 * u + e, nkt - 1)) * HD + c * EPC);
+    }
+  };
+  if (ntile > 0) issue_tile(0, min(KT, npre), kreg, vreg);
+
   for (int tix = 0; tix < ntile; ++tix) {
     const int kbase = tix * KT;
     const int nk = min(KT, npre - kbase);
-    const int64_t off = ((int64_t)it.kvh * a.s_pre + pslot + kbase) * HD;
-    const T *Kb = Kp + off, *Vb = Vp + off;
-    const int64_t ps = a.kp_ps;
     __syncthreads();
-    for (int ch = tid; ch < KT * CPR; ch += 256) {
-      const int key = ch / CPR, c = ch % CPR;
-      const int u = key >> 2;
+    // K: 16-byte chunks, row-swizzled
 #pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-        if (key < nk) {
-          kv = ld16(Kb + p * ps + (int64_t)key * HD + c * EPC);
-          vv = ld16(Vb + p * ps + (int64_t)key * HD + c * EPC);
+    for (int i = 0; i < NKC; ++i) {
+      const int ch = tid + i * 256, key = ch / CPR, c = ch % CPR;
+      if (KFULL || ch < KT * CPR) {
+        const bool ok = key < nk;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const uint4 v = kreg[p][i];
+          Ks[p][key * CPR + (c ^ (key & (KSW - 1)))] =
+              make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
         }
-        Ks[p][key * CPR + (c ^ (key & (KSW - 1)))] = kv;
-        const T *ve = reinterpret_cast<const T *>(&vv);
+      }
+    }
+    // V, transposed: a thread takes 4 keys x one 16-byte chunk of dims and
+    // writes each dim's 4 keys as one store
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) {
-          const int d = c * EPC + e;
-          Vt[p][d * KT + ((u ^ (d & 15)) << 2) + (key & 3)] = ve[e];
+    for (int i = 0; i < NVB; ++i) {
+      const int bk = tid + i * 256, u = bk / CPR, c = bk % CPR;
+      if (VFULL || bk < (KT / 4) * CPR) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          uint4 r[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = 4 * u + e < nk;
+            const uint4 v = vreg[p][i][e];
+            r[e] = make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+          }
+          v_put_transposed<KT>(&Vt[p][0], r, u, c);
         }
       }
     }
     __syncthreads();
+    if (tix + 1 < ntile) issue_tile(kbase + KT, min(KT, npre - kbase - KT), kreg, vreg);
 
     f32x4 s[4];
 #pragma unroll
@@ -179,7 +256,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
-    const float alpha = (m_new == -INFINITY) ? 1.0f : exp2f(m_run - m_new);
+    // arguments are <= 0: v_exp_f32 directly
+    const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
     float p[4][4];
     float psum = 0.0f;
 #pragma unroll
@@ -187,7 +265,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float z = s[kb][e];
-        p[kb][e] = (z == -INFINITY) ? 0.0f : exp2f(z - m_new);
+        p[kb][e] = (z == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(z - m_new);
         psum += p[kb][e];
       }
     l_run = l_run * alpha + psum;
@@ -206,18 +284,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         for (int j = 0; j < 8; ++j) r8[j] = x8[j] - (float)pf.v[j];
         pfl = pack8<T>(r8);
       }
-      const int u1 = 8 * mm + g, u2 = u1 + 4;
 #pragma unroll
       for (int db = 0; db < HD / 16; ++db) {
         const int d = db * 16 + (lane & 15);
         Frag<T> fv;
-        frag_put4(fv, &Vt[0][d * KT + ((u1 ^ (d & 15)) << 2)], 0);
-        frag_put4(fv, &Vt[0][d * KT + ((u2 ^ (d & 15)) << 2)], 4);
+        v_frag<KT>(fv, &Vt[0][0], d, mm, g);
         mma16(acc[db], fv, pf);
         if constexpr (PAIR) {
           Frag<T> fvl;
-          frag_put4(fvl, &Vt[NP - 1][d * KT + ((u1 ^ (d & 15)) << 2)], 0);
-          frag_put4(fvl, &Vt[NP - 1][d * KT + ((u2 ^ (d & 15)) << 2)], 4);
+          v_frag<KT>(fvl, &Vt[NP - 1][0], d, mm, g);
           mma16(acc[db], fvl, pf);
           mma16(acc[db], fv, pfl);
         }
@@ -229,15 +304,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     // own rows of the candidate: row - my_t + 1 .. row of the call's K / V
     // (rows are ordered by candidate, then position). Lane group g holds the
     // query dims 32 ks + 8 g + j (score) and the output dims 16 db + 4 g + e.
-    float qv[HD / 32][8];
-#pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float v = to_f<T>(reinterpret_cast<const T *>(&qf[0][ks].v)[j]);
-        if constexpr (PAIR) v += to_f<T>(reinterpret_cast<const T *>(&qf[NP - 1][ks].v)[j]);
-        qv[ks][j] = v;
-      }
     int tmax = valid ? my_t : 0;
     for (int o = 1; o < 64; o <<= 1) tmax = max(tmax, __shfl_xor(tmax, o));
     const T *Kc = (const T *)a.Ks + (int64_t)it.kvh * a.s_suf * HD;
@@ -255,7 +321,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             const int d = ks * 32 + g * 8 + j;
             float kv = to_f<T>(kr[d]);
             if constexpr (PAIR) kv += to_f<T>(kr[a.ks_ps + d]);
-            part += qv[ks][j] * kv;
+            float qv = to_f<T>(reinterpret_cast<const T *>(&qf[0][ks].v)[j]);
+            if constexpr (PAIR) qv += to_f<T>(reinterpret_cast<const T *>(&qf[NP - 1][ks].v)[j]);
+            part += qv * kv;
           }
       }
       part += __shfl_xor(part, 16);
@@ -263,8 +331,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       if (act) {
         const float z = part * scale2;
         const float m_new = fmaxf(m_run, z);
-        const float alpha = exp2f(m_run - m_new);
-        const float pz = exp2f(z - m_new);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // arguments <= 0
+        const float pz = __builtin_amdgcn_exp2f(z - m_new);
         l_run = l_run * alpha + (g == 0 ? pz : 0.0f);
         const T *vr = Vc + krow * HD;
 #pragma unroll
@@ -287,15 +355,24 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const float inv = 1.0f / l_tot;
   T *O = (T *)a.O;
 #pragma unroll
-  for (int db = 0; db < HD / 16; ++db)
+  for (int db = 0; db < HD / 16; ++db) {
+    // dims 16 db + 4 g .. + 3 of this lane's query, one 8- (bf16) or 16-byte (fp32) store per plane
+    float o[4], lo[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int d = db * 16 + 4 * g + e;
-      const float o = acc[db][e] * inv;
-      const T hi = from_f<T>(o);
-      O[(int64_t)row * a.o_ld + (int64_t)head * HD + d] = hi;
-      if constexpr (PAIR) O[(int64_t)row * a.o_ld + (int64_t)(a.Hq + head) * HD + d] = from_f<T>(o - to_f<T>(hi));
+    for (int e = 0; e < 4; ++e) o[e] = acc[db][e] * inv;
+    T *dst = O + (int64_t)row * a.o_ld + (int64_t)head * HD + db * 16 + 4 * g;
+    if constexpr (sizeof(T) == 2) {
+      const uint2 hi = make_uint2(f2bf2(o[0], o[1]), f2bf2(o[2], o[3]));
+      *reinterpret_cast<uint2 *>(dst) = hi;
+      if constexpr (PAIR) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) lo[e] = o[e] - bf2f((bf16)((e & 1 ? (e < 2 ? hi.x : hi.y) >> 16 : (e < 2 ? hi.x : hi.y)) & 0xffffu));
+        *reinterpret_cast<uint2 *>(dst + (int64_t)a.Hq * HD) = make_uint2(f2bf2(lo[0], lo[1]), f2bf2(lo[2], lo[3]));
+      }
+    } else {
+      *reinterpret_cast<float4 *>(dst) = make_float4(o[0], o[1], o[2], o[3]);
     }
+  }
 }
 
 template <typename T, int HD, bool PAIR>
