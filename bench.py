@@ -247,6 +247,10 @@ def main() -> int:
         "prefix_tokens_per_s": round(T_p * args.steps / phase["prefill"], 1),
         "phase_ms_per_step": {k: round(1e3 * v / args.steps, 2) for k, v in phase.items()},
         "gemm_lmhead_mfma_frac": round(gemm_lm_frac, 4) if gemm_lm_frac else None,
+        # candidate attention over the shared prefix: bytes of the stored K/V
+        # (read once per question and KV head) + Q + O per second, vs HBM peak
+        "shared_prefix_attention_hbm_frac": (round(kernels["attn_cand"]["gbs"] / PEAK_HBM_GBS, 4)
+                                             if kernels.get("attn_cand", {}).get("gbs") else None),
         "roofline": roofline, "kernels": kernels,
     }
 

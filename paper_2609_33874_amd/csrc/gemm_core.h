@@ -13,7 +13,10 @@
 //           L % CPR, so it fetches logical chunk (L % CPR) ^ swz(row)),
 //           NSTAGE stages, NSTAGE - 1 K steps in flight, one barrier per step;
 //   LOAD 4  as LOAD 2 with the MFMA fragments read one MFMA step ahead into
-//           registers (bf16), all NSTAGE stages in flight.
+//           registers (bf16), all NSTAGE stages in flight;
+//   LOAD 5  as LOAD 4 for a (hi, lo) pair A operand: a stage holds the hi and
+//           lo tiles of A and one B tile, and every B fragment feeds both
+//           products (B is staged once instead of once per plane).
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
@@ -34,16 +37,19 @@ struct GCfg {
   static constexpr int MI = WM / 32, NI = WN / 32;
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   static constexpr int BK = CPR * EPC;              // elements per K step
-  static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step
-  static constexpr int BUF = (BM + BN) * CPR;                        // chunks per LDS stage
+  // LOAD 5 (pair-aware): A holds (hi, lo) planes and both are staged, B once
+  static constexpr bool PAIRA = LOAD == 5;
+  static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
+  static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step (per plane)
+  static constexpr int BUF = (BROW0 + BN) * CPR;                     // chunks per LDS stage
   static constexpr size_t LDS_BYTES = sizeof(uint4) * NSTAGE * BUF;
   static constexpr int RPI = 64 / CPR;  // tile rows per direct-load wave instruction
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4, "tile load schedule");
-  static_assert(LOAD == 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
-  static_assert(LOAD != 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 5, "tile load schedule");
+  static_assert(LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
+  static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
 
 // SWZ 0: c ^ (r mod CPR). SWZ 1 (CPR 8): c ^ ((r >> 1) & 7). SWZ 2 (CPR 4):
@@ -102,6 +108,15 @@ __device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fb
   asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
 #pragma unroll
   for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v));
+#pragma unroll
+  for (int j = 0; j < NI; ++j) asm volatile("" : "+v"(fb[j].v));
+}
+
+template <int N, int MI, int NI>
+__device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fl)[MI], Frag<bf16> (&fb)[NI]) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+#pragma unroll
+  for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v), "+v"(fl[i].v));
 #pragma unroll
   for (int j = 0; j < NI; ++j) asm volatile("" : "+v"(fb[j].v));
 }
@@ -190,12 +205,22 @@ __device__ __forceinline__ void kk_frags_asm(uint32_t lds_addr, int buf, int kk,
                                              Frag<bf16> (&fa)[C::MI], Frag<bf16> (&fb)[C::NI]) {
   static_assert(sizeof(typename C::type) == 2, "asm fragment reads are bf16 only");
   const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
-  const int ra = wm * C::WM + (lane & 31), rb = C::BM + wn * C::WN + (lane & 31);
+  const int ra = wm * C::WM + (lane & 31), rb = C::BROW0 + wn * C::WN + (lane & 31);
   const uint32_t stage = lds_addr + (uint32_t)(buf * C::BUF) * 16u;
   const uint32_t a = stage + (uint32_t)(ra * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
-  const uint32_t b = stage + (uint32_t)(rb * C::CPR + (c0 ^ lds_swz<C>(rb - C::BM))) * 16u;
+  const uint32_t b = stage + (uint32_t)(rb * C::CPR + (c0 ^ lds_swz<C>(rb - C::BROW0))) * 16u;
   ds_read_rows<32 * C::CPR * 16>(fa, a, std::make_integer_sequence<int, C::MI>{});
   ds_read_rows<32 * C::CPR * 16>(fb, b, std::make_integer_sequence<int, C::NI>{});
+}
+
+// LOAD 5: the lo-plane fragments of A (the tile BM rows after the hi tile).
+template <class C>
+__device__ __forceinline__ void kk_frags_lo_asm(uint32_t lds_addr, int buf, int kk, int lane, int wm,
+                                                Frag<bf16> (&fl)[C::MI]) {
+  const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
+  const int ra = wm * C::WM + (lane & 31);
+  const uint32_t a = lds_addr + (uint32_t)(buf * C::BUF + (C::BM + ra) * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
+  ds_read_rows<32 * C::CPR * 16>(fl, a, std::make_integer_sequence<int, C::MI>{});
 }
 
 template <class C>
@@ -248,17 +273,21 @@ template <class C>
 __device__ __forceinline__ void tile_issue_direct(const typename C::type *__restrict__ A, int64_t lda,
                                                   const typename C::type *__restrict__ B, int64_t ldb, int M,
                                                   int N, int m0, int n0, int ka, int kb, uint4 *lds, int buf,
-                                                  int wave, int lane) {
-  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR;
+                                                  int wave, int lane, int klo = 0) {
+  uint4 *a = lds + buf * C::BUF, *b = a + C::BROW0 * C::CPR;
   const int sub_r = lane / C::CPR, pc = lane % C::CPR;
 #pragma unroll
-  for (int i = 0; i < C::A_PT; ++i) {
-    const int blk = i * C::NWAVES + wave;
-    const int r = blk * C::RPI + sub_r;
-    const int c = pc ^ lds_swz<C>(r);
-    const int gm = min(m0 + r, M - 1);
-    __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)gm * lda + ka + c * C::EPC),
-                                     (lds_void *)(a + blk * 64), 16, 0, 0);
+  for (int pl = 0; pl < (C::PAIRA ? 2 : 1); ++pl) {
+    // plane pl of A: columns ka (hi) or klo + ka (lo), LDS block pl
+#pragma unroll
+    for (int i = 0; i < C::A_PT; ++i) {
+      const int blk = i * C::NWAVES + wave;
+      const int r = blk * C::RPI + sub_r;
+      const int c = pc ^ lds_swz<C>(r);
+      const int gm = min(m0 + r, M - 1);
+      __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)gm * lda + pl * klo + ka + c * C::EPC),
+                                       (lds_void *)(a + pl * C::BM * C::CPR + blk * 64), 16, 0, 0);
+    }
   }
 #pragma unroll
   for (int i = 0; i < C::B_PT; ++i) {
@@ -363,6 +392,48 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
           wait_frags<0>(fa[cur], fb[cur]);
         }
         kk_mma<C>(fa[cur], fb[cur], acc);
+      }
+    }
+    __builtin_amdgcn_s_barrier();
+  } else if constexpr (C::LOAD == 5) {
+    // Pair-aware: K steps over the KB columns of B; A rows hold [hi | lo]
+    // with the lo plane KB columns after the hi plane; every B fragment feeds
+    // acc += A_hi B + A_lo B. Otherwise as LOAD 4.
+    constexpr int PT = 2 * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = 2 * C::MI + C::NI;
+    const int nk5 = KB / C::BK;
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      if (s < nk5)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, s * C::BK, s * C::BK, lds, s, wave, lane, KB);
+    wait_tiles<PT, NS - 1>(min(NS - 1, nk5 - 1));
+    __builtin_amdgcn_s_barrier();
+    Frag<bf16> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
+    kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
+    kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
+    for (int kt = 0; kt < nk5; ++kt) {
+      const int st = kt % NS;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int cur = kk & 1, nx = cur ^ 1;
+        if (kk + 1 < KK) {
+          kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
+          kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
+          wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
+        } else if (kt + 1 < nk5) {
+          wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 2 - kt));
+          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+          __builtin_amdgcn_s_barrier();
+          const int kn = kt + NS;
+          if (kn < nk5)
+            tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn * C::BK, kn * C::BK, lds, st, wave, lane, KB);
+          kk_frags_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, wn, fa[nx], fb[nx]);
+          kk_frags_lo_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, fl[nx]);
+        } else {
+          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+        }
+        kk_mma<C>(fa[cur], fb[cur], acc);
+        kk_mma<C>(fl[cur], fb[cur], acc);
       }
     }
     __builtin_amdgcn_s_barrier();

@@ -3,9 +3,10 @@
 // needs fused in (fp32 store, residual add, SwiGLU), and the LM head with a
 // full-vocabulary online log-sum-exp epilogue that never writes logits.
 //
-// Large problems use 256x256 tiles (8 waves of 128x64, two LDS stages, MFMA
-// fragments read one step ahead); problems with too few such tiles to fill
-// the 256 CUs use 256x128 tiles (8 waves of 64x64, three stages). Both feed
+// Large problems use 256x256 tiles (8 waves, MFMA fragments read one step
+// ahead; in the pair mode the hi and lo planes of A share each B tile);
+// problems with too few such tiles to fill the 256 CUs use 256x128 tiles
+// (8 waves of 64x64, three stages). Both feed
 // LDS with direct global->LDS loads, one barrier per K step. Tiles are ordered
 // so that each XCD works on a contiguous band (see tile_coords).
 #include <algorithm>
@@ -168,6 +169,9 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
 // rows: the 256x256 tiles with fragments read one MFMA step ahead (two stages
 // of 64 KB), the 256x128 tiles with three stages.
 using BigB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
+// Pair mode: the (hi, lo) planes of A and one B tile per 32-column stage
+// (3 x 16 KB), waves of 64 x 128 so each B fragment serves both planes.
+using PairB = GCfg<bf16, 256, 256, 64, 128, 5, 2, 2, 4>;
 using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
 using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
@@ -211,6 +215,7 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
   if (dtype == 0) {
     // 256x256 tiles when there are enough of them to fill the chip twice over
     const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+    if (big_tiles >= 512 && pair) return run_epi<PairB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
     if (big_tiles >= 512) return run_epi<BigB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
     return run_epi<SmallB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
   }
