@@ -172,6 +172,9 @@ using BigB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 // Pair mode: the (hi, lo) planes of A and one B tile per 32-column stage
 // (3 x 16 KB), waves of 64 x 128 so each B fragment serves both planes.
 using PairB = GCfg<bf16, 256, 256, 64, 128, 5, 2, 2, 4>;
+// ... and for problems with fewer tiles: 128x128 tiles (8 waves of 32x64,
+// three 24 KB stages, two workgroups per CU).
+using PairS = GCfg<bf16, 128, 128, 32, 64, 5, 2, 3, 4>;
 using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
 using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
@@ -215,7 +218,9 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
   if (dtype == 0) {
     // 256x256 tiles when there are enough of them to fill the chip twice over
     const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
-    if (big_tiles >= 512 && pair) return run_epi<PairB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    if (pair)
+      return big_tiles >= 512 ? run_epi<PairB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st)
+                              : run_epi<PairS>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
     if (big_tiles >= 512) return run_epi<BigB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
     return run_epi<SmallB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
   }
