@@ -230,6 +230,24 @@ hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, con
   return hipGetLastError();
 }
 
+// dst row i = src row idx[i] (rows of row_bytes bytes, a multiple of 16).
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint4 *__restrict__ src, int64_t row_chunks,
+                                                          const int32_t *__restrict__ idx, uint4 *__restrict__ dst) {
+  const int i = blockIdx.x;
+  const uint4 *s = src + (int64_t)idx[i] * row_chunks;
+  uint4 *d = dst + (int64_t)i * row_chunks;
+  for (int64_t c = threadIdx.x; c < row_chunks; c += 256) d[c] = s[c];
+}
+
+hipError_t launch_gather_rows(const void *src, int64_t row_bytes, const int32_t *idx, int n, void *dst,
+                              hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, st, (const uint4 *)src, row_bytes / 16, idx,
+                     (uint4 *)dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n, float *s, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(segment_sum_kernel, dim3((n + 255) / 256), dim3(256), 0, st, ell, off, n, s);

@@ -123,6 +123,9 @@ hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, con
                                  const float *lse_last, const void *W, int d, float *ell, hipStream_t st);
 // s[c] = sum of ell[off[c] - off[0] .. off[c+1] - off[0]) in ascending order.
 hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n_cand, float *s, hipStream_t st);
+// dst row i = src row idx[i], rows of row_bytes (a multiple of 16) bytes.
+hipError_t launch_gather_rows(const void *src, int64_t row_bytes, const int32_t *idx, int n, void *dst,
+                              hipStream_t st);
 // Counts ids outside [0, V) into *bad (int, must be zeroed by the caller).
 hipError_t launch_count_bad_ids(const int32_t *ids, int64_t n, int V, int *bad, hipStream_t st);
 // dst[i] = src[i] with fp32 -> T conversion (weights upload helpers).

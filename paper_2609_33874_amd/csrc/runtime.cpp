@@ -452,7 +452,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
 // Q: [planes][R][Hq][hd]; O: [R][planes * Hq * hd]; caches [planes][Hkv][S][hd].
 Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void *O, const void *Kp, const void *Vp,
                      int64_t s_pre, const void *Ks, const void *Vs, int64_t s_suf, const int32_t *row_c,
-                     const int32_t *row_t) {
+                     const int32_t *row_t, int cls = -1) {
   if (pl.a.n_items == 0) return Status::ok();
   const ModelHeader &h = m->h;
   jetk::AttnArgs a = pl.a;
@@ -470,7 +470,7 @@ Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void 
   a.ks_ps = h.n_kv_heads * s_suf * h.head_dim;
   a.row_c = row_c;
   a.row_t = row_t;
-  KTimer t(m, a.mode == 0 ? JET_K_ATTN_PREFIX : JET_K_ATTN_CAND, pl.flops, pl.bytes);
+  KTimer t(m, cls >= 0 ? cls : a.mode == 0 ? JET_K_ATTN_PREFIX : JET_K_ATTN_CAND, pl.flops, pl.bytes);
   LAUNCH(jetk::launch_attention(m->kdt, a, m->st));
   return Status::ok();
 }
@@ -715,19 +715,65 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
       KTimer t(m, JET_K_OTHER, 0, 0);
       LAUNCH(jetk::launch_embed(dt, m->embed, d_tok + t0, nullptr, (int)R, (int)h.d, b.resid, m->st));
     }
-    for (int64_t l = 0; l < h.n_layers; ++l) {
+    // Only the last row of each question goes on past the last layer (to the
+    // LM head, Section 4.1), while every row's K/V of that layer is retained:
+    // when the last layer is an attention layer, its attention, output
+    // projection and FFN run on the last rows alone (attention of the last
+    // row over the whole prefix = the candidate kernel with no own rows).
+    const int64_t L = h.n_layers;
+    const bool last_rows_only = !m->layers[(size_t)(L - 1)].gdn;
+    const int32_t nq = q1 - q0;
+    for (int64_t l = 0; l < L; ++l) {
       const Layer &ly = m->layers[(size_t)l];
       if (ly.gdn) {
         TRY(gdn_layer(m, ly, b, R, gp, p->conv_tail[(size_t)l], nullptr, p->S_pre[(size_t)l]));
-      } else {
-        TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
-        TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr,
-                          0, nullptr, nullptr));
-        TRY(attn_out(m, ly, b, R));
+        TRY(ffn(m, ly, b, R));
+        continue;
       }
+      TRY(attn_in(m, ly, b, R, d_pos, p->kcache[(size_t)l], p->vcache[(size_t)l], T, t0));
+      if (l == L - 1 && last_rows_only) break;
+      TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr,
+                        0, nullptr, nullptr));
+      TRY(attn_out(m, ly, b, R));
       TRY(ffn(m, ly, b, R));
     }
-    {
+    if (last_rows_only) {
+      const Layer &ly = m->layers[(size_t)(L - 1)];
+      QDesc ql;
+      std::vector<int32_t> zero_t((size_t)R, 0);
+      for (int32_t q = q0; q < q1; ++q) {
+        const int64_t P = offs[q + 1] - offs[q];
+        ql.qrow0.push_back(last[(size_t)(q - q0)]);
+        ql.nrows.push_back(1);
+        ql.pre_slot0.push_back(offs[q]);
+        ql.pre_len.push_back((int32_t)P);
+        ql.suf_row0.push_back(0);
+        ql.suf_len.push_back(0);
+      }
+      AttnPlan lp;
+      TRY(plan_attention(m, 1, ql, "pre_lr_", &lp));
+      int32_t *d_zero_t;
+      TRY(upload(m, "pre_lr_t", zero_t, &d_zero_t));
+      TRY(run_attention(m, lp, b.q, R, b.att, p->kcache[(size_t)(L - 1)], p->vcache[(size_t)(L - 1)], T, nullptr,
+                        nullptr, 0, nullptr, d_zero_t, JET_K_ATTN_PREFIX));
+      WaveBufs c;  // the last rows, compacted
+      const size_t pe = (size_t)m->np * m->esz;
+      TRY(ws_t<float>(m, "lr_resid", (size_t)(nq * h.d), &c.resid));
+      TRY(ws(m, "lr_att", (size_t)(nq * h.n_heads * h.head_dim) * pe, &c.att));
+      TRY(ws(m, "lr_xn", (size_t)(nq * h.d) * pe, &c.xn));
+      TRY(ws(m, "lr_act", (size_t)(nq * h.ffn) * pe, &c.act));
+      {
+        KTimer t(m, JET_K_OTHER, 0, 0);
+        LAUNCH(jetk::launch_gather_rows(b.resid, h.d * 4, d_last, nq, c.resid, m->st));
+        LAUNCH(jetk::launch_gather_rows(b.att, (int64_t)(h.n_heads * h.head_dim) * (int64_t)pe, d_last, nq, c.att,
+                                        m->st));
+      }
+      TRY(attn_out(m, ly, c, nq));
+      TRY(ffn(m, ly, c, nq));
+      KTimer t(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_rmsnorm(dt, m->pair, c.resid, nullptr, m->final_norm, (int)nq, (int)h.d, (float)h.rms_eps,
+                                  (char *)p->f_last + (size_t)(q0 * h.d) * m->esz * m->np, m->st));
+    } else {
       KTimer t(m, JET_K_OTHER, 0, 0);
       LAUNCH(jetk::launch_rmsnorm(dt, m->pair, b.resid, d_last, m->final_norm, (int)(q1 - q0), (int)h.d,
                                   (float)h.rms_eps, (char *)p->f_last + (size_t)(q0 * h.d) * m->esz * m->np, m->st));
