@@ -16,7 +16,9 @@
 //           registers (bf16), all NSTAGE stages in flight;
 //   LOAD 5  as LOAD 4 for a (hi, lo) pair A operand: a stage holds the hi and
 //           lo tiles of A and one B tile, and every B fragment feeds both
-//           products (B is staged once instead of once per plane).
+//           products (B is staged once instead of once per plane);
+//   LOAD 6  as LOAD 5 with NSTAGE - 1 tiles in flight, each issued after the
+//           first MFMA step of a tile instead of right after its barrier.
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
@@ -38,7 +40,7 @@ struct GCfg {
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   static constexpr int BK = CPR * EPC;              // elements per K step
   // LOAD 5 (pair-aware): A holds (hi, lo) planes and both are staged, B once
-  static constexpr bool PAIRA = LOAD == 5;
+  static constexpr bool PAIRA = LOAD >= 5;
   static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
   static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step (per plane)
   static constexpr int BUF = (BROW0 + BN) * CPR;                     // chunks per LDS stage
@@ -47,8 +49,9 @@ struct GCfg {
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 5, "tile load schedule");
-  static_assert(LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2, "pipeline depth");
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 5 || LOAD == 6, "tile load schedule");
+  static_assert(LOAD == 6 ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
+                "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
 
@@ -434,6 +437,53 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
         }
         kk_mma<C>(fa[cur], fb[cur], acc);
         kk_mma<C>(fl[cur], fb[cur], acc);
+      }
+    }
+    __builtin_amdgcn_s_barrier();
+  } else if constexpr (C::LOAD == 6) {
+    // As LOAD 5 with NSTAGE - 1 tiles in flight: the stage of tile kt - 1 is
+    // free once the barrier before tile kt has passed, so tile kt + NSTAGE - 1
+    // is loaded into it after the first MFMA step of tile kt rather than
+    // right after the barrier.
+    constexpr int PT = 2 * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = 2 * C::MI + C::NI;
+    const int nk5 = KB / C::BK;
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nk5)
+        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, s * C::BK, s * C::BK, lds, s, wave, lane, KB);
+    wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 1));
+    __builtin_amdgcn_s_barrier();
+    Frag<bf16> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
+    kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
+    kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
+    for (int kt = 0; kt < nk5; ++kt) {
+      const int st = kt % NS;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int cur = kk & 1, nx = cur ^ 1;
+        if (kk + 1 < KK) {
+          kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
+          kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
+          wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
+        } else if (kt + 1 < nk5) {
+          // tiles issued after kt + 1: kt + 2 .. min(kt + NS - 1, nk - 1)
+          wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 2 - kt));
+          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+          __builtin_amdgcn_s_barrier();
+          kk_frags_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, wn, fa[nx], fb[nx]);
+          kk_frags_lo_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, fl[nx]);
+        } else {
+          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+        }
+        kk_mma<C>(fa[cur], fb[cur], acc);
+        kk_mma<C>(fl[cur], fb[cur], acc);
+        if (kk == 0) {
+          const int kn = kt + NS - 1;
+          if (kn < nk5)
+            tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn * C::BK, kn * C::BK, lds, kn % NS, wave, lane,
+                                 KB);
+        }
       }
     }
     __builtin_amdgcn_s_barrier();
