@@ -55,7 +55,8 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
           const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
           if (row < g.M && gcol < g.N) {
             const float gt = acc[i][2 * jp][e], up = acc[i][2 * jp + 1][e];
-            const float v = gt / (1.0f + __expf(-gt)) * up;
+            // silu(g) = g / (1 + e^-g) with the hardware reciprocal (~1 ulp)
+            const float v = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
             const T hi = from_f<T>(v);
             out[(int64_t)row * g.ldo + f] = hi;
             if (g.pair_out) out[(int64_t)row * g.ldo + (g.N >> 1) + f] = from_f<T>(v - to_f<T>(hi));
