@@ -172,7 +172,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < NVB; ++i) {
-      const int bk = tid + i * 256, u = min(bk / CPR, KT / 4 - 1), c = bk % CPR;
+      const int bk = tid + i * 256, u = bk % (KT / 4), c = min(bk / (KT / 4), CPR - 1);
 #pragma unroll
       for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -201,10 +201,12 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       }
     }
     // V, transposed: a thread takes 4 keys x one 16-byte chunk of dims and
-    // writes each dim's 4 keys as one store
+    // writes each dim's 4 keys as one store; the 16 threads of a group take
+    // the 16 key quads of one chunk, so each store of the group fills one
+    // 128-byte row of Vt (distinct banks)
 #pragma unroll
     for (int i = 0; i < NVB; ++i) {
-      const int bk = tid + i * 256, u = bk / CPR, c = bk % CPR;
+      const int bk = tid + i * 256, u = bk % (KT / 4), c = bk / (KT / 4);
       if (VFULL || bk < (KT / 4) * CPR) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
