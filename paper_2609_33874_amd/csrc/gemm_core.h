@@ -141,13 +141,11 @@ __device__ __forceinline__ void wait_tiles(int tiles) {
 
 // Tile order: blockIdx.x enumerates tiles; workgroups are dealt round-robin to
 // the 8 XCDs, so tile ids are remapped to give each XCD a contiguous band of
-// tiles, and inside the band tiles run in groups of gm row-tiles (row-tile
-// fastest). With the 32 tiles an XCD runs at once spanning all column tiles
-// of their rows (gm = 32 / nt_n), every A row panel is fetched once and
-// shared in L2 by the tiles that read it; with more column tiles, gm = 2
-// keeps the two A panels of a group (2 x 256 rows x K) in L2 while the
-// group sweeps the columns, and B streams from the last-level cache.
-__host__ __device__ __forceinline__ int tile_group_rows(int nt_n) { return nt_n <= 16 ? 32 / nt_n : 2; }
+// tiles, and inside the band tiles run in groups of 4 row-tiles (row-tile
+// fastest): the 32 tiles an XCD runs at once then share 4 A row panels and
+// 8 B column panels in its L2 (measured best against groups of 1, 2, 5, 8
+// and of all columns, on every decoder GEMM shape).
+__host__ __device__ __forceinline__ int tile_group_rows(int) { return 4; }
 
 __device__ __forceinline__ void tile_coords(int nt_m, int nt_n, int *tm, int *tn) {
   const int ntiles = nt_m * nt_n;
