@@ -187,11 +187,12 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     const int nk = min(KT, npre - kbase);
     __syncthreads();
     // K: 16-byte chunks, row-swizzled
+    const bool tile_full = nk == KT;  // uniform: no key of the tile to zero
 #pragma unroll
     for (int i = 0; i < NKC; ++i) {
       const int ch = tid + i * 256, key = ch / CPR, c = ch % CPR;
       if (KFULL || ch < KT * CPR) {
-        const bool ok = key < nk;
+        const bool ok = tile_full || key < nk;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
           const uint4 v = kreg[p][i];
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
           uint4 r[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const bool ok = 4 * u + e < nk;
+            const bool ok = tile_full || 4 * u + e < nk;
             const uint4 v = vreg[p][i][e];
             r[e] = make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
           }
@@ -244,35 +245,49 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       }
     }
     float mx = -INFINITY;
+    // tiles every key of which every query of the wave sees skip the mask
+    if (__all(tile_full && (MODE != 0 || kbase + KT - 1 <= qi))) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = kb * 16 + 4 * g + e;
-        bool vis = key < nk;
-        if (MODE == 0) vis = vis && (kbase + key <= qi);
-        const float z = vis ? s[kb][e] * scale2 : -INFINITY;
-        s[kb][e] = z;
-        mx = fmaxf(mx, z);
-      }
+        for (int e = 0; e < 4; ++e) {
+          s[kb][e] *= scale2;
+          mx = fmaxf(mx, s[kb][e]);
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = kb * 16 + 4 * g + e;
+          bool vis = key < nk;
+          if (MODE == 0) vis = vis && (kbase + key <= qi);
+          const float z = vis ? s[kb][e] * scale2 : -INFINITY;
+          s[kb][e] = z;
+          mx = fmaxf(mx, z);
+        }
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // Every query sees key 0 in the first tile (mode 0) or the whole prefix
+    // (mode 1), so m_new is finite: exp2 of the (<= 0) differences directly,
+    // with exp2(-inf) = 0 for masked keys and for the initial m_run.
     const float m_new = fmaxf(m_run, mx);
-    // arguments are <= 0: v_exp_f32 directly
-    const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     float p[4][4];
     float psum = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float z = s[kb][e];
-        p[kb][e] = (z == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(z - m_new);
+        p[kb][e] = __builtin_amdgcn_exp2f(s[kb][e] - m_new);
         psum += p[kb][e];
       }
     l_run = l_run * alpha + psum;
+    if (__any(alpha != 1.0f)) {
 #pragma unroll
-    for (int d = 0; d < HD / 16; ++d) acc[d] *= alpha;
+      for (int d = 0; d < HD / 16; ++d) acc[d] *= alpha;
+    }
     m_run = m_new;
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm) {
