@@ -14,11 +14,10 @@
 //           NSTAGE stages, NSTAGE - 1 K steps in flight, one barrier per step;
 //   LOAD 4  as LOAD 2 with the MFMA fragments read one MFMA step ahead into
 //           registers (bf16), all NSTAGE stages in flight;
-//   LOAD 5  as LOAD 4 for a (hi, lo) pair A operand: a stage holds the hi and
-//           lo tiles of A and one B tile, and every B fragment feeds both
-//           products (B is staged once instead of once per plane);
-//   LOAD 6  as LOAD 5 with NSTAGE - 1 tiles in flight, each issued after the
-//           first MFMA step of a tile instead of right after its barrier.
+//   LOAD 7  for a (hi, lo) pair A operand: a stage holds the hi and lo tiles
+//           of A and one B tile, so every B fragment feeds both products;
+//           NSTAGE - 1 K steps in flight, each step's loads interleaved with
+//           the MFMAs of the step before it (fixed by scheduling groups).
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
@@ -39,8 +38,8 @@ struct GCfg {
   static constexpr int MI = WM / 32, NI = WN / 32;
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   static constexpr int BK = CPR * EPC;              // elements per K step
-  // LOAD 5 (pair-aware): A holds (hi, lo) planes and both are staged, B once
-  static constexpr bool PAIRA = LOAD >= 5;
+  // LOAD 7 (pair-aware): A holds (hi, lo) planes and both are staged, B once
+  static constexpr bool PAIRA = LOAD == 7;
   static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
   static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step (per plane)
   static constexpr int BUF = (BROW0 + BN) * CPR;                     // chunks per LDS stage
@@ -49,8 +48,8 @@ struct GCfg {
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 5 || LOAD == 6, "tile load schedule");
-  static_assert(LOAD == 6 ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7, "tile load schedule");
+  static_assert(LOAD == 7 ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
                 "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
@@ -214,7 +213,7 @@ __device__ __forceinline__ void kk_frags_asm(uint32_t lds_addr, int buf, int kk,
   ds_read_rows<32 * C::CPR * 16>(fb, b, std::make_integer_sequence<int, C::NI>{});
 }
 
-// LOAD 5: the lo-plane fragments of A (the tile BM rows after the hi tile).
+// Pair mode: the lo-plane fragments of A (the tile BM rows after the hi tile).
 template <class C>
 __device__ __forceinline__ void kk_frags_lo_asm(uint32_t lds_addr, int buf, int kk, int lane, int wm,
                                                 Frag<bf16> (&fl)[C::MI]) {
@@ -396,67 +395,39 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
       }
     }
     __builtin_amdgcn_s_barrier();
-  } else if constexpr (C::LOAD == 5) {
+  } else if constexpr (C::LOAD == 7) {
     // Pair-aware: K steps over the KB columns of B; A rows hold [hi | lo]
-    // with the lo plane KB columns after the hi plane; every B fragment feeds
-    // acc += A_hi B + A_lo B. Otherwise as LOAD 4.
+    // with the lo plane KB columns after the hi plane, and each stage holds
+    // A_hi, A_lo and B, so every B fragment feeds acc += A_hi B + A_lo B.
+    // NSTAGE - 1 tiles are in flight: the stage of tile kt - 1 is free once
+    // the barrier inside step kt - 1 has passed, and tile kt + NSTAGE - 1 is
+    // loaded into it during the first MFMA step of tile kt, its loads
+    // interleaved with the MFMAs (a share of the step's MFMAs before each
+    // load) rather than issued by all waves in one burst. Each K step is one
+    // basic block: past the last tile the loads fetch the last tile again
+    // into the free stage (which no MFMA reads any more) and the first
+    // fragments of the next tile are read anyway (and not used), so the
+    // vmcnt wait is a constant and no register copies join two paths.
     constexpr int PT = 2 * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = 2 * C::MI + C::NI;
+    // MFMAs of one step, and how many go before each load
+    constexpr int NMMA = 2 * C::MI * C::NI, R = NMMA >= PT ? NMMA / PT : 1, NG = NMMA >= PT ? PT : NMMA;
+    constexpr int PRE = NS - 1;  // tiles loaded before the loop
     const int nk5 = KB / C::BK;
     const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-      if (s < nk5)
-        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, s * C::BK, s * C::BK, lds, s, wave, lane, KB);
-    wait_tiles<PT, NS - 1>(min(NS - 1, nk5 - 1));
-    __builtin_amdgcn_s_barrier();
-    Frag<bf16> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
-    kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
-    kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
-    for (int kt = 0; kt < nk5; ++kt) {
-      const int st = kt % NS;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int cur = kk & 1, nx = cur ^ 1;
-        if (kk + 1 < KK) {
-          kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
-          kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
-          wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
-        } else if (kt + 1 < nk5) {
-          wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 2 - kt));
-          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
-          __builtin_amdgcn_s_barrier();
-          const int kn = kt + NS;
-          if (kn < nk5)
-            tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn * C::BK, kn * C::BK, lds, st, wave, lane, KB);
-          kk_frags_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, wn, fa[nx], fb[nx]);
-          kk_frags_lo_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, fl[nx]);
-        } else {
-          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
-        }
-        kk_mma<C>(fa[cur], fb[cur], acc);
-        kk_mma<C>(fl[cur], fb[cur], acc);
-      }
+    for (int s = 0; s < PRE; ++s) {
+      const int ks = min(s, nk5 - 1) * C::BK;
+      tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, ks, ks, lds, s, wave, lane, KB);
     }
-    __builtin_amdgcn_s_barrier();
-  } else if constexpr (C::LOAD == 6) {
-    // As LOAD 5 with NSTAGE - 1 tiles in flight: the stage of tile kt - 1 is
-    // free once the barrier before tile kt has passed, so tile kt + NSTAGE - 1
-    // is loaded into it after the first MFMA step of tile kt rather than
-    // right after the barrier.
-    constexpr int PT = 2 * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = 2 * C::MI + C::NI;
-    const int nk5 = KB / C::BK;
-    const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < nk5)
-        tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, s * C::BK, s * C::BK, lds, s, wave, lane, KB);
-    wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 1));
+    wait_vmcnt<(PRE - 1) * PT>();
     __builtin_amdgcn_s_barrier();
     Frag<bf16> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
     kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
     kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
+    int st = 0, sl = NS - 1;  // stage of tile kt; stage of tile kt + NS - 1
     for (int kt = 0; kt < nk5; ++kt) {
-      const int st = kt % NS;
+      const int kn = min(kt + PRE, nk5 - 1) * C::BK;
+      const int snext = st + 1 == NS ? 0 : st + 1;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         const int cur = kk & 1, nx = cur ^ 1;
@@ -464,26 +435,37 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
           kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
           kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
           wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
-        } else if (kt + 1 < nk5) {
-          // tiles issued after kt + 1: kt + 2 .. min(kt + NS - 1, nk - 1)
-          wait_tiles<PT, NS - 2>(min(NS - 2, nk5 - 2 - kt));
+        } else {
+          // own loads of tile kt + 1 have landed; after the barrier every
+          // wave's have, and no wave reads stage kt any more
+          wait_vmcnt<(NS - 2) * PT>();
           wait_frags<0>(fa[cur], fl[cur], fb[cur]);
           __builtin_amdgcn_s_barrier();
-          kk_frags_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, wn, fa[nx], fb[nx]);
-          kk_frags_lo_asm<C>(lds_addr, (kt + 1) % NS, 0, lane, wm, fl[nx]);
-        } else {
-          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+          kk_frags_asm<C>(lds_addr, snext, 0, lane, wm, wn, fa[nx], fb[nx]);
+          kk_frags_lo_asm<C>(lds_addr, snext, 0, lane, wm, fl[nx]);
         }
-        kk_mma<C>(fa[cur], fb[cur], acc);
-        kk_mma<C>(fl[cur], fb[cur], acc);
         if (kk == 0) {
-          const int kn = kt + NS - 1;
-          if (kn < nk5)
-            tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn * C::BK, kn * C::BK, lds, kn % NS, wave, lane,
-                                 KB);
+          __builtin_amdgcn_sched_barrier(0);
+          kk_mma<C>(fa[cur], fb[cur], acc);
+          kk_mma<C>(fl[cur], fb[cur], acc);
+          tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn, kn, lds, sl, wave, lane, KB);
+#pragma unroll
+          for (int i = 0; i < PT; ++i) {
+            if (i < NG) __builtin_amdgcn_sched_group_barrier(0x008, R, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);              // VMEM read
+          }
+          if constexpr (NMMA > R * NG) __builtin_amdgcn_sched_group_barrier(0x008, NMMA - R * NG, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        } else {
+          kk_mma<C>(fa[cur], fb[cur], acc);
+          kk_mma<C>(fl[cur], fb[cur], acc);
+          __builtin_amdgcn_sched_barrier(0);  // the step's MFMAs stay on their side of the barrier
         }
       }
+      st = snext;
+      sl = sl + 1 == NS ? 0 : sl + 1;
     }
+    wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
   }
 }

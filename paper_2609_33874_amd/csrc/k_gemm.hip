@@ -171,13 +171,13 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
 // of 64 KB), the 256x128 tiles with three stages.
 using BigB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 // Pair mode: the (hi, lo) planes of A and one B tile per 32-column stage
-// (3 x 16 KB, three stages, two tiles in flight, each tile's loads issued
-// after the first MFMA step of the step before), waves of 64 x 128 so each B
+// (3 x 16 KB, three stages, two tiles in flight, each tile's loads spread
+// over the first MFMA step of the step before), waves of 64 x 128 so each B
 // fragment serves both planes.
-using PairB = GCfg<bf16, 256, 256, 64, 128, 6, 2, 3, 4>;
+using PairB = GCfg<bf16, 256, 256, 64, 128, 7, 2, 3, 4>;
 // ... and for problems with fewer tiles: 128x128 tiles (8 waves of 32x64,
 // three 24 KB stages, two workgroups per CU).
-using PairS = GCfg<bf16, 128, 128, 32, 64, 5, 2, 3, 4>;
+using PairS = GCfg<bf16, 128, 128, 32, 64, 7, 2, 3, 4>;
 using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
 using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
