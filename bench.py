@@ -122,6 +122,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="dense_1p5b_k4")
+    ap.add_argument("--dtype", choices=["f16", "bf16"], default="f16",
+                    help="f16: bf16 weights held exactly as fp16, fp16 activations (one fp16 product per "
+                         "multiply); bf16: bf16 products over (hi, lo) bf16 activation pairs")
     ap.add_argument("--unshared-steps", type=int, default=None,
                     help="steps of unshared (per-candidate prefix) evaluation for the reuse speedup; "
                          "0 = skip; default 2 on dense_1p5b_k4, else 0")
@@ -161,7 +164,8 @@ def main() -> int:
     stream = torch.cuda.current_stream(dev)
     flags = 0 if args.no_timing else J.JET_FLAG_KERNEL_TIMING
     t = time.perf_counter()
-    model = J.jet_model_load(path, dtype=J.JET_BF16, device=0, hip_stream=stream.cuda_stream, flags=flags)
+    jdt = J.JET_F16 if args.dtype == "f16" else J.JET_BF16
+    model = J.jet_model_load(path, dtype=jdt, device=0, hip_stream=stream.cuda_stream, flags=flags)
     log(f"model loaded in {time.perf_counter() - t:.1f}s")
 
     def make_inputs(w):
@@ -241,7 +245,7 @@ def main() -> int:
         "metric": "questions/sec & scored tokens/sec on 1 MI355X; LM-head+GEMM % MFMA peak",
         "value": round(qps, 3), "unit": "questions/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": args.dtype, "data": "synthetic",
         "config": describe(wname),
         "scored_tokens_per_s": round(T_c * args.steps / elapsed, 1),
         "prefix_tokens_per_s": round(T_p * args.steps / phase["prefill"], 1),

@@ -58,8 +58,13 @@ enum {
  * bf16 pairs (value = hi + lo) so that rounding does not accumulate through
  * deep stacks (fp32 accumulation throughout). JET_FP32: fp32 everything
  * (validation mode). JET_BF16_SINGLE: single bf16 activations and caches;
- * faster, with rounding that grows with depth. */
-enum { JET_BF16 = 0, JET_FP32 = 1, JET_BF16_SINGLE = 2 };
+ * faster, with rounding that grows with depth. JET_F16: the bf16 weights are
+ * held as fp16 (each matrix times a power of two, which makes the conversion
+ * exact), and activations, caches and probabilities are single fp16 values
+ * (11 significant bits against bf16's 8), so every product is one fp16
+ * matrix-core operation at the bf16 rate with fp32 accumulation; needs a bf16
+ * model file. */
+enum { JET_BF16 = 0, JET_FP32 = 1, JET_BF16_SINGLE = 2, JET_F16 = 3 };
 enum { JET_CHOICE = 0, JET_BINARY = 1, JET_ORDINAL = 2 }; /* decision rule */
 
 /* flags for jet_load_opts.flags */
@@ -71,7 +76,7 @@ typedef struct jet_model jet_model;
 typedef struct jet_prefix jet_prefix;
 
 typedef struct {
-  int32_t dtype;                /* JET_BF16, JET_FP32 or JET_BF16_SINGLE (see above) */
+  int32_t dtype;                /* JET_BF16, JET_FP32, JET_BF16_SINGLE or JET_F16 (see above) */
   int32_t device;               /* HIP device ordinal */
   int64_t max_ctx;              /* max positions per sequence; 0 = the file's value */
   int64_t prefill_token_budget; /* max prefix tokens per prefill wave; 0 = no limit.

@@ -6,8 +6,8 @@
 //   A[row = l % 32][k0 + 8 * (l / 32) + j],  B[col = l % 32][k0 + 8 * (l / 32) + j]
 // for j = 0..7 (16 K elements per call), and for a 16x16 product
 //   A[row = l % 16][k0 + 8 * (l / 16) + j],  B[col = l % 16][k0 + 8 * (l / 16) + j]
-// (32 K elements per call). In bf16 this is exactly one
-// v_mfma_f32_32x32x16_bf16 / v_mfma_f32_16x16x32_bf16. In fp32 the same
+// (32 K elements per call). In bf16 (fp16) this is exactly one
+// v_mfma_f32_32x32x16_bf16 (_f16) / v_mfma_f32_16x16x32_bf16 (_f16). In fp32 the same
 // registers feed eight v_mfma_f32_32x32x2f32 / v_mfma_f32_16x16x4f32, call j
 // taking element j of every lane, so both dtypes share all indexing code.
 // Accumulator layouts: 32x32: acc[e] = C[8*(e/4) + 4*(l/32) + e%4][l % 32];
@@ -20,7 +20,9 @@
 namespace jetk {
 
 typedef uint16_t bf16;  // bfloat16 bits in memory
+typedef _Float16 f16;   // IEEE binary16
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -38,13 +40,32 @@ __device__ __forceinline__ uint32_t f2bf2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
+// Two floats -> two binary16 values in one 32-bit word (a in the low half),
+// round to nearest even.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f2h2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
+}
+
 template <typename T> __device__ __forceinline__ float to_f(T v);
 template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ float to_f<bf16>(bf16 v) { return bf2f(v); }
+template <> __device__ __forceinline__ float to_f<f16>(f16 v) { return (float)v; }
 
 template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return f2bf(v); }
+template <> __device__ __forceinline__ f16 from_f<f16>(float v) { return (f16)v; }
+
+// Two floats -> two 16-bit values of type T in one 32-bit word.
+template <typename T> __device__ __forceinline__ uint32_t pack2(float a, float b);
+template <> __device__ __forceinline__ uint32_t pack2<bf16>(float a, float b) { return f2bf2(a, b); }
+template <> __device__ __forceinline__ uint32_t pack2<f16>(float a, float b) { return f2h2(a, b); }
+
+// The 8-element vector type of a 16-bit storage type (MFMA operands).
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16> { typedef bf16x8 type; };
+template <> struct Vec8<f16> { typedef f16x8 type; };
 
 // Eight consecutive K elements of one lane.
 template <typename T> struct Frag;
@@ -52,6 +73,12 @@ template <> struct Frag<bf16> {
   bf16x8 v;
   __device__ __forceinline__ void zero() {
     for (int j = 0; j < 8; ++j) v[j] = (__bf16)0.0f;
+  }
+};
+template <> struct Frag<f16> {
+  f16x8 v;
+  __device__ __forceinline__ void zero() {
+    for (int j = 0; j < 8; ++j) v[j] = (_Float16)0.0f;
   }
 };
 template <> struct Frag<float> {
@@ -64,12 +91,18 @@ template <> struct Frag<float> {
 __device__ __forceinline__ void mma32(f32x16 &acc, const Frag<bf16> &a, const Frag<bf16> &b) {
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v, b.v, acc, 0, 0, 0);
 }
+__device__ __forceinline__ void mma32(f32x16 &acc, const Frag<f16> &a, const Frag<f16> &b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.v, b.v, acc, 0, 0, 0);
+}
 __device__ __forceinline__ void mma32(f32x16 &acc, const Frag<float> &a, const Frag<float> &b) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[j], b.v[j], acc, 0, 0, 0);
 }
 __device__ __forceinline__ void mma16(f32x4 &acc, const Frag<bf16> &a, const Frag<bf16> &b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma16(f32x4 &acc, const Frag<f16> &a, const Frag<f16> &b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.v, b.v, acc, 0, 0, 0);
 }
 __device__ __forceinline__ void mma16(f32x4 &acc, const Frag<float> &a, const Frag<float> &b) {
 #pragma unroll
@@ -84,6 +117,10 @@ __device__ __forceinline__ void st16(void *p, uint4 v) { *reinterpret_cast<uint4
 __device__ __forceinline__ void frag_load(Frag<bf16> &f, const bf16 *p) {
   uint4 u = ld16(p);
   f.v = __builtin_bit_cast(bf16x8, u);
+}
+__device__ __forceinline__ void frag_load(Frag<f16> &f, const f16 *p) {
+  uint4 u = ld16(p);
+  f.v = __builtin_bit_cast(f16x8, u);
 }
 __device__ __forceinline__ void frag_load(Frag<float> &f, const float *p) {
   uint4 a = ld16(p), b = ld16(p + 4);

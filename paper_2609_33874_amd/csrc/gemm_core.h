@@ -17,7 +17,8 @@
 //   LOAD 7  for a (hi, lo) pair A operand: a stage holds the hi and lo tiles
 //           of A and one B tile, so every B fragment feeds both products;
 //           NSTAGE - 1 K steps in flight, each step's loads interleaved with
-//           the MFMAs of the step before it (fixed by scheduling groups).
+//           the MFMAs of the step before it (fixed by scheduling groups);
+//   LOAD 8  the LOAD 7 schedule for a plain (single-plane) A operand.
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
@@ -40,6 +41,7 @@ struct GCfg {
   static constexpr int BK = CPR * EPC;              // elements per K step
   // LOAD 7 (pair-aware): A holds (hi, lo) planes and both are staged, B once
   static constexpr bool PAIRA = LOAD == 7;
+  static constexpr bool INTERLEAVED = LOAD == 7 || LOAD == 8;  // the LOAD 7 / 8 schedule
   static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
   static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step (per plane)
   static constexpr int BUF = (BROW0 + BN) * CPR;                     // chunks per LDS stage
@@ -48,8 +50,8 @@ struct GCfg {
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7, "tile load schedule");
-  static_assert(LOAD == 7 ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8, "tile load schedule");
+  static_assert(INTERLEAVED ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
                 "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
@@ -69,6 +71,10 @@ __device__ __forceinline__ void lds_frag(Frag<T> &f, const uint4 *row, int c0, i
 template <>
 __device__ __forceinline__ void lds_frag<bf16>(Frag<bf16> &f, const uint4 *row, int c0, int swz) {
   f.v = __builtin_bit_cast(bf16x8, row[c0 ^ swz]);
+}
+template <>
+__device__ __forceinline__ void lds_frag<f16>(Frag<f16> &f, const uint4 *row, int c0, int swz) {
+  f.v = __builtin_bit_cast(f16x8, row[c0 ^ swz]);
 }
 template <>
 __device__ __forceinline__ void lds_frag<float>(Frag<float> &f, const uint4 *row, int c0, int swz) {
@@ -92,21 +98,21 @@ __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcn
 // LDS reads issued as inline asm, so that their completion is waited for
 // explicitly (wait_frags) instead of by the compiler's conservative
 // lgkmcnt(0) in front of the first use. The offset is an immediate.
-template <int OFF>
-__device__ __forceinline__ void ds_read16(bf16x8 &v, uint32_t addr) {
+template <int OFF, typename V>
+__device__ __forceinline__ void ds_read16(V &v, uint32_t addr) {
   static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
 }
 
-template <int STRIDE, int N, int... I>
-__device__ __forceinline__ void ds_read_rows(Frag<bf16> (&f)[N], uint32_t addr, std::integer_sequence<int, I...>) {
+template <int STRIDE, typename T, int N, int... I>
+__device__ __forceinline__ void ds_read_rows(Frag<T> (&f)[N], uint32_t addr, std::integer_sequence<int, I...>) {
   (ds_read16<I * STRIDE>(f[I].v, addr), ...);
 }
 
 // Waits until at most N LDS reads are in flight, then ties the fragments to
 // that wait so that no use of them is scheduled above it.
-template <int N, int MI, int NI>
-__device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fb)[NI]) {
+template <int N, typename T, int MI, int NI>
+__device__ __forceinline__ void wait_frags(Frag<T> (&fa)[MI], Frag<T> (&fb)[NI]) {
   asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
 #pragma unroll
   for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v));
@@ -114,8 +120,8 @@ __device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fb
   for (int j = 0; j < NI; ++j) asm volatile("" : "+v"(fb[j].v));
 }
 
-template <int N, int MI, int NI>
-__device__ __forceinline__ void wait_frags(Frag<bf16> (&fa)[MI], Frag<bf16> (&fl)[MI], Frag<bf16> (&fb)[NI]) {
+template <int N, typename T, int MI, int NI>
+__device__ __forceinline__ void wait_frags(Frag<T> (&fa)[MI], Frag<T> (&fl)[MI], Frag<T> (&fb)[NI]) {
   asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
 #pragma unroll
   for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v), "+v"(fl[i].v));
@@ -197,13 +203,14 @@ __device__ __forceinline__ void tile_compute(const uint4 *__restrict__ lds, int 
   }
 }
 
-// Fragments of MFMA step kk of stage `buf`, read as inline asm (bf16): one base
-// address per operand, the 32-row blocks at immediate offsets (the swizzle
-// depends on the row modulo 32 only).
+// Fragments of MFMA step kk of stage `buf`, read as inline asm (16-bit types):
+// one base address per operand, the 32-row blocks at immediate offsets (the
+// swizzle depends on the row modulo 32 only).
 template <class C>
 __device__ __forceinline__ void kk_frags_asm(uint32_t lds_addr, int buf, int kk, int lane, int wm, int wn,
-                                             Frag<bf16> (&fa)[C::MI], Frag<bf16> (&fb)[C::NI]) {
-  static_assert(sizeof(typename C::type) == 2, "asm fragment reads are bf16 only");
+                                             Frag<typename C::type> (&fa)[C::MI],
+                                             Frag<typename C::type> (&fb)[C::NI]) {
+  static_assert(sizeof(typename C::type) == 2, "asm fragment reads are 16-bit only");
   const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
   const int ra = wm * C::WM + (lane & 31), rb = C::BROW0 + wn * C::WN + (lane & 31);
   const uint32_t stage = lds_addr + (uint32_t)(buf * C::BUF) * 16u;
@@ -216,7 +223,7 @@ __device__ __forceinline__ void kk_frags_asm(uint32_t lds_addr, int buf, int kk,
 // Pair mode: the lo-plane fragments of A (the tile BM rows after the hi tile).
 template <class C>
 __device__ __forceinline__ void kk_frags_lo_asm(uint32_t lds_addr, int buf, int kk, int lane, int wm,
-                                                Frag<bf16> (&fl)[C::MI]) {
+                                                Frag<typename C::type> (&fl)[C::MI]) {
   const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
   const int ra = wm * C::WM + (lane & 31);
   const uint32_t a = lds_addr + (uint32_t)(buf * C::BUF + (C::BM + ra) * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
@@ -368,7 +375,7 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
                              lane);
     wait_tiles<PT, NS - 1>(min(NS - 1, nk - 1));
     __builtin_amdgcn_s_barrier();
-    Frag<bf16> fa[2][C::MI], fb[2][C::NI];
+    Frag<typename C::type> fa[2][C::MI], fb[2][C::NI];
     kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
     for (int kt = 0; kt < nk; ++kt) {
       const int st = kt % NS;
@@ -395,10 +402,11 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
       }
     }
     __builtin_amdgcn_s_barrier();
-  } else if constexpr (C::LOAD == 7) {
+  } else if constexpr (C::INTERLEAVED) {
     // Pair-aware: K steps over the KB columns of B; A rows hold [hi | lo]
     // with the lo plane KB columns after the hi plane, and each stage holds
     // A_hi, A_lo and B, so every B fragment feeds acc += A_hi B + A_lo B.
+    // (LOAD 8: A is a single plane, the lo parts drop out.)
     // NSTAGE - 1 tiles are in flight: the stage of tile kt - 1 is free once
     // the barrier inside step kt - 1 has passed, and tile kt + NSTAGE - 1 is
     // loaded into it during the first MFMA step of tile kt, its loads
@@ -408,9 +416,10 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
     // into the free stage (which no MFMA reads any more) and the first
     // fragments of the next tile are read anyway (and not used), so the
     // vmcnt wait is a constant and no register copies join two paths.
-    constexpr int PT = 2 * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = 2 * C::MI + C::NI;
+    constexpr int NPL = C::PAIRA ? 2 : 1;  // planes of A
+    constexpr int PT = NPL * C::A_PT + C::B_PT, NS = C::NSTAGE, KK = C::BK / 16, NR = NPL * C::MI + C::NI;
     // MFMAs of one step, and how many go before each load
-    constexpr int NMMA = 2 * C::MI * C::NI, R = NMMA >= PT ? NMMA / PT : 1, NG = NMMA >= PT ? PT : NMMA;
+    constexpr int NMMA = NPL * C::MI * C::NI, R = NMMA >= PT ? NMMA / PT : 1, NG = NMMA >= PT ? PT : NMMA;
     constexpr int PRE = NS - 1;  // tiles loaded before the loop
     const int nk5 = KB / C::BK;
     const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
@@ -421,9 +430,9 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
     }
     wait_vmcnt<(PRE - 1) * PT>();
     __builtin_amdgcn_s_barrier();
-    Frag<bf16> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
+    Frag<typename C::type> fa[2][C::MI], fl[2][C::MI], fb[2][C::NI];
     kk_frags_asm<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], fb[0]);
-    kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
+    if constexpr (C::PAIRA) kk_frags_lo_asm<C>(lds_addr, 0, 0, lane, wm, fl[0]);
     int st = 0, sl = NS - 1;  // stage of tile kt; stage of tile kt + NS - 1
     for (int kt = 0; kt < nk5; ++kt) {
       const int kn = min(kt + PRE, nk5 - 1) * C::BK;
@@ -433,21 +442,26 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
         const int cur = kk & 1, nx = cur ^ 1;
         if (kk + 1 < KK) {
           kk_frags_asm<C>(lds_addr, st, kk + 1, lane, wm, wn, fa[nx], fb[nx]);
-          kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
-          wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
+          if constexpr (C::PAIRA) {
+            kk_frags_lo_asm<C>(lds_addr, st, kk + 1, lane, wm, fl[nx]);
+            wait_frags<NR>(fa[cur], fl[cur], fb[cur]);
+          } else {
+            wait_frags<NR>(fa[cur], fb[cur]);
+          }
         } else {
           // own loads of tile kt + 1 have landed; after the barrier every
           // wave's have, and no wave reads stage kt any more
           wait_vmcnt<(NS - 2) * PT>();
-          wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+          if constexpr (C::PAIRA) wait_frags<0>(fa[cur], fl[cur], fb[cur]);
+          else wait_frags<0>(fa[cur], fb[cur]);
           __builtin_amdgcn_s_barrier();
           kk_frags_asm<C>(lds_addr, snext, 0, lane, wm, wn, fa[nx], fb[nx]);
-          kk_frags_lo_asm<C>(lds_addr, snext, 0, lane, wm, fl[nx]);
+          if constexpr (C::PAIRA) kk_frags_lo_asm<C>(lds_addr, snext, 0, lane, wm, fl[nx]);
         }
         if (kk == 0) {
           __builtin_amdgcn_sched_barrier(0);
           kk_mma<C>(fa[cur], fb[cur], acc);
-          kk_mma<C>(fl[cur], fb[cur], acc);
+          if constexpr (C::PAIRA) kk_mma<C>(fl[cur], fb[cur], acc);
           tile_issue_direct<C>(A, lda, B, ldb, M, N, m0, n0, kn, kn, lds, sl, wave, lane, KB);
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
@@ -458,7 +472,7 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
           __builtin_amdgcn_sched_barrier(0);
         } else {
           kk_mma<C>(fa[cur], fb[cur], acc);
-          kk_mma<C>(fl[cur], fb[cur], acc);
+          if constexpr (C::PAIRA) kk_mma<C>(fl[cur], fb[cur], acc);
           __builtin_amdgcn_sched_barrier(0);  // the step's MFMAs stay on their side of the barrier
         }
       }

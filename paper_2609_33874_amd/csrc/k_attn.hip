@@ -26,11 +26,11 @@
 
 namespace jetk {
 
-template <typename T> __device__ __forceinline__ Frag<T> pack8(const float (&x)[8]);
-template <> __device__ __forceinline__ Frag<bf16> pack8<bf16>(const float (&x)[8]) {
-  Frag<bf16> f;
-  const uint4 u = make_uint4(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]), f2bf2(x[4], x[5]), f2bf2(x[6], x[7]));
-  f.v = __builtin_bit_cast(bf16x8, u);
+template <typename T> __device__ __forceinline__ Frag<T> pack8(const float (&x)[8]) {
+  static_assert(sizeof(T) == 2, "16-bit types");
+  Frag<T> f;
+  const uint4 u = make_uint4(pack2<T>(x[0], x[1]), pack2<T>(x[2], x[3]), pack2<T>(x[4], x[5]), pack2<T>(x[6], x[7]));
+  f.v = __builtin_bit_cast(typename Vec8<T>::type, u);
   return f;
 }
 template <> __device__ __forceinline__ Frag<float> pack8<float>(const float (&x)[8]) {
@@ -41,10 +41,9 @@ template <> __device__ __forceinline__ Frag<float> pack8<float>(const float (&x)
 }
 
 template <typename T>
-__device__ __forceinline__ void lds_kfrag(Frag<T> &f, const uint4 *row, int c0, int swz);
-template <>
-__device__ __forceinline__ void lds_kfrag<bf16>(Frag<bf16> &f, const uint4 *row, int c0, int swz) {
-  f.v = __builtin_bit_cast(bf16x8, row[c0 ^ swz]);
+__device__ __forceinline__ void lds_kfrag(Frag<T> &f, const uint4 *row, int c0, int swz) {
+  static_assert(sizeof(T) == 2, "16-bit types");
+  f.v = __builtin_bit_cast(typename Vec8<T>::type, row[c0 ^ swz]);
 }
 template <>
 __device__ __forceinline__ void lds_kfrag<float>(Frag<float> &f, const uint4 *row, int c0, int swz) {
@@ -63,11 +62,13 @@ __device__ __forceinline__ void lds_kfrag<float>(Frag<float> &f, const uint4 *ro
 // XOR-swizzled by d so the 16 lanes of a group (16 consecutive d) hit
 // distinct banks.
 __device__ __forceinline__ int vt_unit(const bf16 *, int unit, int d) { return unit ^ ((d >> 1) & 7); }
+__device__ __forceinline__ int vt_unit(const f16 *, int unit, int d) { return unit ^ ((d >> 1) & 7); }
 __device__ __forceinline__ int vt_unit(const float *, int unit, int d) { return unit ^ (d & 15); }
 
 // Writes 4 keys 4u..4u+3 (rows r[0..3], one 16-byte chunk c of dims each).
-template <int KT>
-__device__ __forceinline__ void v_put_transposed(bf16 *vt, const uint4 (&r)[4], int u, int c) {
+template <int KT, typename T>
+__device__ __forceinline__ void v_put_transposed(T *vt, const uint4 (&r)[4], int u, int c) {
+  static_assert(sizeof(T) == 2, "16-bit types");
   const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&r[0]), *w1 = reinterpret_cast<const uint32_t *>(&r[1]);
   const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&r[2]), *w3 = reinterpret_cast<const uint32_t *>(&r[3]);
   const int unit = 4 * (u >> 3) + (u & 3), half = ((u >> 2) & 1) * 4;  // 8-element unit, 4-key half
@@ -94,9 +95,11 @@ __device__ __forceinline__ void v_put_transposed(float *vt, const uint4 (&r)[4],
 }
 
 // PV operand of lane group g for dim d and key half mm (see the layout above).
-template <int KT>
-__device__ __forceinline__ void v_frag(Frag<bf16> &f, const bf16 *vt, int d, int mm, int g) {
-  f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(vt + d * KT + (vt_unit(vt, 4 * mm + g, d) << 3)));
+template <int KT, typename T>
+__device__ __forceinline__ void v_frag(Frag<T> &f, const T *vt, int d, int mm, int g) {
+  static_assert(sizeof(T) == 2, "16-bit types");
+  f.v = __builtin_bit_cast(typename Vec8<T>::type,
+                           *reinterpret_cast<const uint4 *>(vt + d * KT + (vt_unit(vt, 4 * mm + g, d) << 3)));
 }
 template <int KT>
 __device__ __forceinline__ void v_frag(Frag<float> &f, const float *vt, int d, int mm, int g) {
@@ -379,7 +382,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     for (int e = 0; e < 4; ++e) o[e] = acc[db][e] * inv;
     T *dst = O + (int64_t)row * a.o_ld + (int64_t)head * HD + db * 16 + 4 * g;
     if constexpr (sizeof(T) == 2) {
-      const uint2 hi = make_uint2(f2bf2(o[0], o[1]), f2bf2(o[2], o[3]));
+      const uint2 hi = make_uint2(pack2<T>(o[0], o[1]), pack2<T>(o[2], o[3]));
       *reinterpret_cast<uint2 *>(dst) = hi;
       if constexpr (PAIR) {
 #pragma unroll
@@ -411,6 +414,11 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st) {
       if (a.hd == 64) return run_attn<bf16, 64, false>(a, st);
       if (a.hd == 32) return run_attn<bf16, 32, false>(a, st);
     }
+  } else if (dtype == 2) {
+    if (a.pair) return hipErrorInvalidValue;
+    if (a.hd == 128) return run_attn<f16, 128, false>(a, st);
+    if (a.hd == 64) return run_attn<f16, 64, false>(a, st);
+    if (a.hd == 32) return run_attn<f16, 32, false>(a, st);
   } else {
     if (a.hd == 128) return run_attn<float, 128, false>(a, st);
     if (a.hd == 64) return run_attn<float, 64, false>(a, st);

@@ -187,6 +187,9 @@ hipError_t launch_gdn_out(int dtype, int pair, const float *o, const float *x, i
   else if (dtype == 0)
     hipLaunchKernelGGL((gdn_out_kernel<bf16, false>), dim3(R), dim3(256), 0, st, o, x, ldx, zoff, w, eps, H, dv,
                        (bf16 *)y);
+  else if (dtype == 2)
+    hipLaunchKernelGGL((gdn_out_kernel<f16, false>), dim3(R), dim3(256), 0, st, o, x, ldx, zoff, w, eps, H, dv,
+                       (f16 *)y);
   else
     hipLaunchKernelGGL((gdn_out_kernel<float, false>), dim3(R), dim3(256), 0, st, o, x, ldx, zoff, w, eps, H, dv,
                        (float *)y);

@@ -26,6 +26,7 @@ struct GemmArgs {
   void *out;
   int64_t ldo;
   int pair_out;   // SwiGLU: write (hi, lo) bf16 pairs, hi at column f, lo at N/2 + f
+  float oscale;   // every product is multiplied by oscale before the epilogue
 };
 
 // EPI: 0 = store fp32, 1 = fp32 residual add, 2 = SwiGLU into T (B rows
@@ -54,7 +55,7 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
           if (row < g.M && gcol < g.N) {
-            const float gt = acc[i][2 * jp][e], up = acc[i][2 * jp + 1][e];
+            const float gt = acc[i][2 * jp][e] * g.oscale, up = acc[i][2 * jp + 1][e] * g.oscale;
             // silu(g) = g / (1 + e^-g) with the hardware reciprocal (~1 ulp)
             const float v = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
             const T hi = from_f<T>(v);
@@ -74,9 +75,10 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
           const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
           if (row >= g.M || col >= g.N) continue;
           const int64_t o = (int64_t)row * g.ldo + col;
-          if constexpr (EPI == 0) ((float *)g.out)[o] = acc[i][j][e];
-          else if constexpr (EPI == 1) ((float *)g.out)[o] += acc[i][j][e];
-          else ((T *)g.out)[o] = from_f<T>(acc[i][j][e]);
+          const float v = acc[i][j][e] * g.oscale;
+          if constexpr (EPI == 0) ((float *)g.out)[o] = v;
+          else if constexpr (EPI == 1) ((float *)g.out)[o] += v;
+          else ((T *)g.out)[o] = from_f<T>(v);
         }
       }
   }
@@ -91,7 +93,7 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
 template <class C>
 __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::type *__restrict__ W,
                                                           const typename C::type *__restrict__ F, int V, int R,
-                                                          int KW, int K, int tiles_per_split,
+                                                          int KW, int K, int tiles_per_split, float zscale,
                                                           float *__restrict__ part_m, float *__restrict__ part_s) {
   extern __shared__ uint4 lds[];
   const int n0 = blockIdx.x * C::BN, split = blockIdx.y;
@@ -117,7 +119,7 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int v = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          const float z = v < V ? acc[i][j][e] * kLog2e : -INFINITY;
+          const float z = v < V ? acc[i][j][e] * zscale : -INFINITY;
           acc[i][j][e] = z;
           mx = fmaxf(mx, z);
         }
@@ -182,6 +184,12 @@ using SmallB = GCfg<bf16, 256, 128, 64, 64, 2, 1, 3, 8>;
 using CfgF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 using LmF = GCfg<float, 128, 128, 64, 64, 0, 1>;
+// fp16 operands: the LOAD 7 schedule with a single A plane (three 32 KB
+// stages of 32-column A and B tiles), 256x256 tiles with waves of 64 x 128,
+// or 128x128 tiles for problems with fewer tiles; the LM head as in bf16.
+using HalfB = GCfg<f16, 256, 256, 64, 128, 8, 2, 3, 4>;
+using HalfS = GCfg<f16, 128, 128, 32, 64, 8, 2, 3, 4>;
+using LmH = GCfg<f16, 256, 256, 128, 64, 4, 1, 2, 8>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
 template <class C>
@@ -192,11 +200,12 @@ static hipError_t allow_lds(const void *fn) {
 
 template <class C, int EPI>
 static hipError_t run_gemm(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K, int pair,
-                           void *out, int64_t ldo, hipStream_t st) {
+                           void *out, int64_t ldo, float oscale, hipStream_t st) {
   using T = typename C::type;
   static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
   if (once != hipSuccess) return once;
-  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, pair ? 2 * K : K, pair ? 2 * K : K, K, out, ldo, pair};
+  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, pair ? 2 * K : K, pair ? 2 * K : K, K, out, ldo, pair,
+                oscale};
   const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
   return hipGetLastError();
@@ -204,30 +213,35 @@ static hipError_t run_gemm(const void *A, int64_t lda, const void *B, int64_t ld
 
 template <class C>
 static hipError_t run_epi(int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
-                          int pair, void *out, int64_t ldo, hipStream_t st) {
+                          int pair, void *out, int64_t ldo, float oscale, hipStream_t st) {
   switch (epi) {
-    case EPI_STORE_F32: return run_gemm<C, 0>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
-    case EPI_RESID_ADD: return run_gemm<C, 1>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
-    case EPI_SWIGLU: return run_gemm<C, 2>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
-    default: return run_gemm<C, 3>(A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+    case EPI_STORE_F32: return run_gemm<C, 0>(A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
+    case EPI_RESID_ADD: return run_gemm<C, 1>(A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
+    case EPI_SWIGLU: return run_gemm<C, 2>(A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
+    default: return run_gemm<C, 3>(A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
   }
 }
 
-int gemm_k_step(int dtype) { return dtype == 0 ? BigB::BK : CfgF::BK; }
+int gemm_k_step(int dtype) { return dtype == 1 ? CfgF::BK : BigB::BK; }
 
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N,
-                       int K, int pair, void *out, int64_t ldo, hipStream_t st) {
+                       int K, int pair, void *out, int64_t ldo, float oscale, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
+  // 256x256 tiles when there are enough of them to fill the chip twice over
+  const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
   if (dtype == 0) {
-    // 256x256 tiles when there are enough of them to fill the chip twice over
-    const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
     if (pair)
-      return big_tiles >= 512 ? run_epi<PairB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st)
-                              : run_epi<PairS>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
-    if (big_tiles >= 512) return run_epi<BigB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
-    return run_epi<SmallB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, st);
+      return big_tiles >= 512 ? run_epi<PairB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st)
+                              : run_epi<PairS>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
+    if (big_tiles >= 512) return run_epi<BigB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
+    return run_epi<SmallB>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
   }
-  return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, st);
+  if (dtype == 2) {
+    if (pair) return hipErrorInvalidValue;
+    return big_tiles >= 512 ? run_epi<HalfB>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st)
+                            : run_epi<HalfS>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+  }
+  return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
 }
 
 void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit) {
@@ -235,30 +249,32 @@ void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit) {
   // The split of the vocabulary depends on V only, so that a row's
   // log-sum-exp is merged in the same order whatever batch it is in; about
   // 256 splits keep even a one-row-tile launch spread over the CUs.
-  const int bm = dtype == 0 ? LmB::BM : LmF::BM;
+  const int bm = dtype == 1 ? LmF::BM : LmB::BM;
   const int vt = (V + bm - 1) / bm;
   const int tps = std::max(1, vt / 256);
   *tiles_per_split = tps;
   *nsplit = (vt + tps - 1) / tps;
 }
 
-hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
-                             int tiles_per_split, float *part_m, float *part_s, hipStream_t st) {
-  if (R <= 0) return hipSuccess;
-  if (dtype == 0) {
-    static const hipError_t once = allow_lds<LmB>((const void *)lmhead_lse_kernel<LmB>);
-    if (once != hipSuccess) return once;
-    const int nsplit = ((V + LmB::BM - 1) / LmB::BM + tiles_per_split - 1) / tiles_per_split;
-    dim3 grid((R + LmB::BN - 1) / LmB::BN, nsplit);
-    hipLaunchKernelGGL((lmhead_lse_kernel<LmB>), grid, dim3(LmB::NT), LmB::LDS_BYTES, st, (const bf16 *)W,
-                       (const bf16 *)F, V, R, K, pair ? 2 * K : K, tiles_per_split, part_m, part_s);
-  } else {
-    const int nsplit = ((V + LmF::BM - 1) / LmF::BM + tiles_per_split - 1) / tiles_per_split;
-    dim3 grid((R + LmF::BN - 1) / LmF::BN, nsplit);
-    hipLaunchKernelGGL((lmhead_lse_kernel<LmF>), grid, dim3(LmF::NT), LmF::LDS_BYTES, st, (const float *)W,
-                       (const float *)F, V, R, K, K, tiles_per_split, part_m, part_s);
-  }
+template <class C>
+static hipError_t run_lmhead(const void *W, const void *F, int V, int R, int K, int pair, int tiles_per_split,
+                             float wscale, float *part_m, float *part_s, hipStream_t st) {
+  using T = typename C::type;
+  static const hipError_t once = allow_lds<C>((const void *)lmhead_lse_kernel<C>);
+  if (once != hipSuccess) return once;
+  const int nsplit = ((V + C::BM - 1) / C::BM + tiles_per_split - 1) / tiles_per_split;
+  dim3 grid((R + C::BN - 1) / C::BN, nsplit);
+  hipLaunchKernelGGL((lmhead_lse_kernel<C>), grid, dim3(C::NT), C::LDS_BYTES, st, (const T *)W, (const T *)F, V, R,
+                     K, pair ? 2 * K : K, tiles_per_split, wscale * kLog2e, part_m, part_s);
   return hipGetLastError();
+}
+
+hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
+                             int tiles_per_split, float wscale, float *part_m, float *part_s, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0) return run_lmhead<LmB>(W, F, V, R, K, pair, tiles_per_split, wscale, part_m, part_s, st);
+  if (dtype == 2) return run_lmhead<LmH>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, st);
+  return run_lmhead<LmF>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, st);
 }
 
 }  // namespace jetk

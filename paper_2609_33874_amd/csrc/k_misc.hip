@@ -108,7 +108,7 @@ __global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__re
                                                               const float *__restrict__ lse_body,
                                                               const T *__restrict__ f_last,
                                                               const float *__restrict__ lse_last,
-                                                              const T *__restrict__ W, int d,
+                                                              const T *__restrict__ W, int d, float wscale,
                                                               float *__restrict__ ell) {
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__re
     acc += fv * to_f<T>(w[k]);
   }
   acc = warp_sum(acc);
-  if (lane == 0) ell[i] = acc - lse;
+  if (lane == 0) ell[i] = acc * wscale - lse;
 }
 
 __global__ __launch_bounds__(256) void segment_sum_kernel(const float *__restrict__ ell, const int64_t *__restrict__ off,
@@ -160,6 +160,12 @@ __global__ __launch_bounds__(256) void convert_f32_kernel(const float *__restric
     dst[i] = from_f<T>(src[i]);
 }
 
+__global__ __launch_bounds__(256) void bf16_to_f16_kernel(const uint16_t *__restrict__ src, int64_t n, float scale,
+                                                           f16 *__restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = (f16)(bf2f(src[i]) * scale);
+}
+
 __global__ __launch_bounds__(256) void bf16_to_f32_kernel(const uint16_t *__restrict__ src, int64_t n,
                                                            float *__restrict__ dst) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
@@ -183,6 +189,8 @@ hipError_t launch_rmsnorm(int dtype, int pair, const float *x, const int32_t *ma
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, true>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
   else if (dtype == 0)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
+  else if (dtype == 2)
+    hipLaunchKernelGGL((rmsnorm_kernel<f16, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (f16 *)out);
   else
     hipLaunchKernelGGL((rmsnorm_kernel<float, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (float *)out);
   return hipGetLastError();
@@ -199,6 +207,9 @@ hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int3
   else if (dtype == 0)
     hipLaunchKernelGGL((rope_scatter_kernel<bf16, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
                        Hkv, hd, (bf16 *)q_out, q_ps, (bf16 *)k_cache, (bf16 *)v_cache, kv_ps, S, slot0);
+  else if (dtype == 2)
+    hipLaunchKernelGGL((rope_scatter_kernel<f16, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
+                       Hkv, hd, (f16 *)q_out, q_ps, (f16 *)k_cache, (f16 *)v_cache, kv_ps, S, slot0);
   else
     hipLaunchKernelGGL((rope_scatter_kernel<float, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
                        Hkv, hd, (float *)q_out, q_ps, (float *)k_cache, (float *)v_cache, kv_ps, S, slot0);
@@ -213,20 +224,26 @@ hipError_t launch_lse_merge(const float *pm, const float *ps, int nsplit, int R,
 
 hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
                                  int row_base, const void *f_body, const float *lse_body, const void *f_last,
-                                 const float *lse_last, const void *W, int d, float *ell, hipStream_t st) {
+                                 const float *lse_last, const void *W, int d, float wscale, float *ell,
+                                 hipStream_t st) {
   if (n_out <= 0) return hipSuccess;
   dim3 grid((n_out + 3) / 4);
   if (dtype == 0 && pair)
     hipLaunchKernelGGL((gather_logprob_kernel<bf16, true>), grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
-                       (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d, ell);
+                       (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d, wscale,
+                       ell);
   else if (dtype == 0)
     hipLaunchKernelGGL((gather_logprob_kernel<bf16, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
                        row_base, (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d,
-                       ell);
+                       wscale, ell);
+  else if (dtype == 2)
+    hipLaunchKernelGGL((gather_logprob_kernel<f16, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
+                       row_base, (const f16 *)f_body, lse_body, (const f16 *)f_last, lse_last, (const f16 *)W, d,
+                       wscale, ell);
   else
     hipLaunchKernelGGL((gather_logprob_kernel<float, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
                        row_base, (const float *)f_body, lse_body, (const float *)f_last, lse_last,
-                       (const float *)W, d, ell);
+                       (const float *)W, d, wscale, ell);
   return hipGetLastError();
 }
 
@@ -266,6 +283,13 @@ hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst,
   const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
   if (dtype == 0) hipLaunchKernelGGL(convert_f32_kernel<bf16>, dim3(blocks), dim3(256), 0, st, src, n, (bf16 *)dst);
   else hipLaunchKernelGGL(convert_f32_kernel<float>, dim3(blocks), dim3(256), 0, st, src, n, (float *)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(bf16_to_f16_kernel, dim3(blocks), dim3(256), 0, st, src, n, scale, (f16 *)dst);
   return hipGetLastError();
 }
 

@@ -1,6 +1,6 @@
 // Host-side launchers of the HIP kernels (internal to the library).
-// dtype: 0 = bf16 operands, 1 = fp32 operands. Every launcher returns the
-// launch status and enqueues work on `st` only.
+// dtype: 0 = bf16 operands, 1 = fp32 operands, 2 = fp16 operands. Every
+// launcher returns the launch status and enqueues work on `st` only.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -15,17 +15,19 @@ enum { EPI_STORE_F32 = 0, EPI_RESID_ADD = 1, EPI_SWIGLU = 2, EPI_STORE_T = 3 };
 // pair of the activations, [a_hi (K) | a_lo (K)], and C = (A_hi + A_lo) B^T.
 // EPI_SWIGLU expects B rows interleaved in blocks of 32 gate rows then 32 up
 // rows and writes silu(gate) * up to out[M x N/2] (T), or with pair to
-// out[M x N] as [hi (N/2) | lo (N/2)].
+// out[M x N] as [hi (N/2) | lo (N/2)]. Every product is multiplied by oscale
+// before the epilogue (the inverse of a power-of-two weight scale).
 int gemm_k_step(int dtype);
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
-                       int N, int K, int pair, void *out, int64_t ldo, hipStream_t st);
+                       int N, int K, int pair, void *out, int64_t ldo, float oscale, hipStream_t st);
 
 // LM head + online log-sum-exp: partial (max, sum) in base 2 per (split, row).
 // lmhead_plan gives the vocabulary tiles per workgroup and the split count.
 void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit);
-// F: [R][K] rows, or [R][2K] (hi, lo) pairs when pair.
+// F: [R][K] rows, or [R][2K] (hi, lo) pairs when pair. The logits are the
+// products times wscale.
 hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
-                             int tiles_per_split, float *part_m, float *part_s, hipStream_t st);
+                             int tiles_per_split, float wscale, float *part_m, float *part_s, hipStream_t st);
 // lse[r] = ln(sum over splits) from the partials.
 hipError_t launch_lse_merge(const float *part_m, const float *part_s, int nsplit, int R, float *lse,
                             hipStream_t st);
@@ -116,11 +118,13 @@ hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int3
                                const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, int64_t q_ps,
                                void *k_cache, void *v_cache, int64_t kv_ps, int64_t S, int64_t slot0,
                                hipStream_t st);
-// ell[i] = dot(f_row, W[y_i]) - lse_row for output i; the row is f_body[lm_row[i] - row_base]
-// or, when lm_row[i] < 0, f_last[-lm_row[i] - 1]; rows are [hi | lo] pairs when pair.
+// ell[i] = wscale * dot(f_row, W[y_i]) - lse_row for output i; the row is
+// f_body[lm_row[i] - row_base] or, when lm_row[i] < 0, f_last[-lm_row[i] - 1];
+// rows are [hi | lo] pairs when pair.
 hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
                                  int row_base, const void *f_body, const float *lse_body, const void *f_last,
-                                 const float *lse_last, const void *W, int d, float *ell, hipStream_t st);
+                                 const float *lse_last, const void *W, int d, float wscale, float *ell,
+                                 hipStream_t st);
 // s[c] = sum of ell[off[c] - off[0] .. off[c+1] - off[0]) in ascending order.
 hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n_cand, float *s, hipStream_t st);
 // dst row i = src row idx[i], rows of row_bytes (a multiple of 16) bytes.
@@ -131,5 +135,8 @@ hipError_t launch_count_bad_ids(const int32_t *ids, int64_t n, int V, int *bad, 
 // dst[i] = src[i] with fp32 -> T conversion (weights upload helpers).
 hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst, hipStream_t st);
 hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst, hipStream_t st);
+// dst[i] = src[i] * scale as fp16 (bf16 bits in; exact when scale is a power
+// of two that keeps every value inside the fp16 normal range).
+hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst, hipStream_t st);
 
 }  // namespace jetk

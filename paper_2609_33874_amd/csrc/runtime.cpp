@@ -168,12 +168,41 @@ struct Loader {
   }
 
   // Uploads host bytes of `n` elements stored as bf16 (src_bf16) or f32 into a
-  // new device array of the compute dtype.
-  Status put_matrix(const void *src, int64_t n, bool src_bf16, void **out) {
-    const size_t dst_bytes = (size_t)n * m->esz;
+  // new device array of the compute dtype (as stored, with keep_bf16). In the
+  // fp16 mode the bf16 values are multiplied by 2^k, k chosen so that the
+  // largest magnitude lands in [2^14, 2^15): nothing overflows, and every value
+  // of magnitude at least 2^-32 times the largest (all bf16 bits of it above
+  // fp16's smallest step 2^-24) converts exactly. *inv_scale receives 2^-k.
+  Status put_matrix(const void *src, int64_t n, bool src_bf16, void **out, float *inv_scale = nullptr,
+                    bool keep_bf16 = false) {
+    if (inv_scale) *inv_scale = 1.0f;
+    const int kdt = keep_bf16 ? 0 : m->kdt;
+    const size_t dst_bytes = (size_t)n * (kdt == 1 ? 4 : 2);
     TRY(dmalloc(m, dst_bytes, out));
     m->weight_allocs.push_back(*out);
-    if ((m->kdt == 0) == src_bf16) {
+    if (kdt == 2) {
+      if (!src_bf16) return Status::err(JET_E_INVALID, "the fp16 mode needs a bf16 model file");
+      const uint16_t *h = reinterpret_cast<const uint16_t *>(src);
+      uint16_t mx = 0;  // largest magnitude (bf16 bits without the sign order like the magnitudes)
+      for (int64_t i = 0; i < n; ++i) mx = std::max<uint16_t>(mx, (uint16_t)(h[i] & 0x7fffu));
+      if (mx >= 0x7f80u) return Status::err(JET_E_INVALID, "weights hold inf or NaN");
+      int k = 0;
+      if (mx != 0) {
+        const int e = (int)(mx >> 7) - 127;  // max |w| in [2^e, 2^(e+1)) (normal numbers)
+        k = std::min(14 - e, 100);
+      }
+      const float scale = std::ldexp(1.0f, k);
+      if (inv_scale) *inv_scale = std::ldexp(1.0f, -k);
+      void *tmp;
+      TRY(dmalloc(m, (size_t)n * 2, &tmp));
+      hipError_t e = hipMemcpy(tmp, src, (size_t)n * 2, hipMemcpyHostToDevice);
+      if (e == hipSuccess) e = jetk::launch_convert_bf16_to_f16((const uint16_t *)tmp, n, scale, *out, m->st);
+      if (e == hipSuccess) e = hipStreamSynchronize(m->st);
+      dfree(m, tmp, (size_t)n * 2);
+      HIPC(e);
+      return Status::ok();
+    }
+    if ((kdt == 0) == src_bf16) {
       HIPC(hipMemcpy(*out, src, dst_bytes, hipMemcpyHostToDevice));
       return Status::ok();
     }
@@ -188,10 +217,10 @@ struct Loader {
     return Status::ok();
   }
 
-  Status matrix(const std::string &name, void **out) {
+  Status matrix(const std::string &name, void **out, float *inv_scale = nullptr, bool keep_bf16 = false) {
     const TensorInfo *ti;
     TRY(read(name, &ti));
-    return put_matrix(host.data(), ti->numel(), ti->bf16, out);
+    return put_matrix(host.data(), ti->numel(), ti->bf16, out, inv_scale, keep_bf16);
   }
 
   Status vec_f32(const std::string &name, float **out, int64_t expect) {
@@ -226,7 +255,8 @@ struct Loader {
   }
 
   // Concatenates matrices row-wise (all [rows_i][d]) and pads to `pad_rows`.
-  Status concat(const std::vector<std::string> &names, int64_t d, int64_t pad_rows, void **out, int64_t *rows_out) {
+  Status concat(const std::vector<std::string> &names, int64_t d, int64_t pad_rows, void **out, int64_t *rows_out,
+                float *inv_scale) {
     std::vector<char> all;
     bool bf = m->h.bf16;
     const size_t es = bf ? 2 : 4;
@@ -243,11 +273,11 @@ struct Loader {
       rows = pad_rows;
     }
     if (rows_out) *rows_out = rows;
-    return put_matrix(all.data(), rows * d, bf, out);
+    return put_matrix(all.data(), rows * d, bf, out, inv_scale);
   }
 
   // gate/up interleaved in blocks of 32 rows: [g0..g31, u0..u31, g32.., u32.., ...]
-  Status gate_up(const std::string &g, const std::string &u, int64_t F, int64_t d, void **out) {
+  Status gate_up(const std::string &g, const std::string &u, int64_t F, int64_t d, void **out, float *inv_scale) {
     const bool bf = m->h.bf16;
     const size_t es = bf ? 2 : 4, row = (size_t)d * es;
     const TensorInfo *ti;
@@ -259,12 +289,12 @@ struct Loader {
       std::memcpy(&all[(size_t)(2 * b) * 32 * row], &gate[(size_t)b * 32 * row], 32 * row);
       std::memcpy(&all[(size_t)(2 * b + 1) * 32 * row], &host[(size_t)b * 32 * row], 32 * row);
     }
-    return put_matrix(all.data(), 2 * F * d, bf, out);
+    return put_matrix(all.data(), 2 * F * d, bf, out, inv_scale);
   }
 };
 
 Status check_shapes(const ModelHeader &h, int dtype) {
-  const int64_t bk = dtype == JET_BF16 ? 64 : 32;
+  const int64_t bk = dtype == JET_FP32 ? 32 : 64;
   if (dtype != JET_FP32 && !h.bf16)
     return Status::err(JET_E_INVALID, "an f32 model file cannot run in a bf16 mode (its weights are not bf16 values)");
   if (h.head_dim != 32 && h.head_dim != 64 && h.head_dim != 128)
@@ -287,15 +317,16 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   TRY(read_model_header(m->path, &m->h));
   const ModelHeader &h = m->h;
   TRY(check_shapes(h, m->dtype));
-  m->kdt = m->dtype == JET_FP32 ? 1 : 0;
+  m->kdt = m->dtype == JET_FP32 ? 1 : m->dtype == JET_F16 ? 2 : 0;
+  m->edt = m->kdt == 1 ? 1 : 0;
   m->pair = m->dtype == JET_BF16 ? 1 : 0;
   m->np = m->pair ? 2 : 1;
-  m->esz = m->kdt == 0 ? 2 : 4;
+  m->esz = m->kdt == 1 ? 4 : 2;
   m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
   HIPC(hipSetDevice(m->device));
   Loader L{m, {}};
-  TRY(L.matrix("tok_embed", &m->embed));
-  TRY(L.matrix("lm_head", &m->lm_head));
+  TRY(L.matrix("tok_embed", &m->embed, nullptr, /*keep_bf16=*/m->kdt == 2));
+  TRY(L.matrix("lm_head", &m->lm_head, &m->is_lm));
   TRY(L.vec_f32("final_norm", &m->final_norm, h.d));
   m->layers.resize((size_t)h.n_layers);
   for (int64_t i = 0; i < h.n_layers; ++i) {
@@ -305,20 +336,20 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
     TRY(L.vec_f32(p + "attn_norm", &ly.attn_norm, h.d));
     TRY(L.vec_f32(p + "ffn_norm", &ly.ffn_norm, h.d));
     if (!ly.gdn) {
-      TRY(L.concat({p + "wq", p + "wk", p + "wv"}, h.d, 0, &ly.w_qkv, nullptr));
-      TRY(L.matrix(p + "wo", &ly.w_o));
+      TRY(L.concat({p + "wq", p + "wk", p + "wv"}, h.d, 0, &ly.w_qkv, nullptr, &ly.is_qkv));
+      TRY(L.matrix(p + "wo", &ly.w_o, &ly.is_o));
     } else {
       const int64_t H = h.gdn_heads, C = 2 * H * h.gdn_dk + H * h.gdn_dv;
       TRY(L.concat({p + "gdn_wq", p + "gdn_wk", p + "gdn_wv", p + "gdn_wz", p + "gdn_wb", p + "gdn_wa"}, h.d, 0,
-                   &ly.w_in, &ly.n_in));
-      TRY(L.matrix(p + "gdn_wo", &ly.w_o));
+                   &ly.w_in, &ly.n_in, &ly.is_qkv));
+      TRY(L.matrix(p + "gdn_wo", &ly.w_o, &ly.is_o));
       TRY(L.f32_array(p + "gdn_conv", &ly.conv_w, C * h.conv_kernel));
       TRY(L.f32_array(p + "gdn_A_log", &ly.A_log, H));
       TRY(L.f32_array(p + "gdn_dt_bias", &ly.dt_bias, H));
       TRY(L.f32_array(p + "gdn_norm", &ly.gdn_norm, h.gdn_dv));
     }
-    TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu));
-    TRY(L.matrix(p + "w_down", &ly.w_down));
+    TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu, &ly.is_gu));
+    TRY(L.matrix(p + "w_down", &ly.w_down, &ly.is_down));
   }
   // RoPE tables: angles in fp64 on the host, stored as fp32 [max_ctx][hd/2]
   const int64_t half = h.head_dim / 2;
@@ -347,12 +378,12 @@ double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (d
 
 // A holds activations ([hi | lo] pairs in the pair mode, lda counts both).
 Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t M,
-                int64_t N, int64_t K, void *out, int64_t ldo) {
+                int64_t N, int64_t K, void *out, int64_t ldo, float oscale) {
   const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 * m->np : N) *
                            (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
                            (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
   KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * m->np + N * K) * (double)m->esz + out_bytes);
-  LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, m->pair, out, ldo, m->st));
+  LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, m->pair, out, ldo, oscale, m->st));
   return Status::ok();
 }
 
@@ -367,7 +398,8 @@ Status run_lmhead(jet_model *m, const void *F, int64_t R, float *lse) {
   TRY(ws_t<float>(m, "lm_ps", (size_t)(nsplit * R), &ps));
   {
     KTimer t(m, JET_K_LMHEAD, gemm_flops(R, V, d), (double)(V * d + R * d * m->np) * (double)m->esz);
-    LAUNCH(jetk::launch_lmhead_lse(m->kdt, m->lm_head, F, (int)V, (int)R, (int)d, m->pair, tps, pm, ps, m->st));
+    LAUNCH(jetk::launch_lmhead_lse(m->kdt, m->lm_head, F, (int)V, (int)R, (int)d, m->pair, tps, m->is_lm, pm, ps,
+                                   m->st));
   }
   KTimer t2(m, JET_K_OTHER, 0, 0);
   LAUNCH(jetk::launch_lse_merge(pm, ps, nsplit, (int)R, lse, m->st));
@@ -503,9 +535,9 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
                                 b.xn, m->st));
   }
   TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, ly.w_gu, h.d, R, 2 * h.ffn, h.d, b.act,
-               m->np * h.ffn));
+               m->np * h.ffn, ly.is_gu));
   TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, ly.w_down, h.ffn, R, h.d, h.ffn,
-               b.resid, h.d));
+               b.resid, h.d, ly.is_down));
   return Status::ok();
 }
 
@@ -520,7 +552,8 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps,
                                 b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv));
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv,
+               ly.is_qkv));
   KTimer t(m, JET_K_OTHER, 0, 0);
   LAUNCH(jetk::launch_rope_scatter(m->kdt, m->pair, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
                                    (int)h.n_kv_heads, (int)h.head_dim, b.q, R * h.n_heads * h.head_dim, kc, vc,
@@ -531,7 +564,7 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
 Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
   return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, m->np * h.n_heads * h.head_dim, ly.w_o,
-                  h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d);
+                  h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d, ly.is_o);
 }
 
 // Per-wave tables of the delta-rule layers (built on the host, uploaded once).
@@ -566,7 +599,7 @@ Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, co
                                 b.xn, m->st));
   }
   TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_in, h.d, R, ly.n_in, h.d, gx,
-               ly.n_in));
+               ly.n_in, ly.is_qkv));
   {
     KTimer t(m, JET_K_OTHER, 0, 0);
     jetk::GdnConvArgs g{gx, ly.n_in, gp.hist, gp.tail_slot, tail, ly.conv_w, ly.A_log, ly.dt_bias,
@@ -587,7 +620,7 @@ Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, co
                                 (int)dv, (int)R, gy, m->st));
   }
   return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, gy, m->np * H * dv, ly.w_o, H * dv, R, h.d, H * dv,
-                  b.resid, h.d);
+                  b.resid, h.d, ly.is_o);
 }
 
 // Token ids: validated on the host (host memory) or by a device count.
@@ -713,7 +746,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     TRY(wave_bufs(m, R, &b));
     {
       KTimer t(m, JET_K_OTHER, 0, 0);
-      LAUNCH(jetk::launch_embed(dt, m->embed, d_tok + t0, nullptr, (int)R, (int)h.d, b.resid, m->st));
+      LAUNCH(jetk::launch_embed(m->edt, m->embed, d_tok + t0, nullptr, (int)R, (int)h.d, b.resid, m->st));
     }
     // Only the last row of each question goes on past the last layer (to the
     // LM head, Section 4.1), while every row's K/V of that layer is retained:
@@ -884,7 +917,7 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       TRY(ws(m, "cand_v", kvb, &vc));
       {
         KTimer t(m, JET_K_OTHER, 0, 0);
-        LAUNCH(jetk::launch_embed(dt, m->embed, d_tok, d_rtok + r0, (int)R, (int)h.d, b.resid, m->st));
+        LAUNCH(jetk::launch_embed(m->edt, m->embed, d_tok, d_rtok + r0, (int)R, (int)h.d, b.resid, m->st));
       }
       for (int64_t l = 0; l < h.n_layers; ++l) {
         const Layer &ly = m->layers[(size_t)l];
@@ -910,7 +943,8 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
     {
       KTimer t(m, JET_K_OTHER, 0, 0);
       LAUNCH(jetk::launch_gather_logprob(dt, m->pair, d_tok + t0, d_lm + t0, (int)(t1 - t0), (int)r0, f_body,
-                                         lse_body, p->f_last, p->lse_last, m->lm_head, (int)h.d, d_ell + t0, m->st));
+                                         lse_body, p->f_last, p->lse_last, m->lm_head, (int)h.d, m->is_lm, d_ell + t0,
+                                         m->st));
       LAUNCH(jetk::launch_segment_sum(d_ell + t0, d_cto + c0, (int)(c1 - c0), d_sum + c0, m->st));
     }
     m->stats.score_waves++;
@@ -955,7 +989,8 @@ extern "C" int jet_model_load(const char *model_path, const jet_load_opts *opts,
   if (!model_path) return fail(Status::err(JET_E_INVALID, "model_path is NULL"));
   jet_model *m = new jet_model();
   if (opts) {
-    if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32 && opts->dtype != JET_BF16_SINGLE) {
+    if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32 && opts->dtype != JET_BF16_SINGLE &&
+        opts->dtype != JET_F16) {
       delete m;
       return fail(Status::err(JET_E_INVALID, "unknown dtype"));
     }

@@ -22,6 +22,9 @@ struct Layer {
   void *w_o = nullptr;     // [d][Hq hd] (attention) or [d][H dv] (delta rule)
   void *w_gu = nullptr;    // [2F][d], blocks of 32 gate rows then 32 up rows
   void *w_down = nullptr;  // [d][F]
+  // inverse weight scales of w_qkv / w_in, w_o, w_gu, w_down (fp16 mode: the
+  // stored matrices are the file's values times a power of two; else 1)
+  float is_qkv = 1.0f, is_o = 1.0f, is_gu = 1.0f, is_down = 1.0f;
   // gated delta-rule layers
   void *w_in = nullptr;    // [n_in][d]: q, k, v (conv channels), z, b, a, zero pad
   int64_t n_in = 0;
@@ -45,7 +48,8 @@ struct jet_model {
   jet::ModelHeader h;
   std::string path;
   int dtype = JET_BF16;  // requested mode
-  int kdt = 0;           // kernel element type: 0 = bf16, 1 = fp32
+  int kdt = 0;           // kernel element type: 0 = bf16, 1 = fp32, 2 = fp16
+  int edt = 0;           // element type of the embedding table (bf16 in the fp16 mode)
   int pair = 1;          // activations and caches as (hi, lo) bf16 pairs
   int np = 2;            // planes per activation element (2 with pair)
   int device = 0;
@@ -55,6 +59,7 @@ struct jet_model {
   size_t esz = 2;  // bytes per compute element
   size_t bytes_used = 0;
   void *embed = nullptr, *lm_head = nullptr;
+  float is_lm = 1.0f;  // inverse weight scale of lm_head
   float *final_norm = nullptr;
   std::vector<jet::Layer> layers;
   float *rope_cos = nullptr, *rope_sin = nullptr;

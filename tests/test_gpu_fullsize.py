@@ -1,6 +1,7 @@
 """Full-size GPU parity: the real workload shapes in the launch configuration
-that bench.py times (every question on the GPU, bf16), checked against the
-fp64 oracle on sampled questions and through properties that hold at any size.
+that bench.py times (every question on the GPU, in the fp16 mode bench.py
+times and in the pair-bf16 mode), checked against the fp64 oracle on sampled
+questions and through properties that hold at any size.
 """
 import os
 import sys
@@ -25,11 +26,24 @@ def dense_1p5b_path():
     return jet_synth.ensure_model("dense_1p5b")
 
 
+# the fp16 mode (what bench.py times) and the pair-bf16 mode
+DTYPES = [pytest.param(J.JET_F16, id="f16"), pytest.param(J.JET_BF16, id="bf16pair")]
+
+
 @pytest.fixture(scope="module")
-def dense_1p5b_model(dense_1p5b_path):
-    m = J.jet_model_load(dense_1p5b_path, dtype=J.JET_BF16)
-    yield m
-    J.jet_model_free(m)
+def dense_1p5b_models(dense_1p5b_path):
+    models = {}
+
+    def get(dtype):
+        if dtype not in models:
+            for m in models.values():  # one copy of the weights at a time
+                J.jet_model_free(m)
+            models.clear()
+            models[dtype] = J.jet_model_load(dense_1p5b_path, dtype=dtype)
+        return models[dtype]
+    yield get
+    for m in models.values():
+        J.jet_model_free(m)
 
 
 def run(model, wl):
@@ -40,17 +54,27 @@ def run(model, wl):
         J.jet_prefix_free(p)
 
 
-def sampled_parity(path, wl, tok, sums, qs):
-    sub = wl.subset(qs)
-    ref_tok, ref_sum = oracle.score_unshared(path, sub)
+_ORACLE = {}
+
+
+def oracle_subset(path, name, wl, qs):
+    """Oracle scores of questions qs of workload `name` (cached across modes)."""
+    key = (path, name, tuple(qs))
+    if key not in _ORACLE:
+        _ORACLE[key] = oracle.score_unshared(path, wl.subset(qs))
+    return _ORACLE[key]
+
+
+def sampled_parity(path, name, wl, tok, sums, qs, dtype):
+    ref_tok, ref_sum = oracle_subset(path, name, wl, qs)
     got_tok = np.concatenate([tok[wl.cand_tok_offsets[wl.q_cand_offsets[q]]:
                                   wl.cand_tok_offsets[wl.q_cand_offsets[q + 1]]] for q in qs])
     got_sum = np.concatenate([sums[wl.q_cand_offsets[q]:wl.q_cand_offsets[q + 1]] for q in qs])
     dt = np.abs(got_tok - ref_tok).max()
     ds = np.abs(got_sum - ref_sum).max()
-    log(f"[fullsize] questions {qs}: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    log(f"[fullsize] {name} dtype {dtype} questions {qs}: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
     from conftest import record_parity
-    record_parity(f"fullsize/{len(wl.cand_tokens)}tok/q{qs}", max_tok=dt, max_sum=ds)
+    record_parity(f"fullsize/{name}/dtype{dtype}/q{qs}", max_tok=dt, max_sum=ds)
     assert dt <= 2e-2 and ds <= 5e-2
     return ref_sum, got_sum
 
@@ -62,23 +86,27 @@ def properties(wl, tok, sums):
     np.testing.assert_allclose(sums, s, atol=1e-3, rtol=1e-5)
 
 
-def test_dense_1p5b_k4_full(dense_1p5b_path, dense_1p5b_model):
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_dense_1p5b_k4_full(dtype, dense_1p5b_path, dense_1p5b_models):
     wl = jet_synth.make_workload("dense_1p5b_k4")
-    log(f"[fullsize] dense_1p5b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
-    tok, sums = run(dense_1p5b_model, wl)
+    log(f"[fullsize] dense_1p5b_k4 dtype {dtype}: {wl.n_questions} questions, "
+        f"{int(wl.prefix_offsets[-1])} prefix tokens")
+    model = dense_1p5b_models(dtype)
+    tok, sums = run(model, wl)
     properties(wl, tok, sums)
-    sampled_parity(dense_1p5b_path, wl, tok, sums, [0, 97, 255])
-    st = J.jet_stats_get(dense_1p5b_model)
+    sampled_parity(dense_1p5b_path, "dense_1p5b_k4", wl, tok, sums, [0, 97, 255], dtype)
+    st = J.jet_stats_get(model)
     assert st["prefix_tokens"] >= int(wl.prefix_offsets[-1])
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("name", ["dense_1p5b_binary", "dense_1p5b_ordinal"])
-def test_dense_1p5b_decisions_full(name, dense_1p5b_path, dense_1p5b_model):
+def test_dense_1p5b_decisions_full(name, dtype, dense_1p5b_path, dense_1p5b_models):
     wl = jet_synth.make_workload(name)
-    log(f"[fullsize] {name}: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
-    tok, sums = run(dense_1p5b_model, wl)
+    log(f"[fullsize] {name} dtype {dtype}: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    tok, sums = run(dense_1p5b_models(dtype), wl)
     properties(wl, tok, sums)
-    ref_sum, got_sum = sampled_parity(dense_1p5b_path, wl, tok, sums, [0, wl.n_questions - 1])
+    ref_sum, got_sum = sampled_parity(dense_1p5b_path, name, wl, tok, sums, [0, wl.n_questions - 1], dtype)
     mode = J.JET_BINARY if name.endswith("binary") else J.JET_ORDINAL
     K = 2 if mode == J.JET_BINARY else 5
     qo = np.arange(0, len(ref_sum) + 1, K, dtype=np.int64)
@@ -94,30 +122,34 @@ def test_dense_1p5b_decisions_full(name, dense_1p5b_path, dense_1p5b_model):
         assert np.all((v_all >= 0) & (v_all <= K - 1))
 
 
-def test_hybrid_4b_k4_full():
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_hybrid_4b_k4_full(dtype):
     """4B-shape hybrid (24 delta-rule + 8 attention layers): all 128 questions
     on the GPU, the shortest-prefix question checked against the oracle."""
     path = jet_synth.ensure_model("hybrid_4b")
     wl = jet_synth.make_workload("hybrid_4b_k4")
-    log(f"[fullsize] hybrid_4b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
-    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    log(f"[fullsize] hybrid_4b_k4 dtype {dtype}: {wl.n_questions} questions, "
+        f"{int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=dtype)
     try:
         tok, sums = run(m, wl)
     finally:
         J.jet_model_free(m)
     properties(wl, tok, sums)
     q = int(np.argmin(np.diff(wl.prefix_offsets)))
-    sampled_parity(path, wl, tok, sums, [q])
+    sampled_parity(path, "hybrid_4b_k4", wl, tok, sums, [q], dtype)
 
 
-def test_dense_27b_k10_full():
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_dense_27b_k10_full(dtype):
     """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
     GPU; one whole candidate sequence (the shortest question's shortest
     candidate, ~1.1k positions) checked against the oracle, plus properties."""
     path = jet_synth.ensure_model("dense_27b")
     wl = jet_synth.make_workload("dense_27b_k10")
-    log(f"[fullsize] dense_27b_k10: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
-    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    log(f"[fullsize] dense_27b_k10 dtype {dtype}: {wl.n_questions} questions, "
+        f"{int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=dtype)
     try:
         tok, sums = run(m, wl)
     finally:
@@ -127,12 +159,14 @@ def test_dense_27b_k10_full():
     cands = wl.candidates(q)
     j = int(np.argmin([len(y) for y in cands]))
     c = wl.q_cand_offsets[q] + j
-    sub = jet_synth.from_lists([wl.prefix(q)], [[cands[j]]])
-    ref_tok, ref_sum = oracle.score_unshared(path, sub)
+    key = (path, "dense_27b_k10", q, j)
+    if key not in _ORACLE:
+        _ORACLE[key] = oracle.score_unshared(path, jet_synth.from_lists([wl.prefix(q)], [[cands[j]]]))
+    ref_tok, ref_sum = _ORACLE[key]
     got = tok[wl.cand_tok_offsets[c]:wl.cand_tok_offsets[c + 1]]
     dt = np.abs(got - ref_tok).max()
     ds = abs(float(sums[c]) - float(ref_sum[0]))
-    log(f"[fullsize] 27b question {q} candidate {j}: max|d tok|={dt:.3e} |d sum|={ds:.3e}")
+    log(f"[fullsize] 27b dtype {dtype} question {q} candidate {j}: max|d tok|={dt:.3e} |d sum|={ds:.3e}")
     from conftest import record_parity
-    record_parity(f"fullsize/27b/q{q}c{j}", max_tok=dt, max_sum=ds)
+    record_parity(f"fullsize/dense_27b_k10/dtype{dtype}/q{q}c{j}", max_tok=dt, max_sum=ds)
     assert dt <= 2e-2 and ds <= 5e-2

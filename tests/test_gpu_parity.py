@@ -19,7 +19,8 @@ from paper_2609_33874_amd import jet as J
 
 pytestmark = pytest.mark.gpu
 
-TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2), J.JET_BF16_SINGLE: (2e-2, 5e-2)}
+TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2), J.JET_BF16_SINGLE: (2e-2, 5e-2),
+       J.JET_F16: (2e-2, 5e-2)}
 
 
 def log(msg):
@@ -81,6 +82,9 @@ CASES = [
     ("small_hybrid_fp32", "small_hybrid", J.JET_FP32),
     ("small_hybrid_bf16", "small_hybrid", J.JET_BF16),
     ("small_hybrid_bf16", "small_hybrid", J.JET_FP32),
+    ("tiny_dense_bf16", "tiny", J.JET_F16),
+    ("small_gqa_bf16", "small", J.JET_F16),
+    ("small_hybrid_bf16", "small_hybrid", J.JET_F16),
 ]
 
 
@@ -133,7 +137,8 @@ def test_waves_and_budgets_do_not_change_scores(model_dir):
     np.testing.assert_allclose(b_tok, a_tok, atol=1e-5, rtol=0)
 
 
-def test_duplicates_permutation_and_determinism(model_dir):
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
+def test_duplicates_permutation_and_determinism(dtype, model_dir):
     path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
     base = jet_synth.make_workload("small", n_questions=4)
     pre, cands, perm_idx = [], [], []
@@ -145,11 +150,11 @@ def test_duplicates_permutation_and_determinism(model_dir):
         pre.append(base.prefix(q)); cands.append([cs[i] for i in perm])
         perm_idx.append(perm)
     wl = jet_synth.from_lists(pre, cands)
-    t1, s1, _ = run_gpu(path, wl, J.JET_BF16)
-    t2, s2, _ = run_gpu(path, wl, J.JET_BF16)
+    t1, s1, _ = run_gpu(path, wl, dtype)
+    t2, s2, _ = run_gpu(path, wl, dtype)
     np.testing.assert_array_equal(t1, t2)        # run to run: bitwise
     np.testing.assert_array_equal(s1, s2)
-    _, s0, _ = run_gpu(path, base, J.JET_BF16)
+    _, s0, _ = run_gpu(path, base, dtype)
     for q in range(base.n_questions):
         a = wl.q_cand_offsets[q]
         perm = perm_idx[q]
@@ -162,13 +167,14 @@ def test_duplicates_permutation_and_determinism(model_dir):
         assert got[dup[0]] == got[dup[1]]
 
 
-def test_device_resident_inputs_and_outputs(model_dir):
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
+def test_device_resident_inputs_and_outputs(dtype, model_dir):
     import torch
     path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
     wl = jet_synth.make_workload("small", n_questions=5)
-    h_tok, h_sum, _ = run_gpu(path, wl, J.JET_BF16)
+    h_tok, h_sum, _ = run_gpu(path, wl, dtype)
     dev = torch.device("cuda:0")
-    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    m = J.jet_model_load(path, dtype=dtype)
     try:
         pt = torch.from_numpy(wl.prefix_tokens).to(dev)
         ct = torch.from_numpy(wl.cand_tokens).to(dev)
@@ -192,9 +198,10 @@ def test_device_resident_inputs_and_outputs(model_dir):
 
 def test_error_paths_on_gpu(model_dir):
     path = jet_synth.ensure_model("tiny_dense_fp32", cache_dir=model_dir)
-    with pytest.raises(J.JetError) as e:
-        J.jet_model_load(path, dtype=J.JET_BF16)  # f32 weights are not bf16 values
-    assert e.value.code == J.JET_E_INVALID
+    for dt in (J.JET_BF16, J.JET_F16):
+        with pytest.raises(J.JetError) as e:
+            J.jet_model_load(path, dtype=dt)  # f32 weights are not bf16 values
+        assert e.value.code == J.JET_E_INVALID
     m = J.jet_model_load(path, dtype=J.JET_FP32, max_ctx=40)
     try:
         with pytest.raises(J.JetError) as e:
@@ -222,14 +229,15 @@ def test_device_budget_oom(model_dir):
     assert e.value.code == J.JET_E_OOM
 
 
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
 @pytest.mark.parametrize("spec,wname", [("small_hybrid_bf16", "small_hybrid"), ("small_gqa_bf16", "small")])
-def test_candidate_isolation_on_gpu(spec, wname, model_dir):
+def test_candidate_isolation_on_gpu(spec, wname, dtype, model_dir):
     """A candidate scored together with its siblings equals the same candidate
     scored alone against the same prefix, bitwise: the forked recurrent state
     and the own-suffix attention never see a sibling (Section 4.1, 5.6)."""
     path = jet_synth.ensure_model(spec, cache_dir=model_dir)
     wl = jet_synth.make_workload(wname, n_questions=3)
-    m = J.jet_model_load(path, dtype=J.JET_BF16)
+    m = J.jet_model_load(path, dtype=dtype)
     try:
         p = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
         tok, sums = J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
