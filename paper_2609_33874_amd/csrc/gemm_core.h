@@ -51,7 +51,7 @@ struct GCfg {
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
   static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8, "tile load schedule");
-  static_assert(INTERLEAVED ? NSTAGE >= 3 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
+  static_assert(INTERLEAVED ? NSTAGE >= 2 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
                 "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
