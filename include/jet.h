@@ -63,8 +63,11 @@ enum {
  * exact), and activations, caches and probabilities are single fp16 values
  * (11 significant bits against bf16's 8), so every product is one fp16
  * matrix-core operation at the bf16 rate with fp32 accumulation; needs a bf16
- * model file. */
-enum { JET_BF16 = 0, JET_FP32 = 1, JET_BF16_SINGLE = 2, JET_F16 = 3 };
+ * model file. JET_F16P: as JET_F16, with the attention side (the inputs of
+ * the attention layers' projections, q, the K/V caches, the attention
+ * probabilities and output) carried as (hi, lo) fp16 pairs like JET_BF16:
+ * for deep stacks, where single fp16 rounding on that side adds up. */
+enum { JET_BF16 = 0, JET_FP32 = 1, JET_BF16_SINGLE = 2, JET_F16 = 3, JET_F16P = 4 };
 enum { JET_CHOICE = 0, JET_BINARY = 1, JET_ORDINAL = 2 }; /* decision rule */
 
 /* flags for jet_load_opts.flags */
@@ -76,7 +79,7 @@ typedef struct jet_model jet_model;
 typedef struct jet_prefix jet_prefix;
 
 typedef struct {
-  int32_t dtype;                /* JET_BF16, JET_FP32, JET_BF16_SINGLE or JET_F16 (see above) */
+  int32_t dtype;                /* JET_BF16, JET_FP32, JET_BF16_SINGLE, JET_F16 or JET_F16P */
   int32_t device;               /* HIP device ordinal */
   int64_t max_ctx;              /* max positions per sequence; 0 = the file's value */
   int64_t prefill_token_budget; /* max prefix tokens per prefill wave; 0 = no limit.

@@ -386,8 +386,8 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       *reinterpret_cast<uint2 *>(dst) = hi;
       if constexpr (PAIR) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) lo[e] = o[e] - bf2f((bf16)((e & 1 ? (e < 2 ? hi.x : hi.y) >> 16 : (e < 2 ? hi.x : hi.y)) & 0xffffu));
-        *reinterpret_cast<uint2 *>(dst + (int64_t)a.Hq * HD) = make_uint2(f2bf2(lo[0], lo[1]), f2bf2(lo[2], lo[3]));
+        for (int e = 0; e < 4; ++e) lo[e] = o[e] - to_f<T>(from_f<T>(o[e]));
+        *reinterpret_cast<uint2 *>(dst + (int64_t)a.Hq * HD) = make_uint2(pack2<T>(lo[0], lo[1]), pack2<T>(lo[2], lo[3]));
       }
     } else {
       *reinterpret_cast<float4 *>(dst) = make_float4(o[0], o[1], o[2], o[3]);
@@ -415,7 +415,12 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st) {
       if (a.hd == 32) return run_attn<bf16, 32, false>(a, st);
     }
   } else if (dtype == 2) {
-    if (a.pair) return hipErrorInvalidValue;
+    if (a.pair) {
+      if (a.hd == 128) return run_attn<f16, 128, true>(a, st);
+      if (a.hd == 64) return run_attn<f16, 64, true>(a, st);
+      if (a.hd == 32) return run_attn<f16, 32, true>(a, st);
+      return hipErrorInvalidValue;
+    }
     if (a.hd == 128) return run_attn<f16, 128, false>(a, st);
     if (a.hd == 64) return run_attn<f16, 64, false>(a, st);
     if (a.hd == 32) return run_attn<f16, 32, false>(a, st);

@@ -46,6 +46,53 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ 
   }
 }
 
+// One wave per row, 4 rows per block: the row is read once with 16-byte loads
+// into registers (NV float4 per lane, d <= 256 NV, d a multiple of 4), then
+// normalised and written with 8-byte (16-bit T) or 16-byte (fp32) stores.
+template <typename T, bool PAIR, int NV>
+__global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const float *__restrict__ x,
+                                                            const int32_t *__restrict__ map,
+                                                            const float *__restrict__ g, int R, int d, float eps,
+                                                            T *__restrict__ out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const int64_t src = map ? map[r] : r;
+  const float4 *xr = reinterpret_cast<const float4 *>(x + src * d);
+  const float4 *g4 = reinterpret_cast<const float4 *>(g);
+  const int n4 = d >> 2;
+  float4 v[NV];
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = j * 64 + lane;
+    v[j] = i < n4 ? xr[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+  }
+  ss = warp_sum(ss);
+  const float inv = rsqrtf(ss / (float)d + eps);
+  T *o = out + (int64_t)r * d * (PAIR ? 2 : 1);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = j * 64 + lane;
+    if (i >= n4) break;
+    const float4 gg = g4[i];
+    const float y[4] = {v[j].x * inv * gg.x, v[j].y * inv * gg.y, v[j].z * inv * gg.z, v[j].w * inv * gg.w};
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4 *>(o + 4 * i) = make_float4(y[0], y[1], y[2], y[3]);
+    } else {
+      T hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hi[e] = from_f<T>(y[e]);
+      *reinterpret_cast<uint2 *>(o + 4 * i) =
+          make_uint2(pack2<T>(to_f<T>(hi[0]), to_f<T>(hi[1])), pack2<T>(to_f<T>(hi[2]), to_f<T>(hi[3])));
+      if constexpr (PAIR)
+        *reinterpret_cast<uint2 *>(o + d + 4 * i) =
+            make_uint2(pack2<T>(y[0] - to_f<T>(hi[0]), y[1] - to_f<T>(hi[1])),
+                       pack2<T>(y[2] - to_f<T>(hi[2]), y[3] - to_f<T>(hi[3])));
+    }
+  }
+}
+
 // One block per row; thread t handles rotation pairs (i, i + hd/2).
 template <typename T, bool PAIR>
 __device__ __forceinline__ void put_val(T *p, int64_t ps, float v) {
@@ -182,13 +229,39 @@ hipError_t launch_embed(int dtype, const void *E, const int32_t *ids, const int3
   return hipGetLastError();
 }
 
+template <typename T, bool PAIR>
+static bool rmsnorm_rows(const float *x, const int32_t *map, const float *g, int R, int d, float eps, T *out,
+                         hipStream_t st) {
+  if (d % 4) return false;
+  const dim3 grid((R + 3) / 4), block(256);
+  const int nv = (d + 255) / 256;
+  if (nv <= 2) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 2>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else if (nv <= 4) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 4>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else if (nv <= 8) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 8>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else if (nv <= 12) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 12>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else if (nv <= 20) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 20>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else if (nv <= 32) hipLaunchKernelGGL((rmsnorm_rows_kernel<T, PAIR, 32>), grid, block, 0, st, x, map, g, R, d, eps, out);
+  else return false;
+  return true;
+}
+
 hipError_t launch_rmsnorm(int dtype, int pair, const float *x, const int32_t *map, const float *g, int R, int d,
                           float eps, void *out, hipStream_t st) {
   if (R <= 0) return hipSuccess;
+  // one wave per row with the row in registers (d <= 8192, d % 4 == 0)
+  bool done = false;
+  if (dtype == 0 && pair) done = rmsnorm_rows<bf16, true>(x, map, g, R, d, eps, (bf16 *)out, st);
+  else if (dtype == 0) done = rmsnorm_rows<bf16, false>(x, map, g, R, d, eps, (bf16 *)out, st);
+  else if (dtype == 2 && pair) done = rmsnorm_rows<f16, true>(x, map, g, R, d, eps, (f16 *)out, st);
+  else if (dtype == 2) done = rmsnorm_rows<f16, false>(x, map, g, R, d, eps, (f16 *)out, st);
+  else done = rmsnorm_rows<float, false>(x, map, g, R, d, eps, (float *)out, st);
+  if (done) return hipGetLastError();
   if (dtype == 0 && pair)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, true>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
   else if (dtype == 0)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (bf16 *)out);
+  else if (dtype == 2 && pair)
+    hipLaunchKernelGGL((rmsnorm_kernel<f16, true>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (f16 *)out);
   else if (dtype == 2)
     hipLaunchKernelGGL((rmsnorm_kernel<f16, false>), dim3(R), dim3(256), 0, st, x, map, g, d, eps, (f16 *)out);
   else
@@ -207,6 +280,9 @@ hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int3
   else if (dtype == 0)
     hipLaunchKernelGGL((rope_scatter_kernel<bf16, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
                        Hkv, hd, (bf16 *)q_out, q_ps, (bf16 *)k_cache, (bf16 *)v_cache, kv_ps, S, slot0);
+  else if (dtype == 2 && pair)
+    hipLaunchKernelGGL((rope_scatter_kernel<f16, true>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
+                       Hkv, hd, (f16 *)q_out, q_ps, (f16 *)k_cache, (f16 *)v_cache, kv_ps, S, slot0);
   else if (dtype == 2)
     hipLaunchKernelGGL((rope_scatter_kernel<f16, false>), dim3(R), dim3(256), 0, st, qkv, pos, cos_t, sin_t, Hq,
                        Hkv, hd, (f16 *)q_out, q_ps, (f16 *)k_cache, (f16 *)v_cache, kv_ps, S, slot0);

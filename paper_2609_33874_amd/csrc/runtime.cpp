@@ -317,10 +317,12 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   TRY(read_model_header(m->path, &m->h));
   const ModelHeader &h = m->h;
   TRY(check_shapes(h, m->dtype));
-  m->kdt = m->dtype == JET_FP32 ? 1 : m->dtype == JET_F16 ? 2 : 0;
+  m->kdt = m->dtype == JET_FP32 ? 1 : (m->dtype == JET_F16 || m->dtype == JET_F16P) ? 2 : 0;
   m->edt = m->kdt == 1 ? 1 : 0;
   m->pair = m->dtype == JET_BF16 ? 1 : 0;
   m->np = m->pair ? 2 : 1;
+  m->apair = (m->dtype == JET_BF16 || m->dtype == JET_F16P) ? 1 : 0;
+  m->anp = m->apair ? 2 : 1;
   m->esz = m->kdt == 1 ? 4 : 2;
   m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
   HIPC(hipSetDevice(m->device));
@@ -376,14 +378,14 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
 
 double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (double)N * (double)K; }
 
-// A holds activations ([hi | lo] pairs in the pair mode, lda counts both).
-Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t M,
-                int64_t N, int64_t K, void *out, int64_t ldo, float oscale) {
+// A holds activations ([hi | lo] pairs when pair, lda counts both planes).
+Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, int pair, const void *B, int64_t ldb,
+                int64_t M, int64_t N, int64_t K, void *out, int64_t ldo, float oscale) {
   const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 * m->np : N) *
                            (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
                            (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
-  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * m->np + N * K) * (double)m->esz + out_bytes);
-  LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, m->pair, out, ldo, oscale, m->st));
+  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * (pair ? 2 : 1) + N * K) * (double)m->esz + out_bytes);
+  LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, pair, out, ldo, oscale, m->st));
   return Status::ok();
 }
 
@@ -461,7 +463,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   TRY(upload(m, (t + "preslot").c_str(), qd.pre_slot0, &d_preslot));
   jetk::AttnArgs &a = pl->a;
   a.mode = mode;
-  a.pair = m->pair;
+  a.pair = m->apair;
   a.qs = {d_qrow0, d_nrows, d_preslot, d_prelen, d_sufrow0, d_suflen};
   a.items = d_items;
   a.n_items = (int)items.size();
@@ -475,7 +477,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   for (size_t q = 0; q < qd.nrows.size(); ++q)
     if (qd.nrows[q] > 0) kv_rows += (double)qd.pre_len[q] + (double)qd.suf_len[q];
   for (auto n : qd.nrows) qo_rows += n;
-  pl->bytes = (double)m->esz * m->np * (kv_rows * 2.0 * (double)h.n_kv_heads * (double)h.head_dim +
+  pl->bytes = (double)m->esz * m->anp * (kv_rows * 2.0 * (double)h.n_kv_heads * (double)h.head_dim +
                                         qo_rows * 2.0 * (double)h.n_heads * (double)h.head_dim);
   pl->flops = 4.0 * pairs * (double)h.head_dim;
   return Status::ok();
@@ -491,7 +493,7 @@ Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void 
   a.Q = Q;
   a.q_ps = R * h.n_heads * h.head_dim;
   a.O = O;
-  a.o_ld = m->np * h.n_heads * h.head_dim;
+  a.o_ld = m->anp * h.n_heads * h.head_dim;
   a.Kp = Kp;
   a.Vp = Vp;
   a.s_pre = s_pre;
@@ -518,10 +520,10 @@ Status wave_bufs(jet_model *m, int64_t R, WaveBufs *b) {
   const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
   TRY(ws_t<float>(m, "resid", (size_t)(R * h.d), &b->resid));
   TRY(ws_t<float>(m, "qkv", (size_t)(R * nqkv), &b->qkv));
-  const size_t pe = (size_t)m->np * m->esz;  // bytes per activation element
-  TRY(ws(m, "xn", (size_t)(R * h.d) * pe, &b->xn));
-  TRY(ws(m, "q", (size_t)(R * h.n_heads * h.head_dim) * pe, &b->q));
-  TRY(ws(m, "att", (size_t)(R * h.n_heads * h.head_dim) * pe, &b->att));
+  const size_t pe = (size_t)m->np * m->esz, pa = (size_t)m->anp * m->esz;  // bytes per activation element
+  TRY(ws(m, "xn", (size_t)(R * h.d) * std::max(pe, pa), &b->xn));
+  TRY(ws(m, "q", (size_t)(R * h.n_heads * h.head_dim) * pa, &b->q));
+  TRY(ws(m, "att", (size_t)(R * h.n_heads * h.head_dim) * pa, &b->att));
   TRY(ws(m, "act", (size_t)(R * h.ffn) * pe, &b->act));
   return Status::ok();
 }
@@ -534,10 +536,10 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.ffn_norm, (int)R, (int)h.d, (float)h.rms_eps,
                                 b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, ly.w_gu, h.d, R, 2 * h.ffn, h.d, b.act,
-               m->np * h.ffn, ly.is_gu));
-  TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, ly.w_down, h.ffn, R, h.d, h.ffn,
-               b.resid, h.d, ly.is_down));
+  TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, m->pair, ly.w_gu, h.d, R, 2 * h.ffn, h.d,
+               b.act, m->np * h.ffn, ly.is_gu));
+  TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, m->pair, ly.w_down, h.ffn, R, h.d,
+               h.ffn, b.resid, h.d, ly.is_down));
   return Status::ok();
 }
 
@@ -549,13 +551,13 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
   const int64_t nqkv = (h.n_heads + 2 * h.n_kv_heads) * h.head_dim;
   {
     KTimer t(m, JET_K_OTHER, 0, 0);
-    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps,
-                                b.xn, m->st));
+    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->apair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d,
+                                (float)h.rms_eps, b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_qkv, h.d, R, nqkv, h.d, b.qkv, nqkv,
-               ly.is_qkv));
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->anp * h.d, m->apair, ly.w_qkv, h.d, R, nqkv, h.d,
+               b.qkv, nqkv, ly.is_qkv));
   KTimer t(m, JET_K_OTHER, 0, 0);
-  LAUNCH(jetk::launch_rope_scatter(m->kdt, m->pair, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
+  LAUNCH(jetk::launch_rope_scatter(m->kdt, m->apair, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
                                    (int)h.n_kv_heads, (int)h.head_dim, b.q, R * h.n_heads * h.head_dim, kc, vc,
                                    h.n_kv_heads * S * h.head_dim, S, slot0, m->st));
   return Status::ok();
@@ -563,7 +565,7 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
 
 Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
-  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, m->np * h.n_heads * h.head_dim, ly.w_o,
+  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, m->anp * h.n_heads * h.head_dim, m->apair, ly.w_o,
                   h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d, ly.is_o);
 }
 
@@ -598,8 +600,8 @@ Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, co
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d, (float)h.rms_eps,
                                 b.xn, m->st));
   }
-  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, ly.w_in, h.d, R, ly.n_in, h.d, gx,
-               ly.n_in, ly.is_qkv));
+  TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->np * h.d, m->pair, ly.w_in, h.d, R, ly.n_in, h.d,
+               gx, ly.n_in, ly.is_qkv));
   {
     KTimer t(m, JET_K_OTHER, 0, 0);
     jetk::GdnConvArgs g{gx, ly.n_in, gp.hist, gp.tail_slot, tail, ly.conv_w, ly.A_log, ly.dt_bias,
@@ -619,7 +621,7 @@ Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, co
     LAUNCH(jetk::launch_gdn_out(m->kdt, m->pair, go, gx, ly.n_in, (int)C, ly.gdn_norm, (float)h.rms_eps, (int)H,
                                 (int)dv, (int)R, gy, m->st));
   }
-  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, gy, m->np * H * dv, ly.w_o, H * dv, R, h.d, H * dv,
+  return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, gy, m->np * H * dv, m->pair, ly.w_o, H * dv, R, h.d, H * dv,
                   b.resid, h.d, ly.is_o);
 }
 
@@ -672,7 +674,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
   p->n_q = n_q;
   p->prefix_offsets.assign(offs, offs + n_q + 1);
   p->T = T;
-  const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz * m->np;
+  const size_t kv_bytes = (size_t)(h.n_kv_heads * T * h.head_dim) * m->esz * m->anp;
   p->kcache.assign((size_t)h.n_layers, nullptr);
   p->vcache.assign((size_t)h.n_layers, nullptr);
   p->S_pre.assign((size_t)h.n_layers, nullptr);
@@ -790,15 +792,15 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
       TRY(run_attention(m, lp, b.q, R, b.att, p->kcache[(size_t)(L - 1)], p->vcache[(size_t)(L - 1)], T, nullptr,
                         nullptr, 0, nullptr, d_zero_t, JET_K_ATTN_PREFIX));
       WaveBufs c;  // the last rows, compacted
-      const size_t pe = (size_t)m->np * m->esz;
+      const size_t pe = (size_t)m->np * m->esz, pa = (size_t)m->anp * m->esz;
       TRY(ws_t<float>(m, "lr_resid", (size_t)(nq * h.d), &c.resid));
-      TRY(ws(m, "lr_att", (size_t)(nq * h.n_heads * h.head_dim) * pe, &c.att));
-      TRY(ws(m, "lr_xn", (size_t)(nq * h.d) * pe, &c.xn));
+      TRY(ws(m, "lr_att", (size_t)(nq * h.n_heads * h.head_dim) * pa, &c.att));
+      TRY(ws(m, "lr_xn", (size_t)(nq * h.d) * std::max(pe, pa), &c.xn));
       TRY(ws(m, "lr_act", (size_t)(nq * h.ffn) * pe, &c.act));
       {
         KTimer t(m, JET_K_OTHER, 0, 0);
         LAUNCH(jetk::launch_gather_rows(b.resid, h.d * 4, d_last, nq, c.resid, m->st));
-        LAUNCH(jetk::launch_gather_rows(b.att, (int64_t)(h.n_heads * h.head_dim) * (int64_t)pe, d_last, nq, c.att,
+        LAUNCH(jetk::launch_gather_rows(b.att, (int64_t)(h.n_heads * h.head_dim) * (int64_t)pa, d_last, nq, c.att,
                                         m->st));
       }
       TRY(attn_out(m, ly, c, nq));
@@ -912,7 +914,7 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       WaveBufs b;
       TRY(wave_bufs(m, R, &b));
       void *kc, *vc;
-      const size_t kvb = (size_t)(h.n_kv_heads * R * h.head_dim) * m->esz * m->np;
+      const size_t kvb = (size_t)(h.n_kv_heads * R * h.head_dim) * m->esz * m->anp;
       TRY(ws(m, "cand_k", kvb, &kc));
       TRY(ws(m, "cand_v", kvb, &vc));
       {
@@ -990,7 +992,7 @@ extern "C" int jet_model_load(const char *model_path, const jet_load_opts *opts,
   jet_model *m = new jet_model();
   if (opts) {
     if (opts->dtype != JET_BF16 && opts->dtype != JET_FP32 && opts->dtype != JET_BF16_SINGLE &&
-        opts->dtype != JET_F16) {
+        opts->dtype != JET_F16 && opts->dtype != JET_F16P) {
       delete m;
       return fail(Status::err(JET_E_INVALID, "unknown dtype"));
     }

@@ -50,8 +50,11 @@ struct jet_model {
   int dtype = JET_BF16;  // requested mode
   int kdt = 0;           // kernel element type: 0 = bf16, 1 = fp32, 2 = fp16
   int edt = 0;           // element type of the embedding table (bf16 in the fp16 mode)
-  int pair = 1;          // activations and caches as (hi, lo) bf16 pairs
-  int np = 2;            // planes per activation element (2 with pair)
+  int pair = 1;          // FFN, delta-rule and final-norm activations as (hi, lo) pairs
+  int np = 2;            // planes per such activation element (2 with pair)
+  int apair = 1;         // attention-side activations (attention-layer inputs, q, K/V caches,
+                         // probabilities, attention output) as (hi, lo) pairs
+  int anp = 2;           // planes per attention-side element
   int device = 0;
   hipStream_t st = nullptr;
   int64_t max_ctx = 0, prefill_budget = 0, wave_budget = 0, max_bytes = 0;

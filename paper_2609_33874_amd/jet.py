@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libjet.so")
 
 JET_OK, JET_E_INVALID, JET_E_CAPACITY, JET_E_OOM, JET_E_DEVICE, JET_E_IO = range(6)
-JET_BF16, JET_FP32, JET_BF16_SINGLE, JET_F16 = 0, 1, 2, 3
+JET_BF16, JET_FP32, JET_BF16_SINGLE, JET_F16, JET_F16P = 0, 1, 2, 3, 4
 JET_CHOICE, JET_BINARY, JET_ORDINAL = 0, 1, 2
 JET_FLAG_KERNEL_TIMING = 1
 KERNEL_CLASSES = ["gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "lmhead", "attn_prefix",

@@ -20,7 +20,7 @@ from paper_2609_33874_amd import jet as J
 
 pytestmark = pytest.mark.gpu
 
-TOL = {J.JET_FP32: 1e-4, J.JET_BF16: 2e-2, J.JET_F16: 2e-2}
+TOL = {J.JET_FP32: 1e-4, J.JET_BF16: 2e-2, J.JET_F16: 2e-2, J.JET_F16P: 2e-2}
 
 
 def log(msg):
@@ -66,7 +66,7 @@ def compare(path, wl, dtype, name):
     assert np.all(ds <= (m * t if dtype == J.JET_FP32 else 5e-2))
 
 
-@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_FP32, J.JET_F16])
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_FP32, J.JET_F16, J.JET_F16P])
 def test_attention_tile_boundaries(dtype, model_dir):
     path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
     wl = edge_workload(3000, [1, 63, 64, 65, 127, 128, 129, 200], [1, 2, 15, 16, 17], seed=11)

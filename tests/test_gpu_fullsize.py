@@ -28,6 +28,9 @@ def dense_1p5b_path():
 
 # the fp16 mode (what bench.py times) and the pair-bf16 mode
 DTYPES = [pytest.param(J.JET_F16, id="f16"), pytest.param(J.JET_BF16, id="bf16pair")]
+# the 64-layer model: fp16 with attention-side pairs (what bench.py times
+# there), and the pair-bf16 mode
+DTYPES_DEEP = [pytest.param(J.JET_F16P, id="f16p"), pytest.param(J.JET_BF16, id="bf16pair")]
 
 
 @pytest.fixture(scope="module")
@@ -140,7 +143,7 @@ def test_hybrid_4b_k4_full(dtype):
     sampled_parity(path, "hybrid_4b_k4", wl, tok, sums, [q], dtype)
 
 
-@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("dtype", DTYPES_DEEP)
 def test_dense_27b_k10_full(dtype):
     """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
     GPU; one whole candidate sequence (the shortest question's shortest

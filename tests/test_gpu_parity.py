@@ -20,7 +20,7 @@ from paper_2609_33874_amd import jet as J
 pytestmark = pytest.mark.gpu
 
 TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2), J.JET_BF16_SINGLE: (2e-2, 5e-2),
-       J.JET_F16: (2e-2, 5e-2)}
+       J.JET_F16: (2e-2, 5e-2), J.JET_F16P: (2e-2, 5e-2)}
 
 
 def log(msg):
@@ -85,6 +85,8 @@ CASES = [
     ("tiny_dense_bf16", "tiny", J.JET_F16),
     ("small_gqa_bf16", "small", J.JET_F16),
     ("small_hybrid_bf16", "small_hybrid", J.JET_F16),
+    ("small_gqa_bf16", "small", J.JET_F16P),
+    ("small_hybrid_bf16", "small_hybrid", J.JET_F16P),
 ]
 
 
@@ -137,7 +139,7 @@ def test_waves_and_budgets_do_not_change_scores(model_dir):
     np.testing.assert_allclose(b_tok, a_tok, atol=1e-5, rtol=0)
 
 
-@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16, J.JET_F16P])
 def test_duplicates_permutation_and_determinism(dtype, model_dir):
     path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
     base = jet_synth.make_workload("small", n_questions=4)
@@ -229,7 +231,7 @@ def test_device_budget_oom(model_dir):
     assert e.value.code == J.JET_E_OOM
 
 
-@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
+@pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16, J.JET_F16P])
 @pytest.mark.parametrize("spec,wname", [("small_hybrid_bf16", "small_hybrid"), ("small_gqa_bf16", "small")])
 def test_candidate_isolation_on_gpu(spec, wname, dtype, model_dir):
     """A candidate scored together with its siblings equals the same candidate
