@@ -645,20 +645,51 @@ Status check_ids(jet_model *m, const int32_t *ids, int64_t n, bool on_device, co
 // prefill
 // ---------------------------------------------------------------------------
 
+// A freed prefix's buffers go to the model's pool instead of hipFree (which
+// synchronises the device): repeated calls with similar shapes reuse them.
+// Every buffer a prefill takes is written before it is read (caches,
+// snapshots, last rows) or cleared (convolution tails), so stale contents
+// never leak into a new prefix.
+void release_pool(jet_model *m) {
+  for (auto &e : m->pool) dfree(m, e.second, e.first);
+  m->pool.clear();
+}
+
 void free_prefix(jet_prefix *p) {
   if (!p) return;
-  for (void *a : p->allocs) (void)hipFree(a);
   if (p->m) {
-    p->m->bytes_used -= std::min(p->m->bytes_used, p->bytes);
+    for (auto &a : p->allocs) p->m->pool.push_back({a.second, a.first});
     p->m->n_prefixes--;
+  } else {
+    for (auto &a : p->allocs) (void)hipFree(a.first);
   }
   delete p;
 }
 
 Status palloc(jet_prefix *p, size_t bytes, void **out) {
-  TRY(dmalloc(p->m, bytes, out));
-  p->allocs.push_back(*out);
-  p->bytes += bytes == 0 ? 256 : bytes;
+  jet_model *m = p->m;
+  if (bytes == 0) bytes = 256;
+  // the smallest pooled buffer that holds `bytes` without wasting over a quarter
+  size_t best = m->pool.size();
+  for (size_t i = 0; i < m->pool.size(); ++i) {
+    const size_t sz = m->pool[i].first;
+    if (sz >= bytes && sz - bytes <= bytes / 4 && (best == m->pool.size() || sz < m->pool[best].first)) best = i;
+  }
+  size_t got = bytes;
+  if (best < m->pool.size()) {
+    *out = m->pool[best].second;
+    got = m->pool[best].first;
+    m->pool.erase(m->pool.begin() + (std::ptrdiff_t)best);
+  } else {
+    Status s = dmalloc(m, bytes, out);
+    if (!s) {
+      if (m->pool.empty()) return s;
+      release_pool(m);
+      TRY(dmalloc(m, bytes, out));
+    }
+  }
+  p->allocs.push_back({*out, got});
+  p->bytes += got;
   return Status::ok();
 }
 
@@ -970,6 +1001,7 @@ void free_model(jet_model *m) {
   if (m->st) (void)hipStreamSynchronize(m->st);
   for (auto &kv : m->ws) (void)hipFree(kv.second.p);
   for (void *a : m->weight_allocs) (void)hipFree(a);
+  for (auto &e : m->pool) (void)hipFree(e.second);
   for (auto &p : m->pending) {
     (void)hipEventDestroy(p.a);
     (void)hipEventDestroy(p.b);

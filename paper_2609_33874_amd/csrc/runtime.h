@@ -70,6 +70,8 @@ struct jet_model {
   std::vector<jet::PendingTimer> pending;
   std::vector<hipEvent_t> event_pool;
   std::vector<void *> weight_allocs;
+  // device buffers of freed prefixes, kept for the next prefill (sizes in bytes)
+  std::vector<std::pair<size_t, void *>> pool;
   jet_stats stats{};
   int n_prefixes = 0;
 };
@@ -84,6 +86,6 @@ struct jet_prefix {
   std::vector<float *> conv_tail;    // per layer (delta-rule only), [n_q][kc-1][C]
   void *f_last = nullptr;            // [n_q][planes * d] final-normed last prefix rows
   float *lse_last = nullptr;         // [n_q]
-  std::vector<void *> allocs;
+  std::vector<std::pair<void *, size_t>> allocs;  // (buffer, allocated bytes)
   size_t bytes = 0;
 };
