@@ -25,12 +25,22 @@ struct GemmArgs {
   int K, KA, KB;  // K steps over K columns; A column k mod KA, B column k mod KB
   void *out;
   int64_t ldo;
-  int pair_out;   // SwiGLU: write (hi, lo) bf16 pairs, hi at column f, lo at N/2 + f
+  int pair_out;   // SwiGLU / QKV-RoPE: write (hi, lo) pairs
   float oscale;   // every product is multiplied by oscale before the epilogue
+  QkvRope rope;   // EPI_QKV_ROPE only
 };
 
+// (hi, lo) split of v stored at p[0] and p[ps] (lo only with pair).
+template <typename T>
+__device__ __forceinline__ void put_split(T *p, int64_t ps, float v, int pair) {
+  const T hi = from_f<T>(v);
+  p[0] = hi;
+  if (pair) p[ps] = from_f<T>(v - to_f<T>(hi));
+}
+
 // EPI: 0 = store fp32, 1 = fp32 residual add, 2 = SwiGLU into T (B rows
-// interleaved in blocks of 32 gate rows / 32 up rows), 3 = store T.
+// interleaved in blocks of 32 gate rows / 32 up rows), 3 = store T, 4 = RoPE
+// and scatter of q, K, V (waves of 128 columns = one head).
 template <class C, int EPI>
 __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> g) {
   using T = typename C::type;
@@ -43,7 +53,38 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
   gemm_tile<C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  if constexpr (EPI == 2) {
+  if constexpr (EPI == 4) {
+    static_assert(C::WN == 128 && C::NI == 4, "a wave's columns must be one head of 128");
+    const QkvRope &q = g.rope;
+    const int head = (n0 + wn * C::WN) >> 7;  // query heads, then key heads, then value heads
+    const int64_t ps = head < q.Hq ? q.q_ps : q.kv_ps;
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + wm * C::WM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (row >= g.M || head >= q.Hq + 2 * q.Hkv) continue;
+        T *dst;
+        if (head < q.Hq) dst = (T *)q.q_out + ((int64_t)row * q.Hq + head) * 128;
+        else if (head < q.Hq + q.Hkv) dst = (T *)q.k_cache + ((int64_t)(head - q.Hq) * q.S + q.slot0 + row) * 128;
+        else dst = (T *)q.v_cache + ((int64_t)(head - q.Hq - q.Hkv) * q.S + q.slot0 + row) * 128;
+        if (head < q.Hq + q.Hkv) {
+          const int64_t p = q.pos[row];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int d = j * 32 + (lane & 31);
+            const float x1 = acc[i][j][e] * g.oscale, x2 = acc[i][j + 2][e] * g.oscale;
+            const float c = q.cos_t[p * 64 + d], s = q.sin_t[p * 64 + d];
+            // the same operations as rope_scatter_kernel, so both paths round alike
+            put_split<T>(dst + d, ps, fmaf(x1, c, -(x2 * s)), g.pair_out);
+            put_split<T>(dst + d + 64, ps, fmaf(x2, c, x1 * s), g.pair_out);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) put_split<T>(dst + j * 32 + (lane & 31), ps, acc[i][j][e] * g.oscale, g.pair_out);
+        }
+      }
+  } else if constexpr (EPI == 2) {
     T *out = (T *)g.out;
 #pragma unroll
     for (int i = 0; i < C::MI; ++i)
@@ -213,7 +254,7 @@ static hipError_t run_gemm(const void *A, int64_t lda, const void *B, int64_t ld
   static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
   if (once != hipSuccess) return once;
   GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, pair ? 2 * K : K, pair ? 2 * K : K, K, out, ldo, pair,
-                oscale};
+                oscale, QkvRope{}};
   const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
   return hipGetLastError();
@@ -254,6 +295,34 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
     return run_epi<HalfB>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
   }
   return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+}
+
+template <class C>
+static hipError_t run_qkv_rope(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+                               int pair, float oscale, const QkvRope &r, hipStream_t st) {
+  using T = typename C::type;
+  static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, 4>);
+  if (once != hipSuccess) return once;
+  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, pair ? 2 * K : K, pair ? 2 * K : K, K, nullptr, 0,
+                pair, oscale, r};
+  const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_kernel<C, 4>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
+  return hipGetLastError();
+}
+
+bool gemm_qkv_rope_ok(int dtype, int pair, int M, int N, int head_dim) {
+  if (head_dim != 128 || N % 128 || M <= 0) return false;
+  const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+  // the 256x256 configurations have waves of 128 columns
+  return (dtype == 0 && pair && big_tiles >= 512) || (dtype == 2 && big_tiles >= 512);
+}
+
+hipError_t launch_gemm_qkv_rope(int dtype, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N,
+                                int K, int pair, float oscale, const QkvRope &r, hipStream_t st) {
+  if (!gemm_qkv_rope_ok(dtype, pair, M, N, 128)) return hipErrorInvalidValue;
+  if (dtype == 0) return run_qkv_rope<PairB>(A, lda, B, ldb, M, N, K, pair, oscale, r, st);
+  if (pair) return run_qkv_rope<HalfPairB>(A, lda, B, ldb, M, N, K, pair, oscale, r, st);
+  return run_qkv_rope<HalfB>(A, lda, B, ldb, M, N, K, 0, oscale, r, st);
 }
 
 void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit) {

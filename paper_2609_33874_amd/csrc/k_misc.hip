@@ -119,7 +119,8 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *__restri
     const int h = t / half, i = t % half;
     const float x1 = src[h * hd + i], x2 = src[h * hd + i + half];
     const float c = cs[i], s = sn[i];
-    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    // the same operations as the QKV GEMM's RoPE epilogue, so both paths round alike
+    const float y1 = fmaf(x1, c, -(x2 * s)), y2 = fmaf(x2, c, x1 * s);
     if (h < Hq) {
       T *o = q_out + ((int64_t)r * Hq + h) * hd;
       put_val<T, PAIR>(o + i, q_ps, y1);

@@ -8,7 +8,28 @@
 
 namespace jetk {
 
-enum { EPI_STORE_F32 = 0, EPI_RESID_ADD = 1, EPI_SWIGLU = 2, EPI_STORE_T = 3 };
+enum { EPI_STORE_F32 = 0, EPI_RESID_ADD = 1, EPI_SWIGLU = 2, EPI_STORE_T = 3, EPI_QKV_ROPE = 4 };
+
+// Epilogue of the attention input projection (EPI_QKV_ROPE): the columns are
+// Hq query heads, Hkv key heads and Hkv value heads of head_dim 128; RoPE is
+// applied to q and k in registers (pairs (d, d + 64), angle from pos[row])
+// and q, K, V are stored in T like launch_rope_scatter stores them (with
+// pair, (hi, lo) planes at +q_ps and +kv_ps), so the fp32 projection output
+// is never written.
+struct QkvRope {
+  const int32_t *pos;
+  const float *cos_t, *sin_t;  // [positions][64]
+  int Hq, Hkv;
+  void *q_out;
+  int64_t q_ps;
+  void *k_cache, *v_cache;  // [planes][Hkv][S][128]
+  int64_t kv_ps, S, slot0;
+};
+// Whether launch_gemm_qkv_rope can run this problem (head_dim 128 and a tile
+// configuration whose waves cover whole heads).
+bool gemm_qkv_rope_ok(int dtype, int pair, int M, int N, int head_dim);
+hipError_t launch_gemm_qkv_rope(int dtype, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N,
+                                int K, int pair, float oscale, const QkvRope &r, hipStream_t st);
 
 // C[M x N] (epilogue) A[M x K] * B[N x K]^T. K must be a multiple of
 // gemm_k_step(dtype). pair (bf16 only): every A row holds a (hi, lo) bf16

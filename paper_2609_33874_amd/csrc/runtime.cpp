@@ -554,6 +554,17 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->apair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d,
                                 (float)h.rms_eps, b.xn, m->st));
   }
+  if (jetk::gemm_qkv_rope_ok(m->kdt, m->apair, (int)R, (int)nqkv, (int)h.head_dim)) {
+    // projection, RoPE and the K/V scatter in one kernel
+    const double out_bytes = (double)R * (double)nqkv * (double)m->esz * m->anp;
+    KTimer t(m, JET_K_GEMM_QKV, gemm_flops(R, nqkv, h.d),
+             (double)(R * h.d * m->anp + nqkv * h.d) * (double)m->esz + out_bytes);
+    jetk::QkvRope r{d_pos, m->rope_cos, m->rope_sin, (int)h.n_heads, (int)h.n_kv_heads, b.q,
+                    R * h.n_heads * h.head_dim, kc, vc, h.n_kv_heads * S * h.head_dim, S, slot0};
+    LAUNCH(jetk::launch_gemm_qkv_rope(m->kdt, b.xn, m->anp * h.d, ly.w_qkv, h.d, (int)R, (int)nqkv, (int)h.d, m->apair,
+                                      ly.is_qkv, r, m->st));
+    return Status::ok();
+  }
   TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->anp * h.d, m->apair, ly.w_qkv, h.d, R, nqkv, h.d,
                b.qkv, nqkv, ly.is_qkv));
   KTimer t(m, JET_K_OTHER, 0, 0);
