@@ -227,7 +227,8 @@ using LmB = GCfg<bf16, 256, 256, 128, 64, 4, 1, 2, 8>;
 using LmF = GCfg<float, 128, 128, 64, 64, 0, 1>;
 // fp16 operands: the LOAD 7 schedule with a single A plane (three 32 KB
 // stages of 32-column A and B tiles), 256x256 tiles with waves of 64 x 128,
-// or 128x128 tiles for problems with fewer tiles; the LM head as in bf16.
+// or 128x128 tiles for problems with fewer tiles; the LM head on the same
+// 256x256 schedule (16% faster than the two-stage 128-byte-row one).
 using HalfB = GCfg<f16, 256, 256, 64, 128, 8, 2, 3, 4>;
 using HalfS = GCfg<f16, 128, 128, 32, 64, 8, 2, 3, 4>;
 // Residual-add GEMMs with a short K loop (the attention output projection):
@@ -238,7 +239,7 @@ using HalfM = GCfg<f16, 256, 128, 64, 64, 8, 2, 3, 4>;
 // (hi, lo) fp16 pair A operands: the bf16 pair schedules with fp16 operands
 using HalfPairB = GCfg<f16, 256, 256, 64, 128, 7, 2, 3, 4>;
 using HalfPairS = GCfg<f16, 128, 128, 32, 64, 7, 2, 3, 4>;
-using LmH = GCfg<f16, 256, 256, 128, 64, 4, 1, 2, 8>;
+using LmH = GCfg<f16, 256, 256, 64, 128, 8, 2, 3, 4>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
 template <class C>

@@ -169,6 +169,40 @@ def test_duplicates_permutation_and_determinism(dtype, model_dir):
         assert got[dup[0]] == got[dup[1]]
 
 
+@pytest.mark.parametrize("dtype", [J.JET_F16, J.JET_F16P])
+def test_reused_prefix_buffers(dtype, model_dir):
+    """A prefix's device buffers go back to the model's pool when it is freed
+    and the next prefill takes them with their old contents: scores must not
+    depend on that (every buffer is written before it is read)."""
+    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
+    a = jet_synth.make_workload("small", n_questions=6)
+    b = jet_synth.make_workload("small", n_questions=6, seed=7)
+    m = J.jet_model_load(path, dtype=dtype)
+    try:
+        def run(wl):
+            p = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+            try:
+                return J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+            finally:
+                J.jet_prefix_free(p)
+        ta, sa = run(a)        # fresh buffers
+        run(b)                 # same sizes class, other contents
+        ta2, sa2 = run(a)      # buffers reused from the pool
+        np.testing.assert_array_equal(ta, ta2)
+        np.testing.assert_array_equal(sa, sa2)
+        # a second live prefix while the first is held: distinct buffers
+        p1 = J.jet_prefill_prefix(m, a.prefix_offsets, a.prefix_tokens)
+        p2 = J.jet_prefill_prefix(m, b.prefix_offsets, b.prefix_tokens)
+        try:
+            t1, _ = J.jet_score_candidates(m, p1, a.q_cand_offsets, a.cand_tok_offsets, a.cand_tokens)
+            np.testing.assert_array_equal(t1, ta)
+        finally:
+            J.jet_prefix_free(p2)
+            J.jet_prefix_free(p1)
+    finally:
+        J.jet_model_free(m)
+
+
 @pytest.mark.parametrize("dtype", [J.JET_BF16, J.JET_F16])
 def test_device_resident_inputs_and_outputs(dtype, model_dir):
     import torch
