@@ -1,9 +1,11 @@
 // Grouped-query attention on matrix cores for gfx950.
 //
 // One workgroup (4 waves) takes up to 64 query slots of one (question, KV
-// head): slot s is query head kvh * G + s / nrows at row s % nrows, so the
-// G query heads that share a KV head share every K/V tile the workgroup stages
-// in LDS. Two modes:
+// head): slot s is query head kvh * G + s % G at row s / G, so the G query
+// heads that share a KV head share every K/V tile the workgroup stages in
+// LDS, a block's rows lie within 64 / G of each other (causal prefix blocks
+// stop at nearly the same key), and consecutive lanes read consecutive heads
+// of one row of Q and O. Two modes:
 //   mode 0, prefix prefill: query i of a question sees prefix keys 0..i.
 //   mode 1, candidates: a candidate row sees every key of its question's
 //     retained prefix (read-only, staged once per tile for all the slots),
@@ -122,13 +124,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 
   const AttnItem it = a.items[blockIdx.x];
   const int G = a.Hq / a.Hkv;
-  const int nrows = a.qs.nrows[it.q], qrow0 = a.qs.qrow0[it.q];
+  const int qrow0 = a.qs.qrow0[it.q];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
   const int sl = wave * 16 + (lane & 15);
   const bool valid = sl < it.nslots;
   const int slot = it.slot0 + (valid ? sl : 0);
-  const int head = it.kvh * G + slot / nrows;
-  const int qi = slot % nrows;
+  const int head = it.kvh * G + slot % G;
+  const int qi = slot / G;
   const int row = qrow0 + qi;
   const T *Q = (const T *)a.Q;
 

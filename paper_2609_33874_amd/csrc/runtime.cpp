@@ -414,7 +414,8 @@ struct QDesc {
   std::vector<int64_t> pre_slot0;
 };
 
-// Work items: per (question, kv head), blocks of 64 (head, row) slots.
+// Work items: per (question, kv head), blocks of 64 (row, head) slots, slot
+// s = G row + (head - kvh G); a causal block needs the keys up to its last row.
 void build_items(const QDesc &qd, int G, int Hkv, bool causal, std::vector<jetk::AttnItem> *items,
                  double *flops_pairs) {
   items->clear();
@@ -426,9 +427,7 @@ void build_items(const QDesc &qd, int G, int Hkv, bool causal, std::vector<jetk:
     for (int kvh = 0; kvh < Hkv; ++kvh)
       for (int s0 = 0; s0 < total; s0 += 64) {
         const int ns = std::min(64, total - s0);
-        int maxq;
-        if (s0 / n != (s0 + ns - 1) / n) maxq = n - 1;
-        else maxq = (s0 + ns - 1) % n;
+        const int maxq = (s0 + ns - 1) / G;
         items->push_back({(int32_t)q, kvh, s0, ns, maxq + 1});
       }
     if (causal) pairs += (double)G * Hkv * (double)n * (double)(n + 1) / 2.0;
