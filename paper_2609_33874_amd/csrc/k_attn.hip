@@ -112,7 +112,10 @@ __device__ __forceinline__ void v_frag(Frag<float> &f, const float *vt, int d, i
   f.v[4] = __uint_as_float(b.x); f.v[5] = __uint_as_float(b.y); f.v[6] = __uint_as_float(b.z); f.v[7] = __uint_as_float(b.w);
 }
 
-template <typename T, int HD, int MODE, bool PAIR>
+// QB blocks of 16 query slots per wave (64 QB per workgroup): every K and V
+// fragment read from LDS feeds QB MFMAs, and every staged tile serves 64 QB
+// queries.
+template <typename T, int HD, int MODE, bool PAIR, int QB>
 __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int KT = 64;                        // keys per tile
   constexpr int EPC = 16 / (int)sizeof(T);      // elements per 16-byte chunk
@@ -126,30 +129,44 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int G = a.Hq / a.Hkv;
   const int qrow0 = a.qs.qrow0[it.q];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
-  const int sl = wave * 16 + (lane & 15);
-  const bool valid = sl < it.nslots;
-  const int slot = it.slot0 + (valid ? sl : 0);
-  const int head = it.kvh * G + slot % G;
-  const int qi = slot / G;
-  const int row = qrow0 + qi;
+  bool valid[QB];
+  int head[QB], qi[QB], row[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int sl = (wave * QB + qb) * 16 + (lane & 15);
+    valid[qb] = sl < it.nslots;
+    const int slot = it.slot0 + (valid[qb] ? sl : 0);
+    head[qb] = it.kvh * G + slot % G;
+    qi[qb] = slot / G;
+    row[qb] = qrow0 + qi[qb];
+  }
   const T *Q = (const T *)a.Q;
 
-  Frag<T> qf[NP][HD / 32];
+  Frag<T> qf[QB][NP][HD / 32];
 #pragma unroll
-  for (int p = 0; p < NP; ++p)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks) {
-      if (valid) frag_load(qf[p][ks], Q + p * a.q_ps + ((int64_t)row * a.Hq + head) * HD + ks * 32 + g * 8);
-      else qf[p][ks].zero();
-    }
-  int my_t = 0;
-  if (MODE == 1 && valid) my_t = a.row_t[row];
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        if (valid[qb])
+          frag_load(qf[qb][p][ks], Q + p * a.q_ps + ((int64_t)row[qb] * a.Hq + head[qb]) * HD + ks * 32 + g * 8);
+        else qf[qb][p][ks].zero();
+      }
+  int my_t[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) my_t[qb] = (MODE == 1 && valid[qb]) ? a.row_t[row[qb]] : 0;
 
   const float scale2 = a.scale * kLog2e;
-  float m_run = -INFINITY, l_run = 0.0f;
-  f32x4 acc[HD / 16];
+  float m_run[QB], l_run[QB];
+  f32x4 acc[QB][HD / 16];
 #pragma unroll
-  for (int d = 0; d < HD / 16; ++d) acc[d] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.0f;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) acc[qb][d] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
 
   const T *Kp = (const T *)a.Kp, *Vp = (const T *)a.Vp;
   const int64_t pslot = a.qs.pre_slot0[it.q];
@@ -230,178 +247,205 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     __syncthreads();
     if (tix + 1 < ntile) issue_tile(kbase + KT, min(KT, npre - kbase - KT), kreg, vreg);
 
-    f32x4 s[4];
+    f32x4 s[QB][4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      s[kb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) s[qb][kb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       const int key = kb * 16 + (lane & 15);
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
         const int c0 = (ks * 32 + g * 8) / EPC;
         Frag<T> fk;
         lds_kfrag<T>(fk, &Ks[0][key * CPR], c0, key & (KSW - 1));
-        mma16(s[kb], fk, qf[0][ks]);
+        Frag<T> fkl;
+        if constexpr (PAIR) lds_kfrag<T>(fkl, &Ks[NP - 1][key * CPR], c0, key & (KSW - 1));
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          mma16(s[qb][kb], fk, qf[qb][0][ks]);
+          if constexpr (PAIR) {
+            mma16(s[qb][kb], fkl, qf[qb][0][ks]);
+            mma16(s[qb][kb], fk, qf[qb][NP - 1][ks]);
+          }
+        }
+      }
+    }
+    Frag<T> pf[QB][2], pfl[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
+      // tiles every key of which every query of the wave's block sees skip the mask
+      if (__all(tile_full && (MODE != 0 || kbase + KT - 1 <= qi[qb]))) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s[qb][kb][e] *= scale2;
+            mx = fmaxf(mx, s[qb][kb][e]);
+          }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int key = kb * 16 + 4 * g + e;
+            bool vis = key < nk;
+            if (MODE == 0) vis = vis && (kbase + key <= qi[qb]);
+            const float z = vis ? s[qb][kb][e] * scale2 : -INFINITY;
+            s[qb][kb][e] = z;
+            mx = fmaxf(mx, z);
+          }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // Every query sees key 0 in the first tile (mode 0) or the whole prefix
+      // (mode 1), so m_new is finite: exp2 of the (<= 0) differences directly,
+      // with exp2(-inf) = 0 for masked keys and for the initial m_run.
+      const float m_new = fmaxf(m_run[qb], mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+      float p[4][4];
+      float psum = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          p[kb][e] = __builtin_amdgcn_exp2f(s[qb][kb][e] - m_new);
+          psum += p[kb][e];
+        }
+      l_run[qb] = l_run[qb] * alpha + psum;
+      if (__any(alpha != 1.0f)) {
+#pragma unroll
+        for (int d = 0; d < HD / 16; ++d) acc[qb][d] *= alpha;
+      }
+      m_run[qb] = m_new;
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm) {
+        const float x8[8] = {p[2 * mm][0], p[2 * mm][1], p[2 * mm][2], p[2 * mm][3],
+                             p[2 * mm + 1][0], p[2 * mm + 1][1], p[2 * mm + 1][2], p[2 * mm + 1][3]};
+        pf[qb][mm] = pack8<T>(x8);
         if constexpr (PAIR) {
-          Frag<T> fkl;
-          lds_kfrag<T>(fkl, &Ks[NP - 1][key * CPR], c0, key & (KSW - 1));
-          mma16(s[kb], fkl, qf[0][ks]);
-          mma16(s[kb], fk, qf[NP - 1][ks]);
+          float r8[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) r8[j] = x8[j] - (float)pf[qb][mm].v[j];
+          pfl[qb][mm] = pack8<T>(r8);
         }
       }
     }
-    float mx = -INFINITY;
-    // tiles every key of which every query of the wave sees skip the mask
-    if (__all(tile_full && (MODE != 0 || kbase + KT - 1 <= qi))) {
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s[kb][e] *= scale2;
-          mx = fmaxf(mx, s[kb][e]);
-        }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = kb * 16 + 4 * g + e;
-          bool vis = key < nk;
-          if (MODE == 0) vis = vis && (kbase + key <= qi);
-          const float z = vis ? s[kb][e] * scale2 : -INFINITY;
-          s[kb][e] = z;
-          mx = fmaxf(mx, z);
-        }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // Every query sees key 0 in the first tile (mode 0) or the whole prefix
-    // (mode 1), so m_new is finite: exp2 of the (<= 0) differences directly,
-    // with exp2(-inf) = 0 for masked keys and for the initial m_run.
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float p[4][4];
-    float psum = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        p[kb][e] = __builtin_amdgcn_exp2f(s[kb][e] - m_new);
-        psum += p[kb][e];
-      }
-    l_run = l_run * alpha + psum;
-    if (__any(alpha != 1.0f)) {
-#pragma unroll
-      for (int d = 0; d < HD / 16; ++d) acc[d] *= alpha;
-    }
-    m_run = m_new;
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm) {
-      const float x8[8] = {p[2 * mm][0], p[2 * mm][1], p[2 * mm][2], p[2 * mm][3],
-                           p[2 * mm + 1][0], p[2 * mm + 1][1], p[2 * mm + 1][2], p[2 * mm + 1][3]};
-      const Frag<T> pf = pack8<T>(x8);
-      Frag<T> pfl;
-      if constexpr (PAIR) {
-        float r8[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) r8[j] = x8[j] - (float)pf.v[j];
-        pfl = pack8<T>(r8);
-      }
 #pragma unroll
       for (int db = 0; db < HD / 16; ++db) {
         const int d = db * 16 + (lane & 15);
-        Frag<T> fv;
+        Frag<T> fv, fvl;
         v_frag<KT>(fv, &Vt[0][0], d, mm, g);
-        mma16(acc[db], fv, pf);
-        if constexpr (PAIR) {
-          Frag<T> fvl;
-          v_frag<KT>(fvl, &Vt[NP - 1][0], d, mm, g);
-          mma16(acc[db], fvl, pf);
-          mma16(acc[db], fv, pfl);
+        if constexpr (PAIR) v_frag<KT>(fvl, &Vt[NP - 1][0], d, mm, g);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          mma16(acc[qb][db], fv, pf[qb][mm]);
+          if constexpr (PAIR) {
+            mma16(acc[qb][db], fvl, pf[qb][mm]);
+            mma16(acc[qb][db], fv, pfl[qb][mm]);
+          }
         }
       }
     }
   }
 
-  if constexpr (MODE == 1) {
-    // own rows of the candidate: row - my_t + 1 .. row of the call's K / V
-    // (rows are ordered by candidate, then position). Lane group g holds the
-    // query dims 32 ks + 8 g + j (score) and the output dims 16 db + 4 g + e.
-    int tmax = valid ? my_t : 0;
-    for (int o = 1; o < 64; o <<= 1) tmax = max(tmax, __shfl_xor(tmax, o));
-    const T *Kc = (const T *)a.Ks + (int64_t)it.kvh * a.s_suf * HD;
-    const T *Vc = (const T *)a.Vs + (int64_t)it.kvh * a.s_suf * HD;
-    for (int i = 0; i < tmax; ++i) {
-      const bool act = valid && i < my_t;
-      const int64_t krow = (int64_t)row - my_t + 1 + i;
-      float part = 0.0f;
-      if (act) {
-        const T *kr = Kc + krow * HD;
 #pragma unroll
-        for (int ks = 0; ks < HD / 32; ++ks)
+  for (int qb = 0; qb < QB; ++qb) {
+    if constexpr (MODE == 1) {
+      // own rows of the candidate: row - my_t + 1 .. row of the call's K / V
+      // (rows are ordered by candidate, then position). Lane group g holds the
+      // query dims 32 ks + 8 g + j (score) and the output dims 16 db + 4 g + e.
+      int tmax = valid[qb] ? my_t[qb] : 0;
+      for (int o = 1; o < 64; o <<= 1) tmax = max(tmax, __shfl_xor(tmax, o));
+      const T *Kc = (const T *)a.Ks + (int64_t)it.kvh * a.s_suf * HD;
+      const T *Vc = (const T *)a.Vs + (int64_t)it.kvh * a.s_suf * HD;
+      for (int i = 0; i < tmax; ++i) {
+        const bool act = valid[qb] && i < my_t[qb];
+        const int64_t krow = (int64_t)row[qb] - my_t[qb] + 1 + i;
+        float part = 0.0f;
+        if (act) {
+          const T *kr = Kc + krow * HD;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int d = ks * 32 + g * 8 + j;
-            float kv = to_f<T>(kr[d]);
-            if constexpr (PAIR) kv += to_f<T>(kr[a.ks_ps + d]);
-            float qv = to_f<T>(reinterpret_cast<const T *>(&qf[0][ks].v)[j]);
-            if constexpr (PAIR) qv += to_f<T>(reinterpret_cast<const T *>(&qf[NP - 1][ks].v)[j]);
-            part += qv * kv;
-          }
-      }
-      part += __shfl_xor(part, 16);
-      part += __shfl_xor(part, 32);
-      if (act) {
-        const float z = part * scale2;
-        const float m_new = fmaxf(m_run, z);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // arguments <= 0
-        const float pz = __builtin_amdgcn_exp2f(z - m_new);
-        l_run = l_run * alpha + (g == 0 ? pz : 0.0f);
-        const T *vr = Vc + krow * HD;
+          for (int ks = 0; ks < HD / 32; ++ks)
 #pragma unroll
-        for (int db = 0; db < HD / 16; ++db)
+            for (int j = 0; j < 8; ++j) {
+              const int d = ks * 32 + g * 8 + j;
+              float kv = to_f<T>(kr[d]);
+              if constexpr (PAIR) kv += to_f<T>(kr[a.ks_ps + d]);
+              float qv = to_f<T>(reinterpret_cast<const T *>(&qf[qb][0][ks].v)[j]);
+              if constexpr (PAIR) qv += to_f<T>(reinterpret_cast<const T *>(&qf[qb][NP - 1][ks].v)[j]);
+              part += qv * kv;
+            }
+        }
+        part += __shfl_xor(part, 16);
+        part += __shfl_xor(part, 32);
+        if (act) {
+          const float z = part * scale2;
+          const float m_new = fmaxf(m_run[qb], z);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);  // arguments <= 0
+          const float pz = __builtin_amdgcn_exp2f(z - m_new);
+          l_run[qb] = l_run[qb] * alpha + (g == 0 ? pz : 0.0f);
+          const T *vr = Vc + krow * HD;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int d = db * 16 + 4 * g + e;
-            float vv = to_f<T>(vr[d]);
-            if constexpr (PAIR) vv += to_f<T>(vr[a.ks_ps + d]);
-            acc[db][e] = acc[db][e] * alpha + pz * vv;
-          }
-        m_run = m_new;
+          for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int d = db * 16 + 4 * g + e;
+              float vv = to_f<T>(vr[d]);
+              if constexpr (PAIR) vv += to_f<T>(vr[a.ks_ps + d]);
+              acc[qb][db][e] = acc[qb][db][e] * alpha + pz * vv;
+            }
+          m_run[qb] = m_new;
+        }
       }
     }
-  }
 
-  float l_tot = l_run + __shfl_xor(l_run, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-  if (!valid) return;
-  const float inv = 1.0f / l_tot;
-  T *O = (T *)a.O;
+    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (valid[qb]) {
+      const float inv = 1.0f / l_tot;
+      T *O = (T *)a.O;
 #pragma unroll
-  for (int db = 0; db < HD / 16; ++db) {
-    // dims 16 db + 4 g .. + 3 of this lane's query, one 8- (bf16) or 16-byte (fp32) store per plane
-    float o[4], lo[4];
+      for (int db = 0; db < HD / 16; ++db) {
+        // dims 16 db + 4 g .. + 3 of this lane's query, one 8- (bf16) or 16-byte (fp32) store per plane
+        float o[4], lo[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = acc[db][e] * inv;
-    T *dst = O + (int64_t)row * a.o_ld + (int64_t)head * HD + db * 16 + 4 * g;
-    if constexpr (sizeof(T) == 2) {
-      const uint2 hi = make_uint2(pack2<T>(o[0], o[1]), pack2<T>(o[2], o[3]));
-      *reinterpret_cast<uint2 *>(dst) = hi;
-      if constexpr (PAIR) {
+        for (int e = 0; e < 4; ++e) o[e] = acc[qb][db][e] * inv;
+        T *dst = O + (int64_t)row[qb] * a.o_ld + (int64_t)head[qb] * HD + db * 16 + 4 * g;
+        if constexpr (sizeof(T) == 2) {
+          const uint2 hi = make_uint2(pack2<T>(o[0], o[1]), pack2<T>(o[2], o[3]));
+          *reinterpret_cast<uint2 *>(dst) = hi;
+          if constexpr (PAIR) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) lo[e] = o[e] - to_f<T>(from_f<T>(o[e]));
-        *reinterpret_cast<uint2 *>(dst + (int64_t)a.Hq * HD) = make_uint2(pack2<T>(lo[0], lo[1]), pack2<T>(lo[2], lo[3]));
+            for (int e = 0; e < 4; ++e) lo[e] = o[e] - to_f<T>(from_f<T>(o[e]));
+            *reinterpret_cast<uint2 *>(dst + (int64_t)a.Hq * HD) =
+                make_uint2(pack2<T>(lo[0], lo[1]), pack2<T>(lo[2], lo[3]));
+          }
+        } else {
+          *reinterpret_cast<float4 *>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+        }
       }
-    } else {
-      *reinterpret_cast<float4 *>(dst) = make_float4(o[0], o[1], o[2], o[3]);
     }
   }
 }
 
+// Query blocks per wave: two for single 16-bit planes, one for (hi, lo)
+// pairs and fp32 (their fragments take twice the registers).
+template <typename T, bool PAIR>
+constexpr int attn_qb() {
+  return sizeof(T) == 2 && !PAIR ? 2 : 1;
+}
+
+int attn_slots_per_item(int dtype, int pair) { return (dtype == 1 || pair) ? 64 : 128; }
+
 template <typename T, int HD, bool PAIR>
 static hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
+  constexpr int QB = attn_qb<T, PAIR>();
   if (a.n_items <= 0) return hipSuccess;
-  if (a.mode == 0) hipLaunchKernelGGL((attn_kernel<T, HD, 0, PAIR>), dim3(a.n_items), dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((attn_kernel<T, HD, 1, PAIR>), dim3(a.n_items), dim3(256), 0, st, a);
+  if (a.mode == 0) hipLaunchKernelGGL((attn_kernel<T, HD, 0, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((attn_kernel<T, HD, 1, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

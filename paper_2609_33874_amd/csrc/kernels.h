@@ -53,7 +53,8 @@ hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int
 hipError_t launch_lse_merge(const float *part_m, const float *part_s, int nsplit, int R, float *lse,
                             hipStream_t st);
 
-// Attention work item: one (question, kv head, block of <= 64 query slots).
+// Attention work item: one (question, kv head, block of at most
+// attn_slots_per_item query slots).
 struct AttnItem {
   int32_t q, kvh, slot0, nslots, nkeys_pre;
 };
@@ -90,6 +91,8 @@ struct AttnArgs {
   float scale;
 };
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st);
+// Query slots per work item that launch_attention expects (64 or 128).
+int attn_slots_per_item(int dtype, int pair);
 
 // Gated delta-rule layers. Projection output x [R][ldx] = q~ (H dk) | k~ (H dk)
 // | v~ (H dv) | z (H dv) | b (H) | a (H), fp32. hist[3 r + j - 1] names the

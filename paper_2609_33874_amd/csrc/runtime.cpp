@@ -414,9 +414,10 @@ struct QDesc {
   std::vector<int64_t> pre_slot0;
 };
 
-// Work items: per (question, kv head), blocks of 64 (row, head) slots, slot
-// s = G row + (head - kvh G); a causal block needs the keys up to its last row.
-void build_items(const QDesc &qd, int G, int Hkv, bool causal, std::vector<jetk::AttnItem> *items,
+// Work items: per (question, kv head), blocks of `block` (row, head) slots,
+// slot s = G row + (head - kvh G); a causal block needs the keys up to its
+// last row.
+void build_items(const QDesc &qd, int G, int Hkv, bool causal, int block, std::vector<jetk::AttnItem> *items,
                  double *flops_pairs) {
   items->clear();
   double pairs = 0;
@@ -425,8 +426,8 @@ void build_items(const QDesc &qd, int G, int Hkv, bool causal, std::vector<jetk:
     if (n <= 0) continue;
     const int total = G * n;
     for (int kvh = 0; kvh < Hkv; ++kvh)
-      for (int s0 = 0; s0 < total; s0 += 64) {
-        const int ns = std::min(64, total - s0);
+      for (int s0 = 0; s0 < total; s0 += block) {
+        const int ns = std::min(block, total - s0);
         const int maxq = (s0 + ns - 1) / G;
         items->push_back({(int32_t)q, kvh, s0, ns, maxq + 1});
       }
@@ -448,7 +449,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   const int G = (int)(h.n_heads / h.n_kv_heads);
   std::vector<jetk::AttnItem> items;
   double pairs = 0;
-  build_items(qd, G, (int)h.n_kv_heads, mode == 0, &items, &pairs);
+  build_items(qd, G, (int)h.n_kv_heads, mode == 0, jetk::attn_slots_per_item(m->kdt, m->apair), &items, &pairs);
   jetk::AttnItem *d_items;
   int32_t *d_qrow0, *d_nrows, *d_prelen, *d_sufrow0, *d_suflen;
   int64_t *d_preslot;
