@@ -18,53 +18,99 @@
 
 namespace jetk {
 
-// One block per row. x: projection output [R][ldx] = q~ | k~ | v~ | z | b | a.
-__global__ __launch_bounds__(256) void gdn_conv_kernel(GdnConvArgs g) {
-  extern __shared__ float sc[];  // C conv + SiLU outputs of this row
-  const int r = blockIdx.x, tid = threadIdx.x;
+// Convolution, gates and normalisation of the delta-rule inputs. x:
+// projection output [R][ldx] = q~ | k~ | v~ | z | b | a. One half-wave (32
+// lanes, 4 channels each) takes one group of 128 channels (one head of q~, k~
+// or v~; dk = dv = 128) over a block of GDN_CONV_RB consecutive rows, walked in
+// order: the inputs of the previous three rows stay in registers and are
+// reused whenever a row's history names the row before it (a row of the same
+// sequence), so every input element is read once. The l2 norm of a q / k head
+// is a reduction over the 32 lanes of the half-wave.
+constexpr int GDN_CONV_RB = 16;
+
+__device__ __forceinline__ float4 ld4f(const float *p, bool aligned) {
+  if (aligned) return *reinterpret_cast<const float4 *>(p);
+  return make_float4(p[0], p[1], p[2], p[3]);
+}
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+
+__global__ __launch_bounds__(256) void gdn_conv_kernel(GdnConvArgs g, int R) {
   const int H = g.H, dk = g.dk, dv = g.dv;
   const int C = 2 * H * dk + H * dv;
-  const float *xr = g.x + (int64_t)r * g.ldx;
-  const float *src[3];
+  const int ngroups = C / 128;
+  const int hw = blockIdx.x * 8 + (threadIdx.x >> 5), lane = threadIdx.x & 31;
+  const int nrb = (R + GDN_CONV_RB - 1) / GDN_CONV_RB;
+  if (hw >= nrb * ngroups) return;  // no barriers or LDS below
+  const int rb = hw / ngroups, cg = hw % ngroups;
+  const int c = cg * 128 + lane * 4;
+  const bool al = (g.ldx & 3) == 0;
+  float4 w[4];  // taps of channels c .. c + 3; tap 3 multiplies the current row
 #pragma unroll
-  for (int j = 1; j <= 3; ++j) {
-    const int h = g.hist[(int64_t)r * 3 + j - 1];
-    src[j - 1] = h >= 0 ? g.x + (int64_t)h * g.ldx : (h == -1 ? nullptr : g.tail + (int64_t)(-2 - h) * C);
-  }
-  const int ts = g.tail_slot ? g.tail_slot[r] : -1;
-  for (int c = tid; c < C; c += 256) {
-    float acc = g.conv_w[c * 4 + 3] * xr[c];
-#pragma unroll
-    for (int j = 1; j <= 3; ++j)
-      if (src[j - 1]) acc += g.conv_w[c * 4 + 3 - j] * src[j - 1][c];
-    sc[c] = acc / (1.0f + __expf(-acc));
-    if (ts >= 0) g.tail[(int64_t)ts * C + c] = xr[c];
-  }
-  __syncthreads();
-  const int wave = tid >> 6, lane = tid & 63;
+  for (int e = 0; e < 4; ++e) w[e] = *reinterpret_cast<const float4 *>(g.conv_w + (int64_t)(c + e) * 4);
   const float qscale = rsqrtf((float)dk);
-  for (int hh = wave; hh < 2 * H; hh += 4) {
-    const int base = hh * dk;
-    float ss = 0.0f;
-    for (int i = lane; i < dk; i += 64) ss += sc[base + i] * sc[base + i];
-    ss = warp_sum(ss);
-    float inv = rsqrtf(ss + 1e-6f);
-    float *out;
-    if (hh < H) {
-      inv *= qscale;
-      out = g.q + ((int64_t)r * H + hh) * dk;
-    } else {
-      out = g.k + ((int64_t)r * H + hh - H) * dk;
+  const int r0 = rb * GDN_CONV_RB, r1 = min(R, r0 + GDN_CONV_RB);
+  float4 win[3] = {};  // inputs of rows r - 1, r - 2, r - 3
+  for (int r = r0; r < r1; ++r) {
+    const float4 xc = ld4f(g.x + (int64_t)r * g.ldx + c, al);
+    float4 src[3];
+    bool has[3];
+#pragma unroll
+    for (int j = 1; j <= 3; ++j) {
+      const int h = g.hist[(int64_t)r * 3 + j - 1];
+      has[j - 1] = h != -1;
+      if (h == r - j && r - j >= r0) src[j - 1] = win[j - 1];
+      else if (h >= 0) src[j - 1] = ld4f(g.x + (int64_t)h * g.ldx + c, al);
+      else if (h <= -2) src[j - 1] = *reinterpret_cast<const float4 *>(g.tail + (int64_t)(-2 - h) * C + c);
+      else src[j - 1] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
-    for (int i = lane; i < dk; i += 64) out[i] = sc[base + i] * inv;
-  }
-  for (int i = tid; i < H * dv; i += 256) g.v[(int64_t)r * H * dv + i] = sc[2 * H * dk + i];
-  if (tid < H) {
-    const float b = xr[C + H * dv + tid], a = xr[C + H * dv + H + tid];
-    const float xa = a + g.dt_bias[tid];
-    const float sp = xa > 20.0f ? xa : log1pf(__expf(xa));
-    g.beta[(int64_t)r * H + tid] = 1.0f / (1.0f + __expf(-b));
-    g.alpha[(int64_t)r * H + tid] = __expf(-__expf(g.A_log[tid]) * sp);
+    const float xv[4] = {xc.x, xc.y, xc.z, xc.w};
+    float y[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float wt[4] = {w[e].x, w[e].y, w[e].z, w[e].w};
+      float acc = wt[3] * xv[e];
+#pragma unroll
+      for (int j = 1; j <= 3; ++j) {
+        const float sv[4] = {src[j - 1].x, src[j - 1].y, src[j - 1].z, src[j - 1].w};
+        if (has[j - 1]) acc += wt[3 - j] * sv[e];
+      }
+      y[e] = silu_f(acc);
+    }
+    if (g.tail_slot) {
+      const int ts = g.tail_slot[r];
+      if (ts >= 0) *reinterpret_cast<float4 *>(g.tail + (int64_t)ts * C + c) = xc;
+    }
+    if (cg < 2 * H) {
+      float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o);
+      float inv = rsqrtf(ss + 1e-6f);
+      float *out;
+      if (cg < H) {
+        inv *= qscale;
+        out = g.q + ((int64_t)r * H + cg) * dk;
+      } else {
+        out = g.k + ((int64_t)r * H + cg - H) * dk;
+      }
+      *reinterpret_cast<float4 *>(out + lane * 4) = make_float4(y[0] * inv, y[1] * inv, y[2] * inv, y[3] * inv);
+    } else {
+      *reinterpret_cast<float4 *>(g.v + ((int64_t)r * H + cg - 2 * H) * dv + lane * 4) =
+          make_float4(y[0], y[1], y[2], y[3]);
+    }
+    if (cg == 0) {
+      const float *xr = g.x + (int64_t)r * g.ldx;
+      for (int hh = lane; hh < H; hh += 32) {
+        const float b = xr[C + H * dv + hh], a = xr[C + H * dv + H + hh];
+        const float xa = a + g.dt_bias[hh];
+        const float sp = xa > 20.0f ? xa : log1pf(__expf(xa));
+        g.beta[(int64_t)r * H + hh] = 1.0f / (1.0f + __expf(-b));
+        g.alpha[(int64_t)r * H + hh] = __expf(-__expf(g.A_log[hh]) * sp);
+      }
+    }
+    win[2] = win[1];
+    win[1] = win[0];
+    win[0] = xc;
   }
 }
 
@@ -165,9 +211,9 @@ __global__ __launch_bounds__(256) void gdn_out_kernel(const float *__restrict__ 
 
 hipError_t launch_gdn_conv(const GdnConvArgs &g, int R, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  const size_t lds = sizeof(float) * (size_t)(2 * g.H * g.dk + g.H * g.dv);
-  if (lds > 65536) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gdn_conv_kernel, dim3(R), dim3(256), lds, st, g);
+  if (g.dk != 128 || g.dv != 128) return hipErrorInvalidValue;
+  const int64_t groups = (int64_t)((R + GDN_CONV_RB - 1) / GDN_CONV_RB) * (3 * g.H);
+  hipLaunchKernelGGL(gdn_conv_kernel, dim3((unsigned)((groups + 7) / 8)), dim3(256), 0, st, g, R);
   return hipGetLastError();
 }
 
