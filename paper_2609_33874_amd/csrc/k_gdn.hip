@@ -13,6 +13,8 @@
 // candidate from a private register copy of its question's state snapshot and
 // never writes it back, so candidates cannot see each other (the isolation
 // the paper checks in Section 5.6), while all candidates run in one batch.
+#include <utility>
+
 #include "device.h"
 #include "kernels.h"
 
@@ -116,9 +118,42 @@ __global__ __launch_bounds__(256) void gdn_conv_kernel(GdnConvArgs g, int R) {
 
 // One workgroup of 128 threads per (sequence, head); thread i owns state row
 // i (dv = dk = 128 values in registers). Steps are walked in order; k and q of
-// 32 steps at a time are staged in LDS and read by all threads.
+// 32 steps at a time are staged in LDS. Every product with k or q takes the
+// element from a neighbouring lane instead of a private copy: each row of 16
+// lanes loads the step's k and q once, lane n holding elements 8n .. 8n + 7,
+// and an FMA reads element j from lane j / 8 of its row through the DPP
+// row_newbcast operand modifier (16-byte LDS reads per step: 4 instead of 96
+// workgroup-wide broadcasts, which bounded the kernel by LDS bandwidth).
+//
+// The state is held as S = c X with a scalar c (uniform over the workgroup),
+// so the decay S <- alpha S costs one multiply of c instead of one per state
+// element: with c' = alpha c,
+//   S k = c' (X k),  S <- S + delta k^T  is  X <- X + (delta / c') k^T,
+//   o = c' (X q).
+// X is rescaled into S (c = 1) whenever c' falls below 2^-40, so X stays
+// within 2^40 of S, and a vanishing alpha is applied to X directly.
 constexpr int GDN_D = 128;
 constexpr int GDN_CHUNK = 32;
+
+// acc += (x taken from lane N of this lane's row of 16) * b
+template <int N>
+__device__ __forceinline__ void fmac_rowbc(float &acc, float x, float b) {
+  asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf" : "+v"(acc) : "v"(x), "v"(b), "n"(N));
+}
+
+// p[j % 4] += s[j] k[j] (k[j] = kk[j % 8] of lane j / 8)
+template <int... J>
+__device__ __forceinline__ void gdn_dot(const float (&s)[GDN_D], const float (&kk)[8], float (&p)[4],
+                                        std::integer_sequence<int, J...>) {
+  (fmac_rowbc<J / 8>(p[J % 4], kk[J % 8], s[J]), ...);
+}
+
+// s[j] += e k[j], then p[j % 4] += s[j] q[j] (k[j], q[j] from lane j / 8)
+template <int... J>
+__device__ __forceinline__ void gdn_update_dot(float (&s)[GDN_D], const float (&kk)[8], const float (&qq)[8], float e,
+                                               float (&p)[4], std::integer_sequence<int, J...>) {
+  ((fmac_rowbc<J / 8>(s[J], kk[J % 8], e), fmac_rowbc<J / 8>(p[J % 4], qq[J % 8], s[J])), ...);
+}
 
 __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
   __shared__ float4 ks[GDN_CHUNK][GDN_D / 4], qs[GDN_CHUNK][GDN_D / 4];
@@ -126,7 +161,7 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
   const int H = g.H;
   const int si = blockIdx.x / H, h = blockIdx.x % H;
   const GdnSeq sq = g.seqs[si];
-  const int i = threadIdx.x;
+  const int i = threadIdx.x, ln = i & 15;
   float s[GDN_D];
   if (sq.init >= 0) {
     const float4 *src = reinterpret_cast<const float4 *>(g.S_init + (((int64_t)sq.init * H + h) * GDN_D + i) * GDN_D);
@@ -139,6 +174,7 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
 #pragma unroll
     for (int c = 0; c < GDN_D; ++c) s[c] = 0.0f;
   }
+  float cs = 1.0f;  // the state is cs s
   for (int t0 = 0; t0 < sq.len; t0 += GDN_CHUNK) {
     const int nt = min(GDN_CHUNK, sq.len - t0);
     __syncthreads();
@@ -158,25 +194,27 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
       const int64_t row = sq.row0 + t0 + tt;
       const float a = al[tt], b = be[tt];
       const float vv = g.v[(row * H + h) * GDN_D + i];
-      float pred = 0.0f;
+      const float4 k0 = ks[tt][2 * ln], k1 = ks[tt][2 * ln + 1];
+      const float4 q0 = qs[tt][2 * ln], q1 = qs[tt][2 * ln + 1];
+      const float kk[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+      const float qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+      cs *= a;
+      if (cs < 0x1p-40f) {  // uniform: fold c into X
 #pragma unroll
-      for (int c = 0; c < GDN_D / 4; ++c) {
-        const float4 kk = ks[tt][c];
-        s[4 * c] *= a; s[4 * c + 1] *= a; s[4 * c + 2] *= a; s[4 * c + 3] *= a;
-        pred += s[4 * c] * kk.x + s[4 * c + 1] * kk.y + s[4 * c + 2] * kk.z + s[4 * c + 3] * kk.w;
+        for (int c = 0; c < GDN_D; ++c) s[c] *= cs;
+        cs = 1.0f;
       }
-      const float delta = b * (vv - pred);
-      float out = 0.0f;
-#pragma unroll
-      for (int c = 0; c < GDN_D / 4; ++c) {
-        const float4 kk = ks[tt][c], qq = qs[tt][c];
-        s[4 * c] += delta * kk.x; s[4 * c + 1] += delta * kk.y;
-        s[4 * c + 2] += delta * kk.z; s[4 * c + 3] += delta * kk.w;
-        out += s[4 * c] * qq.x + s[4 * c + 1] * qq.y + s[4 * c + 2] * qq.z + s[4 * c + 3] * qq.w;
-      }
-      g.o[(row * H + h) * GDN_D + i] = out;
+      float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      gdn_dot(s, kk, p, std::make_integer_sequence<int, GDN_D>{});
+      const float pred = cs * ((p[0] + p[1]) + (p[2] + p[3]));
+      const float e = b * (vv - pred) / cs;
+      float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      gdn_update_dot(s, kk, qq, e, o, std::make_integer_sequence<int, GDN_D>{});
+      g.o[(row * H + h) * GDN_D + i] = cs * ((o[0] + o[1]) + (o[2] + o[3]));
     }
   }
+#pragma unroll
+  for (int c = 0; c < GDN_D; ++c) s[c] *= cs;
   if (sq.fin >= 0) {
     float4 *dst = reinterpret_cast<float4 *>(g.S_fin + (((int64_t)sq.fin * H + h) * GDN_D + i) * GDN_D);
 #pragma unroll
