@@ -38,6 +38,108 @@ __device__ __forceinline__ void put_split(T *p, int64_t ps, float v, int pair) {
   if (pair) p[ps] = from_f<T>(v - to_f<T>(hi));
 }
 
+// Orders a wave's LDS writes before its following LDS reads of other lanes'
+// data (a wave's LDS operations complete in order).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Residual add and SwiGLU epilogues through the LDS (free once the K loop has
+// ended): each wave writes a slab of its accumulators (16 rows of fp32, or 32
+// rows of T for SwiGLU) into its own LDS region and reads it back as 16-byte
+// row chunks, so every global access moves 16 bytes instead of 2 or 4. The
+// arithmetic is that of the per-element epilogues in gemm_kernel. Returns
+// false (nothing done) where the output rows are not 16-byte aligned or the
+// LDS is too small.
+template <class C, int EPI>
+__device__ __forceinline__ bool staged_epilogue(const GemmArgs<typename C::type> &g, int m0, int n0,
+                                                f32x16 (&acc)[C::MI][C::NI], uint4 *lds) {
+  using T = typename C::type;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+  if constexpr (EPI == 1) {
+    constexpr int SC = C::WN < 64 ? C::WN : 64, LDF = SC + 4;  // slab columns, padded row (floats)
+    constexpr int CH = 16 * SC / 4 / 64;                        // float4 chunks per lane per slab
+    static_assert(CH >= 1 && (16 * SC / 4) % 64 == 0, "slab of whole chunk rounds");
+    if constexpr ((size_t)C::NWAVES * 16 * LDF * 4 > C::LDS_BYTES) {
+      return false;
+    } else {
+      if ((g.ldo & 3) || (g.N & 3)) return false;
+      float *wl = reinterpret_cast<float *>(lds) + wave * 16 * LDF;
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+        for (int hr = 0; hr < 2; ++hr)  // rows 16 hr .. 16 hr + 15 of the 32-row block
+#pragma unroll
+          for (int jh = 0; jh < C::WN / SC; ++jh) {
+#pragma unroll
+            for (int jj = 0; jj < SC / 32; ++jj)
+#pragma unroll
+              for (int e = 8 * hr; e < 8 * hr + 8; ++e) {
+                const int r = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3) - 16 * hr;
+                wl[r * LDF + jj * 32 + (lane & 31)] = acc[i][jh * (SC / 32) + jj][e] * g.oscale;
+              }
+            wave_lds_sync();
+#pragma unroll
+            for (int t = 0; t < CH; ++t) {
+              const int q = t * 64 + lane, r = q / (SC / 4), c4 = q % (SC / 4);
+              const int row = m0 + wm * C::WM + i * 32 + 16 * hr + r;
+              const int col = n0 + wn * C::WN + jh * SC + 4 * c4;
+              if (row < g.M && col < g.N) {
+                const float4 v = *reinterpret_cast<const float4 *>(wl + r * LDF + 4 * c4);
+                float4 *o = reinterpret_cast<float4 *>((float *)g.out + (int64_t)row * g.ldo + col);
+                float4 x = *o;
+                x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+                *o = x;
+              }
+            }
+            wave_lds_sync();
+          }
+      return true;
+    }
+  } else if constexpr (EPI == 2 && sizeof(T) == 2) {
+    constexpr int OC = C::WN / 2, LDH = OC + 8;  // output columns of a wave, padded row (elements)
+    constexpr int CH = 32 * OC / 8 / 64;         // 16-byte chunks per lane per 32-row slab
+    static_assert(CH >= 1 && (32 * OC / 8) % 64 == 0, "slab of whole chunk rounds");
+    if constexpr ((size_t)C::NWAVES * 32 * LDH * sizeof(T) > C::LDS_BYTES) {
+      return false;
+    } else {
+      if (g.pair_out || (g.ldo & 7)) return false;
+      T *wl = reinterpret_cast<T *>(lds) + wave * 32 * LDH;
+      const int f0 = (n0 + wn * C::WN) >> 1;  // first output column of the wave
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i) {
+#pragma unroll
+        for (int jp = 0; jp < C::NI / 2; ++jp)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float gt = acc[i][2 * jp][e] * g.oscale, up = acc[i][2 * jp + 1][e] * g.oscale;
+            // silu(g) = g / (1 + e^-g) with the hardware reciprocal (~1 ulp)
+            const float v = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
+            const int r = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            wl[r * LDH + jp * 32 + (lane & 31)] = from_f<T>(v);
+          }
+        wave_lds_sync();
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+          const int q = t * 64 + lane, r = q / (OC / 8), c8 = q % (OC / 8);
+          const int row = m0 + wm * C::WM + i * 32 + r;
+          const int gcol = n0 + wn * C::WN + 64 * (c8 / 4);  // first gate column of the chunk's block
+          if (row < g.M && gcol < g.N)
+            *reinterpret_cast<uint4 *>((T *)g.out + (int64_t)row * g.ldo + f0 + 8 * c8) =
+                *reinterpret_cast<const uint4 *>(wl + r * LDH + 8 * c8);
+        }
+        wave_lds_sync();
+      }
+      return true;
+    }
+  } else {
+    return false;
+  }
+}
+
 // EPI: 0 = store fp32, 1 = fp32 residual add, 2 = SwiGLU into T (B rows
 // interleaved in blocks of 32 gate rows / 32 up rows), 3 = store T, 4 = RoPE
 // and scatter of q, K, V (waves of 128 columns = one head).
@@ -51,6 +153,7 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
   const int m0 = tm * C::BM, n0 = tn * C::BN;
   f32x16 acc[C::MI][C::NI];
   gemm_tile<C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
+  if (staged_epilogue<C, EPI>(g, m0, n0, acc, lds)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   if constexpr (EPI == 4) {
