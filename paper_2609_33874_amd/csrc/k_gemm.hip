@@ -46,20 +46,24 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Residual add and SwiGLU epilogues through the LDS (free once the K loop has
-// ended): each wave writes a slab of its accumulators (16 rows of fp32, or 32
-// rows of T for SwiGLU) into its own LDS region and reads it back as 16-byte
+// fp32 store, residual add and SwiGLU epilogues through the LDS (free once
+// the K loop has ended): each wave writes a slab of its accumulators (16 rows
+// of fp32, or 32 rows of T for SwiGLU) into its own LDS region and reads it back as 16-byte
 // row chunks, so every global access moves 16 bytes instead of 2 or 4. The
 // arithmetic is that of the per-element epilogues in gemm_kernel. Returns
-// false (nothing done) where the output rows are not 16-byte aligned or the
-// LDS is too small.
+// false (nothing done) for tiles of fewer than 256 rows, where the output rows
+// are not 16-byte aligned, or where the LDS is too small.
 template <class C, int EPI>
 __device__ __forceinline__ bool staged_epilogue(const GemmArgs<typename C::type> &g, int m0, int n0,
                                                 f32x16 (&acc)[C::MI][C::NI], uint4 *lds) {
   using T = typename C::type;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  if constexpr (EPI == 1) {
+  if constexpr (C::BM < 256) {
+    // smaller tiles run several workgroups per CU; the staging registers
+    // would cost one of them
+    return false;
+  } else if constexpr (EPI == 0 || EPI == 1) {
     constexpr int SC = C::WN < 64 ? C::WN : 64, LDF = SC + 4;  // slab columns, padded row (floats)
     constexpr int CH = 16 * SC / 4 / 64;                        // float4 chunks per lane per slab
     static_assert(CH >= 1 && (16 * SC / 4) % 64 == 0, "slab of whole chunk rounds");
@@ -90,9 +94,13 @@ __device__ __forceinline__ bool staged_epilogue(const GemmArgs<typename C::type>
               if (row < g.M && col < g.N) {
                 const float4 v = *reinterpret_cast<const float4 *>(wl + r * LDF + 4 * c4);
                 float4 *o = reinterpret_cast<float4 *>((float *)g.out + (int64_t)row * g.ldo + col);
-                float4 x = *o;
-                x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
-                *o = x;
+                if constexpr (EPI == 0) {
+                  *o = v;
+                } else {
+                  float4 x = *o;
+                  x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+                  *o = x;
+                }
               }
             }
             wave_lds_sync();
