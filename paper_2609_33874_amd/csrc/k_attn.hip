@@ -440,13 +440,22 @@ constexpr int attn_qb() {
 
 int attn_slots_per_item(int dtype, int pair) { return (dtype == 1 || pair) ? 64 : 128; }
 
+template <typename T, int HD, bool PAIR, int QB>
+static hipError_t run_attn_qb(const AttnArgs &a, hipStream_t st) {
+  if (a.mode == 0) hipLaunchKernelGGL((attn_kernel<T, HD, 0, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((attn_kernel<T, HD, 1, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 template <typename T, int HD, bool PAIR>
 static hipError_t run_attn(const AttnArgs &a, hipStream_t st) {
   constexpr int QB = attn_qb<T, PAIR>();
   if (a.n_items <= 0) return hipSuccess;
-  if (a.mode == 0) hipLaunchKernelGGL((attn_kernel<T, HD, 0, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((attn_kernel<T, HD, 1, PAIR, QB>), dim3(a.n_items), dim3(256), 0, st, a);
-  return hipGetLastError();
+  if (a.qb < 1 || a.qb > QB) return hipErrorInvalidValue;
+  if constexpr (QB == 2) {
+    if (a.qb == 2) return run_attn_qb<T, HD, PAIR, 2>(a, st);
+  }
+  return run_attn_qb<T, HD, PAIR, 1>(a, st);
 }
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st) {

@@ -87,11 +87,14 @@ struct AttnArgs {
   AttnQuestions qs;
   const AttnItem *items;
   int n_items;
+  int qb;  // blocks of 16 query slots per wave the items were built for: 64 qb slots per item
   int Hq, Hkv, hd;
   float scale;
 };
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t st);
-// Query slots per work item that launch_attention expects (64 or 128).
+// Largest query-slot count per work item launch_attention supports (64 or
+// 128); the items of a launch hold at most 64 * AttnArgs::qb slots, qb being
+// 1 or, where this returns 128, 2.
 int attn_slots_per_item(int dtype, int pair);
 
 // Gated delta-rule layers. Projection output x [R][ldx] = q~ (H dk) | k~ (H dk)

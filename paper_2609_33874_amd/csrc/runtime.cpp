@@ -449,7 +449,13 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   const int G = (int)(h.n_heads / h.n_kv_heads);
   std::vector<jetk::AttnItem> items;
   double pairs = 0;
-  build_items(qd, G, (int)h.n_kv_heads, mode == 0, jetk::attn_slots_per_item(m->kdt, m->apair), &items, &pairs);
+  // Prefix attention: 128-slot items (two query blocks per wave) where the
+  // kernel supports them. Candidate attention: 64-slot items always, so that
+  // a candidate runs the same kernel (and rounds alike) whatever batch it is
+  // in, and the few query slots a question's candidates have (often well
+  // under 64 per KV head) do not leave most of an item idle.
+  const int block = mode == 0 && jetk::attn_slots_per_item(m->kdt, m->apair) >= 128 ? 128 : 64;
+  build_items(qd, G, (int)h.n_kv_heads, mode == 0, block, &items, &pairs);
   jetk::AttnItem *d_items;
   int32_t *d_qrow0, *d_nrows, *d_prelen, *d_sufrow0, *d_suflen;
   int64_t *d_preslot;
@@ -467,6 +473,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   a.qs = {d_qrow0, d_nrows, d_preslot, d_prelen, d_sufrow0, d_suflen};
   a.items = d_items;
   a.n_items = (int)items.size();
+  a.qb = block / 64;
   a.Hq = (int)h.n_heads;
   a.Hkv = (int)h.n_kv_heads;
   a.hd = (int)h.head_dim;
