@@ -53,13 +53,22 @@ __global__ __launch_bounds__(256) void gdn_conv_kernel(GdnConvArgs g, int R) {
   const float qscale = rsqrtf((float)dk);
   const int r0 = rb * GDN_CONV_RB, r1 = min(R, r0 + GDN_CONV_RB);
   float4 win[3] = {};  // inputs of rows r - 1, r - 2, r - 3
+  // row r + 1's input and history are fetched while row r is processed
+  float4 xn = ld4f(g.x + (int64_t)r0 * g.ldx + c, al);
+  int hn[3] = {g.hist[(int64_t)r0 * 3], g.hist[(int64_t)r0 * 3 + 1], g.hist[(int64_t)r0 * 3 + 2]};
   for (int r = r0; r < r1; ++r) {
-    const float4 xc = ld4f(g.x + (int64_t)r * g.ldx + c, al);
+    const float4 xc = xn;
+    const int hc[3] = {hn[0], hn[1], hn[2]};
+    if (r + 1 < r1) {
+      xn = ld4f(g.x + (int64_t)(r + 1) * g.ldx + c, al);
+#pragma unroll
+      for (int j = 0; j < 3; ++j) hn[j] = g.hist[(int64_t)(r + 1) * 3 + j];
+    }
     float4 src[3];
     bool has[3];
 #pragma unroll
     for (int j = 1; j <= 3; ++j) {
-      const int h = g.hist[(int64_t)r * 3 + j - 1];
+      const int h = hc[j - 1];
       has[j - 1] = h != -1;
       if (h == r - j && r - j >= r0) src[j - 1] = win[j - 1];
       else if (h >= 0) src[j - 1] = ld4f(g.x + (int64_t)h * g.ldx + c, al);
