@@ -385,6 +385,42 @@ static hipError_t run_epi(int epi, const void *A, int64_t lda, const void *B, in
 
 int gemm_k_step(int dtype) { return dtype == 1 ? CfgF::BK : BigB::BK; }
 
+// Workgroups of gemm_kernel<C, EPI> the device holds at once (0 if unknown).
+template <class C, int EPI>
+static int resident_groups() {
+  static const int n = [] {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (allow_lds<C>((const void *)gemm_kernel<C, EPI>) != hipSuccess || hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)gemm_kernel<C, EPI>, C::NT,
+                                                     C::LDS_BYTES) != hipSuccess)
+      return 0;
+    return cus * per_cu;
+  }();
+  return n;
+}
+
+// fp16 GEMM on the tile configuration C whose last round of tiles would
+// leave over half of the device idle: the row tiles holding that round run
+// as a second launch of 128x128 tiles (several per CU), which fills the
+// device better; every output element is computed alike in both.
+template <class C, int EPI>
+static hipError_t run_gemm_tail(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K, void *out,
+                                int64_t ldo, float oscale, hipStream_t st) {
+  const int nt_m = (M + C::BM - 1) / C::BM, nt_n = (N + C::BN - 1) / C::BN;
+  const int64_t tiles = (int64_t)nt_m * nt_n;
+  const int slots = resident_groups<C, EPI>();
+  const int64_t rem = slots > 0 ? tiles % slots : 0;
+  const int tail_mt = rem > 0 ? (int)((rem + nt_n - 1) / nt_n) : 0;
+  if (rem == 0 || rem > slots / 2 || tail_mt >= nt_m) return run_gemm<C, EPI>(A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+  const int M1 = (nt_m - tail_mt) * C::BM;
+  const size_t osz = EPI == 0 || EPI == 1 ? sizeof(float) : sizeof(f16);
+  hipError_t e = run_gemm<C, EPI>(A, lda, B, ldb, M1, N, K, 0, out, ldo, oscale, st);
+  if (e != hipSuccess) return e;
+  return run_gemm<HalfS, EPI>((const f16 *)A + (int64_t)M1 * lda, lda, B, ldb, M - M1, N, K, 0,
+                              (char *)out + (size_t)M1 * (size_t)ldo * osz, ldo, oscale, st);
+}
+
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N,
                        int K, int pair, void *out, int64_t ldo, float oscale, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
@@ -403,8 +439,13 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
                               : run_epi<HalfPairS>(epi, A, lda, B, ldb, M, N, K, pair, out, ldo, oscale, st);
     if (big_tiles < 512) return run_epi<HalfS>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
     if (epi == EPI_RESID_ADD && K <= 2048)
-      return run_gemm<HalfM, 1>(A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
-    return run_epi<HalfB>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+      return run_gemm_tail<HalfM, 1>(A, lda, B, ldb, M, N, K, out, ldo, oscale, st);
+    switch (epi) {
+      case EPI_STORE_F32: return run_gemm_tail<HalfB, 0>(A, lda, B, ldb, M, N, K, out, ldo, oscale, st);
+      case EPI_RESID_ADD: return run_gemm_tail<HalfB, 1>(A, lda, B, ldb, M, N, K, out, ldo, oscale, st);
+      case EPI_SWIGLU: return run_gemm_tail<HalfB, 2>(A, lda, B, ldb, M, N, K, out, ldo, oscale, st);
+      default: return run_gemm_tail<HalfB, 3>(A, lda, B, ldb, M, N, K, out, ldo, oscale, st);
+    }
   }
   return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
 }
