@@ -151,7 +151,7 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the scoring path has no "
-              "multi-GPU mode in this build", file=sys.stderr)
+              "multi-GPU mode (questions shard across GPUs with no exchange but the sums; not implemented)", file=sys.stderr)
         return 2
     if args.calibrate_copy:
         return calibrate_copy()
