@@ -456,6 +456,19 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   // under 64 per KV head) do not leave most of an item idle.
   const int block = mode == 0 && jetk::attn_slots_per_item(m->kdt, m->apair) >= 128 ? 128 : 64;
   build_items(qd, G, (int)h.n_kv_heads, mode == 0, block, &items, &pairs);
+  // Longest work first: the dispatcher hands out workgroups in order, so long
+  // items no longer run alone at the end (an item's result does not depend
+  // on its position in the launch). Questions are ordered by length and each
+  // question's items stay together (they share its K/V in L2), the longest
+  // of them first.
+  auto qlen = [&](const jetk::AttnItem &it) {
+    return (int64_t)qd.pre_len[(size_t)it.q] + qd.suf_len[(size_t)it.q];
+  };
+  std::stable_sort(items.begin(), items.end(), [&](const jetk::AttnItem &x, const jetk::AttnItem &y) {
+    if (qlen(x) != qlen(y)) return qlen(x) > qlen(y);
+    if (x.q != y.q) return x.q < y.q;
+    return x.nkeys_pre > y.nkeys_pre;
+  });
   jetk::AttnItem *d_items;
   int32_t *d_qrow0, *d_nrows, *d_prelen, *d_sufrow0, *d_suflen;
   int64_t *d_preslot;
