@@ -143,6 +143,9 @@ def test_hybrid_4b_k4_full(dtype):
     sampled_parity(path, "hybrid_4b_k4", wl, tok, sums, [q], dtype)
 
 
+# The fp64 oracle of one 27B-shape candidate sequence runs for minutes on the
+# host, longer than a per-test limit meant for GPU calls.
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("dtype", DTYPES_DEEP)
 def test_dense_27b_k10_full(dtype):
     """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
