@@ -34,4 +34,5 @@ catch.
 """
 from .model import Model, forward, final_logprobs, upcast  # noqa: F401
 from .score import (score_unshared, score_incremental, log_softmax_rows,  # noqa: F401
-                    normalize, decide_choice, decide_binary, decide_ordinal, decide)
+                    normalize, decide_choice, decide_binary, decide_ordinal, decide,
+                    answer_classes, evaluate)

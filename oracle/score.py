@@ -14,6 +14,10 @@
 * ``normalize`` / ``decide_*``: Eq. 4 and Eq. 5 with the rules of
   Section 3.3; ties go to the lowest candidate index, binary sets are ordered
   (false, true), ordinal levels are zero-based.
+* ``answer_classes`` / ``evaluate``: equivalent labels (Section 3.3: labels
+  with the same answer text share one likelihood and are pooled in
+  evaluation) and the accuracy / gold negative log-likelihood of the
+  evaluation protocol (Section 5), straight from those definitions.
 """
 from __future__ import annotations
 
@@ -170,3 +174,37 @@ def decide(mode: str, q_cand_offsets: np.ndarray, sums: np.ndarray):
         else:
             value.append(None)
     return qs, np.asarray(choice, np.int32), value
+
+
+# --------------------------------------------------------------------------
+# evaluation against reference answers (Section 3.3, Section 5)
+# --------------------------------------------------------------------------
+
+def answer_classes(q_cand_offsets, cand_tok_offsets, cand_tokens) -> np.ndarray:
+    """Per candidate: the index, within its question, of the first candidate
+    whose token sequence is identical (identical text under one tokenizer)."""
+    out = np.zeros(int(q_cand_offsets[-1]), np.int32)
+    for q in range(len(q_cand_offsets) - 1):
+        a, b = int(q_cand_offsets[q]), int(q_cand_offsets[q + 1])
+        seqs = [tuple(int(t) for t in cand_tokens[cand_tok_offsets[c]:cand_tok_offsets[c + 1]])
+                for c in range(a, b)]
+        for j in range(b - a):
+            out[a + j] = seqs.index(seqs[j])
+    return out
+
+
+def evaluate(q_cand_offsets, sums, gold, classes=None):
+    """Per question: correct (the predicted label, Eq. 5's argmax, has the
+    gold answer's text) and gold NLL = -ln of the summed q (Eq. 4) over the
+    labels with the gold answer's text; plus their means over questions."""
+    correct, nll = [], []
+    for q in range(len(q_cand_offsets) - 1):
+        a, b = int(q_cand_offsets[q]), int(q_cand_offsets[q + 1])
+        cls = list(range(b - a)) if classes is None else [int(x) for x in classes[a:b]]
+        p = normalize(sums[a:b])
+        g = cls[int(gold[q])]
+        correct.append(int(cls[decide_choice(sums[a:b])] == g))
+        nll.append(-np.log(sum(p[j] for j in range(b - a) if cls[j] == g)))
+    correct = np.asarray(correct, np.int32)
+    nll = np.asarray(nll, np.float64)
+    return correct, nll, float(np.mean(correct)), float(np.mean(nll))

@@ -103,6 +103,61 @@ def test_decisions_closed_forms():
         oracle.decide_binary(s5)
 
 
+def test_evaluation_closed_forms():
+    """Accuracy and gold NLL (Section 5) with pooled equivalent labels
+    (Section 3.3), against values fixed by the paper and by closed forms."""
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")))
+    s = np.log(np.array(g["likelihoods"]))
+    # worked example: q = (0.75, 0.25); gold = first label -> -ln 0.75, correct
+    c, nll, acc, mnll = oracle.evaluate([0, 2], s, [0])
+    assert c[0] == 1 and nll[0] == pytest.approx(-math.log(g["normalized"][0]), abs=1e-15)
+    c, nll, _, _ = oracle.evaluate([0, 2], s, [1])
+    assert c[0] == 0 and nll[0] == pytest.approx(-math.log(g["normalized"][1]), abs=1e-15)
+    # equal scores over K labels, r of them with the gold text: NLL = ln(K / r)
+    K = 6
+    cls = np.array([0, 1, 0, 3, 0, 5], np.int32)  # labels 0, 2, 4 share a text
+    for gold, r in ((2, 3), (1, 1), (5, 1)):
+        c, nll, _, _ = oracle.evaluate([0, K], np.full(K, -2.5), [gold], cls)
+        assert nll[0] == pytest.approx(math.log(K / r), abs=1e-15)
+        # ties go to label 0, whose text is accepted only for the first group
+        assert c[0] == int(cls[gold] == 0)
+    # any label with the gold text is accepted: predicted label 2, gold label 0
+    c, nll, _, _ = oracle.evaluate([0, 3], np.array([-3.0, -9.0, -1.0]), [0], np.array([0, 1, 0]))
+    assert c[0] == 1
+    z = math.exp(-3.0) + math.exp(-9.0) + math.exp(-1.0)
+    assert nll[0] == pytest.approx(-math.log((math.exp(-3.0) + math.exp(-1.0)) / z), abs=1e-14)
+    # binary: gold true -> softplus(s0 - s1); correct iff q(true) > 1/2
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        sb = rng.normal(-5, 2, size=2)
+        if rng.random() < 0.2:
+            sb[1] = sb[0]
+        c, nll, _, _ = oracle.evaluate([0, 2], sb, [1])
+        assert nll[0] == pytest.approx(math.log1p(math.exp(sb[0] - sb[1])), abs=1e-13)
+        assert c[0] == int(oracle.decide_binary(sb) > 0.5)
+    # a question with one candidate: certain, correct
+    c, nll, _, _ = oracle.evaluate([0, 1], np.array([-40.0]), [0])
+    assert c[0] == 1 and nll[0] == 0.0
+    # means over questions
+    qco = [0, 2, 5, 6]
+    sm = np.array([-1.0, -2.0, -3.0, -3.0, -3.0, -7.0])
+    c, nll, acc, mnll = oracle.evaluate(qco, sm, [1, 2, 0])
+    assert list(c) == [0, 0, 1]
+    assert acc == pytest.approx(1 / 3, abs=1e-16)
+    assert mnll == pytest.approx((math.log1p(math.exp(1.0)) + math.log(3.0) + 0.0) / 3, abs=1e-14)
+
+
+def test_answer_classes_by_token_sequence():
+    """Equivalent labels are those with identical token sequences within one
+    question (hand-computed classes; Section 3.3)."""
+    seqs = [[5, 6], [7], [5, 6], [5], [7], [5, 6, 1],  # question 0
+            [7], [7]]                                  # question 1: same tokens again
+    qco = np.array([0, 6, 8], np.int64)
+    cto = np.concatenate([[0], np.cumsum([len(x) for x in seqs])]).astype(np.int64)
+    toks = np.concatenate(seqs).astype(np.int32)
+    np.testing.assert_array_equal(oracle.answer_classes(qco, cto, toks), [0, 1, 0, 3, 1, 5, 0, 0])
+
+
 def test_zero_weights_give_uniform_vocabulary(model_dir):
     g = json.load(open(os.path.join(GOLDEN, "zero_model_logprob.json")))["per_token"]
     for spec, wname in (("tiny_dense_fp32", "tiny"), ("micro_hybrid_fp32", "micro_hybrid")):
