@@ -224,6 +224,15 @@ def main() -> int:
     elapsed = time.perf_counter() - t0
     stats = J.jet_stats_get(model)
     ms_step = 1e3 * elapsed / args.steps
+    # evaluation utilities on the last step's scores (host; outside the timed
+    # steps): equivalent labels and accuracy / gold NLL against seeded
+    # synthetic gold labels (random weights: the values themselves mean nothing)
+    sums = inp[3].cpu().numpy()
+    gold = np.random.default_rng(7).integers(0, np.diff(wl.q_cand_offsets)).astype(np.int32)
+    te = time.perf_counter()
+    cls = J.jet_answer_classes(wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+    J.jet_evaluate(wl.q_cand_offsets, sums, gold, cls)
+    eval_ms = 1e3 * (time.perf_counter() - te)
     qps = Q * args.steps / elapsed
 
     # per-kernel-class rates from the HIP events around every launch
@@ -274,6 +283,7 @@ def main() -> int:
         "shared_prefix_attention_hbm_frac": (round(kernels["attn_cand"]["gbs"] / PEAK_HBM_GBS, 4)
                                              if kernels.get("attn_cand", {}).get("gbs") else None),
         "roofline": roofline, "kernels": kernels,
+        "evaluate_ms": round(eval_ms, 3),
     }
 
     if args.unshared_steps > 0:

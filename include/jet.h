@@ -190,6 +190,51 @@ int jet_decide(int32_t mode, int32_t n_q, const int64_t *q_cand_offsets,
                double *out_value);
 
 /*
+ * jet_answer_classes - label equivalence by answer text (Section 3.3: labels
+ * whose answer text is the same receive the same likelihood and count as one
+ * answer in evaluation). Two candidates of one question are equivalent when
+ * their token sequences are identical. Host only; integer work.
+ *   q_cand_offsets: host, int64[n_q + 1]; each question needs >= 1 candidate.
+ *   cand_tok_offsets: host, int64[N + 1] (N = q_cand_offsets[n_q]); each
+ *     candidate needs >= 1 token.
+ *   cand_tokens: host, int32[cand_tok_offsets[N]].
+ *   out_class: host, int32[N]: the zero-based index, within its question, of
+ *     the first candidate with the same token sequence (its own index when no
+ *     earlier candidate matches).
+ * Errors: JET_E_INVALID.
+ */
+int jet_answer_classes(int32_t n_q, const int64_t *q_cand_offsets,
+                       const int64_t *cand_tok_offsets, const int32_t *cand_tokens,
+                       int32_t *out_class);
+
+/*
+ * jet_evaluate - accuracy and gold negative log-likelihood against reference
+ * answers (Section 3.3 on equivalent labels; Section 5, evaluation protocol).
+ * Pure host function in fp64.
+ *   q_cand_offsets: host, int64[n_q + 1]; each question needs >= 1 candidate.
+ *   cand_sum: host, float[N], the candidate scores s_c (finite).
+ *   cand_class: host, int32[N] or NULL: answer class of every candidate
+ *     (e.g. from jet_answer_classes), compared within a question only; NULL
+ *     puts every candidate in a class of its own.
+ *   gold: host, int32[n_q]: zero-based index of the reference answer's
+ *     candidate within its question.
+ *   out_correct: host, int32[n_q] or NULL: 1 when the predicted candidate
+ *     (argmax s, lowest index on ties: jet_decide's choice; for a binary
+ *     question the same as q(true) > 1/2) is in the gold candidate's class.
+ *   out_gold_nll: host, double[n_q] or NULL: -ln of the summed probability
+ *     q(c) (Eq. 4) of the gold class, evaluated in log form
+ *     (M + ln sum_c e^(s_c - M)) - (M_g + ln sum_{c in gold class} e^(s_c - M_g))
+ *     with M, M_g the maxima over the question and over the gold class, so it
+ *     stays finite for any finite scores.
+ *   out_accuracy / out_mean_nll: host, double or NULL: means over the
+ *     questions, summed in question order.
+ * Errors: JET_E_INVALID (offsets, gold out of range, non-finite score).
+ */
+int jet_evaluate(int32_t n_q, const int64_t *q_cand_offsets, const float *cand_sum,
+                 const int32_t *cand_class, const int32_t *gold, int32_t *out_correct,
+                 double *out_gold_nll, double *out_accuracy, double *out_mean_nll);
+
+/*
  * jet_candidate_layout - the integer row layout that jet_score_candidates
  * builds (host only; exported so that it can be checked on its own).
  *   prefix_offsets / q_cand_offsets / cand_tok_offsets: host, as above.

@@ -8,6 +8,7 @@
 // position (Section 4.1: the prefix output supplies first-token probabilities).
 #include "host.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -176,6 +177,86 @@ extern "C" int jet_decide(int32_t mode, int32_t n_q, const int64_t *q_cand_offse
       }
     }
   }
+  return JET_OK;
+}
+
+// Equivalent labels (Section 3.3): identical token sequences within a question.
+extern "C" int jet_answer_classes(int32_t n_q, const int64_t *q_cand_offsets,
+                                  const int64_t *cand_tok_offsets, const int32_t *cand_tokens,
+                                  int32_t *out_class) {
+  clear_error();
+  if (n_q < 1) return fail(Status::err(JET_E_INVALID, "n_q must be >= 1"));
+  Status s = check_offsets(q_cand_offsets, n_q, 1, "q_cand_offsets");
+  if (!s) return fail(s);
+  const int64_t N = q_cand_offsets[n_q];
+  s = check_offsets(cand_tok_offsets, N, 1, "cand_tok_offsets");
+  if (!s) return fail(s);
+  if (!cand_tokens) return fail(Status::err(JET_E_INVALID, "cand_tokens is NULL"));
+  if (!out_class) return fail(Status::err(JET_E_INVALID, "out_class is NULL"));
+  std::vector<int32_t> cls(N);
+  for (int32_t q = 0; q < n_q; ++q) {
+    const int64_t a = q_cand_offsets[q], b = q_cand_offsets[q + 1];
+    for (int64_t c = a; c < b; ++c) {
+      const int64_t len = cand_tok_offsets[c + 1] - cand_tok_offsets[c];
+      int64_t first = c;
+      for (int64_t d = a; d < c && first == c; ++d) {
+        if (cls[d] != d - a) continue;  // compare with class representatives only
+        if (cand_tok_offsets[d + 1] - cand_tok_offsets[d] != len) continue;
+        if (std::equal(cand_tokens + cand_tok_offsets[c], cand_tokens + cand_tok_offsets[c + 1],
+                       cand_tokens + cand_tok_offsets[d]))
+          first = d;
+      }
+      cls[c] = (int32_t)(first - a);
+    }
+  }
+  std::memcpy(out_class, cls.data(), sizeof(int32_t) * (size_t)N);
+  return JET_OK;
+}
+
+// Accuracy and gold NLL over the normalised candidate distribution (Eq. 4),
+// with equivalent labels pooled (Section 3.3; Section 5, evaluation protocol).
+extern "C" int jet_evaluate(int32_t n_q, const int64_t *q_cand_offsets, const float *cand_sum,
+                            const int32_t *cand_class, const int32_t *gold, int32_t *out_correct,
+                            double *out_gold_nll, double *out_accuracy, double *out_mean_nll) {
+  clear_error();
+  if (n_q < 1) return fail(Status::err(JET_E_INVALID, "n_q must be >= 1"));
+  Status s = check_offsets(q_cand_offsets, n_q, 1, "q_cand_offsets");
+  if (!s) return fail(s);
+  const int64_t N = q_cand_offsets[n_q];
+  if (!cand_sum) return fail(Status::err(JET_E_INVALID, "cand_sum is NULL"));
+  if (!gold) return fail(Status::err(JET_E_INVALID, "gold is NULL"));
+  for (int32_t q = 0; q < n_q; ++q)
+    if (gold[q] < 0 || gold[q] >= q_cand_offsets[q + 1] - q_cand_offsets[q])
+      return fail(Status::err(JET_E_INVALID, "gold index " + std::to_string(gold[q]) +
+                                                 " outside the candidates of question " + std::to_string(q)));
+  for (int64_t i = 0; i < N; ++i)
+    if (!std::isfinite(cand_sum[i]))
+      return fail(Status::err(JET_E_INVALID, "non-finite candidate score at " + std::to_string(i)));
+  auto cls = [&](int64_t c, int64_t a) -> int64_t { return cand_class ? (int64_t)cand_class[c] : c - a; };
+  double acc = 0.0, nll_sum = 0.0;
+  for (int32_t q = 0; q < n_q; ++q) {
+    const int64_t a = q_cand_offsets[q], b = q_cand_offsets[q + 1];
+    const int64_t g = cls(a + gold[q], a);
+    int64_t best = a;
+    double M = cand_sum[a], Mg = -INFINITY;
+    for (int64_t c = a + 1; c < b; ++c)
+      if ((double)cand_sum[c] > M) { M = cand_sum[c]; best = c; }
+    for (int64_t c = a; c < b; ++c)
+      if (cls(c, a) == g) Mg = std::max(Mg, (double)cand_sum[c]);
+    double z = 0.0, zg = 0.0;
+    for (int64_t c = a; c < b; ++c) {
+      z += std::exp((double)cand_sum[c] - M);
+      if (cls(c, a) == g) zg += std::exp((double)cand_sum[c] - Mg);
+    }
+    const int correct = cls(best, a) == g;
+    const double nll = (M + std::log(z)) - (Mg + std::log(zg));
+    if (out_correct) out_correct[q] = correct;
+    if (out_gold_nll) out_gold_nll[q] = nll;
+    acc += correct;
+    nll_sum += nll;
+  }
+  if (out_accuracy) *out_accuracy = acc / n_q;
+  if (out_mean_nll) *out_mean_nll = nll_sum / n_q;
   return JET_OK;
 }
 

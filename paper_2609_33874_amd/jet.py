@@ -25,7 +25,7 @@ ERROR_NAMES = {1: "JET_E_INVALID", 2: "JET_E_CAPACITY", 3: "JET_E_OOM", 4: "JET_
 
 # every symbol include/jet.h declares
 EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_score_candidates", "jet_decide",
-           "jet_candidate_layout", "jet_stats_get", "jet_stats_reset", "jet_model_info",
+           "jet_answer_classes", "jet_evaluate", "jet_candidate_layout", "jet_stats_get", "jet_stats_reset", "jet_model_info",
            "jet_prefix_free", "jet_model_free", "jet_last_error"]
 
 
@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.jet_prefill_prefix.argtypes = [P, I32, P, P, ctypes.POINTER(P)]
         L.jet_score_candidates.argtypes = [P, P, P, P, P, P, P]
         L.jet_decide.argtypes = [I32, I32, P, P, P, P, P]
+        L.jet_answer_classes.argtypes = [I32, P, P, P, P]
+        L.jet_evaluate.argtypes = [I32, P, P, P, P, P, P, P, P]
         L.jet_candidate_layout.argtypes = [I32, P, P, P, I64, I64, P, P, P, P, P, P]
         L.jet_stats_get.argtypes = [P, ctypes.POINTER(jet_stats)]
         L.jet_stats_reset.argtypes = [P]
@@ -166,6 +168,33 @@ def jet_decide(mode: int, q_cand_offsets, cand_sum):
     _check(lib().jet_decide(mode, n_q, qo, cs, q.ctypes.data_as(ctypes.c_void_p),
                             choice.ctypes.data_as(ctypes.c_void_p), value.ctypes.data_as(ctypes.c_void_p)))
     return q, choice, value
+
+
+def jet_answer_classes(q_cand_offsets, cand_tok_offsets, cand_tokens):
+    """Per candidate, the index within its question of the first candidate
+    with the same token sequence (equivalent labels, Section 3.3)."""
+    qo, k1 = _ptr(q_cand_offsets, np.int64)
+    co, k2 = _ptr(cand_tok_offsets, np.int64)
+    ct, k3 = _ptr(cand_tokens, np.int32)
+    out = np.empty(len(k2) - 1, np.int32)
+    _check(lib().jet_answer_classes(len(k1) - 1, qo, co, ct, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def jet_evaluate(q_cand_offsets, cand_sum, gold, cand_class=None):
+    """(correct[n_q], gold_nll[n_q], accuracy, mean_nll) against reference
+    answers, equivalent labels pooled (Section 3.3; Section 5)."""
+    qo, k1 = _ptr(q_cand_offsets, np.int64)
+    cs, k2 = _ptr(cand_sum, np.float32)
+    gd, k3 = _ptr(gold, np.int32)
+    cc, k4 = (None, None) if cand_class is None else _ptr(cand_class, np.int32)
+    n_q = len(k1) - 1
+    correct = np.empty(n_q, np.int32)
+    nll = np.empty(n_q, np.float64)
+    acc, mnll = ctypes.c_double(), ctypes.c_double()
+    _check(lib().jet_evaluate(n_q, qo, cs, cc, gd, correct.ctypes.data_as(ctypes.c_void_p),
+                              nll.ctypes.data_as(ctypes.c_void_p), ctypes.byref(acc), ctypes.byref(mnll)))
+    return correct, nll, acc.value, mnll.value
 
 
 def jet_candidate_layout(prefix_offsets, q_cand_offsets, cand_tok_offsets, max_ctx: int = 0):

@@ -47,6 +47,26 @@ def check_parity(wl, tok, sums, ref_tok, ref_sums, dtype):
     return dt.max(), ds.max()
 
 
+def check_evaluation(wl, sums, ref_sums, max_ds):
+    """Accuracy / gold NLL through the C ABI on the GPU's scores against the
+    oracle's evaluation of its own scores, seeded gold labels. Each
+    log-sum-exp moves by at most max|d s|, so the NLL by at most twice that."""
+    rng = np.random.default_rng(11)
+    K = np.diff(wl.q_cand_offsets)
+    gold = np.array([rng.integers(0, k) for k in K], np.int32)
+    cls = J.jet_answer_classes(wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+    np.testing.assert_array_equal(cls, oracle.answer_classes(wl.q_cand_offsets, wl.cand_tok_offsets,
+                                                             wl.cand_tokens))
+    c, nll, _, _ = J.jet_evaluate(wl.q_cand_offsets, sums, gold, cls)
+    oc, onll, _, _ = oracle.evaluate(wl.q_cand_offsets, ref_sums, gold, cls)
+    assert np.abs(nll - onll).max() <= 2 * max_ds + 1e-12
+    for q in range(wl.n_questions):
+        a, b = wl.q_cand_offsets[q], wl.q_cand_offsets[q + 1]
+        r = np.sort(ref_sums[a:b])
+        if b - a < 2 or r[-1] - r[-2] > 0.1:
+            assert c[q] == oc[q], q
+
+
 def run_gpu(path, wl, dtype, **kw):
     m = J.jet_model_load(path, dtype=dtype, **kw)
     try:
@@ -101,6 +121,7 @@ def test_scores_match_oracle(spec, wname, dtype, model_dir):
     log(f"[parity] max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
     from conftest import record_parity
     record_parity(f"{spec}/{wname}/dtype{dtype}", max_tok=dt, max_sum=ds)
+    check_evaluation(wl, sums, ref_sums, ds)
     # work counters follow the closed forms of shared-prefix evaluation (Section 4.1)
     P = np.diff(wl.prefix_offsets)
     m = np.diff(wl.cand_tok_offsets)

@@ -70,6 +70,71 @@ def test_decide_rejects_bad_requests():
         J.jet_decide(7, [0, 2], np.zeros(2, np.float32))
 
 
+def _eval_case(seed, n_q=200, kmax=8):
+    """Seeded questions with 1..kmax candidates of 1..3 tokens from a small
+    alphabet (so labels with identical text occur), scores with ties."""
+    rng = np.random.default_rng(seed)
+    ks = rng.integers(1, kmax + 1, size=n_q)
+    qco = np.concatenate([[0], np.cumsum(ks)]).astype(np.int64)
+    N = int(qco[-1])
+    lens = rng.integers(1, 4, size=N)
+    cto = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    toks = rng.integers(0, 3, size=int(cto[-1])).astype(np.int32)
+    sums = rng.normal(-12.0, 4.0, size=N).astype(np.float32)
+    tie = rng.random(N) < 0.15
+    sums[1:][tie[1:]] = sums[:-1][tie[1:]]
+    gold = np.array([rng.integers(0, k) for k in ks], np.int32)
+    return qco, cto, toks, sums, gold
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_evaluate_matches_oracle(seed):
+    qco, cto, toks, sums, gold = _eval_case(seed)
+    cls = J.jet_answer_classes(qco, cto, toks)
+    np.testing.assert_array_equal(cls, oracle.answer_classes(qco, cto, toks))
+    assert (cls != np.arange(len(cls)) - np.repeat(qco[:-1], np.diff(qco))).any()  # duplicates present
+    for cc in (cls, None):
+        c, nll, acc, mnll = J.jet_evaluate(qco, sums, gold, cc)
+        oc, onll, oacc, omnll = oracle.evaluate(qco, sums.astype(np.float64), gold, cc)
+        np.testing.assert_array_equal(c, oc)
+        np.testing.assert_allclose(nll, onll, rtol=1e-12, atol=1e-13)
+        assert acc == oacc and mnll == pytest.approx(omnll, rel=1e-12, abs=1e-13)
+        # the prediction is jet_decide's choice
+        _, ch, _ = J.jet_decide(J.JET_CHOICE, qco, sums)
+        ref = cc if cc is not None else np.arange(len(sums)) - np.repeat(qco[:-1], np.diff(qco))
+        np.testing.assert_array_equal(c, ref[qco[:-1] + ch] == ref[qco[:-1] + gold])
+
+
+def test_evaluate_edge_cases():
+    # the gold class far below the rest: NLL stays finite (log form)
+    c, nll, acc, mnll = J.jet_evaluate([0, 2], np.array([0.0, -1000.0], np.float32), [1])
+    assert c[0] == 0 and nll[0] == pytest.approx(1000.0, abs=1e-9)
+    # every label with the gold text: NLL exactly 0 and correct
+    c, nll, _, _ = J.jet_evaluate([0, 3], np.array([-1.0, -5.0, -2.0], np.float32), [1], [0, 0, 0])
+    assert c[0] == 1 and nll[0] == 0.0
+    # one candidate
+    c, nll, acc, mnll = J.jet_evaluate([0, 1], np.array([-3.0], np.float32), [0])
+    assert (c[0], nll[0], acc, mnll) == (1, 0.0, 1.0, 0.0)
+    # binary: correct iff q(true) > 1/2, ties to false
+    s = np.array([-2.0, -2.0, -3.0, -1.0], np.float32)
+    c, _, _, _ = J.jet_evaluate([0, 2, 4], s, [1, 1])
+    _, _, v = J.jet_decide(J.JET_BINARY, [0, 2, 4], s)
+    np.testing.assert_array_equal(c, (v > 0.5).astype(np.int32))
+
+
+def test_evaluate_rejects_bad_requests():
+    z = np.zeros(3, np.float32)
+    for args in (([0, 3], z, [3]), ([0, 3], z, [-1]), ([0, 3, 3], z, [0, 0]),
+                 ([0, 3], np.array([0, np.inf, 0], np.float32), [0])):
+        with pytest.raises(J.JetError) as e:
+            J.jet_evaluate(*args)
+        assert e.value.code == J.JET_E_INVALID
+    with pytest.raises(J.JetError):
+        J.jet_answer_classes([0, 2], [0, 1, 1], np.zeros(1, np.int32))  # empty candidate
+    with pytest.raises(J.JetError):
+        J.jet_answer_classes([0, 0], [0], np.zeros(0, np.int32))        # question without candidates
+
+
 def _expected_layout(wl):
     """Definition: y_{c,t} sits at position P + t - 1 and is predicted by the
     row holding y_{c,t-1}; y_{c,1} by the last prefix position."""
