@@ -16,7 +16,9 @@ Header keys: ``arch`` ("dense" | "hybrid"), ``dtype`` ("bf16" | "f32", the
 storage type of every matrix), ``d_model``, ``n_layers``, ``n_heads``,
 ``n_kv_heads``, ``head_dim``, ``ffn``, ``vocab``, ``rms_eps``, ``rope_theta``,
 ``layer_types`` (list of "attn" | "gdn"), ``gdn_heads``, ``gdn_dk``, ``gdn_dv``,
-``conv_kernel``, ``max_ctx``, ``seed``, ``init_std``, ``zero``, and ``tensors``:
+``conv_kernel``, ``n_experts`` (0: dense SwiGLU FFN; else every FFN is a
+mixture of experts), ``top_k``, ``moe_ffn``, ``shared_ffn`` (0: no shared
+expert), ``max_ctx``, ``seed``, ``init_std``, ``zero``, and ``tensors``:
 a list of ``{name, dtype, shape, offset, nbytes}``. Matrices use the
 ``[out_features, in_features]`` convention. Norm gains, ``A_log`` and
 ``dt_bias`` are stored as f32 whatever the matrix dtype is.
@@ -88,6 +90,31 @@ MODEL_SPECS: dict[str, dict] = {
                               n_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
                               vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
                               conv_kernel=4, max_ctx=8192),
+    # Small mixture-of-experts hybrid (3 delta-rule + 1 attention layer, every
+    # FFN 8 routed experts of 128, top 2, plus a gated shared expert of 128).
+    "small_moe_bf16": dict(arch="hybrid", dtype="bf16", d_model=256, n_layers=4,
+                           n_heads=2, n_kv_heads=1, head_dim=128, ffn=128,
+                           vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
+                           conv_kernel=4, n_experts=8, top_k=2, moe_ffn=128,
+                           shared_ffn=128, max_ctx=8192),
+    "small_moe_fp32": dict(arch="hybrid", dtype="f32", d_model=256, n_layers=4,
+                           n_heads=2, n_kv_heads=1, head_dim=128, ffn=128,
+                           vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
+                           conv_kernel=4, n_experts=8, top_k=2, moe_ffn=128,
+                           shared_ffn=128, max_ctx=8192),
+    # 35B-A3B-shape mixture-of-experts hybrid: 10 x [3 delta-rule + 1 GQA
+    # attention layer], d=2048, every FFN 256 routed experts of 512 (top 8)
+    # plus a gated shared expert of 512: 33.7B parameters, 2.5B active per token.
+    "moe_35b_a3b": dict(arch="hybrid", dtype="bf16", d_model=2048, n_layers=40,
+                        n_heads=16, n_kv_heads=2, head_dim=128, ffn=512,
+                        vocab=151936, gdn_heads=16, gdn_dk=128, gdn_dv=128,
+                        conv_kernel=4, n_experts=256, top_k=8, moe_ffn=512,
+                        shared_ffn=512, max_ctx=8192),
+    # Micro mixture of experts for oracle self-checks on the CPU.
+    "micro_moe_fp32": dict(arch="dense", dtype="f32", d_model=64, n_layers=2,
+                           n_heads=4, n_kv_heads=2, head_dim=16, ffn=32,
+                           vocab=512, n_experts=4, top_k=2, moe_ffn=32,
+                           shared_ffn=32, max_ctx=4096),
     # Micro hybrid for oracle self-checks on the CPU: L=4, d=64.
     "micro_hybrid_fp32": dict(arch="hybrid", dtype="f32", d_model=64, n_layers=4,
                               n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
@@ -95,7 +122,8 @@ MODEL_SPECS: dict[str, dict] = {
                               conv_kernel=4, max_ctx=4096),
 }
 
-DEFAULTS = dict(rms_eps=1e-6, rope_theta=1.0e6, init_std=0.02)
+DEFAULTS = dict(rms_eps=1e-6, rope_theta=1.0e6, init_std=0.02, n_experts=0, top_k=0,
+                moe_ffn=0, shared_ffn=0)
 
 
 def full_spec(spec: dict | str) -> dict:
@@ -141,10 +169,22 @@ def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
                     (p + "gdn_dt_bias", "f32", (H,), "zeros"),
                     (p + "gdn_norm", "f32", (dv,), "ones"),
                     (p + "gdn_wo", mt, (d, H * dv), "normal")]
-        out += [(p + "ffn_norm", "f32", (d,), "ones"),
-                (p + "w_gate", mt, (F, d), "normal"),
-                (p + "w_up", mt, (F, d), "normal"),
-                (p + "w_down", mt, (d, F), "normal")]
+        out.append((p + "ffn_norm", "f32", (d,), "ones"))
+        if s["n_experts"] == 0:
+            out += [(p + "w_gate", mt, (F, d), "normal"),
+                    (p + "w_up", mt, (F, d), "normal"),
+                    (p + "w_down", mt, (d, F), "normal")]
+        else:
+            E, Fe, Fs = s["n_experts"], s["moe_ffn"], s["shared_ffn"]
+            out += [(p + "moe_router", mt, (E, d), "normal"),
+                    (p + "moe_gate", mt, (E, Fe, d), "normal"),
+                    (p + "moe_up", mt, (E, Fe, d), "normal"),
+                    (p + "moe_down", mt, (E, d, Fe), "normal")]
+            if Fs:
+                out += [(p + "shared_router", mt, (1, d), "normal"),
+                        (p + "shared_gate", mt, (Fs, d), "normal"),
+                        (p + "shared_up", mt, (Fs, d), "normal"),
+                        (p + "shared_down", mt, (d, Fs), "normal")]
     out += [("final_norm", "f32", (d,), "ones"), ("lm_head", mt, (V, d), "normal")]
     return out
 
@@ -329,6 +369,9 @@ WORKLOADS: dict[str, dict] = {
     "dense_27b_k10": dict(model="dense_27b", Q=64, P=(1024, 4096), ids="zipf", K=10, m=(8, 40)),
     "small_hybrid": dict(model="small_hybrid_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
     "micro_hybrid": dict(model="micro_hybrid_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
+    "moe_35b_a3b_k4": dict(model="moe_35b_a3b", Q=128, P=(200, 1500), ids="zipf", K=4, m=(1, 24)),
+    "small_moe": dict(model="small_moe_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
+    "micro_moe": dict(model="micro_moe_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
 }
 
 

@@ -10,6 +10,12 @@ each one is written as its textbook definition:
 * ``attention``: softmax(q k^T / sqrt(hd)) v per query head, key/value head
   ``h // (Hq/Hkv)``, key j visible to query i iff pos_j <= pos_i.
 * FFN: down(silu(gate(a)) * up(a)).
+* ``moe_ffn`` (models with experts): the router scores every expert with one
+  linear map; each row keeps its top_k experts by router logit (lowest expert
+  index first among equal logits) and mixes their FFN outputs with weights
+  softmax over the kept logits (the full softmax renormalised over the kept
+  experts); a shared expert's FFN output is added scaled by
+  sigmoid(shared_router . a).
 * ``gdn_*``: gated delta rule (per head, state S of shape [dv, dk]):
   S <- alpha S;  S <- S + beta (v - S k) k^T;  o = S q, with
   q, k l2-normalised (eps 1e-6), q scaled by 1/sqrt(dk), beta = sigmoid(b),
@@ -17,8 +23,8 @@ each one is written as its textbook definition:
   convolution (kernel 4) + SiLU in front of q, k, v, and an output
   RMSNorm(o) * silu(z) per head.
 
-Pins (tests): transformers' Qwen2 decoder and Qwen3-Next gated delta-rule
-layer on the same weights, all-zero weights, RoPE and attention special
+Pins (tests): transformers' Qwen2 decoder, Qwen3-Next gated delta-rule
+layer and Qwen2-MoE sparse block on the same weights, all-zero weights, RoPE and attention special
 cases, gated delta-rule closed forms.
 """
 from __future__ import annotations
@@ -47,13 +53,21 @@ class Model:
         self.V = self.h["vocab"]
         self.eps = float(self.h["rms_eps"])
         self.layer_types = self.h["layer_types"]
+        self.n_experts = int(self.h.get("n_experts", 0))
+        self.top_k = int(self.h.get("top_k", 0))
 
     def w(self, name: str) -> np.ndarray:
         return upcast(jet_synth.tensor_raw(self.path, name, self.h))
 
     def layer(self, i: int) -> dict:
+        """Weights of block i; the per-expert matrices are read by ``expert``."""
         p = f"blk.{i}."
-        return {k[len(p):]: self.w(k) for k in self._index if k.startswith(p)}
+        return {k[len(p):]: self.w(k) for k in self._index
+                if k.startswith(p) and k[len(p):] not in ("moe_gate", "moe_up", "moe_down")}
+
+    def expert(self, i: int, name: str, e: int) -> np.ndarray:
+        """Matrix e of the [E, rows, cols] expert tensor ``name`` of block i."""
+        return upcast(jet_synth.tensor_raw(self.path, f"blk.{i}.{name}", self.h)[e])
 
 
 # --------------------------------------------------------------------------
@@ -104,6 +118,34 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
         p = np.exp(s)
         p /= p.sum(axis=1, keepdims=True)
         out[:, h, :] = p @ v[:, kh, :]
+    return out
+
+
+def swiglu_ffn(a: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray) -> np.ndarray:
+    return (silu(a @ Wg.T) * (a @ Wu.T)) @ Wd.T
+
+
+def moe_route(logits: np.ndarray, top_k: int) -> tuple[np.ndarray, np.ndarray]:
+    """Per row: the top_k expert indices by logit (lowest index first among
+    equal logits) and their weights, softmax over the kept logits."""
+    sel = np.argsort(-logits, axis=1, kind="stable")[:, :top_k]
+    z = np.take_along_axis(logits, sel, axis=1)
+    w = np.exp(z - z.max(axis=1, keepdims=True))
+    return sel, w / w.sum(axis=1, keepdims=True)
+
+
+def moe_ffn(model: "Model", li: int, W: dict, a: np.ndarray) -> np.ndarray:
+    """Mixture-of-experts FFN of block li on rows a [n, d]."""
+    sel, wts = moe_route(a @ W["moe_router"].T, model.top_k)
+    out = np.zeros_like(a)
+    for e in np.unique(sel):
+        rows, slot = np.nonzero(sel == e)
+        y = swiglu_ffn(a[rows], model.expert(li, "moe_gate", e), model.expert(li, "moe_up", e),
+                       model.expert(li, "moe_down", e))
+        out[rows] += wts[rows, slot][:, None] * y
+    if "shared_gate" in W:
+        g = 1.0 / (1.0 + np.exp(-(a @ W["shared_router"].T)))
+        out += g * swiglu_ffn(a, W["shared_gate"], W["shared_up"], W["shared_down"])
     return out
 
 
@@ -242,7 +284,10 @@ def forward(model: Model, seqs: list, starts: list | None = None,
         for r0 in range(0, x.shape[0], row_chunk):
             r = slice(r0, min(r0 + row_chunk, x.shape[0]))
             a = rmsnorm(x[r], W["ffn_norm"], model.eps)
-            x[r] = x[r] + (silu(a @ W["w_gate"].T) * (a @ W["w_up"].T)) @ W["w_down"].T
+            if model.n_experts:
+                x[r] = x[r] + moe_ffn(model, li, W, a)
+            else:
+                x[r] = x[r] + swiglu_ffn(a, W["w_gate"], W["w_up"], W["w_down"])
         del W
     return [x[sl] for sl in slices], out_states
 

@@ -55,6 +55,14 @@ def pin_hybrid_path(model_dir):
     return p
 
 
+@pytest.fixture(scope="module")
+def pin_moe_path(model_dir):
+    p = os.path.join(model_dir, "pin_moe.jetm")
+    if not os.path.exists(p):
+        jet_synth.write_model(p, _spec("micro_moe_fp32", init_std=0.15))
+    return p
+
+
 # --------------------------------------------------------------------------
 # Section 3.1-3.3: log-probabilities, sums, normalisation, decisions
 # --------------------------------------------------------------------------
@@ -411,9 +419,84 @@ def test_gdn_recurrence_matches_transformers_recurrent_form():
 # invariants of the scoring method (Section 4.1, Section 5.6)
 # --------------------------------------------------------------------------
 
-@pytest.mark.parametrize("which", ["dense", "hybrid"])
-def test_prefix_sharing_equals_unshared(which, pin_dense_path, pin_hybrid_path):
-    path = pin_dense_path if which == "dense" else pin_hybrid_path
+def _hf_moe_block(m, li):
+    """transformers' Qwen2-MoE sparse block (router, experts, gated shared
+    expert) in float64 holding block li's weights of the oracle's model."""
+    import torch
+    from transformers.models.qwen2_moe.configuration_qwen2_moe import Qwen2MoeConfig
+    from transformers.models.qwen2_moe.modeling_qwen2_moe import Qwen2MoeSparseMoeBlock
+    h = m.h
+    cfg = Qwen2MoeConfig(hidden_size=h["d_model"], num_experts=h["n_experts"],
+                         num_experts_per_tok=h["top_k"], norm_topk_prob=True,
+                         moe_intermediate_size=h["moe_ffn"], shared_expert_intermediate_size=h["shared_ffn"],
+                         hidden_act="silu")
+    blk = Qwen2MoeSparseMoeBlock(cfg).double()
+    W = m.layer(li)
+    T = lambda x: torch.from_numpy(np.ascontiguousarray(x))
+    with torch.no_grad():
+        blk.gate.weight.copy_(T(W["moe_router"]))
+        for e in range(h["n_experts"]):
+            blk.experts.gate_up_proj[e].copy_(T(np.concatenate([m.expert(li, "moe_gate", e),
+                                                                m.expert(li, "moe_up", e)])))
+            blk.experts.down_proj[e].copy_(T(m.expert(li, "moe_down", e)))
+        blk.shared_expert.gate_proj.weight.copy_(T(W["shared_gate"]))
+        blk.shared_expert.up_proj.weight.copy_(T(W["shared_up"]))
+        blk.shared_expert.down_proj.weight.copy_(T(W["shared_down"]))
+        blk.shared_expert_gate.weight.copy_(T(W["shared_router"]))
+    return blk, W
+
+
+def test_moe_block_matches_transformers_qwen2moe(pin_moe_path):
+    """The oracle's mixture-of-experts FFN against transformers' Qwen2-MoE
+    sparse block on the same weights and inputs (its router softmax runs in
+    float32, hence the tolerance)."""
+    import torch
+    m = om.Model(pin_moe_path)
+    a = np.random.default_rng(5).normal(size=(40, m.d))
+    for li in range(len(m.layer_types)):
+        blk, W = _hf_moe_block(m, li)
+        with torch.no_grad():
+            ref = blk(torch.from_numpy(a)[None])
+        ref = (ref[0] if isinstance(ref, tuple) else ref)[0].numpy()
+        got = om.moe_ffn(m, li, W, a)
+        assert np.abs(ref).max() > 1e-2
+        np.testing.assert_allclose(got, ref, rtol=0, atol=2e-6 * np.abs(ref).max())
+
+
+def test_moe_routing_special_cases(pin_moe_path):
+    """Equal router logits keep the lowest-index experts with equal weights;
+    keeping every expert gives the full softmax mixture; no shared expert
+    and one expert reduce to the dense SwiGLU FFN."""
+    m = om.Model(pin_moe_path)
+    W = dict(m.layer(0))
+    a = np.random.default_rng(6).normal(size=(7, m.d))
+    ffn = [om.swiglu_ffn(a, m.expert(0, "moe_gate", e), m.expert(0, "moe_up", e), m.expert(0, "moe_down", e))
+           for e in range(m.n_experts)]
+    g = 1.0 / (1.0 + np.exp(-(a @ W["shared_router"].T)))
+    shared = g * om.swiglu_ffn(a, W["shared_gate"], W["shared_up"], W["shared_down"])
+    W0 = dict(W, moe_router=np.zeros_like(W["moe_router"]))
+    k = m.top_k
+    np.testing.assert_allclose(om.moe_ffn(m, 0, W0, a), sum(ffn[:k]) / k + shared, rtol=0, atol=1e-12)
+    sel, w = om.moe_route(np.array([[0.5, 2.0, 2.0, -1.0]]), 2)
+    assert list(sel[0]) == [1, 2] and np.allclose(w, 0.5)
+    m_all = om.Model(pin_moe_path)
+    m_all.top_k = m.n_experts
+    z = a @ W["moe_router"].T
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    np.testing.assert_allclose(om.moe_ffn(m_all, 0, W, a), sum(p[:, [e]] * ffn[e] for e in range(m.n_experts)) + shared,
+                               rtol=0, atol=1e-12)
+    m_one = om.Model(pin_moe_path)
+    m_one.top_k = 1
+    Wn = {k_: v for k_, v in W.items() if not k_.startswith("shared_")}
+    best = np.argmax(z, axis=1)
+    np.testing.assert_allclose(om.moe_ffn(m_one, 0, Wn, a), np.stack([ffn[best[i]][i] for i in range(len(a))]),
+                               rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("which", ["dense", "hybrid", "moe"])
+def test_prefix_sharing_equals_unshared(which, pin_dense_path, pin_hybrid_path, pin_moe_path):
+    path = {"dense": pin_dense_path, "hybrid": pin_hybrid_path, "moe": pin_moe_path}[which]
     V = jet_synth.read_header(path)["vocab"]
     wl = jet_synth.make_workload("micro_hybrid", vocab=V, Q=3, P=(4, 17), K=4, m=(1, 6))
     a, sa = oracle.score_unshared(path, wl)
