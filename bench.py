@@ -95,7 +95,10 @@ def describe(wname: str) -> dict:
     s = jet_synth.full_spec(r["model"])
     return {"workload": wname,
             "model": (f"{s['arch']} {s['n_layers']}L d={s['d_model']} heads {s['n_heads']}/{s['n_kv_heads']} "
-                      f"hd={s['head_dim']} ffn={s['ffn']} vocab={s['vocab']} {s['dtype']} random N(0,0.02)"),
+                      f"hd={s['head_dim']} "
+                      + (f"experts {s['n_experts']} top {s['top_k']} expert ffn={s['moe_ffn']} "
+                         f"shared ffn={s['shared_ffn']} " if s["n_experts"] else f"ffn={s['ffn']} ")
+                      + f"vocab={s['vocab']} {s['dtype']} random N(0,0.02)"),
             "questions": r["Q"], "prefix_len": list(r["P"]), "prefix_ids": r["ids"],
             "candidates_per_question": r["K"], "candidate_len": list(r["m"])}
 

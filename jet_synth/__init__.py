@@ -102,6 +102,12 @@ MODEL_SPECS: dict[str, dict] = {
                            vocab=2048, gdn_heads=2, gdn_dk=128, gdn_dv=128,
                            conv_kernel=4, n_experts=8, top_k=2, moe_ffn=128,
                            shared_ffn=128, max_ctx=8192),
+    # Two-layer dense decoder with mixture-of-experts FFNs (for the
+    # single-bf16 mode, whose rounding grows with depth).
+    "tiny_moe_bf16": dict(arch="dense", dtype="bf16", d_model=256, n_layers=2,
+                          n_heads=2, n_kv_heads=1, head_dim=128, ffn=128,
+                          vocab=2048, n_experts=8, top_k=2, moe_ffn=128,
+                          shared_ffn=128, max_ctx=8192),
     # 35B-A3B-shape mixture-of-experts hybrid: 10 x [3 delta-rule + 1 GQA
     # attention layer], d=2048, every FFN 256 routed experts of 512 (top 8)
     # plus a gated shared expert of 512: 33.7B parameters, 2.5B active per token.
@@ -371,6 +377,7 @@ WORKLOADS: dict[str, dict] = {
     "micro_hybrid": dict(model="micro_hybrid_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
     "moe_35b_a3b_k4": dict(model="moe_35b_a3b", Q=128, P=(200, 1500), ids="zipf", K=4, m=(1, 24)),
     "small_moe": dict(model="small_moe_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
+    "tiny_moe": dict(model="tiny_moe_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
     "micro_moe": dict(model="micro_moe_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
 }
 

@@ -28,6 +28,10 @@ struct GemmArgs {
   int pair_out;   // SwiGLU / QKV-RoPE: write (hi, lo) pairs
   float oscale;   // every product is multiplied by oscale before the epilogue
   QkvRope rope;   // EPI_QKV_ROPE only
+  // grouped GEMM: row tile t uses B + tile_group[t] * group_stride; tiles
+  // with tile_group -1 do nothing (null: one B for all tiles)
+  const int *tile_group = nullptr;
+  int64_t group_stride = 0;
 };
 
 // (hi, lo) split of v stored at p[0] and p[ps] (lo only with pair).
@@ -159,8 +163,14 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
   int tm, tn;
   tile_coords(nt_m, nt_n, &tm, &tn);
   const int m0 = tm * C::BM, n0 = tn * C::BN;
+  const T *B = g.B;
+  if (g.tile_group) {
+    const int grp = g.tile_group[tm];
+    if (grp < 0) return;
+    B += (int64_t)grp * g.group_stride;
+  }
   f32x16 acc[C::MI][C::NI];
-  gemm_tile<C>(g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
+  gemm_tile<C>(g.A, g.lda, B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
   if (staged_epilogue<C, EPI>(g, m0, n0, acc, lds)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
@@ -448,6 +458,49 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
     }
   }
   return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+}
+
+template <class C, int EPI>
+static hipError_t run_gemm_grouped(const void *A, int64_t lda, const void *B, int64_t ldb, int64_t group_stride,
+                                   const int *tile_group, int M, int N, int K, void *out, int64_t ldo, float oscale,
+                                   hipStream_t st) {
+  using T = typename C::type;
+  static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
+  if (once != hipSuccess) return once;
+  GemmArgs<T> g{(const T *)A, (const T *)B, lda, ldb, M, N, K, K, K, out, ldo, 0, oscale, QkvRope{},
+                tile_group, group_stride};
+  const int tiles = (M / C::BM) * ((N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
+  return hipGetLastError();
+}
+
+template <class C>
+static hipError_t run_grouped_epi(int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
+                                  int64_t group_stride, const int *tile_group, int M, int N, int K, void *out,
+                                  int64_t ldo, float oscale, hipStream_t st) {
+  switch (epi) {
+    case EPI_STORE_F32:
+      return run_gemm_grouped<C, 0>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+    case EPI_RESID_ADD:
+      return run_gemm_grouped<C, 1>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+    case EPI_SWIGLU:
+      return run_gemm_grouped<C, 2>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int gemm_group_rows(int dtype) { return dtype == 2 ? HalfS::BM : dtype == 1 ? CfgF::BM : SmallB::BM; }
+
+hipError_t launch_gemm_grouped(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
+                               int64_t group_stride, const int *tile_group, int M, int N, int K, void *out,
+                               int64_t ldo, float oscale, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (!tile_group || M % gemm_group_rows(dtype)) return hipErrorInvalidValue;
+  if (dtype == 2)
+    return run_grouped_epi<HalfS>(epi, A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+  if (dtype == 1)
+    return run_grouped_epi<CfgF>(epi, A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+  return run_grouped_epi<SmallB>(epi, A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
 }
 
 template <class C>

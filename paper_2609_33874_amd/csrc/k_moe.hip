@@ -1,0 +1,200 @@
+// Mixture-of-experts FFN pieces around the grouped expert GEMMs: top-k
+// routing, placement of each (row, choice) in its expert's segment, the row
+// scatter into that segment, and the weighted combine back into the residual.
+//
+// Layout: every expert owns a segment of the permuted row buffer that starts
+// at a multiple of the grouped GEMM's tile rows (bm), so each row tile of the
+// grouped GEMM belongs to one expert (tile_group[tile] = expert, -1 past the
+// last segment). A row's results do not depend on where in its segment it
+// lands (the GEMM computes every row alike), and the combine adds a row's
+// choices in the order of its top-k list, so outputs are deterministic.
+#include "device.h"
+#include "kernels.h"
+
+namespace jetk {
+
+// One wave per row: top_k experts by router logit (lowest index first among
+// equal logits), their weights softmax over the kept logits, the shared
+// expert's gate sigmoid(logit[E]) when present, and per-expert counts.
+__global__ __launch_bounds__(256) void moe_route_kernel(MoeRouteArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const float *z = a.logits + (int64_t)r * a.ldl;
+  constexpr int PER = kMoeMaxExperts / 64;
+  float v[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = i * 64 + lane;
+    v[i] = e < a.E ? z[e] : -INFINITY;
+  }
+  float zsel[kMoeMaxTopK];
+  int esel[kMoeMaxTopK];
+  for (int j = 0; j < a.top_k; ++j) {
+    // lane-local best, ties to the lower index (indices grow with i)
+    float bv = -INFINITY;
+    int be = 0x7fffffff;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = i * 64 + lane;
+      if (e < a.E && (v[i] > bv || (v[i] == bv && e < be))) {
+        bv = v[i];
+        be = e;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o);
+      const int oe = __shfl_xor(be, o);
+      if (ov > bv || (ov == bv && oe < be)) {
+        bv = ov;
+        be = oe;
+      }
+    }
+    if (be < 0 || be >= a.E) be = 0;  // only when no finite logit is left (NaN input)
+    zsel[j] = bv;
+    esel[j] = be;
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (i * 64 + lane == be) v[i] = -INFINITY;
+  }
+  if (lane != 0) return;
+  // zsel[0] is the largest kept logit
+  float s = 0.0f;
+  for (int j = 0; j < a.top_k; ++j) s += __expf(zsel[j] - zsel[0]);
+  const float inv = 1.0f / s;
+  for (int j = 0; j < a.top_k; ++j) {
+    a.sel[(int64_t)r * a.top_k + j] = esel[j];
+    a.wts[(int64_t)r * a.top_k + j] = __expf(zsel[j] - zsel[0]) * inv;
+    atomicAdd(&a.counts[esel[j]], 1);
+  }
+  if (a.shared_gate) a.shared_gate[r] = 1.0f / (1.0f + __expf(-z[a.E]));
+}
+
+// One workgroup: segment starts (counts rounded up to bm), the cursors the
+// scatter advances, the expert of every row tile, and the counts cleared for
+// the next layer.
+__global__ __launch_bounds__(256) void moe_plan_kernel(int *__restrict__ counts, int E, int bm, int max_tiles,
+                                                       int *__restrict__ cursor, int *__restrict__ tile_group) {
+  __shared__ int off[kMoeMaxExperts + 1];
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int e = 0; e < E; ++e) {
+      off[e] = acc;
+      acc += (counts[e] + bm - 1) / bm * bm;
+    }
+    off[E] = acc;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += 256) {
+    cursor[e] = off[e];
+    counts[e] = 0;
+  }
+  for (int t = threadIdx.x; t < max_tiles; t += 256) {
+    const int row = t * bm;
+    int g = -1;
+    if (row < off[E]) {
+      int lo = 0, hi = E - 1;  // last e with off[e] <= row
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= row) lo = mid;
+        else hi = mid - 1;
+      }
+      g = lo;
+    }
+    tile_group[t] = g;
+  }
+}
+
+// One wave per (row, choice) i = row * top_k + j: claims a place in the
+// chosen expert's segment and copies the row (row_chunks 16-byte chunks) there.
+__global__ __launch_bounds__(256) void moe_scatter_kernel(const uint4 *__restrict__ x, int64_t row_chunks,
+                                                          const int *__restrict__ sel, int n, int top_k,
+                                                          int *__restrict__ cursor, int *__restrict__ slot_of,
+                                                          uint4 *__restrict__ xp) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= n) return;
+  int slot = 0;
+  if (lane == 0) {
+    slot = atomicAdd(&cursor[sel[i]], 1);
+    slot_of[i] = slot;
+  }
+  slot = __shfl(slot, 0);
+  const uint4 *src = x + (int64_t)(i / top_k) * row_chunks;
+  uint4 *dst = xp + (int64_t)slot * row_chunks;
+  for (int64_t c = lane; c < row_chunks; c += 64) dst[c] = src[c];
+}
+
+// One workgroup per row: resid += sum_j w_j y[slot_j] (j in top-k order)
+// + g * y_shared, the mixture summed first, in fp32.
+__global__ __launch_bounds__(256) void moe_combine_kernel(const float *__restrict__ y, const int *__restrict__ slot_of,
+                                                          const float *__restrict__ wts, int top_k,
+                                                          const float *__restrict__ ys,
+                                                          const float *__restrict__ gate, int d,
+                                                          float *__restrict__ resid) {
+  const int r = blockIdx.x;
+  const int *sl = slot_of + (int64_t)r * top_k;
+  const float *w = wts + (int64_t)r * top_k;
+  for (int c = threadIdx.x * 4; c < d; c += 1024) {
+    float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int j = 0; j < top_k; ++j) {
+      const float4 v = *(const float4 *)(y + (int64_t)sl[j] * d + c);
+      const float wj = w[j];
+      o.x += wj * v.x;
+      o.y += wj * v.y;
+      o.z += wj * v.z;
+      o.w += wj * v.w;
+    }
+    if (ys) {
+      const float g = gate[r];
+      const float4 v = *(const float4 *)(ys + (int64_t)r * d + c);
+      o.x += g * v.x;
+      o.y += g * v.y;
+      o.z += g * v.z;
+      o.w += g * v.w;
+    }
+    float4 *dst = (float4 *)(resid + (int64_t)r * d + c);
+    float4 x = *dst;
+    x.x += o.x;
+    x.y += o.y;
+    x.z += o.z;
+    x.w += o.w;
+    *dst = x;
+  }
+}
+
+hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  if (a.E < 1 || a.E > kMoeMaxExperts || a.top_k < 1 || a.top_k > kMoeMaxTopK || a.top_k > a.E)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_route_kernel, dim3((a.R + 3) / 4), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_plan(int *counts, int E, int bm, int max_tiles, int *cursor, int *tile_group,
+                           hipStream_t st) {
+  if (E < 1 || E > kMoeMaxExperts || bm < 1 || max_tiles < 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, counts, E, bm, max_tiles, cursor, tile_group);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, const int *sel, int R, int top_k, int *cursor,
+                              int *slot_of, void *xp, hipStream_t st) {
+  const int n = R * top_k;
+  if (n <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_scatter_kernel, dim3((n + 3) / 4), dim3(256), 0, st, (const uint4 *)x, row_bytes / 16, sel,
+                     n, top_k, cursor, slot_of, (uint4 *)xp);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
+                              const float *gate, int R, int d, float *resid, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_combine_kernel, dim3(R), dim3(256), 0, st, y, slot_of, wts, top_k, ys, gate, d, resid);
+  return hipGetLastError();
+}
+
+}  // namespace jetk

@@ -166,4 +166,43 @@ hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst
 // of two that keeps every value inside the fp16 normal range).
 hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst, hipStream_t st);
 
+
+// ---- mixture-of-experts FFN (k_moe.hip) ----
+constexpr int kMoeMaxExperts = 512;
+constexpr int kMoeMaxTopK = 16;
+
+// Router logits [R][ldl] fp32 (E expert columns, then the shared expert's gate
+// logit at column E when shared_gate is set) -> sel/wts [R][top_k] (experts by
+// logit, lowest index first among equals; softmax over the kept logits),
+// shared_gate[R] = sigmoid(logit E); counts[E] (zero on entry) += selections.
+struct MoeRouteArgs {
+  const float *logits;
+  int64_t ldl;
+  int R, E, top_k;
+  int *sel;
+  float *wts;
+  float *shared_gate;
+  int *counts;
+};
+hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st);
+// Segment starts (counts rounded up to bm) into cursor[E], the expert of each
+// of max_tiles row tiles (-1 past the last segment) into tile_group; counts
+// are cleared.
+hipError_t launch_moe_plan(int *counts, int E, int bm, int max_tiles, int *cursor, int *tile_group,
+                           hipStream_t st);
+// Row i / top_k of x copied to row slot_of[i] of xp, the next free place of
+// expert sel[i] (rows of row_bytes, a multiple of 16).
+hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, const int *sel, int R, int top_k, int *cursor,
+                              int *slot_of, void *xp, hipStream_t st);
+// resid[r] += sum_j wts[r][j] y[slot_of[r][j]] + gate[r] ys[r] (ys may be null).
+hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
+                              const float *gate, int R, int d, float *resid, hipStream_t st);
+// Grouped GEMM: row tile t of A (tiles of gemm_group_rows(dtype) rows) is
+// multiplied by B + tile_group[t] * group_stride (elements); tiles with
+// tile_group -1 are skipped. Otherwise as launch_gemm (no pair operands).
+int gemm_group_rows(int dtype);
+hipError_t launch_gemm_grouped(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
+                               int64_t group_stride, const int *tile_group, int M, int N, int K, void *out,
+                               int64_t ldo, float oscale, hipStream_t st);
+
 }  // namespace jetk

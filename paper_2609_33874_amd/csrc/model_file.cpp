@@ -159,6 +159,10 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
   get_int(root, "gdn_dk", &h->gdn_dk, false);
   get_int(root, "gdn_dv", &h->gdn_dv, false);
   get_int(root, "conv_kernel", &h->conv_kernel, false);
+  get_int(root, "n_experts", &h->n_experts, false);
+  get_int(root, "top_k", &h->top_k, false);
+  get_int(root, "moe_ffn", &h->moe_ffn, false);
+  get_int(root, "shared_ffn", &h->shared_ffn, false);
   if (const JVal *v = root.get("rms_eps")) h->rms_eps = v->num;
   if (const JVal *v = root.get("rope_theta")) h->rope_theta = v->num;
   const JVal *lt = root.get("layer_types");

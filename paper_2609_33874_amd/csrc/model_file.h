@@ -28,6 +28,9 @@ struct ModelHeader {
   bool bf16 = false;  // matrix storage dtype
   int64_t d = 0, n_layers = 0, n_heads = 0, n_kv_heads = 0, head_dim = 0, ffn = 0, vocab = 0;
   int64_t gdn_heads = 0, gdn_dk = 0, gdn_dv = 0, conv_kernel = 0, max_ctx = 0;
+  // mixture-of-experts FFN (n_experts > 0): top_k routed experts of moe_ffn
+  // hidden units per row, plus a gated shared expert of shared_ffn (0: none)
+  int64_t n_experts = 0, top_k = 0, moe_ffn = 0, shared_ffn = 0;
   double rms_eps = 1e-6, rope_theta = 1e6;
   std::vector<int> layer_is_gdn;
   std::map<std::string, TensorInfo> tensors;

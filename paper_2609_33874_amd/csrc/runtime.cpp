@@ -276,6 +276,29 @@ struct Loader {
     return put_matrix(all.data(), rows * d, bf, out, inv_scale);
   }
 
+  // Expert tensors [E][F][d] gate and up -> [E][2F][d], each expert's rows
+  // interleaved like gate_up.
+  Status expert_gate_up(const std::string &g, const std::string &u, int64_t E, int64_t F, int64_t d, void **out,
+                        float *inv_scale) {
+    const bool bf = m->h.bf16;
+    const size_t es = bf ? 2 : 4, row = (size_t)d * es;
+    const TensorInfo *ti;
+    TRY(read(g, &ti));
+    if (ti->numel() != E * F * d) return Status::err(JET_E_IO, g + ": unexpected size");
+    std::vector<char> gate = host;
+    TRY(read(u, &ti));
+    if (ti->numel() != E * F * d) return Status::err(JET_E_IO, u + ": unexpected size");
+    std::vector<char> all((size_t)(2 * E * F) * row);
+    for (int64_t e = 0; e < E; ++e) {
+      const size_t src = (size_t)(e * F) * row, dst = (size_t)(e * 2 * F) * row;
+      for (int64_t b = 0; b < F / 32; ++b) {
+        std::memcpy(&all[dst + (size_t)(2 * b) * 32 * row], &gate[src + (size_t)b * 32 * row], 32 * row);
+        std::memcpy(&all[dst + (size_t)(2 * b + 1) * 32 * row], &host[src + (size_t)b * 32 * row], 32 * row);
+      }
+    }
+    return put_matrix(all.data(), 2 * E * F * d, bf, out, inv_scale);
+  }
+
   // gate/up interleaved in blocks of 32 rows: [g0..g31, u0..u31, g32.., u32.., ...]
   Status gate_up(const std::string &g, const std::string &u, int64_t F, int64_t d, void **out, float *inv_scale) {
     const bool bf = m->h.bf16;
@@ -303,6 +326,17 @@ Status check_shapes(const ModelHeader &h, int dtype) {
   if (h.d % bk || (h.n_heads * h.head_dim) % bk || h.ffn % bk)
     return Status::err(JET_E_INVALID, "d_model, n_heads*head_dim and ffn must be multiples of " + std::to_string(bk));
   if (h.ffn % 32) return Status::err(JET_E_INVALID, "ffn must be a multiple of 32");
+  if (h.n_experts) {
+    if (h.n_experts > jetk::kMoeMaxExperts || h.top_k < 1 || h.top_k > h.n_experts ||
+        h.top_k > jetk::kMoeMaxTopK)
+      return Status::err(JET_E_INVALID, "mixture of experts: need 1 <= top_k <= n_experts <= " +
+                                            std::to_string(jetk::kMoeMaxExperts) + " and top_k <= " +
+                                            std::to_string(jetk::kMoeMaxTopK));
+    if (h.moe_ffn < 64 || h.moe_ffn % 64 || h.shared_ffn % 64 || h.d % 4)
+      return Status::err(JET_E_INVALID, "mixture of experts: moe_ffn and shared_ffn must be multiples of 64");
+    if (dtype == JET_BF16)
+      return Status::err(JET_E_INVALID, "mixture-of-experts models run in the f32, f16, f16p and bf16-single modes");
+  }
   if (h.hybrid) {
     if (h.gdn_dk != 128 || h.gdn_dv != 128 || h.conv_kernel != 4 || h.gdn_heads < 1)
       return Status::err(JET_E_INVALID, "delta-rule layers need dk = dv = 128 and a width-4 convolution");
@@ -350,8 +384,21 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
       TRY(L.f32_array(p + "gdn_dt_bias", &ly.dt_bias, H));
       TRY(L.f32_array(p + "gdn_norm", &ly.gdn_norm, h.gdn_dv));
     }
-    TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu, &ly.is_gu));
-    TRY(L.matrix(p + "w_down", &ly.w_down, &ly.is_down));
+    if (h.n_experts) {
+      const int64_t nr = ((h.n_experts + (h.shared_ffn ? 1 : 0)) + 63) / 64 * 64;
+      std::vector<std::string> rn{p + "moe_router"};
+      if (h.shared_ffn) rn.push_back(p + "shared_router");
+      TRY(L.concat(rn, h.d, nr, &ly.w_router, &ly.n_router, &ly.is_router));
+      TRY(L.expert_gate_up(p + "moe_gate", p + "moe_up", h.n_experts, h.moe_ffn, h.d, &ly.w_egu, &ly.is_egu));
+      TRY(L.matrix(p + "moe_down", &ly.w_edown, &ly.is_edown));
+      if (h.shared_ffn) {
+        TRY(L.gate_up(p + "shared_gate", p + "shared_up", h.shared_ffn, h.d, &ly.w_sgu, &ly.is_sgu));
+        TRY(L.matrix(p + "shared_down", &ly.w_sdown, &ly.is_sdown));
+      }
+    } else {
+      TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu, &ly.is_gu));
+      TRY(L.matrix(p + "w_down", &ly.w_down, &ly.is_down));
+    }
   }
   // RoPE tables: angles in fp64 on the host, stored as fp32 [max_ctx][hd/2]
   const int64_t half = h.head_dim / 2;
@@ -548,6 +595,69 @@ Status wave_bufs(jet_model *m, int64_t R, WaveBufs *b) {
   return Status::ok();
 }
 
+// Mixture-of-experts FFN on x = RMSNorm(resid) (in b.xn): router GEMM,
+// top-k routing, rows scattered into per-expert segments, grouped gate/up
+// (SwiGLU) and down GEMMs over the segments, the shared expert on all rows,
+// then resid += sum_j w_j y_j + sigmoid(g) y_shared.
+Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
+  const ModelHeader &h = m->h;
+  const int E = (int)h.n_experts, k = (int)h.top_k;
+  const int64_t Fe = h.moe_ffn, Fs = h.shared_ffn, d = h.d;
+  const int bm = jetk::gemm_group_rows(m->kdt);
+  const int64_t S = (R * k + (int64_t)E * (bm - 1) + bm - 1) / bm * bm;  // rows of all segments, at most
+  float *logits, *wts, *sg = nullptr, *y, *ys = nullptr;
+  int *sel, *counts, *cursor, *tiles, *slot;
+  void *xp, *hp, *hs = nullptr;
+  TRY(ws_t<float>(m, "moe_logits", (size_t)(R * ly.n_router), &logits));
+  TRY(ws_t<int>(m, "moe_sel", (size_t)(R * k), &sel));
+  TRY(ws_t<float>(m, "moe_wts", (size_t)(R * k), &wts));
+  TRY(ws_t<int>(m, "moe_counts", (size_t)E, &counts));
+  TRY(ws_t<int>(m, "moe_cursor", (size_t)E, &cursor));
+  TRY(ws_t<int>(m, "moe_tiles", (size_t)(S / bm), &tiles));
+  TRY(ws_t<int>(m, "moe_slot", (size_t)(R * k), &slot));
+  TRY(ws(m, "moe_xp", (size_t)(S * d) * m->esz, &xp));
+  TRY(ws(m, "moe_h", (size_t)(S * Fe) * m->esz, &hp));
+  TRY(ws_t<float>(m, "moe_y", (size_t)(S * d), &y));
+  if (Fs) {
+    TRY(ws_t<float>(m, "moe_sg", (size_t)R, &sg));
+    TRY(ws(m, "moe_hs", (size_t)(R * Fs) * m->esz, &hs));
+    TRY(ws_t<float>(m, "moe_ys", (size_t)(R * d), &ys));
+  }
+  TRY(run_gemm(m, JET_K_OTHER, jetk::EPI_STORE_F32, b.xn, d, 0, ly.w_router, d, R, ly.n_router, d, logits,
+               ly.n_router, ly.is_router));
+  {
+    KTimer t(m, JET_K_OTHER, 0, (double)(R * ly.n_router) * 4.0);
+    HIPC(hipMemsetAsync(counts, 0, sizeof(int) * (size_t)E, m->st));
+    LAUNCH(jetk::launch_moe_route(jetk::MoeRouteArgs{logits, ly.n_router, (int)R, E, k, sel, wts, sg, counts},
+                                  m->st));
+    LAUNCH(jetk::launch_moe_plan(counts, E, bm, (int)(S / bm), cursor, tiles, m->st));
+    LAUNCH(jetk::launch_moe_scatter(b.xn, d * (int64_t)m->esz, sel, (int)R, k, cursor, slot, xp, m->st));
+  }
+  {
+    const double rows = (double)(R * k);
+    KTimer t(m, JET_K_GEMM_GATEUP, 2.0 * rows * (double)(2 * Fe) * (double)d,
+             (rows * (double)d + rows * (double)Fe) * (double)m->esz);
+    LAUNCH(jetk::launch_gemm_grouped(m->kdt, jetk::EPI_SWIGLU, xp, d, ly.w_egu, d, 2 * Fe * d, tiles, (int)S,
+                                     (int)(2 * Fe), (int)d, hp, Fe, ly.is_egu, m->st));
+  }
+  {
+    const double rows = (double)(R * k);
+    KTimer t(m, JET_K_GEMM_DOWN, 2.0 * rows * (double)d * (double)Fe,
+             rows * (double)Fe * (double)m->esz + rows * (double)d * 4.0);
+    LAUNCH(jetk::launch_gemm_grouped(m->kdt, jetk::EPI_STORE_F32, hp, Fe, ly.w_edown, Fe, d * Fe, tiles, (int)S,
+                                     (int)d, (int)Fe, y, d, ly.is_edown, m->st));
+  }
+  if (Fs) {
+    TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, d, 0, ly.w_sgu, d, R, 2 * Fs, d, hs, Fs, ly.is_sgu));
+    TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_STORE_F32, hs, Fs, 0, ly.w_sdown, Fs, R, d, Fs, ys, d, ly.is_sdown));
+  }
+  {
+    KTimer t(m, JET_K_OTHER, 0, (double)(R * (k + 2) * d) * 4.0);
+    LAUNCH(jetk::launch_moe_combine(y, slot, wts, k, ys, sg, (int)R, (int)d, b.resid, m->st));
+  }
+  return Status::ok();
+}
+
 // The FFN sublayer: resid += down(silu(gate(x)) * up(x)), x = RMSNorm(resid).
 Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
@@ -556,6 +666,7 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, ly.ffn_norm, (int)R, (int)h.d, (float)h.rms_eps,
                                 b.xn, m->st));
   }
+  if (h.n_experts) return moe_ffn(m, ly, b, R);
   TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, m->pair, ly.w_gu, h.d, R, 2 * h.ffn, h.d,
                b.act, m->np * h.ffn, ly.is_gu));
   TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, m->pair, ly.w_down, h.ffn, R, h.d,

@@ -30,6 +30,13 @@ struct Layer {
   int64_t n_in = 0;
   float *conv_w = nullptr; // [C][kc], C = 2 H dk + H dv
   float *A_log = nullptr, *dt_bias = nullptr, *gdn_norm = nullptr;
+  // mixture-of-experts FFN (replaces w_gu / w_down)
+  void *w_router = nullptr;  // [n_router][d]: E expert rows, the shared expert's gate row, zero pad
+  int64_t n_router = 0;
+  void *w_egu = nullptr;     // [E][2 Fe][d], each expert's gate/up interleaved like w_gu
+  void *w_edown = nullptr;   // [E][d][Fe]
+  void *w_sgu = nullptr, *w_sdown = nullptr;  // shared expert, like w_gu / w_down
+  float is_router = 1.0f, is_egu = 1.0f, is_edown = 1.0f, is_sgu = 1.0f, is_sdown = 1.0f;
 };
 
 struct DevBuf {

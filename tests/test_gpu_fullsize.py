@@ -143,6 +143,28 @@ def test_hybrid_4b_k4_full(dtype):
     sampled_parity(path, "hybrid_4b_k4", wl, tok, sums, [q], dtype)
 
 
+# The fp64 oracle of a 35B-shape question reads every expert of every layer
+# (minutes on the host).
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("dtype", [pytest.param(J.JET_F16, id="f16")])
+def test_moe_35b_a3b_k4_full(dtype):
+    """35B-A3B-shape mixture-of-experts hybrid (30 delta-rule + 10 attention
+    layers, 256 experts, top 8, shared expert): all 128 questions on the GPU,
+    the shortest-prefix question checked against the oracle."""
+    path = jet_synth.ensure_model("moe_35b_a3b")
+    wl = jet_synth.make_workload("moe_35b_a3b_k4")
+    log(f"[fullsize] moe_35b_a3b_k4 dtype {dtype}: {wl.n_questions} questions, "
+        f"{int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=dtype)
+    try:
+        tok, sums = run(m, wl)
+    finally:
+        J.jet_model_free(m)
+    properties(wl, tok, sums)
+    q = int(np.argmin(np.diff(wl.prefix_offsets)))
+    sampled_parity(path, "moe_35b_a3b_k4", wl, tok, sums, [q], dtype)
+
+
 # The fp64 oracle of one 27B-shape candidate sequence runs for minutes on the
 # host, longer than a per-test limit meant for GPU calls.
 @pytest.mark.timeout(900)
