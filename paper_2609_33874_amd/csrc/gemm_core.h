@@ -480,6 +480,17 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
       sl = sl + 1 == NS ? 0 : sl + 1;
     }
     wait_vmcnt<0>();
+    // The last step also read fragments past the last tile (unused). Wait for
+    // those reads with both fragment buffers held live: otherwise the
+    // compiler may give their registers to the caller's epilogue while the
+    // reads are still in flight, and a late read overwrites its values.
+    if constexpr (C::PAIRA) {
+      wait_frags<0>(fa[0], fl[0], fb[0]);
+      wait_frags<0>(fa[1], fl[1], fb[1]);
+    } else {
+      wait_frags<0>(fa[0], fb[0]);
+      wait_frags<0>(fa[1], fb[1]);
+    }
     __builtin_amdgcn_s_barrier();
   }
 }
