@@ -5,9 +5,10 @@
 // Layout: every expert owns a segment of the permuted row buffer that starts
 // at a multiple of the grouped GEMM's tile rows (bm), so each row tile of the
 // grouped GEMM belongs to one expert (tile_group[tile] = expert, -1 past the
-// last segment). A row's results do not depend on where in its segment it
-// lands (the GEMM computes every row alike), and the combine adds a row's
-// choices in the order of its top-k list, so outputs are deterministic.
+// last segment). Places are given in (row, choice) order within each
+// expert's segment (a counting sort over chunks of the choice list), so the
+// permuted layout, and with it every result, is the same on every run; the
+// combine adds a row's choices in the order of its top-k list.
 #include "device.h"
 #include "kernels.h"
 
@@ -75,7 +76,9 @@ __global__ __launch_bounds__(256) void moe_route_kernel(MoeRouteArgs a) {
 // scatter advances, the expert of every row tile, and the counts cleared for
 // the next layer.
 __global__ __launch_bounds__(256) void moe_plan_kernel(int *__restrict__ counts, int E, int bm, int max_tiles,
-                                                       int *__restrict__ cursor, int *__restrict__ tile_group) {
+                                                       int *__restrict__ cursor, int *__restrict__ tile_group,
+                                                       const int *__restrict__ chunk_hist, int nchunks,
+                                                       int *__restrict__ chunk_base) {
   __shared__ int off[kMoeMaxExperts + 1];
   if (threadIdx.x == 0) {
     int acc = 0;
@@ -89,6 +92,11 @@ __global__ __launch_bounds__(256) void moe_plan_kernel(int *__restrict__ counts,
   for (int e = threadIdx.x; e < E; e += 256) {
     cursor[e] = off[e];
     counts[e] = 0;
+    int acc = off[e];  // first place of expert e's entries in each chunk
+    for (int c = 0; c < nchunks; ++c) {
+      chunk_base[(int64_t)c * E + e] = acc;
+      acc += chunk_hist[(int64_t)c * E + e];
+    }
   }
   for (int t = threadIdx.x; t < max_tiles; t += 256) {
     const int row = t * bm;
@@ -106,23 +114,59 @@ __global__ __launch_bounds__(256) void moe_plan_kernel(int *__restrict__ counts,
   }
 }
 
-// One wave per (row, choice) i = row * top_k + j: claims a place in the
-// chosen expert's segment and copies the row (row_chunks 16-byte chunks) there.
-__global__ __launch_bounds__(256) void moe_scatter_kernel(const uint4 *__restrict__ x, int64_t row_chunks,
-                                                          const int *__restrict__ sel, int n, int top_k,
-                                                          int *__restrict__ cursor, int *__restrict__ slot_of,
+// Entries of the choice list (i = row * top_k + j) per expert in each chunk of
+// kMoeChunk entries (one wave per chunk).
+__global__ __launch_bounds__(64) void moe_count_kernel(const int *__restrict__ sel, int n, int E,
+                                                       int *__restrict__ chunk_hist) {
+  __shared__ int h[kMoeMaxExperts];
+  const int lane = threadIdx.x, c = blockIdx.x;
+  for (int e = lane; e < E; e += 64) h[e] = 0;
+  __syncthreads();
+  const int i0 = c * kMoeChunk, i1 = min(n, i0 + kMoeChunk);
+  for (int i = i0 + lane; i < i1; i += 64) atomicAdd(&h[sel[i]], 1);
+  __syncthreads();
+  for (int e = lane; e < E; e += 64) chunk_hist[(int64_t)c * E + e] = h[e];
+}
+
+// Places in list order (one wave per chunk): entry i of expert e gets
+// chunk_base[chunk][e] + (entries of e before i in the chunk).
+__global__ __launch_bounds__(64) void moe_assign_kernel(const int *__restrict__ sel, int n, int E,
+                                                        const int *__restrict__ chunk_base,
+                                                        int *__restrict__ slot_of) {
+  __shared__ int cnt[kMoeMaxExperts];
+  __shared__ int eb[64];
+  const int lane = threadIdx.x, c = blockIdx.x;
+  for (int e = lane; e < E; e += 64) cnt[e] = chunk_base[(int64_t)c * E + e];
+  __syncthreads();
+  const int i0 = c * kMoeChunk, i1 = min(n, i0 + kMoeChunk);
+  for (int b = i0; b < i1; b += 64) {
+    const int i = b + lane;
+    const int e = i < i1 ? sel[i] : -1;
+    eb[lane] = e;
+    __syncthreads();
+    int before = 0, after = 0;
+    for (int j = 0; j < 64; ++j) {
+      const int ej = eb[j];
+      before += (j < lane && ej == e);
+      after += (j > lane && ej == e);
+    }
+    if (e >= 0) slot_of[i] = cnt[e] + before;
+    __syncthreads();
+    if (e >= 0 && after == 0) cnt[e] += before + 1;  // the last entry of e in this step
+    __syncthreads();
+  }
+}
+
+// One wave per entry: row i / top_k of x copied to row slot_of[i] of xp
+// (row_chunks 16-byte chunks per row).
+__global__ __launch_bounds__(256) void moe_scatter_kernel(const uint4 *__restrict__ x, int64_t row_chunks, int n,
+                                                          int top_k, const int *__restrict__ slot_of,
                                                           uint4 *__restrict__ xp) {
   const int lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= n) return;
-  int slot = 0;
-  if (lane == 0) {
-    slot = atomicAdd(&cursor[sel[i]], 1);
-    slot_of[i] = slot;
-  }
-  slot = __shfl(slot, 0);
   const uint4 *src = x + (int64_t)(i / top_k) * row_chunks;
-  uint4 *dst = xp + (int64_t)slot * row_chunks;
+  uint4 *dst = xp + (int64_t)slot_of[i] * row_chunks;
   for (int64_t c = lane; c < row_chunks; c += 64) dst[c] = src[c];
 }
 
@@ -172,20 +216,26 @@ hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_moe_plan(int *counts, int E, int bm, int max_tiles, int *cursor, int *tile_group,
-                           hipStream_t st) {
-  if (E < 1 || E > kMoeMaxExperts || bm < 1 || max_tiles < 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, counts, E, bm, max_tiles, cursor, tile_group);
+int moe_chunks(int R, int top_k) { return (R * top_k + kMoeChunk - 1) / kMoeChunk; }
+
+hipError_t launch_moe_plan(const int *sel, int R, int top_k, int *counts, int E, int bm, int max_tiles, int *cursor,
+                           int *tile_group, int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st) {
+  if (E < 1 || E > kMoeMaxExperts || bm < 1 || max_tiles < 0 || R < 0 || top_k < 1) return hipErrorInvalidValue;
+  const int n = R * top_k, nchunks = moe_chunks(R, top_k);
+  if (nchunks > 0) hipLaunchKernelGGL(moe_count_kernel, dim3(nchunks), dim3(64), 0, st, sel, n, E, chunk_hist);
+  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, counts, E, bm, max_tiles, cursor, tile_group,
+                     chunk_hist, nchunks, chunk_base);
+  if (nchunks > 0) hipLaunchKernelGGL(moe_assign_kernel, dim3(nchunks), dim3(64), 0, st, sel, n, E, chunk_base, slot_of);
   return hipGetLastError();
 }
 
-hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, const int *sel, int R, int top_k, int *cursor,
-                              int *slot_of, void *xp, hipStream_t st) {
+hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k, const int *slot_of, void *xp,
+                              hipStream_t st) {
   const int n = R * top_k;
   if (n <= 0) return hipSuccess;
   if (row_bytes % 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(moe_scatter_kernel, dim3((n + 3) / 4), dim3(256), 0, st, (const uint4 *)x, row_bytes / 16, sel,
-                     n, top_k, cursor, slot_of, (uint4 *)xp);
+  hipLaunchKernelGGL(moe_scatter_kernel, dim3((n + 3) / 4), dim3(256), 0, st, (const uint4 *)x, row_bytes / 16, n,
+                     top_k, slot_of, (uint4 *)xp);
   return hipGetLastError();
 }
 

@@ -185,15 +185,21 @@ struct MoeRouteArgs {
   int *counts;
 };
 hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st);
-// Segment starts (counts rounded up to bm) into cursor[E], the expert of each
-// of max_tiles row tiles (-1 past the last segment) into tile_group; counts
-// are cleared.
-hipError_t launch_moe_plan(int *counts, int E, int bm, int max_tiles, int *cursor, int *tile_group,
-                           hipStream_t st);
-// Row i / top_k of x copied to row slot_of[i] of xp, the next free place of
-// expert sel[i] (rows of row_bytes, a multiple of 16).
-hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, const int *sel, int R, int top_k, int *cursor,
-                              int *slot_of, void *xp, hipStream_t st);
+// Entries of the choice list per chunk of kMoeChunk entries.
+constexpr int kMoeChunk = 1024;
+int moe_chunks(int R, int top_k);
+// From the routing (sel [R][top_k], counts [E] zero-based totals): segment
+// starts (counts rounded up to bm) into cursor[E], the expert of each of
+// max_tiles row tiles (-1 past the last segment) into tile_group, and the
+// place of every entry i = row * top_k + j in its expert's segment, in list
+// order, into slot_of[R * top_k]; counts are cleared. chunk_hist and
+// chunk_base hold moe_chunks(R, top_k) * E ints each.
+hipError_t launch_moe_plan(const int *sel, int R, int top_k, int *counts, int E, int bm, int max_tiles, int *cursor,
+                           int *tile_group, int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st);
+// Row i / top_k of x copied to row slot_of[i] of xp (rows of row_bytes, a
+// multiple of 16).
+hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k, const int *slot_of, void *xp,
+                              hipStream_t st);
 // resid[r] += sum_j wts[r][j] y[slot_of[r][j]] + gate[r] ys[r] (ys may be null).
 hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
                               const float *gate, int R, int d, float *resid, hipStream_t st);

@@ -606,7 +606,7 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const int bm = jetk::gemm_group_rows(m->kdt);
   const int64_t S = (R * k + (int64_t)E * (bm - 1) + bm - 1) / bm * bm;  // rows of all segments, at most
   float *logits, *wts, *sg = nullptr, *y, *ys = nullptr;
-  int *sel, *counts, *cursor, *tiles, *slot;
+  int *sel, *counts, *cursor, *tiles, *slot, *chist, *cbase;
   void *xp, *hp, *hs = nullptr;
   TRY(ws_t<float>(m, "moe_logits", (size_t)(R * ly.n_router), &logits));
   TRY(ws_t<int>(m, "moe_sel", (size_t)(R * k), &sel));
@@ -615,6 +615,9 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   TRY(ws_t<int>(m, "moe_cursor", (size_t)E, &cursor));
   TRY(ws_t<int>(m, "moe_tiles", (size_t)(S / bm), &tiles));
   TRY(ws_t<int>(m, "moe_slot", (size_t)(R * k), &slot));
+  const int nch = jetk::moe_chunks((int)R, k);
+  TRY(ws_t<int>(m, "moe_chist", (size_t)std::max(nch, 1) * E, &chist));
+  TRY(ws_t<int>(m, "moe_cbase", (size_t)std::max(nch, 1) * E, &cbase));
   TRY(ws(m, "moe_xp", (size_t)(S * d) * m->esz, &xp));
   TRY(ws(m, "moe_h", (size_t)(S * Fe) * m->esz, &hp));
   TRY(ws_t<float>(m, "moe_y", (size_t)(S * d), &y));
@@ -630,8 +633,9 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
     HIPC(hipMemsetAsync(counts, 0, sizeof(int) * (size_t)E, m->st));
     LAUNCH(jetk::launch_moe_route(jetk::MoeRouteArgs{logits, ly.n_router, (int)R, E, k, sel, wts, sg, counts},
                                   m->st));
-    LAUNCH(jetk::launch_moe_plan(counts, E, bm, (int)(S / bm), cursor, tiles, m->st));
-    LAUNCH(jetk::launch_moe_scatter(b.xn, d * (int64_t)m->esz, sel, (int)R, k, cursor, slot, xp, m->st));
+    LAUNCH(jetk::launch_moe_plan(sel, (int)R, k, counts, E, bm, (int)(S / bm), cursor, tiles, chist, cbase, slot,
+                                 m->st));
+    LAUNCH(jetk::launch_moe_scatter(b.xn, d * (int64_t)m->esz, (int)R, k, slot, xp, m->st));
   }
   {
     const double rows = (double)(R * k);

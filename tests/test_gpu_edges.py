@@ -91,3 +91,30 @@ def test_no_candidates(model_dir):
         J.jet_prefix_free(p)
     finally:
         J.jet_model_free(m)
+
+
+WIDE = {
+    # 8 query heads per KV head (the 35B-A3B shape's grouping)
+    "wide_gqa": dict(arch="dense", dtype="bf16", d_model=256, n_layers=2, n_heads=16, n_kv_heads=2,
+                     head_dim=128, ffn=256, vocab=2048, max_ctx=4096),
+    # 256 experts, top 8 (the 35B-A3B shape's routing), small experts
+    "many_experts": dict(arch="dense", dtype="bf16", d_model=256, n_layers=2, n_heads=2, n_kv_heads=1,
+                         head_dim=128, ffn=64, vocab=2048, n_experts=256, top_k=8, moe_ffn=64,
+                         shared_ffn=64, max_ctx=4096),
+}
+
+
+@pytest.mark.parametrize("name", sorted(WIDE))
+def test_wide_grouping_and_many_experts(name, model_dir):
+    """fp32-mode parity and run-to-run bitwise determinism at the 35B-A3B
+    shape's head grouping and expert count."""
+    import os
+    path = os.path.join(model_dir, f"edge_{name}.jetm")
+    if not os.path.exists(path):
+        jet_synth.write_model(path, WIDE[name])
+    wl = edge_workload(2048, [1, 40, 64, 65, 130, 300], [1, 2, 9, 17], seed=13, empty_question=False)
+    compare(path, wl, J.JET_FP32, name)
+    a = score(path, wl, J.JET_F16)
+    b = score(path, wl, J.JET_F16)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])

@@ -146,23 +146,49 @@ def test_hybrid_4b_k4_full(dtype):
 # The fp64 oracle of a 35B-shape question reads every expert of every layer
 # (minutes on the host).
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("dtype", [pytest.param(J.JET_F16, id="f16")])
-def test_moe_35b_a3b_k4_full(dtype):
+def test_moe_35b_a3b_k4_full():
     """35B-A3B-shape mixture-of-experts hybrid (30 delta-rule + 10 attention
-    layers, 256 experts, top 8, shared expert): all 128 questions on the GPU,
-    the shortest-prefix question checked against the oracle."""
+    layers, 256 experts, top 8, shared expert): all 128 questions on the GPU
+    in the fp16 mode (properties, bitwise the same on a second run), and the
+    shortest-prefix question in the fp32 mode against the oracle.
+
+    Routing is a discrete choice among router logits that lie close together
+    (about 0.05 apart between the 8th and 9th of 256 at this initialisation):
+    a rounding difference that reorders two of them swaps an expert, which
+    moves the row's output by a finite step. At 40 layers x ~200 rows per
+    sequence the fp16 mode's activation rounding does this many times per
+    sequence, so its error against the fp64 oracle is logged, not bounded;
+    the fp32 mode does it rarely, and is held to the 16-bit tolerance. The
+    same head grouping and expert count are held to the fp32 tolerance at
+    small size (test_gpu_edges.py)."""
     path = jet_synth.ensure_model("moe_35b_a3b")
     wl = jet_synth.make_workload("moe_35b_a3b_k4")
-    log(f"[fullsize] moe_35b_a3b_k4 dtype {dtype}: {wl.n_questions} questions, "
-        f"{int(wl.prefix_offsets[-1])} prefix tokens")
-    m = J.jet_model_load(path, dtype=dtype)
+    log(f"[fullsize] moe_35b_a3b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+    m = J.jet_model_load(path, dtype=J.JET_F16)
     try:
         tok, sums = run(m, wl)
+        tok2, sums2 = run(m, wl)
     finally:
         J.jet_model_free(m)
+    np.testing.assert_array_equal(tok, tok2)
+    np.testing.assert_array_equal(sums, sums2)
     properties(wl, tok, sums)
     q = int(np.argmin(np.diff(wl.prefix_offsets)))
-    sampled_parity(path, "moe_35b_a3b_k4", wl, tok, sums, [q], dtype)
+    ref_tok, ref_sum = oracle_subset(path, "moe_35b_a3b_k4", wl, [q])
+    sub = wl.subset([q])
+    a, b = wl.cand_tok_offsets[wl.q_cand_offsets[q]], wl.cand_tok_offsets[wl.q_cand_offsets[q + 1]]
+    log(f"[fullsize] moe f16 question {q}: max|d tok|={np.abs(tok[a:b] - ref_tok).max():.3e}")
+    m = J.jet_model_load(path, dtype=J.JET_FP32)
+    try:
+        tok32, sums32 = run(m, sub)
+    finally:
+        J.jet_model_free(m)
+    dt = np.abs(tok32 - ref_tok).max()
+    ds = np.abs(sums32 - ref_sum).max()
+    log(f"[fullsize] moe fp32 question {q}: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    from conftest import record_parity
+    record_parity(f"fullsize/moe_35b_a3b_k4/dtype{J.JET_FP32}/q{[q]}", max_tok=dt, max_sum=ds)
+    assert dt <= 2e-2 and ds <= 5e-2
 
 
 # The fp64 oracle of one 27B-shape candidate sequence runs for minutes on the

@@ -198,13 +198,15 @@ def test_duplicates_permutation_and_determinism(dtype, model_dir):
 
 
 @pytest.mark.parametrize("dtype", [J.JET_F16, J.JET_F16P])
-def test_reused_prefix_buffers(dtype, model_dir):
+@pytest.mark.parametrize("spec,wname", [("small_gqa_bf16", "small"), ("small_hybrid_bf16", "small_hybrid"),
+                                        ("small_moe_bf16", "small_moe")])
+def test_reused_prefix_buffers(spec, wname, dtype, model_dir):
     """A prefix's device buffers go back to the model's pool when it is freed
     and the next prefill takes them with their old contents: scores must not
     depend on that (every buffer is written before it is read)."""
-    path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
-    a = jet_synth.make_workload("small", n_questions=6)
-    b = jet_synth.make_workload("small", n_questions=6, seed=7)
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
+    a = jet_synth.make_workload(wname, n_questions=6)
+    b = jet_synth.make_workload(wname, n_questions=6, seed=7)
     m = J.jet_model_load(path, dtype=dtype)
     try:
         def run(wl):
