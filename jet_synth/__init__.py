@@ -34,6 +34,7 @@ from __future__ import annotations
 
 import json
 import os
+import shutil
 import struct
 import zlib
 from concurrent.futures import ThreadPoolExecutor
@@ -255,6 +256,10 @@ def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
                            for t in tensors])
     hjson = json.dumps(header).encode()
     assert len(hjson) <= hdr_room
+    free = shutil.disk_usage(os.path.dirname(os.path.abspath(path))).free
+    if free < off + (1 << 30):
+        # a memory-mapped write past the end of the disk would end the process with SIGBUS
+        raise OSError(f"{path}: {off / 2**30:.1f} GiB needed, {free / 2**30:.1f} GiB free")
     tmp = path + ".tmp"
     with open(tmp, "wb") as f:
         f.truncate(off)

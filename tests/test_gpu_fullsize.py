@@ -3,6 +3,7 @@ that bench.py times (every question on the GPU, in the fp16 mode bench.py
 times and in the pair-bf16 mode), checked against the fp64 oracle on sampled
 questions and through properties that hold at any size.
 """
+import contextlib
 import os
 import sys
 
@@ -47,6 +48,20 @@ def dense_1p5b_models(dense_1p5b_path):
     yield get
     for m in models.values():
         J.jet_model_free(m)
+
+
+@contextlib.contextmanager
+def large_model(spec):
+    """Path of a large model file; a file this test wrote is deleted afterwards
+    (the largest files do not all fit on the disk at once)."""
+    path = os.path.join(jet_synth.model_cache_dir(), f"{spec}_s{jet_synth.MASTER_SEED}.jetm")
+    existed = os.path.exists(path)
+    path = jet_synth.ensure_model(spec)
+    try:
+        yield path
+    finally:
+        if not existed and os.path.exists(path):
+            os.remove(path)
 
 
 def run(model, wl):
@@ -161,7 +176,11 @@ def test_moe_35b_a3b_k4_full():
     the fp32 mode does it rarely, and is held to the 16-bit tolerance. The
     same head grouping and expert count are held to the fp32 tolerance at
     small size (test_gpu_edges.py)."""
-    path = jet_synth.ensure_model("moe_35b_a3b")
+    with large_model("moe_35b_a3b") as path:
+        _moe_35b_a3b_k4_full(path)
+
+
+def _moe_35b_a3b_k4_full(path):
     wl = jet_synth.make_workload("moe_35b_a3b_k4")
     log(f"[fullsize] moe_35b_a3b_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
     m = J.jet_model_load(path, dtype=J.JET_F16)
@@ -191,15 +210,21 @@ def test_moe_35b_a3b_k4_full():
     assert dt <= 2e-2 and ds <= 5e-2
 
 
+@pytest.fixture(scope="module")
+def dense_27b_path():
+    with large_model("dense_27b") as path:
+        yield path
+
+
 # The fp64 oracle of one 27B-shape candidate sequence runs for minutes on the
 # host, longer than a per-test limit meant for GPU calls.
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("dtype", DTYPES_DEEP)
-def test_dense_27b_k10_full(dtype):
+def test_dense_27b_k10_full(dtype, dense_27b_path):
     """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
     GPU; one whole candidate sequence (the shortest question's shortest
     candidate, ~1.1k positions) checked against the oracle, plus properties."""
-    path = jet_synth.ensure_model("dense_27b")
+    path = dense_27b_path
     wl = jet_synth.make_workload("dense_27b_k10")
     log(f"[fullsize] dense_27b_k10 dtype {dtype}: {wl.n_questions} questions, "
         f"{int(wl.prefix_offsets[-1])} prefix tokens")
