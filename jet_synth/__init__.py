@@ -383,6 +383,8 @@ WORKLOADS: dict[str, dict] = {
     "moe_35b_a3b_k4": dict(model="moe_35b_a3b", Q=128, P=(200, 1500), ids="zipf", K=4, m=(1, 24)),
     "small_moe": dict(model="small_moe_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
     "tiny_moe": dict(model="tiny_moe_bf16", Q=8, P=(20, 200), ids="zipf", K=4, m=(1, 12)),
+    # enough prefix rows that the expert segments average over 1024 rows
+    "tiny_moe_long": dict(model="tiny_moe_bf16", Q=16, P=(250, 400), ids="zipf", K=4, m=(1, 12)),
     "micro_moe": dict(model="micro_moe_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
 }
 

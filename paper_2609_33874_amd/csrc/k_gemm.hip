@@ -489,13 +489,17 @@ static hipError_t run_grouped_epi(int epi, const void *A, int64_t lda, const voi
   }
 }
 
-int gemm_group_rows(int dtype) { return dtype == 2 ? HalfS::BM : dtype == 1 ? CfgF::BM : SmallB::BM; }
+int gemm_group_rows(int dtype, int big) {
+  return dtype == 2 ? (big ? HalfB::BM : HalfS::BM) : dtype == 1 ? CfgF::BM : SmallB::BM;
+}
 
-hipError_t launch_gemm_grouped(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
+hipError_t launch_gemm_grouped(int dtype, int big, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
                                int64_t group_stride, const int *tile_group, int M, int N, int K, void *out,
                                int64_t ldo, float oscale, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (!tile_group || M % gemm_group_rows(dtype)) return hipErrorInvalidValue;
+  if (!tile_group || M % gemm_group_rows(dtype, big)) return hipErrorInvalidValue;
+  if (dtype == 2 && big)
+    return run_grouped_epi<HalfB>(epi, A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
   if (dtype == 2)
     return run_grouped_epi<HalfS>(epi, A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
   if (dtype == 1)

@@ -15,8 +15,8 @@
 namespace jetk {
 
 // One wave per row: top_k experts by router logit (lowest index first among
-// equal logits), their weights softmax over the kept logits, the shared
-// expert's gate sigmoid(logit[E]) when present, and per-expert counts.
+// equal logits), their weights softmax over the kept logits, and the shared
+// expert's gate sigmoid(logit[E]) when present.
 __global__ __launch_bounds__(256) void moe_route_kernel(MoeRouteArgs a) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -67,32 +67,35 @@ __global__ __launch_bounds__(256) void moe_route_kernel(MoeRouteArgs a) {
   for (int j = 0; j < a.top_k; ++j) {
     a.sel[(int64_t)r * a.top_k + j] = esel[j];
     a.wts[(int64_t)r * a.top_k + j] = __expf(zsel[j] - zsel[0]) * inv;
-    atomicAdd(&a.counts[esel[j]], 1);
   }
   if (a.shared_gate) a.shared_gate[r] = 1.0f / (1.0f + __expf(-z[a.E]));
 }
 
-// One workgroup: segment starts (counts rounded up to bm), the cursors the
-// scatter advances, the expert of every row tile, and the counts cleared for
-// the next layer.
-__global__ __launch_bounds__(256) void moe_plan_kernel(int *__restrict__ counts, int E, int bm, int max_tiles,
-                                                       int *__restrict__ cursor, int *__restrict__ tile_group,
+// One workgroup: per-expert totals from the chunk counts, segment starts
+// (totals rounded up to bm), the first place of each expert's entries in each
+// chunk, and the expert of every row tile.
+__global__ __launch_bounds__(256) void moe_plan_kernel(int E, int bm, int max_tiles, int *__restrict__ tile_group,
                                                        const int *__restrict__ chunk_hist, int nchunks,
                                                        int *__restrict__ chunk_base) {
   __shared__ int off[kMoeMaxExperts + 1];
+  for (int e = threadIdx.x; e < E; e += 256) {
+    int t = 0;
+    for (int c = 0; c < nchunks; ++c) t += chunk_hist[(int64_t)c * E + e];
+    off[e] = t;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
     int acc = 0;
     for (int e = 0; e < E; ++e) {
+      const int t = off[e];
       off[e] = acc;
-      acc += (counts[e] + bm - 1) / bm * bm;
+      acc += (t + bm - 1) / bm * bm;
     }
     off[E] = acc;
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += 256) {
-    cursor[e] = off[e];
-    counts[e] = 0;
-    int acc = off[e];  // first place of expert e's entries in each chunk
+    int acc = off[e];
     for (int c = 0; c < nchunks; ++c) {
       chunk_base[(int64_t)c * E + e] = acc;
       acc += chunk_hist[(int64_t)c * E + e];
@@ -218,13 +221,13 @@ hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st) {
 
 int moe_chunks(int R, int top_k) { return (R * top_k + kMoeChunk - 1) / kMoeChunk; }
 
-hipError_t launch_moe_plan(const int *sel, int R, int top_k, int *counts, int E, int bm, int max_tiles, int *cursor,
-                           int *tile_group, int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st) {
+hipError_t launch_moe_plan(const int *sel, int R, int top_k, int E, int bm, int max_tiles, int *tile_group,
+                           int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st) {
   if (E < 1 || E > kMoeMaxExperts || bm < 1 || max_tiles < 0 || R < 0 || top_k < 1) return hipErrorInvalidValue;
   const int n = R * top_k, nchunks = moe_chunks(R, top_k);
   if (nchunks > 0) hipLaunchKernelGGL(moe_count_kernel, dim3(nchunks), dim3(64), 0, st, sel, n, E, chunk_hist);
-  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, counts, E, bm, max_tiles, cursor, tile_group,
-                     chunk_hist, nchunks, chunk_base);
+  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, E, bm, max_tiles, tile_group, chunk_hist, nchunks,
+                     chunk_base);
   if (nchunks > 0) hipLaunchKernelGGL(moe_assign_kernel, dim3(nchunks), dim3(64), 0, st, sel, n, E, chunk_base, slot_of);
   return hipGetLastError();
 }

@@ -174,7 +174,7 @@ constexpr int kMoeMaxTopK = 16;
 // Router logits [R][ldl] fp32 (E expert columns, then the shared expert's gate
 // logit at column E when shared_gate is set) -> sel/wts [R][top_k] (experts by
 // logit, lowest index first among equals; softmax over the kept logits),
-// shared_gate[R] = sigmoid(logit E); counts[E] (zero on entry) += selections.
+// shared_gate[R] = sigmoid(logit E).
 struct MoeRouteArgs {
   const float *logits;
   int64_t ldl;
@@ -182,20 +182,19 @@ struct MoeRouteArgs {
   int *sel;
   float *wts;
   float *shared_gate;
-  int *counts;
 };
 hipError_t launch_moe_route(const MoeRouteArgs &a, hipStream_t st);
 // Entries of the choice list per chunk of kMoeChunk entries.
 constexpr int kMoeChunk = 1024;
 int moe_chunks(int R, int top_k);
-// From the routing (sel [R][top_k], counts [E] zero-based totals): segment
-// starts (counts rounded up to bm) into cursor[E], the expert of each of
-// max_tiles row tiles (-1 past the last segment) into tile_group, and the
-// place of every entry i = row * top_k + j in its expert's segment, in list
-// order, into slot_of[R * top_k]; counts are cleared. chunk_hist and
-// chunk_base hold moe_chunks(R, top_k) * E ints each.
-hipError_t launch_moe_plan(const int *sel, int R, int top_k, int *counts, int E, int bm, int max_tiles, int *cursor,
-                           int *tile_group, int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st);
+// From the routing (sel [R][top_k]): segment starts (per-expert totals
+// rounded up to bm), the expert of each of max_tiles row tiles (-1 past the
+// last segment) into tile_group, and the place of every entry
+// i = row * top_k + j in its expert's segment, in list order, into
+// slot_of[R * top_k]. chunk_hist and chunk_base hold moe_chunks(R, top_k) * E
+// ints each.
+hipError_t launch_moe_plan(const int *sel, int R, int top_k, int E, int bm, int max_tiles, int *tile_group,
+                           int *chunk_hist, int *chunk_base, int *slot_of, hipStream_t st);
 // Row i / top_k of x copied to row slot_of[i] of xp (rows of row_bytes, a
 // multiple of 16).
 hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k, const int *slot_of, void *xp,
@@ -203,11 +202,12 @@ hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k
 // resid[r] += sum_j wts[r][j] y[slot_of[r][j]] + gate[r] ys[r] (ys may be null).
 hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
                               const float *gate, int R, int d, float *resid, hipStream_t st);
-// Grouped GEMM: row tile t of A (tiles of gemm_group_rows(dtype) rows) is
+// Grouped GEMM: row tile t of A (tiles of gemm_group_rows(dtype, big) rows) is
 // multiplied by B + tile_group[t] * group_stride (elements); tiles with
 // tile_group -1 are skipped. Otherwise as launch_gemm (no pair operands).
-int gemm_group_rows(int dtype);
-hipError_t launch_gemm_grouped(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
+// big (fp16 only): 256-row tiles, for segments of many rows.
+int gemm_group_rows(int dtype, int big);
+hipError_t launch_gemm_grouped(int dtype, int big, int epi, const void *A, int64_t lda, const void *B, int64_t ldb,
                                int64_t group_stride, const int *tile_group, int M, int N, int K, void *out,
                                int64_t ldo, float oscale, hipStream_t st);
 

@@ -603,16 +603,17 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
   const int E = (int)h.n_experts, k = (int)h.top_k;
   const int64_t Fe = h.moe_ffn, Fs = h.shared_ffn, d = h.d;
-  const int bm = jetk::gemm_group_rows(m->kdt);
+  // 256-row tiles when the segments average 1024 rows or more (padding costs
+  // at most an eighth), else 128
+  const int big = m->kdt == 2 && R * k >= 1024 * (int64_t)E;
+  const int bm = jetk::gemm_group_rows(m->kdt, big);
   const int64_t S = (R * k + (int64_t)E * (bm - 1) + bm - 1) / bm * bm;  // rows of all segments, at most
   float *logits, *wts, *sg = nullptr, *y, *ys = nullptr;
-  int *sel, *counts, *cursor, *tiles, *slot, *chist, *cbase;
+  int *sel, *tiles, *slot, *chist, *cbase;
   void *xp, *hp, *hs = nullptr;
   TRY(ws_t<float>(m, "moe_logits", (size_t)(R * ly.n_router), &logits));
   TRY(ws_t<int>(m, "moe_sel", (size_t)(R * k), &sel));
   TRY(ws_t<float>(m, "moe_wts", (size_t)(R * k), &wts));
-  TRY(ws_t<int>(m, "moe_counts", (size_t)E, &counts));
-  TRY(ws_t<int>(m, "moe_cursor", (size_t)E, &cursor));
   TRY(ws_t<int>(m, "moe_tiles", (size_t)(S / bm), &tiles));
   TRY(ws_t<int>(m, "moe_slot", (size_t)(R * k), &slot));
   const int nch = jetk::moe_chunks((int)R, k);
@@ -630,25 +631,22 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
                ly.n_router, ly.is_router));
   {
     KTimer t(m, JET_K_OTHER, 0, (double)(R * ly.n_router) * 4.0);
-    HIPC(hipMemsetAsync(counts, 0, sizeof(int) * (size_t)E, m->st));
-    LAUNCH(jetk::launch_moe_route(jetk::MoeRouteArgs{logits, ly.n_router, (int)R, E, k, sel, wts, sg, counts},
-                                  m->st));
-    LAUNCH(jetk::launch_moe_plan(sel, (int)R, k, counts, E, bm, (int)(S / bm), cursor, tiles, chist, cbase, slot,
-                                 m->st));
+    LAUNCH(jetk::launch_moe_route(jetk::MoeRouteArgs{logits, ly.n_router, (int)R, E, k, sel, wts, sg}, m->st));
+    LAUNCH(jetk::launch_moe_plan(sel, (int)R, k, E, bm, (int)(S / bm), tiles, chist, cbase, slot, m->st));
     LAUNCH(jetk::launch_moe_scatter(b.xn, d * (int64_t)m->esz, (int)R, k, slot, xp, m->st));
   }
   {
     const double rows = (double)(R * k);
     KTimer t(m, JET_K_GEMM_GATEUP, 2.0 * rows * (double)(2 * Fe) * (double)d,
              (rows * (double)d + rows * (double)Fe) * (double)m->esz);
-    LAUNCH(jetk::launch_gemm_grouped(m->kdt, jetk::EPI_SWIGLU, xp, d, ly.w_egu, d, 2 * Fe * d, tiles, (int)S,
+    LAUNCH(jetk::launch_gemm_grouped(m->kdt, big, jetk::EPI_SWIGLU, xp, d, ly.w_egu, d, 2 * Fe * d, tiles, (int)S,
                                      (int)(2 * Fe), (int)d, hp, Fe, ly.is_egu, m->st));
   }
   {
     const double rows = (double)(R * k);
     KTimer t(m, JET_K_GEMM_DOWN, 2.0 * rows * (double)d * (double)Fe,
              rows * (double)Fe * (double)m->esz + rows * (double)d * 4.0);
-    LAUNCH(jetk::launch_gemm_grouped(m->kdt, jetk::EPI_STORE_F32, hp, Fe, ly.w_edown, Fe, d * Fe, tiles, (int)S,
+    LAUNCH(jetk::launch_gemm_grouped(m->kdt, big, jetk::EPI_STORE_F32, hp, Fe, ly.w_edown, Fe, d * Fe, tiles, (int)S,
                                      (int)d, (int)Fe, y, d, ly.is_edown, m->st));
   }
   if (Fs) {

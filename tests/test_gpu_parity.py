@@ -114,6 +114,7 @@ CASES = [
     ("small_moe_bf16", "small_moe", J.JET_F16P),
     ("tiny_moe_bf16", "tiny_moe", J.JET_BF16_SINGLE),
     ("tiny_moe_bf16", "tiny_moe", J.JET_F16),
+    ("tiny_moe_bf16", "tiny_moe_long", J.JET_F16),   # 256-row expert tiles in the prefill
 ]
 
 
