@@ -485,6 +485,8 @@ static hipError_t run_grouped_epi(int epi, const void *A, int64_t lda, const voi
       return run_gemm_grouped<C, 1>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
     case EPI_SWIGLU:
       return run_gemm_grouped<C, 2>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
+    case EPI_STORE_T:
+      return run_gemm_grouped<C, 3>(A, lda, B, ldb, group_stride, tile_group, M, N, K, out, ldo, oscale, st);
     default: return hipErrorInvalidValue;
   }
 }

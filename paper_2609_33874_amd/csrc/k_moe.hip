@@ -174,8 +174,10 @@ __global__ __launch_bounds__(256) void moe_scatter_kernel(const uint4 *__restric
 }
 
 // One workgroup per row: resid += sum_j w_j y[slot_j] (j in top-k order)
-// + g * y_shared, the mixture summed first, in fp32.
-__global__ __launch_bounds__(256) void moe_combine_kernel(const float *__restrict__ y, const int *__restrict__ slot_of,
+// + g * y_shared, the mixture summed first, in fp32 (expert outputs y are
+// stored in the compute type).
+template <typename T>
+__global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ y, const int *__restrict__ slot_of,
                                                           const float *__restrict__ wts, int top_k,
                                                           const float *__restrict__ ys,
                                                           const float *__restrict__ gate, int d,
@@ -184,29 +186,27 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const float *__restric
   const int *sl = slot_of + (int64_t)r * top_k;
   const float *w = wts + (int64_t)r * top_k;
   for (int c = threadIdx.x * 4; c < d; c += 1024) {
-    float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int j = 0; j < top_k; ++j) {
-      const float4 v = *(const float4 *)(y + (int64_t)sl[j] * d + c);
+      const T *v = y + (int64_t)sl[j] * d + c;
       const float wj = w[j];
-      o.x += wj * v.x;
-      o.y += wj * v.y;
-      o.z += wj * v.z;
-      o.w += wj * v.w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] += wj * to_f<T>(v[q]);
     }
     if (ys) {
       const float g = gate[r];
       const float4 v = *(const float4 *)(ys + (int64_t)r * d + c);
-      o.x += g * v.x;
-      o.y += g * v.y;
-      o.z += g * v.z;
-      o.w += g * v.w;
+      o[0] += g * v.x;
+      o[1] += g * v.y;
+      o[2] += g * v.z;
+      o[3] += g * v.w;
     }
     float4 *dst = (float4 *)(resid + (int64_t)r * d + c);
     float4 x = *dst;
-    x.x += o.x;
-    x.y += o.y;
-    x.z += o.z;
-    x.w += o.w;
+    x.x += o[0];
+    x.y += o[1];
+    x.z += o[2];
+    x.w += o[3];
     *dst = x;
   }
 }
@@ -242,11 +242,19 @@ hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k
   return hipGetLastError();
 }
 
-hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
-                              const float *gate, int R, int d, float *resid, hipStream_t st) {
+hipError_t launch_moe_combine(int dtype, const void *y, const int *slot_of, const float *wts, int top_k,
+                              const float *ys, const float *gate, int R, int d, float *resid, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if (d % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(moe_combine_kernel, dim3(R), dim3(256), 0, st, y, slot_of, wts, top_k, ys, gate, d, resid);
+  if (dtype == 2)
+    hipLaunchKernelGGL(moe_combine_kernel<f16>, dim3(R), dim3(256), 0, st, (const f16 *)y, slot_of, wts, top_k, ys,
+                       gate, d, resid);
+  else if (dtype == 0)
+    hipLaunchKernelGGL(moe_combine_kernel<bf16>, dim3(R), dim3(256), 0, st, (const bf16 *)y, slot_of, wts, top_k, ys,
+                       gate, d, resid);
+  else
+    hipLaunchKernelGGL(moe_combine_kernel<float>, dim3(R), dim3(256), 0, st, (const float *)y, slot_of, wts, top_k,
+                       ys, gate, d, resid);
   return hipGetLastError();
 }
 

@@ -199,9 +199,10 @@ hipError_t launch_moe_plan(const int *sel, int R, int top_k, int E, int bm, int 
 // multiple of 16).
 hipError_t launch_moe_scatter(const void *x, int64_t row_bytes, int R, int top_k, const int *slot_of, void *xp,
                               hipStream_t st);
-// resid[r] += sum_j wts[r][j] y[slot_of[r][j]] + gate[r] ys[r] (ys may be null).
-hipError_t launch_moe_combine(const float *y, const int *slot_of, const float *wts, int top_k, const float *ys,
-                              const float *gate, int R, int d, float *resid, hipStream_t st);
+// resid[r] += sum_j wts[r][j] y[slot_of[r][j]] + gate[r] ys[r] (ys fp32, may be
+// null); y in the compute type of dtype.
+hipError_t launch_moe_combine(int dtype, const void *y, const int *slot_of, const float *wts, int top_k,
+                              const float *ys, const float *gate, int R, int d, float *resid, hipStream_t st);
 // Grouped GEMM: row tile t of A (tiles of gemm_group_rows(dtype, big) rows) is
 // multiplied by B + tile_group[t] * group_stride (elements); tiles with
 // tile_group -1 are skipped. Otherwise as launch_gemm (no pair operands).

@@ -608,9 +608,9 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const int big = m->kdt == 2 && R * k >= 1024 * (int64_t)E;
   const int bm = jetk::gemm_group_rows(m->kdt, big);
   const int64_t S = (R * k + (int64_t)E * (bm - 1) + bm - 1) / bm * bm;  // rows of all segments, at most
-  float *logits, *wts, *sg = nullptr, *y, *ys = nullptr;
+  float *logits, *wts, *sg = nullptr, *ys = nullptr;
   int *sel, *tiles, *slot, *chist, *cbase;
-  void *xp, *hp, *hs = nullptr;
+  void *xp, *hp, *y, *hs = nullptr;
   TRY(ws_t<float>(m, "moe_logits", (size_t)(R * ly.n_router), &logits));
   TRY(ws_t<int>(m, "moe_sel", (size_t)(R * k), &sel));
   TRY(ws_t<float>(m, "moe_wts", (size_t)(R * k), &wts));
@@ -621,7 +621,7 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   TRY(ws_t<int>(m, "moe_cbase", (size_t)std::max(nch, 1) * E, &cbase));
   TRY(ws(m, "moe_xp", (size_t)(S * d) * m->esz, &xp));
   TRY(ws(m, "moe_h", (size_t)(S * Fe) * m->esz, &hp));
-  TRY(ws_t<float>(m, "moe_y", (size_t)(S * d), &y));
+  TRY(ws(m, "moe_y", (size_t)(S * d) * m->esz, &y));  // expert outputs in the compute type
   if (Fs) {
     TRY(ws_t<float>(m, "moe_sg", (size_t)R, &sg));
     TRY(ws(m, "moe_hs", (size_t)(R * Fs) * m->esz, &hs));
@@ -645,8 +645,8 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   {
     const double rows = (double)(R * k);
     KTimer t(m, JET_K_GEMM_DOWN, 2.0 * rows * (double)d * (double)Fe,
-             rows * (double)Fe * (double)m->esz + rows * (double)d * 4.0);
-    LAUNCH(jetk::launch_gemm_grouped(m->kdt, big, jetk::EPI_STORE_F32, hp, Fe, ly.w_edown, Fe, d * Fe, tiles, (int)S,
+             rows * (double)Fe * (double)m->esz + rows * (double)d * (double)m->esz);
+    LAUNCH(jetk::launch_gemm_grouped(m->kdt, big, jetk::EPI_STORE_T, hp, Fe, ly.w_edown, Fe, d * Fe, tiles, (int)S,
                                      (int)d, (int)Fe, y, d, ly.is_edown, m->st));
   }
   if (Fs) {
@@ -654,8 +654,8 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
     TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_STORE_F32, hs, Fs, 0, ly.w_sdown, Fs, R, d, Fs, ys, d, ly.is_sdown));
   }
   {
-    KTimer t(m, JET_K_OTHER, 0, (double)(R * (k + 2) * d) * 4.0);
-    LAUNCH(jetk::launch_moe_combine(y, slot, wts, k, ys, sg, (int)R, (int)d, b.resid, m->st));
+    KTimer t(m, JET_K_OTHER, 0, (double)(R * d) * ((double)k * (double)m->esz + 12.0));
+    LAUNCH(jetk::launch_moe_combine(m->kdt, y, slot, wts, k, ys, sg, (int)R, (int)d, b.resid, m->st));
   }
   return Status::ok();
 }
