@@ -505,11 +505,11 @@ def test_prefix_sharing_equals_unshared(which, pin_dense_path, pin_hybrid_path, 
     np.testing.assert_allclose(sa, sb, atol=1e-10, rtol=0)
 
 
-@pytest.mark.parametrize("which", ["dense", "hybrid"])
-def test_isolation_and_planted_leak(which, pin_dense_path, pin_hybrid_path):
+@pytest.mark.parametrize("which", ["dense", "hybrid", "moe"])
+def test_isolation_and_planted_leak(which, pin_dense_path, pin_hybrid_path, pin_moe_path):
     """Scoring a candidate after its siblings equals scoring it alone; the
     planted leak (state not restored between candidates) is detected."""
-    path = pin_dense_path if which == "dense" else pin_hybrid_path
+    path = {"dense": pin_dense_path, "hybrid": pin_hybrid_path, "moe": pin_moe_path}[which]
     V = jet_synth.read_header(path)["vocab"]
     wl = jet_synth.make_workload("micro_hybrid", vocab=V, Q=2, P=(6, 12), K=4, m=(2, 6))
     full, _ = oracle.score_incremental(path, wl)
