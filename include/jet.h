@@ -122,11 +122,16 @@ typedef struct {
 
 /*
  * jet_model_load - read a model file and upload its weights.
- *   model_path: host string, path of a model file (JSON header + raw tensors).
+ *   model_path: host string, path of a model file (JSON header + raw tensors):
+ *     a dense or hybrid (gated delta-rule + attention) decoder whose FFNs are
+ *     either SwiGLU or mixtures of experts (routed top-k experts plus an
+ *     optional gated shared expert; Section 4.2 names routed experts).
  *   opts: host, may be NULL (defaults: JET_BF16, device 0, no limits, null stream).
  *   out: host, receives the model handle.
  * Errors: JET_E_IO (file), JET_E_INVALID (unsupported shape or dtype
- *   combination: an f32 file cannot be run in a bf16 mode), JET_E_OOM, JET_E_DEVICE.
+ *   combination: an f32 file cannot be run in a bf16 mode; mixture-of-experts
+ *   models run in the JET_FP32, JET_F16, JET_F16P and JET_BF16_SINGLE modes,
+ *   not JET_BF16), JET_E_OOM, JET_E_DEVICE.
  */
 int jet_model_load(const char *model_path, const jet_load_opts *opts, jet_model **out);
 
