@@ -193,3 +193,18 @@ def test_model_load_reports_io_errors(tmp_path):
     with pytest.raises(J.JetError) as e:
         J.jet_model_load(str(bad))
     assert e.value.code in (J.JET_E_IO, J.JET_E_DEVICE)
+
+
+def test_moe_model_shapes():
+    """The 35B-A3B-shape mixture-of-experts model: 33.7B parameters, 2.5B of
+    them used per token (8 of 256 experts), every FFN a router, 256 experts
+    and a gated shared expert; the small MoE models round-trip their header."""
+    s = jet_synth.full_spec("moe_35b_a3b")
+    total = jet_synth.n_params("moe_35b_a3b")
+    E, k, Fe, d, L = s["n_experts"], s["top_k"], s["moe_ffn"], s["d_model"], s["n_layers"]
+    active = total - L * (E - k) * 3 * Fe * d
+    assert round(total / 1e9, 1) == 33.7 and round(active / 1e9, 1) == 2.5
+    names = {t[0]: t[2] for t in jet_synth.tensor_list("moe_35b_a3b")}
+    assert names["blk.0.moe_gate"] == (256, 512, 2048) and names["blk.0.moe_down"] == (256, 2048, 512)
+    assert names["blk.39.shared_router"] == (1, 2048) and "blk.0.w_gate" not in names
+    assert s["layer_types"] == ["gdn", "gdn", "gdn", "attn"] * 10
