@@ -424,3 +424,36 @@ def make_workload(name: str, seed: int = MASTER_SEED, n_questions: int | None = 
         ml = g_mlen.integers(r["m"][0], r["m"][1] + 1, size=r["K"])
         cands.append([g_cid.integers(0, V, size=int(m)).astype(np.int32) for m in ml])
     return from_lists(prefixes, cands)
+
+
+# --------------------------------------------------------------------------
+# digests (to tie stored expected values to the exact inputs they came from)
+# --------------------------------------------------------------------------
+
+def tensor_digests(path: str, threads: int | None = None) -> dict[str, str]:
+    """sha256 of every tensor's stored bytes, by tensor name."""
+    import hashlib
+    h = read_header(path)
+    mm = np.memmap(path, dtype=np.uint8, mode="r")
+
+    def one(t):
+        d = hashlib.sha256()
+        a, n = t["offset"], t["nbytes"]
+        for o in range(a, a + n, 1 << 26):   # hashlib releases the GIL on large buffers
+            d.update(memoryview(mm[o:min(o + (1 << 26), a + n)]))
+        return t["name"], d.hexdigest()
+
+    nthr = threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(nthr) as ex:
+        return dict(ex.map(one, h["tensors"]))
+
+
+def workload_digest(wl: Workload) -> str:
+    """sha256 over the five CSR arrays of a workload (fixed dtypes, in order)."""
+    import hashlib
+    d = hashlib.sha256()
+    for a, dt in ((wl.prefix_offsets, np.int64), (wl.prefix_tokens, np.int32),
+                  (wl.q_cand_offsets, np.int64), (wl.cand_tok_offsets, np.int64),
+                  (wl.cand_tokens, np.int32)):
+        d.update(np.ascontiguousarray(a, dtype=dt).tobytes())
+    return d.hexdigest()

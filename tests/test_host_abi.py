@@ -54,6 +54,30 @@ def test_decide_matches_oracle_rules():
         assert v[i] == pytest.approx(oracle.decide_ordinal(s[qo[i]:qo[i + 1]].astype(np.float64)), abs=1e-13)
 
 
+def test_decide_ordinal_hand_values():
+    """jet_decide's ordinal rule against hand values (Section 3.3: zero-based
+    levels in supplied order), independent of the oracle."""
+    # K equal scores: (K - 1) / 2 ; one level 60 nats ahead: its index
+    cases = [(np.full(5, -3.5), 2.0), (np.full(10, 0.0), 4.5), (np.full(2, -1.0), 0.5)]
+    for K, j in ((5, 0), (5, 3), (7, 6)):
+        s = np.full(K, -80.0)
+        s[j] = -20.0
+        cases.append((s, float(j)))
+    # q = (1/2, 1/3, 1/6) -> 2/3 ; the worked example as two levels -> 0.25
+    cases.append((np.log([3.0, 2.0, 1.0]), 2.0 / 3.0))
+    cases.append((np.log([0.06, 0.02]), 0.25))
+    qo = np.concatenate([[0], np.cumsum([len(c[0]) for c in cases])]).astype(np.int64)
+    s = np.concatenate([c[0] for c in cases]).astype(np.float32)
+    _, _, v = J.jet_decide(J.JET_ORDINAL, qo, s)
+    # float32 inputs move q by ~1e-7 relative
+    np.testing.assert_allclose(v, [c[1] for c in cases], rtol=0, atol=1e-6)
+    # two levels: exactly the binary probability of the second
+    _, _, vb = J.jet_decide(J.JET_BINARY, np.array([0, 2, 4], np.int64), np.concatenate([[-3.2, -1.5], [0.0, -9.0]]).astype(np.float32))
+    _, _, vo = J.jet_decide(J.JET_ORDINAL, np.array([0, 2, 4], np.int64),
+                            np.concatenate([[-3.2, -1.5], [0.0, -9.0]]).astype(np.float32))
+    np.testing.assert_allclose(vo, vb, rtol=0, atol=1e-15)
+
+
 def test_decide_rejects_bad_requests():
     with pytest.raises(J.JetError) as e:
         J.jet_decide(J.JET_BINARY, [0, 3], np.zeros(3, np.float32))

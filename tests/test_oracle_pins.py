@@ -101,7 +101,6 @@ def test_decisions_closed_forms():
     assert oracle.decide_binary(s) == pytest.approx(1.0 / (1.0 + math.exp(-(s[1] - s[0]))), abs=1e-15)
     s5 = np.array([-4.0, -2.0, -2.5, -7.0, -3.0])
     q = oracle.normalize(s5)
-    assert oracle.decide_ordinal(s5) == pytest.approx(sum(i * q[i] for i in range(5)), abs=1e-15)
     # equal scores: lowest index wins; duplicates split the mass
     assert oracle.decide_choice(np.array([-1.0, -0.5, -0.5])) == 1
     np.testing.assert_allclose(oracle.normalize(np.array([-2.0, -2.0])), [0.5, 0.5], atol=1e-16)
@@ -109,6 +108,43 @@ def test_decisions_closed_forms():
     np.testing.assert_allclose(oracle.normalize(s5 + 123.0), q, atol=1e-15)
     with pytest.raises(ValueError):
         oracle.decide_binary(s5)
+
+
+def _ordinal_pins(decide_ordinal):
+    """Hand values of the expected zero-based level (Section 3.3, Eq. 5's
+    ordinal rule with levels 0..K-1 in supplied order)."""
+    g = json.load(open(os.path.join(GOLDEN, "worked_example.json")))
+    # worked example as a two-level scale: q = (0.75, 0.25) -> E = 0 * 0.75 + 1 * 0.25
+    assert decide_ordinal(np.log(np.array(g["likelihoods"]))) == pytest.approx(0.25, abs=1e-15)
+    # K equal scores: q uniform, E = (K - 1) / 2
+    for K in (2, 3, 5, 10):
+        assert decide_ordinal(np.full(K, -3.7)) == pytest.approx((K - 1) / 2, abs=1e-13)
+    # one level 60 nats ahead: E is its (zero-based) index to exp(-60)*K^2
+    for K, j in ((5, 0), (5, 3), (7, 6)):
+        s = np.full(K, -80.0)
+        s[j] = -20.0
+        assert decide_ordinal(s) == pytest.approx(j, abs=1e-20 + 1e-24 * K)
+    # two levels: E equals q(level 1), i.e. the binary rule sigma(s1 - s0)
+    for s in ([-3.2, -1.5], [0.0, -9.0], [2.0, 2.0]):
+        assert decide_ordinal(np.array(s)) == pytest.approx(1.0 / (1.0 + math.exp(s[0] - s[1])), abs=1e-15)
+    # three levels with q = (1/2, 1/3, 1/6): E = 1/3 + 2/6 = 2/3
+    assert decide_ordinal(np.log([3.0, 2.0, 1.0])) == pytest.approx(2.0 / 3.0, abs=1e-15)
+
+
+def test_decide_ordinal_hand_values():
+    _ordinal_pins(oracle.decide_ordinal)
+
+
+@pytest.mark.parametrize("mistake", ["one_based", "reversed_levels", "unnormalised"])
+def test_decide_ordinal_pin_detects_planted_mistakes(mistake):
+    def planted(s):
+        q = oracle.normalize(s) if mistake != "unnormalised" else np.exp(np.asarray(s) - np.max(s))
+        K = len(q)
+        lev = {"one_based": np.arange(1, K + 1), "reversed_levels": np.arange(K)[::-1],
+               "unnormalised": np.arange(K)}[mistake]
+        return float(np.sum(lev * q))
+    with pytest.raises(AssertionError):
+        _ordinal_pins(planted)
 
 
 def test_evaluation_closed_forms():
