@@ -23,8 +23,11 @@
  *   produce errors).
  * Ownership: the caller owns every array passed in or out; the library reads
  *   and writes them only during the call and keeps no pointer to them. The
- *   library owns the opaque handles; a jet_prefix borrows its jet_model and
- *   must be freed before it.
+ *   library owns the opaque handles; a jet_prefix borrows its jet_model.
+ *   Free prefixes before their model. If the model is freed first, its
+ *   prefixes' device buffers are freed with it and each such prefix is
+ *   detached: it can no longer be scored against (JET_E_INVALID) and
+ *   jet_prefix_free still releases its handle.
  * Memory kinds: arrays documented as "host" must be host memory. Arrays
  *   documented as "host or device" may be host memory or device memory of
  *   the model's GPU (the kind is queried with hipPointerGetAttributes).
@@ -267,10 +270,18 @@ int jet_candidate_layout(int32_t n_q, const int64_t *prefix_offsets,
 int jet_stats_get(const jet_model *model, jet_stats *out);
 int jet_stats_reset(jet_model *model);
 
-/* Model facts: vocabulary size, layer count, max_ctx, compute dtype. */
+/* Model facts: vocabulary size, layer count, max_ctx, compute dtype, and (fp16
+ * modes) how many weights the load's fp16 conversion rounded: each matrix is
+ * scaled by a power of two so its largest magnitude lies in [2^14, 2^15),
+ * which keeps every bf16 value of magnitude >= 2^-32 times the matrix's
+ * largest exact; smaller values round to fp16's step (0 in other modes).
+ * Every out pointer may be NULL. */
 int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n_layers,
-                   int64_t *max_ctx, int32_t *dtype);
+                   int64_t *max_ctx, int32_t *dtype, int64_t *f16_inexact_weights);
 
+/* Release a prefix (its device buffers go back to the model for the next
+ * prefill) and a model (weights, work buffers, and the buffers of every
+ * prefix of it not yet freed; see Ownership above). NULL is a no-op. */
 void jet_prefix_free(jet_prefix *prefix);
 void jet_model_free(jet_model *model);
 

@@ -208,10 +208,18 @@ __global__ __launch_bounds__(256) void convert_f32_kernel(const float *__restric
     dst[i] = from_f<T>(src[i]);
 }
 
+// bf16 * scale (a power of two: exact in fp32) rounded to fp16; values the
+// rounding changed are counted into *inexact.
 __global__ __launch_bounds__(256) void bf16_to_f16_kernel(const uint16_t *__restrict__ src, int64_t n, float scale,
-                                                           f16 *__restrict__ dst) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
-    dst[i] = (f16)(bf2f(src[i]) * scale);
+                                                           f16 *__restrict__ dst, unsigned long long *inexact) {
+  unsigned long long cnt = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const float v = bf2f(src[i]) * scale;
+    const f16 h = (f16)v;
+    cnt += ((float)h != v);
+    dst[i] = h;
+  }
+  if (cnt) atomicAdd(inexact, cnt);
 }
 
 __global__ __launch_bounds__(256) void bf16_to_f32_kernel(const uint16_t *__restrict__ src, int64_t n,
@@ -363,10 +371,11 @@ hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst,
   return hipGetLastError();
 }
 
-hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst, hipStream_t st) {
+hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst,
+                                      unsigned long long *inexact, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
-  hipLaunchKernelGGL(bf16_to_f16_kernel, dim3(blocks), dim3(256), 0, st, src, n, scale, (f16 *)dst);
+  hipLaunchKernelGGL(bf16_to_f16_kernel, dim3(blocks), dim3(256), 0, st, src, n, scale, (f16 *)dst, inexact);
   return hipGetLastError();
 }
 

@@ -164,7 +164,10 @@ hipError_t launch_convert_f32(int dtype, const float *src, int64_t n, void *dst,
 hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst, hipStream_t st);
 // dst[i] = src[i] * scale as fp16 (bf16 bits in; exact when scale is a power
 // of two that keeps every value inside the fp16 normal range).
-hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst, hipStream_t st);
+// dst = fp16(bf16 src * scale); adds the number of values that did not convert
+// exactly to *inexact (device counter)
+hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst,
+                                      unsigned long long *inexact, hipStream_t st);
 
 
 // ---- mixture-of-experts FFN (k_moe.hip) ----

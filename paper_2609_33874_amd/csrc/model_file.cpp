@@ -113,11 +113,19 @@ struct JParser {
   }
 };
 
+// A whole number in [0, 2^53] (every size and offset in a header is one).
+bool as_count(const JVal &v, int64_t *out) {
+  if (v.kind != JVal::NUM || !(v.num >= 0.0) || v.num > 9007199254740992.0 || v.num != (double)(int64_t)v.num)
+    return false;
+  *out = (int64_t)v.num;
+  return true;
+}
+
+// Absent and not required: true, *out untouched. Present: must be a count.
 bool get_int(const JVal &o, const char *k, int64_t *out, bool required = true) {
   const JVal *v = o.get(k);
-  if (!v || v->kind != JVal::NUM) return !required;
-  *out = (int64_t)v->num;
-  return true;
+  if (!v) return !required;
+  return as_count(*v, out);
 }
 
 }  // namespace
@@ -155,16 +163,19 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
             get_int(root, "head_dim", &h->head_dim) && get_int(root, "ffn", &h->ffn) &&
             get_int(root, "vocab", &h->vocab) && get_int(root, "max_ctx", &h->max_ctx);
   if (!ok) return Status::err(JET_E_IO, path + ": header lacks a model dimension");
-  get_int(root, "gdn_heads", &h->gdn_heads, false);
-  get_int(root, "gdn_dk", &h->gdn_dk, false);
-  get_int(root, "gdn_dv", &h->gdn_dv, false);
-  get_int(root, "conv_kernel", &h->conv_kernel, false);
-  get_int(root, "n_experts", &h->n_experts, false);
-  get_int(root, "top_k", &h->top_k, false);
-  get_int(root, "moe_ffn", &h->moe_ffn, false);
-  get_int(root, "shared_ffn", &h->shared_ffn, false);
-  if (const JVal *v = root.get("rms_eps")) h->rms_eps = v->num;
-  if (const JVal *v = root.get("rope_theta")) h->rope_theta = v->num;
+  ok = get_int(root, "gdn_heads", &h->gdn_heads, false) && get_int(root, "gdn_dk", &h->gdn_dk, false) &&
+       get_int(root, "gdn_dv", &h->gdn_dv, false) && get_int(root, "conv_kernel", &h->conv_kernel, false) &&
+       get_int(root, "n_experts", &h->n_experts, false) && get_int(root, "top_k", &h->top_k, false) &&
+       get_int(root, "moe_ffn", &h->moe_ffn, false) && get_int(root, "shared_ffn", &h->shared_ffn, false);
+  if (!ok) return Status::err(JET_E_IO, path + ": a model dimension is not a non-negative whole number");
+  if (const JVal *v = root.get("rms_eps")) {
+    if (v->kind != JVal::NUM || !(v->num > 0.0)) return Status::err(JET_E_IO, path + ": bad rms_eps");
+    h->rms_eps = v->num;
+  }
+  if (const JVal *v = root.get("rope_theta")) {
+    if (v->kind != JVal::NUM || !(v->num > 0.0)) return Status::err(JET_E_IO, path + ": bad rope_theta");
+    h->rope_theta = v->num;
+  }
   const JVal *lt = root.get("layer_types");
   if (!lt || lt->kind != JVal::ARR || (int64_t)lt->arr.size() != h->n_layers)
     return Status::err(JET_E_IO, path + ": layer_types missing or wrong length");
@@ -178,13 +189,22 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
   for (auto &t : ts->arr) {
     TensorInfo ti;
     const JVal *nm = t.get("name"), *tdt = t.get("dtype"), *sh = t.get("shape");
-    if (!nm || !tdt || !sh || sh->kind != JVal::ARR) return Status::err(JET_E_IO, path + ": bad tensor entry");
+    if (!nm || nm->kind != JVal::STR || !tdt || tdt->kind != JVal::STR || !sh || sh->kind != JVal::ARR ||
+        (tdt->str != "bf16" && tdt->str != "f32"))
+      return Status::err(JET_E_IO, path + ": bad tensor entry");
     ti.name = nm->str;
     ti.bf16 = tdt->str == "bf16";
-    for (auto &s : sh->arr) ti.shape.push_back((int64_t)s.num);
+    int64_t numel = 1;
+    for (auto &s : sh->arr) {
+      int64_t dim = 0;
+      if (!as_count(s, &dim) || (dim > 0 && numel > (INT64_C(1) << 40) / dim))
+        return Status::err(JET_E_IO, path + ": tensor " + ti.name + " has a bad shape");
+      numel *= dim;
+      ti.shape.push_back(dim);
+    }
     if (!get_int(t, "offset", &ti.offset) || !get_int(t, "nbytes", &ti.nbytes))
       return Status::err(JET_E_IO, path + ": tensor lacks offset/nbytes");
-    if (ti.nbytes != ti.numel() * (ti.bf16 ? 2 : 4))
+    if (ti.nbytes != numel * (ti.bf16 ? 2 : 4))
       return Status::err(JET_E_IO, path + ": tensor " + ti.name + " size mismatch");
     h->tensors[ti.name] = ti;
   }

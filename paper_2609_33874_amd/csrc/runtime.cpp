@@ -158,6 +158,7 @@ Status sync(jet_model *m) {
 struct Loader {
   jet_model *m;
   std::vector<char> host;
+  unsigned long long *inexact = nullptr;  // device counter of inexact fp16 conversions
 
   Status read(const std::string &name, const TensorInfo **ti) {
     auto it = m->h.tensors.find(name);
@@ -196,7 +197,7 @@ struct Loader {
       void *tmp;
       TRY(dmalloc(m, (size_t)n * 2, &tmp));
       hipError_t e = hipMemcpy(tmp, src, (size_t)n * 2, hipMemcpyHostToDevice);
-      if (e == hipSuccess) e = jetk::launch_convert_bf16_to_f16((const uint16_t *)tmp, n, scale, *out, m->st);
+      if (e == hipSuccess) e = jetk::launch_convert_bf16_to_f16((const uint16_t *)tmp, n, scale, *out, inexact, m->st);
       if (e == hipSuccess) e = hipStreamSynchronize(m->st);
       dfree(m, tmp, (size_t)n * 2);
       HIPC(e);
@@ -361,6 +362,11 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
   HIPC(hipSetDevice(m->device));
   Loader L{m, {}};
+  if (m->kdt == 2) {
+    TRY(dmalloc(m, sizeof(unsigned long long), (void **)&L.inexact));
+    m->weight_allocs.push_back(L.inexact);
+    HIPC(hipMemset(L.inexact, 0, sizeof(unsigned long long)));
+  }
   TRY(L.matrix("tok_embed", &m->embed, nullptr, /*keep_bf16=*/m->kdt == 2));
   TRY(L.matrix("lm_head", &m->lm_head, &m->is_lm));
   TRY(L.vec_f32("final_norm", &m->final_norm, h.d));
@@ -416,6 +422,11 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   m->weight_allocs.push_back(m->rope_sin);
   HIPC(hipMemcpy(m->rope_cos, c.data(), c.size() * 4, hipMemcpyHostToDevice));
   HIPC(hipMemcpy(m->rope_sin, s.data(), s.size() * 4, hipMemcpyHostToDevice));
+  if (L.inexact) {
+    unsigned long long n = 0;
+    HIPC(hipMemcpy(&n, L.inexact, sizeof(n), hipMemcpyDeviceToHost));
+    m->f16_inexact = (int64_t)n;
+  }
   return Status::ok();
 }
 
@@ -803,8 +814,15 @@ void free_prefix(jet_prefix *p) {
   if (!p) return;
   if (p->m) {
     for (auto &a : p->allocs) p->m->pool.push_back({a.second, a.first});
-    p->m->n_prefixes--;
+    auto &live = p->m->live;
+    for (size_t i = 0; i < live.size(); ++i)
+      if (live[i] == p) {
+        live.erase(live.begin() + (std::ptrdiff_t)i);
+        break;
+      }
   } else {
+    // a prefix that never got a model, or whose model was freed (its
+    // buffers were freed then and the list is empty)
     for (auto &a : p->allocs) (void)hipFree(a.first);
   }
   delete p;
@@ -1005,6 +1023,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
 Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_t *cto, const int32_t *tokens,
              float *out_tok, float *out_sum) {
   const ModelHeader &h = m->h;
+  if (!p->m) return Status::err(JET_E_INVALID, "prefix is detached: its model was freed");
   if (p->m != m) return Status::err(JET_E_INVALID, "prefix belongs to another model");
   if (!out_sum) return Status::err(JET_E_INVALID, "out_cand_sum is NULL");
   CandLayout L;
@@ -1143,6 +1162,20 @@ void free_model(jet_model *m) {
   if (!m) return;
   (void)hipSetDevice(m->device);
   if (m->st) (void)hipStreamSynchronize(m->st);
+  // prefixes still alive lose their buffers now and are detached, so that a
+  // later jet_prefix_free only deletes the handle
+  for (jet_prefix *p : m->live) {
+    for (auto &a : p->allocs) (void)hipFree(a.first);
+    p->allocs.clear();
+    p->kcache.clear();
+    p->vcache.clear();
+    p->S_pre.clear();
+    p->conv_tail.clear();
+    p->f_last = nullptr;
+    p->lse_last = nullptr;
+    p->m = nullptr;
+  }
+  m->live.clear();
   for (auto &kv : m->ws) (void)hipFree(kv.second.p);
   for (void *a : m->weight_allocs) (void)hipFree(a);
   for (auto &e : m->pool) (void)hipFree(e.second);
@@ -1204,7 +1237,7 @@ extern "C" int jet_prefill_prefix(jet_model *model, int32_t n_q, const int64_t *
   if (hipSetDevice(model->device) != hipSuccess) return fail(Status::err(JET_E_DEVICE, "hipSetDevice failed"));
   jet_prefix *p = new jet_prefix();
   p->m = model;
-  model->n_prefixes++;
+  model->live.push_back(p);
   Status s = prefill(model, n_q, prefix_offsets, prefix_tokens, p);
   if (!s) {
     (void)hipStreamSynchronize(model->st);
@@ -1246,9 +1279,10 @@ extern "C" int jet_stats_reset(jet_model *model) {
 }
 
 extern "C" int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n_layers, int64_t *max_ctx,
-                              int32_t *dtype) {
+                              int32_t *dtype, int64_t *f16_inexact_weights) {
   clear_error();
   if (!model) return fail(Status::err(JET_E_INVALID, "NULL model"));
+  if (f16_inexact_weights) *f16_inexact_weights = model->f16_inexact;
   if (vocab) *vocab = model->h.vocab;
   if (n_layers) *n_layers = model->h.n_layers;
   if (max_ctx) *max_ctx = model->max_ctx;

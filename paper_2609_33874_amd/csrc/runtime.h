@@ -12,6 +12,7 @@
 #include "model_file.h"
 
 struct jet_model;
+struct jet_prefix;
 
 namespace jet {
 
@@ -70,6 +71,7 @@ struct jet_model {
   size_t bytes_used = 0;
   void *embed = nullptr, *lm_head = nullptr;
   float is_lm = 1.0f;  // inverse weight scale of lm_head
+  int64_t f16_inexact = 0;  // fp16 modes: weights whose scaled fp16 value is not the file's bf16 value
   float *final_norm = nullptr;
   std::vector<jet::Layer> layers;
   float *rope_cos = nullptr, *rope_sin = nullptr;
@@ -80,11 +82,13 @@ struct jet_model {
   // device buffers of freed prefixes, kept for the next prefill (sizes in bytes)
   std::vector<std::pair<size_t, void *>> pool;
   jet_stats stats{};
-  int n_prefixes = 0;
+  // prefixes made from this model and not yet freed; freeing the model frees
+  // their device buffers and detaches them (their handle stays valid to free)
+  std::vector<jet_prefix *> live;
 };
 
 struct jet_prefix {
-  jet_model *m = nullptr;
+  jet_model *m = nullptr;            // NULL once the model has been freed
   int32_t n_q = 0;
   std::vector<int64_t> prefix_offsets;
   int64_t T = 0;                     // total prefix tokens

@@ -78,7 +78,7 @@ def lib() -> ctypes.CDLL:
         L.jet_candidate_layout.argtypes = [I32, P, P, P, I64, I64, P, P, P, P, P, P]
         L.jet_stats_get.argtypes = [P, ctypes.POINTER(jet_stats)]
         L.jet_stats_reset.argtypes = [P]
-        L.jet_model_info.argtypes = [P, P, P, P, P]
+        L.jet_model_info.argtypes = [P, P, P, P, P, P]
         L.jet_prefix_free.argtypes = [P]
         L.jet_prefix_free.restype = None
         L.jet_model_free.argtypes = [P]
@@ -228,10 +228,12 @@ def jet_stats_reset(model) -> None:
 
 
 def jet_model_info(model) -> dict:
-    v, nl, mc = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    v, nl, mc, ni = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     dt = ctypes.c_int32()
-    _check(lib().jet_model_info(model, ctypes.byref(v), ctypes.byref(nl), ctypes.byref(mc), ctypes.byref(dt)))
-    return dict(vocab=v.value, n_layers=nl.value, max_ctx=mc.value, dtype=dt.value)
+    _check(lib().jet_model_info(model, ctypes.byref(v), ctypes.byref(nl), ctypes.byref(mc), ctypes.byref(dt),
+                                ctypes.byref(ni)))
+    return dict(vocab=v.value, n_layers=nl.value, max_ctx=mc.value, dtype=dt.value,
+                f16_inexact_weights=ni.value)
 
 
 def jet_prefix_free(prefix) -> None:

@@ -118,3 +118,74 @@ def test_wide_grouping_and_many_experts(name, model_dir):
     b = score(path, wl, J.JET_F16)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_model_freed_before_its_prefix():
+    """Freeing a model first frees its live prefixes' buffers and detaches
+    them: scoring against a detached prefix is refused, freeing it works, and
+    the device is fine for the next model (jet.h, Ownership)."""
+    path = jet_synth.ensure_model("small_gqa_bf16")
+    wl = jet_synth.make_workload("small", n_questions=3)
+    m = J.jet_model_load(path, dtype=J.JET_F16)
+    p1 = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+    p2 = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+    J.jet_prefix_free(p2)          # one freed in order, one left alive
+    ref_tok, ref_sum = J.jet_score_candidates(m, p1, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+    J.jet_model_free(m)
+    m2 = J.jet_model_load(path, dtype=J.JET_F16)
+    try:
+        with pytest.raises(J.JetError) as e:
+            J.jet_score_candidates(m2, p1, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+        assert e.value.code == J.JET_E_INVALID
+        J.jet_prefix_free(p1)
+        p3 = J.jet_prefill_prefix(m2, wl.prefix_offsets, wl.prefix_tokens)
+        try:
+            tok, sums = J.jet_score_candidates(m2, p3, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+        finally:
+            J.jet_prefix_free(p3)
+    finally:
+        J.jet_model_free(m2)
+    np.testing.assert_array_equal(tok, ref_tok)
+    np.testing.assert_array_equal(sums, ref_sum)
+
+
+def _inexact_f16(vals_bf16_bits, k):
+    """How many bf16 values (bits) times 2^k numpy's fp16 rounding changes."""
+    v = (vals_bf16_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64) * 2.0 ** k
+    return int(np.count_nonzero(v.astype(np.float16).astype(np.float64) != v))
+
+
+def test_fp16_load_counts_inexact_weights(tmp_path):
+    """The fp16 modes scale each matrix by 2^k (largest magnitude into
+    [2^14, 2^15)) and convert; values far below the largest round. The loader
+    reports how many: planted tiny values in one matrix change the count by
+    exactly numpy's count of fp16 roundings of that matrix."""
+    import shutil
+    src = jet_synth.ensure_model("small_gqa_bf16")
+    path = str(tmp_path / "planted.jetm")
+    shutil.copy(src, path)
+    m = J.jet_model_load(src, dtype=J.JET_F16)
+    try:
+        n0 = J.jet_model_info(m)["f16_inexact_weights"]
+    finally:
+        J.jet_model_free(m)
+    h = jet_synth.read_header(path)
+    t = next(t for t in h["tensors"] if t["name"] == "blk.0.wo")   # loaded as one matrix
+    w = np.memmap(path, dtype=np.uint16, mode="r+", offset=t["offset"], shape=(t["nbytes"] // 2,))
+    mag = ((w.astype(np.uint32) & 0x7FFF) << 16).view(np.float32)
+    k = 14 - int(np.floor(np.log2(float(mag.max()))))
+    before = _inexact_f16(np.array(w), k)
+    # 2^-45 * (1 + 2^-7), -2^-40 * 1.5, 2^-50: far below fp16's step after scaling
+    planted = np.array([2.0 ** -45 * (1 + 2.0 ** -7), -(2.0 ** -40) * 1.5, 2.0 ** -50], np.float32)
+    w[[3, 1000, 5000]] = (planted.view(np.uint32) >> 16).astype(np.uint16)
+    w.flush()
+    after = _inexact_f16(np.array(w), k)
+    del w
+    assert after - before >= 2
+    m = J.jet_model_load(path, dtype=J.JET_F16)
+    try:
+        n1 = J.jet_model_info(m)["f16_inexact_weights"]
+    finally:
+        J.jet_model_free(m)
+    log(f"[edges] inexact fp16 weights: {n0} -> {n1} (numpy: {before} -> {after} in blk.0.wo)")
+    assert n1 - n0 == after - before
