@@ -75,7 +75,11 @@ enum { JET_CHOICE = 0, JET_BINARY = 1, JET_ORDINAL = 2 }; /* decision rule */
 
 /* flags for jet_load_opts.flags */
 enum {
-  JET_FLAG_KERNEL_TIMING = 1 /* time every launch with HIP events (jet_stats) */
+  JET_FLAG_KERNEL_TIMING = 1, /* time every launch with HIP events (jet_stats) */
+  JET_FLAG_RECORD_ROUTES = 2  /* mixture-of-experts models: keep the experts each
+                                 layer chose for each row (jet_routes_get);
+                                 a diagnostic for checking routing, it
+                                 synchronises the stream at every such layer */
 };
 
 typedef struct jet_model jet_model;
@@ -282,6 +286,22 @@ int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n_layers,
 /* Release a prefix (its device buffers go back to the model for the next
  * prefill) and a model (weights, work buffers, and the buffers of every
  * prefix of it not yet freed; see Ownership above). NULL is a no-op. */
+/* jet_routes_get - the experts chosen by the most recent prefill (which = 0)
+ * or scoring call (which = 1) of a mixture-of-experts model loaded with
+ * JET_FLAG_RECORD_ROUTES (Section 4.2: routed experts). The top_k experts
+ * kept by layer l for row r are out_ids[(l * rows + r) * top_k + j],
+ * j < top_k, in the routing kernel's order (descending router logit, ties
+ * to the lower expert index); rows that layer did not route hold -1.
+ * Rows: prefill, the call's prefix tokens in input order (the last layer of
+ * a prefill routes only each question's last token when that layer is an
+ * attention layer); scoring, the candidate body rows in the order of
+ * jet_candidate_layout. out_rows / out_layers / out_top_k: host, may be
+ * NULL; out_ids: host, may be NULL (sizes only), else cap_ids >= layers *
+ * rows * top_k elements. Errors: JET_E_INVALID (no experts, flag not set,
+ * bad which), JET_E_CAPACITY (cap_ids too small). */
+int jet_routes_get(const jet_model *model, int32_t which, int64_t *out_rows, int32_t *out_layers,
+                   int32_t *out_top_k, int32_t *out_ids, int64_t cap_ids);
+
 void jet_prefix_free(jet_prefix *prefix);
 void jet_model_free(jet_model *model);
 

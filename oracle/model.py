@@ -134,9 +134,36 @@ def moe_route(logits: np.ndarray, top_k: int) -> tuple[np.ndarray, np.ndarray]:
     return sel, w / w.sum(axis=1, keepdims=True)
 
 
-def moe_ffn(model: "Model", li: int, W: dict, a: np.ndarray) -> np.ndarray:
-    """Mixture-of-experts FFN of block li on rows a [n, d]."""
-    sel, wts = moe_route(a @ W["moe_router"].T, model.top_k)
+def moe_ffn(model: "Model", li: int, W: dict, a: np.ndarray, forced: np.ndarray | None = None,
+            gaps: list | None = None) -> np.ndarray:
+    """Mixture-of-experts FFN of block li on rows a [n, d].
+
+    ``forced`` [n, top_k] (optional) names the experts to keep per row, for
+    checking a routing decided elsewhere: a row whose first entry is -1 is
+    routed here; any other row keeps exactly the named experts, mixed with
+    weights softmax over *these* logits at those experts (the same rule as
+    unforced routing, applied to the given set). For every forced row,
+    ``gaps`` (if a list) receives min(logit of a kept expert) - max(logit of
+    an expert not kept): >= 0 when the set is a top-k of these logits,
+    negative by how far it is from one.
+    """
+    logits = a @ W["moe_router"].T
+    sel, wts = moe_route(logits, model.top_k)
+    if forced is not None:
+        rows = np.nonzero(forced[:, 0] >= 0)[0]
+        if len(rows):
+            fs = forced[rows].astype(np.int64)
+            z = np.take_along_axis(logits[rows], fs, axis=1)
+            w = np.exp(z - z.max(axis=1, keepdims=True))
+            sel = sel.copy()
+            wts = wts.copy()
+            sel[rows] = fs
+            wts[rows] = w / w.sum(axis=1, keepdims=True)
+            if gaps is not None:
+                out_mask = np.ones((len(rows), logits.shape[1]), bool)
+                np.put_along_axis(out_mask, fs, False, axis=1)
+                rest = np.where(out_mask, logits[rows], -np.inf).max(axis=1)
+                gaps.append(z.min(axis=1) - rest)
     out = np.zeros_like(a)
     for e in np.unique(sel):
         rows, slot = np.nonzero(sel == e)
@@ -250,15 +277,18 @@ def _gdn_layer(h, W, a_rows, seq_slices, states, li, want_state, eps):
 
 def forward(model: Model, seqs: list, starts: list | None = None,
             states: list | None = None, want_state: bool = False,
-            row_chunk: int = 8192):
+            row_chunk: int = 8192, routes: list | None = None, route_gaps: list | None = None):
     """Run every layer over a batch of independent token sequences.
 
     seqs[i] holds new token ids whose first position is starts[i]; states[i]
     is None (fresh sequence) or the per-layer state returned by an earlier
     call for the tokens before them. Independent sequences are stacked as
     rows of the same matrix products; attention and the recurrence are run
-    per sequence. Returns (list of hidden states [n_i, d] before the final
-    norm, list of per-layer states or None).
+    per sequence. Mixture-of-experts models only: routes[i] (optional) is an
+    int array [n_layers, n_i, top_k] of experts to keep per layer and row
+    (-1 rows routed here, see ``moe_ffn``); route_gaps collects the forced
+    rows' top-k gaps of every layer. Returns (list of hidden states [n_i, d]
+    before the final norm, list of per-layer states or None).
     """
     h = model.h
     starts = starts or [0] * len(seqs)
@@ -270,6 +300,9 @@ def forward(model: Model, seqs: list, starts: list | None = None,
     E = jet_synth.tensor_raw(model.path, "tok_embed", h)
     x = upcast(E[ids])
     out_states = [[None] * len(model.layer_types) for _ in seqs] if want_state else None
+    forced_all = None
+    if routes is not None:
+        forced_all = np.concatenate([np.asarray(r, np.int64) for r in routes], axis=1)  # [L, rows, k]
     for li, lt in enumerate(model.layer_types):
         W = model.layer(li)
         a = rmsnorm(x, W["attn_norm"], model.eps)
@@ -285,7 +318,8 @@ def forward(model: Model, seqs: list, starts: list | None = None,
             r = slice(r0, min(r0 + row_chunk, x.shape[0]))
             a = rmsnorm(x[r], W["ffn_norm"], model.eps)
             if model.n_experts:
-                x[r] = x[r] + moe_ffn(model, li, W, a)
+                fr = None if forced_all is None else forced_all[li, r]
+                x[r] = x[r] + moe_ffn(model, li, W, a, fr, route_gaps)
             else:
                 x[r] = x[r] + swiglu_ffn(a, W["w_gate"], W["w_up"], W["w_down"])
         del W

@@ -51,23 +51,29 @@ def _groups(wl, max_rows: int):
         yield group
 
 
-def score_unshared(model: Model | str, wl, max_rows: int = 16384):
+def score_unshared(model: Model | str, wl, max_rows: int = 16384, routes: dict | None = None,
+                   route_gaps: list | None = None):
     """Per-token log-probs [sum m] (input token order) and sums [N] (Eq. 3).
 
     Each candidate is an independent full forward with no prefix sharing.
+    Mixture-of-experts models: ``routes`` (optional) maps a candidate index
+    to the experts to keep along its sequence x || y_c[1..m-1], an int array
+    [n_layers, P + m - 1, top_k] (see ``forward``).
     """
     model = Model(model) if isinstance(model, str) else model
     W_lm = model.w("lm_head")
     out_tok = np.zeros(len(wl.cand_tokens))
     for group in _groups(wl, max_rows):
-        seqs, meta = [], []
+        seqs, meta, rts = [], [], []
         for q in group:
             x = wl.prefix(q)
             for j, y in enumerate(wl.candidates(q)):
                 c = int(wl.q_cand_offsets[q]) + j
                 seqs.append(np.concatenate([x, y[:-1]]).astype(np.int64))
                 meta.append((c, len(x), y))
-        hid, _ = forward(model, seqs)
+                if routes is not None:
+                    rts.append(routes[c])
+        hid, _ = forward(model, seqs, routes=rts if routes is not None else None, route_gaps=route_gaps)
         rows, tgts, dst = [], [], []
         for (c, P, y), hs in zip(meta, hid):
             m = len(y)

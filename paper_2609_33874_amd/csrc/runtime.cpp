@@ -606,6 +606,36 @@ Status wave_bufs(jet_model *m, int64_t R, WaveBufs *b) {
   return Status::ok();
 }
 
+// Copies a routing result [R][k] (device) into the current route record
+// (JET_FLAG_RECORD_ROUTES; synchronises the stream).
+Status record_routes(jet_model *m, const int *sel, int64_t R, int k) {
+  std::vector<int32_t> h((size_t)(R * k));
+  HIPC(hipMemcpyAsync(h.data(), sel, h.size() * 4, hipMemcpyDeviceToHost, m->st));
+  HIPC(hipStreamSynchronize(m->st));
+  auto &rec = m->routes[m->rt_which];
+  const int64_t rows = m->route_rows[m->rt_which];
+  if ((int64_t)m->rt_rowmap.size() != R) return Status::err(JET_E_DEVICE, "route record: row map mismatch");
+  for (int64_t r = 0; r < R; ++r)
+    for (int j = 0; j < k; ++j)
+      rec[(size_t)((m->rt_layer * rows + m->rt_rowmap[(size_t)r]) * k + j)] = h[(size_t)(r * k + j)];
+  return Status::ok();
+}
+
+// Route recording: which record the next FFN calls write, and their rows.
+void route_rows_begin(jet_model *m, int which, int64_t rows) {
+  m->rt_which = -1;
+  if (!(m->flags & JET_FLAG_RECORD_ROUTES) || !m->h.n_experts) return;
+  m->routes[which].assign((size_t)(m->h.n_layers * rows * m->h.top_k), -1);
+  m->route_rows[which] = rows;
+}
+void route_rows_set(jet_model *m, int which, int64_t layer, int64_t base, int64_t R, const int32_t *idx = nullptr) {
+  if (!(m->flags & JET_FLAG_RECORD_ROUTES) || !m->h.n_experts) return;
+  m->rt_which = which;
+  m->rt_layer = layer;
+  m->rt_rowmap.resize((size_t)R);
+  for (int64_t r = 0; r < R; ++r) m->rt_rowmap[(size_t)r] = base + (idx ? idx[r] : r);
+}
+
 // Mixture-of-experts FFN on x = RMSNorm(resid) (in b.xn): router GEMM,
 // top-k routing, rows scattered into per-expert segments, grouped gate/up
 // (SwiGLU) and down GEMMs over the segments, the shared expert on all rows,
@@ -643,6 +673,7 @@ Status moe_ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   {
     KTimer t(m, JET_K_OTHER, 0, (double)(R * ly.n_router) * 4.0);
     LAUNCH(jetk::launch_moe_route(jetk::MoeRouteArgs{logits, ly.n_router, (int)R, E, k, sel, wts, sg}, m->st));
+    if (m->rt_which >= 0) TRY(record_routes(m, sel, R, k));
     LAUNCH(jetk::launch_moe_plan(sel, (int)R, k, E, bm, (int)(S / bm), tiles, chist, cbase, slot, m->st));
     LAUNCH(jetk::launch_moe_scatter(b.xn, d * (int64_t)m->esz, (int)R, k, slot, xp, m->st));
   }
@@ -895,6 +926,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     d_tok = dt;
   }
   const int dt = m->kdt;
+  route_rows_begin(m, 0, T);
   // waves of whole questions under the prefill token budget
   int32_t q0 = 0;
   while (q0 < n_q) {
@@ -955,6 +987,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
       const Layer &ly = m->layers[(size_t)l];
       if (ly.gdn) {
         TRY(gdn_layer(m, ly, b, R, gp, p->conv_tail[(size_t)l], nullptr, p->S_pre[(size_t)l]));
+        route_rows_set(m, 0, l, t0, R);
         TRY(ffn(m, ly, b, R));
         continue;
       }
@@ -963,6 +996,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
       TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T, nullptr, nullptr,
                         0, nullptr, nullptr));
       TRY(attn_out(m, ly, b, R));
+      route_rows_set(m, 0, l, t0, R);
       TRY(ffn(m, ly, b, R));
     }
     if (last_rows_only) {
@@ -997,6 +1031,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
                                         m->st));
       }
       TRY(attn_out(m, ly, c, nq));
+      route_rows_set(m, 0, L - 1, t0, nq, last.data());
       TRY(ffn(m, ly, c, nq));
       KTimer t(m, JET_K_OTHER, 0, 0);
       LAUNCH(jetk::launch_rmsnorm(dt, m->pair, c.resid, nullptr, m->final_norm, (int)nq, (int)h.d, (float)h.rms_eps,
@@ -1009,6 +1044,7 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     m->stats.prefill_waves++;
     q0 = q1;
   }
+  m->rt_which = -1;
   TRY(run_lmhead(m, p->f_last, n_q, p->lse_last));
   TRY(sync(m));
   m->stats.prefix_tokens += T;
@@ -1059,6 +1095,7 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
   for (int32_t q = 0; q < p->n_q; ++q)
     for (int64_t c = qco[q]; c < qco[q + 1]; ++c) cand_q[(size_t)c] = q;
   auto row0 = [&](int64_t c) { return c < N ? (int64_t)L.cand_row0[(size_t)c] : L.n_rows; };
+  route_rows_begin(m, 1, L.n_rows);
 
   int64_t c0 = 0;
   while (c0 < N) {
@@ -1125,8 +1162,10 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
                             d_rc + r0, d_rt + r0));
           TRY(attn_out(m, ly, b, R));
         }
+        route_rows_set(m, 1, l, r0, R);
         TRY(ffn(m, ly, b, R));
       }
+      m->rt_which = -1;
       TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz * m->np, &f_body));
       TRY(ws_t<float>(m, "lse_body", (size_t)R, &lse_body));
       {
@@ -1287,6 +1326,24 @@ extern "C" int jet_model_info(const jet_model *model, int64_t *vocab, int64_t *n
   if (n_layers) *n_layers = model->h.n_layers;
   if (max_ctx) *max_ctx = model->max_ctx;
   if (dtype) *dtype = model->dtype;
+  return JET_OK;
+}
+
+extern "C" int jet_routes_get(const jet_model *model, int32_t which, int64_t *out_rows, int32_t *out_layers,
+                              int32_t *out_top_k, int32_t *out_ids, int64_t cap_ids) {
+  clear_error();
+  if (!model) return fail(Status::err(JET_E_INVALID, "NULL model"));
+  if (!model->h.n_experts) return fail(Status::err(JET_E_INVALID, "the model has no experts"));
+  if (!(model->flags & JET_FLAG_RECORD_ROUTES))
+    return fail(Status::err(JET_E_INVALID, "the model was loaded without JET_FLAG_RECORD_ROUTES"));
+  if (which != 0 && which != 1) return fail(Status::err(JET_E_INVALID, "which must be 0 (prefill) or 1 (score)"));
+  const auto &rec = model->routes[which];
+  if (out_ids && (int64_t)rec.size() > cap_ids)
+    return fail(Status::err(JET_E_CAPACITY, "cap_ids smaller than layers * rows * top_k"));
+  if (out_rows) *out_rows = model->route_rows[which];
+  if (out_layers) *out_layers = (int32_t)model->h.n_layers;
+  if (out_top_k) *out_top_k = (int32_t)model->h.top_k;
+  if (out_ids && !rec.empty()) std::memcpy(out_ids, rec.data(), rec.size() * sizeof(int32_t));
   return JET_OK;
 }
 

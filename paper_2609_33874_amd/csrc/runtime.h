@@ -85,6 +85,15 @@ struct jet_model {
   // prefixes made from this model and not yet freed; freeing the model frees
   // their device buffers and detaches them (their handle stays valid to free)
   std::vector<jet_prefix *> live;
+  // JET_FLAG_RECORD_ROUTES: experts chosen per (layer, row) by the latest
+  // prefill (0) and scoring (1) call, [n_layers][rows][top_k], -1 = not routed
+  std::vector<int32_t> routes[2];
+  int64_t route_rows[2] = {0, 0};
+  // set around each FFN call while recording: the record, the layer, and the
+  // record row of each of the call's rows
+  int rt_which = -1;
+  int64_t rt_layer = 0;
+  std::vector<int64_t> rt_rowmap;
 };
 
 struct jet_prefix {

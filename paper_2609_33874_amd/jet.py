@@ -19,6 +19,7 @@ JET_OK, JET_E_INVALID, JET_E_CAPACITY, JET_E_OOM, JET_E_DEVICE, JET_E_IO = range
 JET_BF16, JET_FP32, JET_BF16_SINGLE, JET_F16, JET_F16P = 0, 1, 2, 3, 4
 JET_CHOICE, JET_BINARY, JET_ORDINAL = 0, 1, 2
 JET_FLAG_KERNEL_TIMING = 1
+JET_FLAG_RECORD_ROUTES = 2
 KERNEL_CLASSES = ["gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "lmhead", "attn_prefix",
                   "attn_cand", "gdn", "other"]
 ERROR_NAMES = {1: "JET_E_INVALID", 2: "JET_E_CAPACITY", 3: "JET_E_OOM", 4: "JET_E_DEVICE", 5: "JET_E_IO"}
@@ -26,7 +27,7 @@ ERROR_NAMES = {1: "JET_E_INVALID", 2: "JET_E_CAPACITY", 3: "JET_E_OOM", 4: "JET_
 # every symbol include/jet.h declares
 EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_score_candidates", "jet_decide",
            "jet_answer_classes", "jet_evaluate", "jet_candidate_layout", "jet_stats_get", "jet_stats_reset", "jet_model_info",
-           "jet_prefix_free", "jet_model_free", "jet_last_error"]
+           "jet_routes_get", "jet_prefix_free", "jet_model_free", "jet_last_error"]
 
 
 class JetError(RuntimeError):
@@ -79,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.jet_stats_get.argtypes = [P, ctypes.POINTER(jet_stats)]
         L.jet_stats_reset.argtypes = [P]
         L.jet_model_info.argtypes = [P, P, P, P, P, P]
+        L.jet_routes_get.argtypes = [P, I32, P, P, P, P, I64]
         L.jet_prefix_free.argtypes = [P]
         L.jet_prefix_free.restype = None
         L.jet_model_free.argtypes = [P]
@@ -234,6 +236,16 @@ def jet_model_info(model) -> dict:
                                 ctypes.byref(ni)))
     return dict(vocab=v.value, n_layers=nl.value, max_ctx=mc.value, dtype=dt.value,
                 f16_inexact_weights=ni.value)
+
+
+def jet_routes_get(model, which: int) -> np.ndarray:
+    """Experts chosen per (layer, row) by the latest prefill (0) or scoring
+    (1) call: int32 [n_layers, rows, top_k], -1 where a layer routed no row."""
+    rows, nl, k = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().jet_routes_get(model, which, ctypes.byref(rows), ctypes.byref(nl), ctypes.byref(k), None, 0))
+    out = np.empty((nl.value, rows.value, k.value), np.int32)
+    _check(lib().jet_routes_get(model, which, None, None, None, out.ctypes.data_as(ctypes.c_void_p), out.size))
+    return out
 
 
 def jet_prefix_free(prefix) -> None:

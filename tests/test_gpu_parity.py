@@ -328,3 +328,43 @@ def test_candidate_isolation_on_gpu(spec, wname, dtype, model_dir):
         J.jet_prefix_free(p)
     finally:
         J.jet_model_free(m)
+
+
+@pytest.mark.parametrize("dtype", [J.JET_FP32, J.JET_F16])
+def test_moe_routes_recorded_and_valid(dtype, model_dir):
+    """The experts the GPU kept (JET_FLAG_RECORD_ROUTES) are a top-k of the
+    oracle's logits up to rounding, and the oracle run on exactly those sets
+    matches the GPU's scores at the mode's tolerance; recording does not
+    change the scores."""
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from _routes import candidate_routes
+    spec = "small_moe_fp32" if dtype == J.JET_FP32 else "small_moe_bf16"
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
+    wl = jet_synth.make_workload("small_moe")
+    m = J.jet_model_load(path, dtype=dtype, flags=J.JET_FLAG_RECORD_ROUTES)
+    try:
+        p = J.jet_prefill_prefix(m, wl.prefix_offsets, wl.prefix_tokens)
+        try:
+            tok, sums = J.jet_score_candidates(m, p, wl.q_cand_offsets, wl.cand_tok_offsets, wl.cand_tokens)
+            pre, cand = J.jet_routes_get(m, 0), J.jet_routes_get(m, 1)
+        finally:
+            J.jet_prefix_free(p)
+    finally:
+        J.jet_model_free(m)
+    h = jet_synth.read_header(path)
+    L, k, T = h["n_layers"], h["top_k"], int(wl.prefix_offsets[-1])
+    assert pre.shape == (L, T, k) and cand.shape == (L, int(np.sum(np.diff(wl.cand_tok_offsets) - 1)), k)
+    # every row routed by every layer (the last layer is a delta-rule layer here)
+    assert np.all(pre >= 0) and np.all(cand >= 0) and np.all(pre < h["n_experts"])
+    assert np.all(np.sort(pre, axis=2)[:, :, 1:] != np.sort(pre, axis=2)[:, :, :-1])  # distinct experts
+    ref = run_gpu(path, wl, dtype)
+    np.testing.assert_array_equal(tok, ref[0])
+    qs = list(range(wl.n_questions))
+    gaps = []
+    ref_tok, ref_sum = oracle.score_unshared(path, wl.subset(qs), routes=candidate_routes(wl, pre, cand, qs),
+                                             route_gaps=gaps)
+    g = np.concatenate(gaps)
+    log(f"[routes] {spec} dtype {dtype}: {len(g)} rows, {int(np.sum(g < 0))} not the oracle's top-k, "
+        f"smallest margin {g.min():.3e}")
+    assert g.min() >= -(1e-3 if dtype == J.JET_FP32 else 2e-2)
+    check_parity(wl, tok, sums, ref_tok, ref_sum, dtype)

@@ -530,6 +530,68 @@ def test_moe_routing_special_cases(pin_moe_path):
                                rtol=0, atol=1e-12)
 
 
+def test_moe_forced_routing_pins(pin_moe_path):
+    """Forced routing (checking a routing decided elsewhere) against the
+    unforced rule: forcing the rule's own choice changes nothing, -1 rows are
+    routed by the rule, a forced set S equals the unforced mixture of a model
+    that holds only the experts S (all kept), the order inside S does not
+    matter, and the reported gap is the logit margin of the set."""
+    m = om.Model(pin_moe_path)
+    W = dict(m.layer(0))
+    k, E = m.top_k, m.n_experts
+    a = np.random.default_rng(11).normal(size=(9, m.d))
+    z = a @ W["moe_router"].T
+    own, _ = om.moe_route(z, k)
+    base = om.moe_ffn(m, 0, W, a)
+    gaps = []
+    np.testing.assert_array_equal(om.moe_ffn(m, 0, W, a, own, gaps), base)
+    srt = np.sort(z, axis=1)[:, ::-1]
+    np.testing.assert_allclose(gaps[0], srt[:, k - 1] - srt[:, k], rtol=0, atol=1e-14)
+    assert np.all(gaps[0] >= 0)
+    np.testing.assert_array_equal(om.moe_ffn(m, 0, W, a, np.full((len(a), k), -1)), base)
+    # one forced set for every row, against a model holding only those experts
+    S = np.array([E - 1, 0][:k] + list(range(1, k - 1)))
+    sub = om.Model(pin_moe_path)
+    sub.n_experts = sub.top_k = k
+    sub.expert = lambda li, name, e: m.expert(li, name, int(S[e]))
+    Wsub = dict(W, moe_router=W["moe_router"][S])
+    ref = om.moe_ffn(sub, 0, Wsub, a)
+    forced = np.tile(S, (len(a), 1))
+    g2 = []
+    np.testing.assert_allclose(om.moe_ffn(m, 0, W, a, forced, g2), ref, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(om.moe_ffn(m, 0, W, a, forced[:, ::-1].copy()), ref, rtol=0, atol=1e-12)
+    out = np.ones((len(a), E), bool)
+    out[:, S] = False
+    np.testing.assert_allclose(g2[0], z[:, S].min(axis=1) - np.where(out, z, -np.inf).max(axis=1), atol=1e-14)
+    # the k-th expert swapped for the (k+1)-th: gap is minus the k-th margin
+    order = np.argsort(-z, axis=1, kind="stable")
+    swap = order[:, :k].copy()
+    swap[:, k - 1] = order[:, k]
+    g3 = []
+    om.moe_ffn(m, 0, W, a, swap, g3)
+    np.testing.assert_allclose(g3[0], -(srt[:, k - 1] - srt[:, k]), rtol=0, atol=1e-14)
+
+
+def test_moe_forced_routes_follow_their_sequence(pin_moe_path):
+    """forward(routes=...) aligns each sequence's forced rows with that
+    sequence: two sequences stacked, one forced and one left to the rule,
+    each equal to its own forward alone."""
+    m = om.Model(pin_moe_path)
+    rng = np.random.default_rng(12)
+    V, L, k = m.V, len(m.layer_types), m.top_k
+    s0 = rng.integers(0, V, 11)
+    s1 = rng.integers(0, V, 7)
+    r0 = np.stack([np.stack([rng.permutation(m.n_experts)[:k] for _ in range(len(s0))]) for _ in range(L)])
+    r1 = np.full((L, len(s1), k), -1)
+    both, _ = om.forward(m, [s0, s1], routes=[r0, r1])
+    alone0, _ = om.forward(m, [s0], routes=[r0])
+    alone1, _ = om.forward(m, [s1])
+    np.testing.assert_allclose(both[0], alone0[0], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(both[1], alone1[0], rtol=0, atol=1e-12)
+    plain0, _ = om.forward(m, [s0])
+    assert np.abs(plain0[0] - alone0[0]).max() > 1e-6   # the forced experts did change sequence 0
+
+
 @pytest.mark.parametrize("which", ["dense", "hybrid", "moe"])
 def test_prefix_sharing_equals_unshared(which, pin_dense_path, pin_hybrid_path, pin_moe_path):
     path = {"dense": pin_dense_path, "hybrid": pin_hybrid_path, "moe": pin_moe_path}[which]
