@@ -354,9 +354,15 @@ def test_moe_routes_recorded_and_valid(dtype, model_dir):
     h = jet_synth.read_header(path)
     L, k, T = h["n_layers"], h["top_k"], int(wl.prefix_offsets[-1])
     assert pre.shape == (L, T, k) and cand.shape == (L, int(np.sum(np.diff(wl.cand_tok_offsets) - 1)), k)
-    # every row routed by every layer (the last layer is a delta-rule layer here)
-    assert np.all(pre >= 0) and np.all(cand >= 0) and np.all(pre < h["n_experts"])
-    assert np.all(np.sort(pre, axis=2)[:, :, 1:] != np.sort(pre, axis=2)[:, :, :-1])  # distinct experts
+    # every body row routed by every layer; prefix rows by every layer but
+    # the last (an attention layer: it runs only each question's last row)
+    last = wl.prefix_offsets[1:] - 1
+    assert h["layer_types"][-1] == "attn"
+    assert np.all(pre[:-1] >= 0) and np.all(cand >= 0) and np.all(pre[-1, last] >= 0)
+    assert np.count_nonzero(pre[-1, :, 0] >= 0) == wl.n_questions and np.all(pre[-1][pre[-1, :, 0] < 0] == -1)
+    assert np.all(pre < h["n_experts"]) and np.all(cand < h["n_experts"])
+    srt = np.sort(np.concatenate([pre[:-1].reshape(-1, k), cand.reshape(-1, k)]), axis=1)
+    assert np.all(srt[:, 1:] != srt[:, :-1])  # distinct experts per row
     ref = run_gpu(path, wl, dtype)
     np.testing.assert_array_equal(tok, ref[0])
     qs = list(range(wl.n_questions))
