@@ -103,16 +103,33 @@ def describe(wname: str) -> dict:
             "candidates_per_question": r["K"], "candidate_len": list(r["m"])}
 
 
-def cpu_baseline(path: str, wl, min_seconds: float = 10.0, max_questions: int = 16) -> dict:
-    """The fp64 oracle (independent full forward per candidate) on the first
-    questions of the workload, one at a time, until at least min_seconds of
-    CPU work (at most max_questions questions)."""
-    import oracle
+def cpu_facts() -> dict:
+    """The host CPU the oracle runs on: model, logical CPUs, BLAS threads."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "blas_threads": int(threads)}
+
+
+def cpu_baseline(path: str, wl, min_seconds: float = 10.0, max_questions: int = 16) -> dict:
+    """The fp64 oracle (independent full forward per candidate) on the first
+    questions of the workload, one at a time, until at least min_seconds of
+    CPU work (at most max_questions questions)."""
+    import oracle
+    facts = cpu_facts()
+    threads = facts["blas_threads"]
     done, dt = [], 0.0
     for q in range(min(max_questions, wl.n_questions)):
         sub = wl.subset([q])
@@ -127,10 +144,145 @@ def cpu_baseline(path: str, wl, min_seconds: float = 10.0, max_questions: int = 
     P = int(sub.prefix_offsets[-1])
     m = np.diff(sub.cand_tok_offsets)
     return {"value": len(done) / dt, "unit": "questions/s", "cores": int(threads), "kind": "oracle",
-            "seconds": dt,
+            "seconds": dt, **facts,
             "sample": (f"questions 0..{done[-1]} of the workload ({len(done)} questions: {P} prefix tokens, "
                        f"{len(m)} candidates, {int(m.sum())} scored tokens); every candidate an independent "
                        f"fp64 forward")}
+
+
+def cpu_baseline_layers(path: str, wl, layers=(1, 2)) -> dict:
+    """The fp64 oracle where one question is far beyond seconds of CPU work:
+    the first candidate of question 0 run through the first layers[0] and
+    layers[1] layers of the model (embedding, those layers, final norm, LM
+    head over the full vocabulary, Eq. 2-3), timed; the difference is the
+    time of one layer at that sequence length, the rest the per-call fixed
+    part. Extrapolated to question 0 as the oracle runs it: one call with
+    every candidate an independent sequence of P + m - 1 rows through all
+    layers (layer time scaled by rows: the projections and FFN, linear in
+    rows, are over 90% of a layer's work at these lengths)."""
+    import jet_synth
+    import oracle
+    facts = cpu_facts()
+    cands = wl.candidates(0)
+    sub = jet_synth.from_lists([wl.prefix(0)], [[cands[0]]])
+    model = oracle.Model(path)
+    all_layers = list(model.layer_types)
+    t = []
+    for n in layers:
+        model.layer_types = all_layers[:n]
+        t0 = time.perf_counter()
+        oracle.score_unshared(model, sub)
+        t.append(time.perf_counter() - t0)
+        log(f"oracle, question 0 candidate 0, first {n} layer(s): {t[-1]:.1f}s")
+    per_layer = (t[1] - t[0]) / (layers[1] - layers[0])
+    fixed = max(t[0] - layers[0] * per_layer, 0.0)
+    P = len(wl.prefix(0))
+    rows_sample = P + len(cands[0]) - 1
+    rows_q = sum(P + len(y) - 1 for y in cands)
+    t_q = fixed + len(all_layers) * per_layer * rows_q / rows_sample
+    return {"value": 1.0 / t_q, "unit": "questions/s", "cores": facts["blas_threads"], "kind": "oracle",
+            "seconds": sum(t), "extrapolated_seconds_per_question": round(t_q, 1), **facts,
+            "sample": (f"question 0, candidate 0 ({rows_sample} positions): the oracle through the first "
+                       f"{layers[0]} and {layers[1]} of {len(all_layers)} layers plus the full-vocabulary LM "
+                       f"head, timed ({t[0]:.1f}s, {t[1]:.1f}s); per-layer time {per_layer:.2f}s, fixed part "
+                       f"{fixed:.2f}s; extrapolated to question 0's {len(cands)} candidates ({rows_q} "
+                       f"positions) through all {len(all_layers)} layers")}
+
+
+REUSE_WORKLOAD = "dense_1p5b_k4"
+
+
+def unshared_workload(wl):
+    """Every candidate as its own question (its prefix prefilled again)."""
+    import jet_synth
+    pre, cands = [], []
+    for q in range(wl.n_questions):
+        for y in wl.candidates(q):
+            pre.append(wl.prefix(q))
+            cands.append([y])
+    return jet_synth.from_lists(pre, cands)
+
+
+class Runner:
+    """One model on cuda:0 and the timed step of the hot path."""
+
+    def __init__(self, wname: str, dtype: str, timing: bool):
+        import torch
+        import jet_synth
+        from paper_2609_33874_amd import jet as J
+        self.torch, self.J = torch, J
+        self.wname = wname
+        spec = jet_synth.WORKLOADS[wname]["model"]
+        t = time.perf_counter()
+        self.path = jet_synth.ensure_model(spec)
+        log(f"model file {self.path} ready in {time.perf_counter() - t:.1f}s")
+        self.wl = jet_synth.make_workload(wname)
+        self.mode = {"binary": J.JET_BINARY, "ordinal": J.JET_ORDINAL}.get(MODE_OF.get(wname, ""), J.JET_CHOICE)
+        self.dev = torch.device("cuda:0")
+        stream = torch.cuda.current_stream(self.dev)
+        flags = J.JET_FLAG_KERNEL_TIMING if timing else 0
+        jdt = {"f16": J.JET_F16, "f16p": J.JET_F16P, "bf16": J.JET_BF16}[dtype]
+        t = time.perf_counter()
+        self.model = J.jet_model_load(self.path, dtype=jdt, device=0, hip_stream=stream.cuda_stream, flags=flags)
+        self.load_s = time.perf_counter() - t
+        log(f"model loaded in {self.load_s:.1f}s")
+        self.phase = {"prefill": 0.0, "score": 0.0, "decide": 0.0}
+
+    def inputs(self, w):
+        torch = self.torch
+        return (torch.from_numpy(w.prefix_tokens).to(self.dev), torch.from_numpy(w.cand_tokens).to(self.dev),
+                torch.empty(int(w.cand_tok_offsets[-1]), dtype=torch.float32, device=self.dev),
+                torch.empty(w.n_candidates, dtype=torch.float32, device=self.dev))
+
+    def step(self, w, inp):
+        J = self.J
+        d_pre, d_cand, o_tok, o_sum = inp
+        a = time.perf_counter()
+        p = J.jet_prefill_prefix(self.model, w.prefix_offsets, d_pre)
+        b = time.perf_counter()
+        J.jet_score_candidates(self.model, p, w.q_cand_offsets, w.cand_tok_offsets, d_cand, o_tok, o_sum)
+        c = time.perf_counter()
+        sums = o_sum.cpu().numpy()
+        J.jet_decide(self.mode, w.q_cand_offsets, sums)
+        d = time.perf_counter()
+        J.jet_prefix_free(p)
+        self.phase["prefill"] += b - a
+        self.phase["score"] += c - b
+        self.phase["decide"] += d - c
+
+    def timed(self, w, inp, steps: int, what: str) -> float:
+        """Seconds for `steps` steps, bracketed by device synchronisation."""
+        self.torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(w, inp)
+            log(f"{what} step {i + 1}/{steps} done")
+        self.torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    def free(self):
+        self.J.jet_model_free(self.model)
+
+
+def prefix_reuse(steps: int, unshared_steps: int) -> dict:
+    """Shared vs unshared evaluation of the dense 1.5B choice workload with
+    the same kernels (only the prefix sharing switched off)."""
+    r = Runner(REUSE_WORKLOAD, "f16", timing=False)
+    try:
+        inp = r.inputs(r.wl)
+        r.step(r.wl, inp)
+        ms_sh = 1e3 * r.timed(r.wl, inp, steps, "shared (reuse)") / steps
+        del inp
+        un = unshared_workload(r.wl)
+        uinp = r.inputs(un)
+        r.step(un, uinp)  # warm-up (workspace growth)
+        ms_un = 1e3 * r.timed(un, uinp, unshared_steps, "unshared (reuse)") / unshared_steps
+        del uinp
+    finally:
+        r.free()
+    return {"workload": REUSE_WORKLOAD, "dtype": "f16", "steps": steps, "unshared_steps": unshared_steps,
+            "shared_ms_per_step": round(ms_sh, 3), "unshared_ms_per_step": round(ms_un, 3),
+            "speedup": round(ms_un / ms_sh, 3)}
 
 
 def main() -> int:
@@ -138,15 +290,20 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="dense_1p5b_k4")
+    ap.add_argument("--workload", default="dense_27b_k10",
+                    help="default: the 27B-shape dense workload (the largest configuration on one GPU)")
     ap.add_argument("--dtype", choices=["f16", "f16p", "bf16"], default=None,
                     help="f16: bf16 weights held exactly as fp16, fp16 activations (one fp16 product per "
                          "multiply); f16p: f16 with (hi, lo) fp16 pairs on the attention side; bf16: bf16 "
                          "products over (hi, lo) bf16 activation pairs. Default: the fastest mode that meets "
                          "the tolerances on the workload (f16p on dense_27b_k10, else f16)")
     ap.add_argument("--unshared-steps", type=int, default=None,
-                    help="steps of unshared (per-candidate prefix) evaluation for the reuse speedup; "
+                    help="steps of unshared (per-candidate prefix) evaluation of the timed workload; "
                          "0 = skip; default 2 on dense_1p5b_k4, else 0")
+    ap.add_argument("--reuse-steps", type=int, default=3,
+                    help="shared steps of the dense 1.5B choice workload for its prefix-reuse speedup "
+                         "(with 2 unshared steps), run after the timed workload when that is another "
+                         "workload; 0 = skip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with HIP events")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -160,8 +317,6 @@ def main() -> int:
         return calibrate_copy()
 
     import torch
-    import jet_synth
-    from paper_2609_33874_amd import jet as J
 
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
@@ -170,62 +325,22 @@ def main() -> int:
     if args.dtype is None:
         args.dtype = DEFAULT_DTYPE.get(wname, "f16")
     if args.unshared_steps is None:
-        args.unshared_steps = 2 if wname == "dense_1p5b_k4" else 0
-    spec = jet_synth.WORKLOADS[wname]["model"]
-    t = time.perf_counter()
-    path = jet_synth.ensure_model(spec)
-    log(f"model file {path} ready in {time.perf_counter() - t:.1f}s")
-    wl = jet_synth.make_workload(wname)
-    mode = {"binary": J.JET_BINARY, "ordinal": J.JET_ORDINAL}.get(MODE_OF.get(wname, ""), J.JET_CHOICE)
-    Q, N = wl.n_questions, wl.n_candidates
+        args.unshared_steps = 2 if wname == REUSE_WORKLOAD else 0
+    r = Runner(wname, args.dtype, timing=not args.no_timing)
+    J, wl = r.J, r.wl
+    Q = wl.n_questions
     T_p = int(wl.prefix_offsets[-1])
     T_c = int(wl.cand_tok_offsets[-1])
-
-    dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream(dev)
-    flags = 0 if args.no_timing else J.JET_FLAG_KERNEL_TIMING
-    t = time.perf_counter()
-    jdt = {"f16": J.JET_F16, "f16p": J.JET_F16P, "bf16": J.JET_BF16}[args.dtype]
-    model = J.jet_model_load(path, dtype=jdt, device=0, hip_stream=stream.cuda_stream, flags=flags)
-    log(f"model loaded in {time.perf_counter() - t:.1f}s")
-
-    def make_inputs(w):
-        return (torch.from_numpy(w.prefix_tokens).to(dev), torch.from_numpy(w.cand_tokens).to(dev),
-                torch.empty(int(w.cand_tok_offsets[-1]), dtype=torch.float32, device=dev),
-                torch.empty(w.n_candidates, dtype=torch.float32, device=dev))
-
-    phase = {"prefill": 0.0, "score": 0.0, "decide": 0.0}
-
-    def step(w, inp):
-        d_pre, d_cand, o_tok, o_sum = inp
-        a = time.perf_counter()
-        p = J.jet_prefill_prefix(model, w.prefix_offsets, d_pre)
-        b = time.perf_counter()
-        J.jet_score_candidates(model, p, w.q_cand_offsets, w.cand_tok_offsets, d_cand, o_tok, o_sum)
-        c = time.perf_counter()
-        sums = o_sum.cpu().numpy()
-        J.jet_decide(mode, w.q_cand_offsets, sums)
-        d = time.perf_counter()
-        J.jet_prefix_free(p)
-        phase["prefill"] += b - a
-        phase["score"] += c - b
-        phase["decide"] += d - c
-
-    inp = make_inputs(wl)
+    inp = r.inputs(wl)
     for i in range(args.warmup):
-        step(wl, inp)
+        r.step(wl, inp)
         log(f"warmup step {i + 1}/{args.warmup} done")
-    J.jet_stats_reset(model)
-    for k in phase:
-        phase[k] = 0.0
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(wl, inp)
-        log(f"step {i + 1}/{args.steps} done")
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    stats = J.jet_stats_get(model)
+    J.jet_stats_reset(r.model)
+    for k in r.phase:
+        r.phase[k] = 0.0
+    elapsed = r.timed(wl, inp, args.steps, "timed")
+    phase = dict(r.phase)
+    stats = J.jet_stats_get(r.model)
     ms_step = 1e3 * elapsed / args.steps
     # evaluation utilities on the last step's scores (host; outside the timed
     # steps): equivalent labels and accuracy / gold NLL against seeded
@@ -280,6 +395,7 @@ def main() -> int:
         "scored_tokens_per_s": round(T_c * args.steps / elapsed, 1),
         "prefix_tokens_per_s": round(T_p * args.steps / phase["prefill"], 1),
         "phase_ms_per_step": {k: round(1e3 * v / args.steps, 2) for k, v in phase.items()},
+        "model_load_s": round(r.load_s, 1),
         "gemm_lmhead_mfma_frac": round(gemm_lm_frac, 4) if gemm_lm_frac else None,
         # candidate attention over the shared prefix: bytes of the stored K/V
         # (read once per question and KV head) + Q + O per second, vs HBM peak
@@ -290,29 +406,24 @@ def main() -> int:
     }
 
     if args.unshared_steps > 0:
-        pre, cands = [], []
-        for q in range(Q):
-            for y in wl.candidates(q):
-                pre.append(wl.prefix(q))
-                cands.append([y])
-        un = jet_synth.from_lists(pre, cands)
-        uinp = make_inputs(un)
-        step(un, uinp)  # warm-up (workspace growth)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        for i in range(args.unshared_steps):
-            step(un, uinp)
-            log(f"unshared step {i + 1}/{args.unshared_steps} done")
-        torch.cuda.synchronize()
-        ms_un = 1e3 * (time.perf_counter() - t1) / args.unshared_steps
+        un = unshared_workload(wl)
+        uinp = r.inputs(un)
+        r.step(un, uinp)  # warm-up (workspace growth)
+        ms_un = 1e3 * r.timed(un, uinp, args.unshared_steps, "unshared") / args.unshared_steps
         result["unshared_ms_per_step"] = round(ms_un, 3)
         result["prefix_reuse_speedup"] = round(ms_un / ms_step, 3)
         del uinp
-
-    J.jet_model_free(model)
+    del inp
+    r.free()
+    if wname != REUSE_WORKLOAD and args.reuse_steps > 0:
+        result["prefix_reuse"] = prefix_reuse(args.reuse_steps, 2)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the CPU")
-        result["cpu_baseline"] = cpu_baseline(path, wl)
+        P0 = len(wl.prefix(0))
+        if P0 * len(wl.candidates(0)) > 8000:   # one question is minutes of fp64 work
+            result["cpu_baseline"] = cpu_baseline_layers(r.path, wl)
+        else:
+            result["cpu_baseline"] = cpu_baseline(r.path, wl)
     print(json.dumps(result), flush=True)
     return 0
 

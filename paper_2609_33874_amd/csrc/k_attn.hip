@@ -11,10 +11,10 @@
 //     retained prefix (read-only, staged once per tile for all the slots),
 //     then the rows of its own candidate up to itself, and nothing of its
 //     siblings, so candidates stay isolated (Section 4.1). The own rows (at
-//     most m - 1) are walked per query in a fixed order with fp32 FMAs, so a
-//     candidate's score does not depend on where it sits in the batch:
-//     candidates with equal text get bitwise-equal scores and the fixed
-//     tie order decides between them (Section 3.3).
+//     most m - 1) are staged as extra tiles aligned to each candidate's first
+//     row, so a candidate's score does not depend on where it sits in the
+//     batch: candidates with equal text get bitwise-equal scores and the
+//     fixed tie order decides between them (Section 3.3).
 // Scores are computed transposed, S^T = K Q^T with 16x16x32 MFMAs, so each
 // lane owns one query column; the online softmax runs in base 2 and the
 // probabilities feed O^T += V^T P^T directly from registers. V is staged
@@ -185,12 +185,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int64_t ps = a.kp_ps;
   const T *kvbase_k = Kp + ((int64_t)it.kvh * a.s_pre + pslot) * HD;
   const T *kvbase_v = Vp + ((int64_t)it.kvh * a.s_pre + pslot) * HD;
-  auto issue_tile = [&](int kb, int nkt, uint4 (&kr)[NP][NKC], uint4 (&vr)[NP][NVB][4]) {
+  // loads of rows kb .. kb + nkt - 1 of a [rows][HD] K / V plane pair (plane stride pstride)
+  auto issue_tile = [&](const T *kbase_p, const T *vbase_p, int64_t pstride, int kb, int nkt) {
 #pragma unroll
     for (int i = 0; i < NKC; ++i) {
       const int ch = tid + i * 256, key = min(ch / CPR, nkt - 1), c = ch % CPR;
 #pragma unroll
-      for (int p = 0; p < NP; ++p) kr[p][i] = ld16(kvbase_k + p * ps + (int64_t)(kb + key) * HD + c * EPC);
+      for (int p = 0; p < NP; ++p) kreg[p][i] = ld16(kbase_p + p * pstride + (int64_t)(kb + key) * HD + c * EPC);
     }
 #pragma unroll
     for (int i = 0; i < NVB; ++i) {
@@ -199,16 +200,15 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       for (int p = 0; p < NP; ++p)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          vr[p][i][e] = ld16(kvbase_v + p * ps + (int64_t)(kb + min(4 * u + e, nkt - 1)) * HD + c * EPC);
+          vreg[p][i][e] = ld16(vbase_p + p * pstride + (int64_t)(kb + min(4 * u + e, nkt - 1)) * HD + c * EPC);
     }
   };
-  if (ntile > 0) issue_tile(0, min(KT, npre), kreg, vreg);
-
-  for (int tix = 0; tix < ntile; ++tix) {
-    const int kbase = tix * KT;
-    const int nk = min(KT, npre - kbase);
-    __syncthreads();
-    // K: 16-byte chunks, row-swizzled
+  // the loaded tile into LDS (keys nk .. KT - 1 zeroed): K as 16-byte
+  // chunks, row-swizzled; V transposed: a thread takes 4 keys x one 16-byte
+  // chunk of dims and writes each dim's 4 keys as one store; the 16 threads
+  // of a group take the 16 key quads of one chunk, so each store of the group
+  // fills one 128-byte row of Vt (distinct banks)
+  auto store_tile = [&](int nk) {
     const bool tile_full = nk == KT;  // uniform: no key of the tile to zero
 #pragma unroll
     for (int i = 0; i < NKC; ++i) {
@@ -223,10 +223,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         }
       }
     }
-    // V, transposed: a thread takes 4 keys x one 16-byte chunk of dims and
-    // writes each dim's 4 keys as one store; the 16 threads of a group take
-    // the 16 key quads of one chunk, so each store of the group fills one
-    // 128-byte row of Vt (distinct banks)
 #pragma unroll
     for (int i = 0; i < NVB; ++i) {
       const int bk = tid + i * 256, u = bk % (KT / 4), c = bk / (KT / 4);
@@ -244,14 +240,20 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         }
       }
     }
-    __syncthreads();
-    if (tix + 1 < ntile) issue_tile(kbase + KT, min(KT, npre - kbase - KT), kreg, vreg);
-
+  };
+  // Scores of the staged tile (keys 0 .. nk - 1), online softmax and the PV
+  // product. all_visible(qb): every key of the tile is visible to every
+  // query of the wave's block qb (uniform); visible(qb, key): key of the
+  // tile is visible to this lane's query of block qb. Groups of 16 keys past
+  // nk are skipped: their scores are masked and their products with the
+  // zeroed V rows add exact zeros.
+  auto tile_compute = [&](int nk, auto all_visible, auto visible) {
     f32x4 s[QB][4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) s[qb][kb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      if (kb * 16 >= nk) continue;
       const int key = kb * 16 + (lane & 15);
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
@@ -274,8 +276,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = -INFINITY;
-      // tiles every key of which every query of the wave's block sees skip the mask
-      if (__all(tile_full && (MODE != 0 || kbase + KT - 1 <= qi[qb]))) {
+      if (all_visible(qb)) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -288,10 +289,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int key = kb * 16 + 4 * g + e;
-            bool vis = key < nk;
-            if (MODE == 0) vis = vis && (kbase + key <= qi[qb]);
-            const float z = vis ? s[qb][kb][e] * scale2 : -INFINITY;
+            const float z = visible(qb, kb * 16 + 4 * g + e) ? s[qb][kb][e] * scale2 : -INFINITY;
             s[qb][kb][e] = z;
             mx = fmaxf(mx, z);
           }
@@ -299,8 +297,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       // Every query sees key 0 in the first tile (mode 0) or the whole prefix
-      // (mode 1), so m_new is finite: exp2 of the (<= 0) differences directly,
-      // with exp2(-inf) = 0 for masked keys and for the initial m_run.
+      // (mode 1, before any own-key tile), so m_new is finite: exp2 of the
+      // (<= 0) differences directly, with exp2(-inf) = 0 for masked keys and
+      // for the initial m_run. A tile with no key visible to a query leaves
+      // its m_run, l_run and acc bitwise unchanged (alpha = 1, p = 0).
       const float m_new = fmaxf(m_run[qb], mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
       float p[4][4];
@@ -333,6 +333,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm) {
+      if (mm * 32 >= nk) continue;
 #pragma unroll
       for (int db = 0; db < HD / 16; ++db) {
         const int d = db * 16 + (lane & 15);
@@ -349,59 +350,59 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         }
       }
     }
+  };
+
+  if (ntile > 0) issue_tile(kvbase_k, kvbase_v, ps, 0, min(KT, npre));
+  for (int tix = 0; tix < ntile; ++tix) {
+    const int kbase = tix * KT;
+    const int nk = min(KT, npre - kbase);
+    __syncthreads();
+    store_tile(nk);
+    __syncthreads();
+    if (tix + 1 < ntile) issue_tile(kvbase_k, kvbase_v, ps, kbase + KT, min(KT, npre - kbase - KT));
+    const bool tile_full = nk == KT;
+    // tiles every key of which every query of the wave's block sees skip the mask
+    tile_compute(nk, [&](int qb) { return __all(tile_full && (MODE != 0 || kbase + KT - 1 <= qi[qb])); },
+                 [&](int qb, int key) { return key < nk && (MODE != 0 || kbase + key <= qi[qb]); });
+  }
+
+  if constexpr (MODE == 1) {
+    // Own keys of the candidates: the item's rows r_first .. r_last are
+    // consecutive body rows of the call, ordered by candidate, then
+    // position. Each candidate's keys are staged in tiles that start at its
+    // first body row (key j of the tile = its row first + 64 i + j), and a
+    // query sees only the tiles of its own candidate (rows up to itself):
+    // the tile a query reads and the position of each key in it do not
+    // depend on which other candidates share the batch or the item, so a
+    // candidate rounds alike alone and among its siblings (Section 3.3: equal
+    // text, equal score). Tiles of other candidates leave a query unchanged.
+    if (a.s_suf > 0) {
+      const int r_first = qrow0 + it.slot0 / G;
+      const int r_last = qrow0 + (it.slot0 + it.nslots - 1) / G;
+      const T *kown = (const T *)a.Ks + (int64_t)it.kvh * a.s_suf * HD;
+      const T *vown = (const T *)a.Vs + (int64_t)it.kvh * a.s_suf * HD;
+      int first[QB];  // first body row of this lane's query's candidate
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) first[qb] = valid[qb] ? row[qb] - my_t[qb] + 1 : -1;
+      int cs = r_first - a.row_t[r_first] + 1;
+      while (cs <= r_last) {
+        const int cend = min(cs + a.row_n[cs] - 1, r_last);  // keys after r_last have no query here
+        for (int ts = cs; ts <= cend; ts += KT) {
+          const int nk = min(KT, cend - ts + 1);
+          __syncthreads();
+          issue_tile(kown, vown, a.ks_ps, ts, nk);
+          store_tile(nk);
+          __syncthreads();
+          tile_compute(nk, [&](int) { return false; },
+                       [&](int qb, int key) { return key < nk && first[qb] == cs && ts + key <= row[qb]; });
+        }
+        cs += a.row_n[cs];
+      }
+    }
   }
 
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    if constexpr (MODE == 1) {
-      // own rows of the candidate: row - my_t + 1 .. row of the call's K / V
-      // (rows are ordered by candidate, then position). Lane group g holds the
-      // query dims 32 ks + 8 g + j (score) and the output dims 16 db + 4 g + e.
-      int tmax = valid[qb] ? my_t[qb] : 0;
-      for (int o = 1; o < 64; o <<= 1) tmax = max(tmax, __shfl_xor(tmax, o));
-      const T *Kc = (const T *)a.Ks + (int64_t)it.kvh * a.s_suf * HD;
-      const T *Vc = (const T *)a.Vs + (int64_t)it.kvh * a.s_suf * HD;
-      for (int i = 0; i < tmax; ++i) {
-        const bool act = valid[qb] && i < my_t[qb];
-        const int64_t krow = (int64_t)row[qb] - my_t[qb] + 1 + i;
-        float part = 0.0f;
-        if (act) {
-          const T *kr = Kc + krow * HD;
-#pragma unroll
-          for (int ks = 0; ks < HD / 32; ++ks)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const int d = ks * 32 + g * 8 + j;
-              float kv = to_f<T>(kr[d]);
-              if constexpr (PAIR) kv += to_f<T>(kr[a.ks_ps + d]);
-              float qv = to_f<T>(reinterpret_cast<const T *>(&qf[qb][0][ks].v)[j]);
-              if constexpr (PAIR) qv += to_f<T>(reinterpret_cast<const T *>(&qf[qb][NP - 1][ks].v)[j]);
-              part += qv * kv;
-            }
-        }
-        part += __shfl_xor(part, 16);
-        part += __shfl_xor(part, 32);
-        if (act) {
-          const float z = part * scale2;
-          const float m_new = fmaxf(m_run[qb], z);
-          const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);  // arguments <= 0
-          const float pz = __builtin_amdgcn_exp2f(z - m_new);
-          l_run[qb] = l_run[qb] * alpha + (g == 0 ? pz : 0.0f);
-          const T *vr = Vc + krow * HD;
-#pragma unroll
-          for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int d = db * 16 + 4 * g + e;
-              float vv = to_f<T>(vr[d]);
-              if constexpr (PAIR) vv += to_f<T>(vr[a.ks_ps + d]);
-              acc[qb][db][e] = acc[qb][db][e] * alpha + pz * vv;
-            }
-          m_run[qb] = m_new;
-        }
-      }
-    }
-
     float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16);
     l_tot += __shfl_xor(l_tot, 32);
     if (valid[qb]) {

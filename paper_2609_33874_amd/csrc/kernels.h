@@ -68,8 +68,10 @@ struct AttnQuestions {
   const int32_t *suf_len;
 };
 // mode 0: causal prefix attention (query i of a question sees prefix keys 0..i).
-// mode 1: candidate attention: every prefix key, plus the suffix keys j with
-//         row_c[j] == row_c[i] and row_t[j] <= row_t[i].
+// mode 1: candidate attention: every prefix key, plus the suffix keys of its
+//         own candidate up to itself: rows i - row_t[i] + 1 .. i of the call's
+//         K / V (rows are ordered by candidate, then position; row_n[i] is the
+//         number of body rows of row i's candidate).
 // pair: Q, K, V are (hi, lo) bf16 planes (the lo plane at +q_ps / +kp_ps /
 // +ks_ps elements) and O rows hold [hi (Hq hd) | lo (Hq hd)].
 struct AttnArgs {
@@ -83,7 +85,7 @@ struct AttnArgs {
   int64_t s_pre, kp_ps;
   const void *Ks, *Vs;  // own-suffix keys of the call [planes][Hkv][S_suf][hd]
   int64_t s_suf, ks_ps;
-  const int32_t *row_c, *row_t;  // per call row (candidate mode)
+  const int32_t *row_n, *row_t;  // per call row (candidate mode)
   AttnQuestions qs;
   const AttnItem *items;
   int n_items;

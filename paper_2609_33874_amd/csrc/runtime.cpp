@@ -563,7 +563,7 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
 
 // Q: [planes][R][Hq][hd]; O: [R][planes * Hq * hd]; caches [planes][Hkv][S][hd].
 Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void *O, const void *Kp, const void *Vp,
-                     int64_t s_pre, const void *Ks, const void *Vs, int64_t s_suf, const int32_t *row_c,
+                     int64_t s_pre, const void *Ks, const void *Vs, int64_t s_suf, const int32_t *row_n,
                      const int32_t *row_t, int cls = -1) {
   if (pl.a.n_items == 0) return Status::ok();
   const ModelHeader &h = m->h;
@@ -580,7 +580,7 @@ Status run_attention(jet_model *m, AttnPlan &pl, const void *Q, int64_t R, void 
   a.Vs = Vs;
   a.s_suf = s_suf;
   a.ks_ps = h.n_kv_heads * s_suf * h.head_dim;
-  a.row_c = row_c;
+  a.row_n = row_n;
   a.row_t = row_t;
   KTimer t(m, cls >= 0 ? cls : a.mode == 0 ? JET_K_ATTN_PREFIX : JET_K_ATTN_CAND, pl.flops, pl.bytes);
   LAUNCH(jetk::launch_attention(m->kdt, a, m->st));
@@ -1081,7 +1081,13 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
   int64_t *d_cto;
   TRY(upload(m, "row_pos", L.row_pos, &d_rpos));
   TRY(upload(m, "row_tok", L.row_tok, &d_rtok));
-  TRY(upload(m, "row_c", L.row_c, &d_rc));
+  // body rows of each row's candidate (the candidate attention's own-key tiles)
+  std::vector<int32_t> row_n((size_t)L.n_rows);
+  for (int64_t r = 0; r < L.n_rows; ++r) {
+    const int64_t c = L.row_c[(size_t)r];
+    row_n[(size_t)r] = (int32_t)(cto[c + 1] - cto[c] - 1);
+  }
+  TRY(upload(m, "row_n", row_n, &d_rc));
   TRY(upload(m, "row_t", L.row_t, &d_rt));
   TRY(upload(m, "lm_row", L.lm_row, &d_lm));
   std::vector<int64_t> cto_v(cto, cto + N + 1);
