@@ -183,6 +183,34 @@ int jet_score_candidates(jet_model *model, const jet_prefix *prefix,
                          const int32_t *cand_tokens, float *out_token_logprob,
                          float *out_cand_sum);
 
+/* Size of the fixed per-device scratch of jet_score_candidates_noalloc. */
+#define JET_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * jet_score_candidates_noalloc - jet_score_candidates for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc). Same arguments, results and
+ * errors as jet_score_candidates, computed by the same kernels; no call of it
+ * allocates or frees device memory. Its work buffers (token staging, row
+ * tables, activations, attention caches of the candidate rows, log-sum-exp
+ * partials) are carved from a fixed device array of
+ * JET_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it has loaded
+ * a model on, until the process ends; candidates run in waves of whole
+ * candidates sized to fit it (at most the model's wave_token_budget rows).
+ * Limits: JET_E_CAPACITY when the call's token tables and one wave holding
+ * its longest candidate do not fit the scratch (large mixture-of-experts
+ * models need more than it holds). The scratch is shared by every call on
+ * one GPU and keeps the last call's contents: calls that overlap on one GPU
+ * (other threads, other models on the same device) race and must be
+ * serialised by the caller. It still synchronises the model's stream before
+ * returning, like every call here. Kernel timing (JET_FLAG_KERNEL_TIMING) is
+ * not recorded for these calls.
+ */
+int jet_score_candidates_noalloc(jet_model *model, const jet_prefix *prefix,
+                                 const int64_t *q_cand_offsets, const int64_t *cand_tok_offsets,
+                                 const int32_t *cand_tokens, float *out_token_logprob,
+                                 float *out_cand_sum);
+
 /*
  * jet_decide - turn candidate scores into decisions (Section 3.2 Eq. 4,
  * Section 3.3 Eq. 5). Pure host function in fp64; touches no device.

@@ -57,8 +57,24 @@ void dfree(jet_model *m, void *p, size_t bytes) {
   m->bytes_used -= std::min(m->bytes_used, bytes == 0 ? (size_t)256 : bytes);
 }
 
-// Grow-only named workspace buffer.
+// Grow-only named workspace buffer; while the model has an arena (the
+// allocation-free entry point), a buffer carved from it instead.
 Status ws(jet_model *m, const char *name, size_t bytes, void **p) {
+  if (m->arena) {
+    auto it = m->arena_map.find(name);
+    if (it != m->arena_map.end() && it->second.second >= bytes) {
+      *p = m->arena + it->second.first;
+      return Status::ok();
+    }
+    const size_t off = (m->arena_top + 255) & ~(size_t)255;
+    if (off > m->arena_cap || bytes > m->arena_cap - off)
+      return Status::err(JET_E_CAPACITY, std::string("scratch of ") + std::to_string(m->arena_cap) +
+                                             " bytes exhausted (buffer " + name + ")");
+    m->arena_map[name] = {off, bytes};
+    m->arena_top = off + bytes;
+    *p = m->arena + off;
+    return Status::ok();
+  }
   DevBuf &b = m->ws[name];
   if (b.bytes < bytes) {
     dfree(m, b.p, b.bytes);
@@ -108,7 +124,7 @@ struct KTimer {
     m->stats.kernel_launches[cls]++;
     m->stats.kernel_flops[cls] += flops;
     m->stats.kernel_bytes[cls] += bytes;
-    if (m->flags & JET_FLAG_KERNEL_TIMING) {
+    if ((m->flags & JET_FLAG_KERNEL_TIMING) && !m->arena) {
       a = get();
       b = get();
       (void)hipEventRecord(a, m->st);
@@ -361,6 +377,10 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   m->esz = m->kdt == 1 ? 4 : 2;
   m->max_ctx = (o && o->max_ctx > 0) ? o->max_ctx : h.max_ctx;
   HIPC(hipSetDevice(m->device));
+  // the device address of the allocation-free entry point's scratch, looked
+  // up once per device (its failure only disables that entry point)
+  m->scratch_status = noalloc_scratch_init(m->device);
+  if (m->scratch_status != hipSuccess) (void)hipGetLastError();
   Loader L{m, {}};
   if (m->kdt == 2) {
     TRY(dmalloc(m, sizeof(unsigned long long), (void **)&L.inexact));
@@ -1056,6 +1076,53 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
 // candidate scoring
 // ---------------------------------------------------------------------------
 
+// Drops the arena buffers carved since the call-level mark (a new wave).
+void arena_reset(jet_model *m) {
+  for (auto it = m->arena_map.begin(); it != m->arena_map.end();) {
+    if (it->second.first >= m->arena_mark) it = m->arena_map.erase(it);
+    else ++it;
+  }
+  m->arena_top = m->arena_mark;
+}
+
+// Upper bound of the work-buffer bytes of one scoring wave: per body row,
+// and fixed (mixture-of-experts segment padding, alignment of each buffer).
+// Mirrors the workspace requests of the scoring path (wave buffers, the
+// candidate rows' K/V, the final-norm rows, log-sum-exp partials, attention
+// work items, delta-rule and expert buffers).
+void wave_bytes_bound(const jet_model *m, double *per_row, double *fixed) {
+  const ModelHeader &h = m->h;
+  const double d = (double)h.d, esz = (double)m->esz;
+  const double pe = m->np * esz, pa = m->anp * esz;
+  const double nqkv = (double)((h.n_heads + 2 * h.n_kv_heads) * h.head_dim), hq = (double)(h.n_heads * h.head_dim);
+  int tps = 1, nsplit = 1;
+  jetk::lmhead_plan(m->kdt, (int)h.vocab, 1, &tps, &nsplit);
+  double r = d * 4 + nqkv * 4 + d * std::max(pe, pa) + 2 * hq * pa + (double)h.ffn * pe;  // wave buffers
+  r += 2.0 * (double)(h.n_kv_heads * h.head_dim) * esz * m->anp;                           // own K / V
+  r += d * esz * m->np + 4;                                                                  // final-norm rows, lse
+  r += 2.0 * nsplit * 4;                                                                     // LM-head partials
+  r += 40.0 * (double)h.n_kv_heads + 28;  // attention items and per-question tables (at most one question per row)
+  double f = 64.0 * 256;                  // alignment of every buffer
+  if (h.hybrid) {
+    const double H = (double)h.gdn_heads, dk = (double)h.gdn_dk, dv = (double)h.gdn_dv;
+    int64_t n_in = 0;
+    for (const Layer &ly : m->layers) n_in = std::max(n_in, ly.n_in);
+    r += (double)n_in * 4 + 2 * H * dk * 4 + 2 * H * dv * 4 + 2 * H * 4 + H * dv * esz * m->np + 12 + 16;
+  }
+  if (h.n_experts) {
+    const double k = (double)h.top_k, E = (double)h.n_experts, Fe = (double)h.moe_ffn, Fs = (double)h.shared_ffn;
+    const double bm = (double)std::max(jetk::gemm_group_rows(m->kdt, 0), jetk::gemm_group_rows(m->kdt, 1));
+    int64_t n_router = 0;
+    for (const Layer &ly : m->layers) n_router = std::max(n_router, ly.n_router);
+    r += (double)n_router * 4 + 3 * k * 4 + (k / bm) * 4 + 2 * E * 4 * k / jetk::kMoeChunk;
+    r += k * (2 * d + Fe) * esz;          // routed rows: gathered input, hidden, output
+    r += 4 + Fs * esz + d * 4;            // shared expert
+    f += (E * bm + bm) * (2 * d + Fe) * esz + 4 * (E + 2) + 2 * E * 4;
+  }
+  *per_row = r;
+  *fixed = f;
+}
+
 Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_t *cto, const int32_t *tokens,
              float *out_tok, float *out_sum) {
   const ModelHeader &h = m->h;
@@ -1103,10 +1170,30 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
   auto row0 = [&](int64_t c) { return c < N ? (int64_t)L.cand_row0[(size_t)c] : L.n_rows; };
   route_rows_begin(m, 1, L.n_rows);
 
+  int64_t budget = m->wave_budget;
+  if (m->arena) {
+    // allocation-free call: the buffers above stay for the whole call; every
+    // wave's buffers are carved after them, in waves sized to fit
+    m->arena_mark = m->arena_top;
+    double per_row = 0, fixed = 0;
+    wave_bytes_bound(m, &per_row, &fixed);
+    const double room = (double)m->arena_cap - (double)m->arena_mark - fixed;
+    const int64_t fit = room > per_row ? (int64_t)(room / per_row) : 0;
+    int64_t longest = 0;
+    for (int64_t c = 0; c < N; ++c) longest = std::max<int64_t>(longest, cto[c + 1] - cto[c] - 1);
+    if (fit < std::max<int64_t>(longest, 1))
+      return Status::err(JET_E_CAPACITY, "the scratch of " + std::to_string(m->arena_cap) +
+                                             " bytes holds the call's tables and " + std::to_string(fit) +
+                                             " candidate rows per wave; the longest candidate needs " +
+                                             std::to_string(longest));
+    budget = budget > 0 ? std::min(budget, fit) : fit;
+  }
+
   int64_t c0 = 0;
   while (c0 < N) {
+    if (m->arena) arena_reset(m);
     int64_t c1 = c0 + 1;
-    while (c1 < N && (m->wave_budget <= 0 || row0(c1 + 1) - row0(c0) <= m->wave_budget)) ++c1;
+    while (c1 < N && (budget <= 0 || row0(c1 + 1) - row0(c0) <= budget)) ++c1;
     const int64_t r0 = row0(c0), r1 = row0(c1), R = r1 - r0;
     const int64_t t0 = cto[c0], t1 = cto[c1];
     void *f_body = nullptr;
@@ -1303,6 +1390,33 @@ extern "C" int jet_score_candidates(jet_model *model, const jet_prefix *prefix, 
   Status s = score(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens, out_token_logprob, out_cand_sum);
   if (!s) {
     (void)hipStreamSynchronize(model->st);
+    drain_timers(model);
+    return fail(s);
+  }
+  return JET_OK;
+}
+
+extern "C" int jet_score_candidates_noalloc(jet_model *model, const jet_prefix *prefix,
+                                            const int64_t *q_cand_offsets, const int64_t *cand_tok_offsets,
+                                            const int32_t *cand_tokens, float *out_token_logprob,
+                                            float *out_cand_sum) {
+  clear_error();
+  if (!model || !prefix) return fail(Status::err(JET_E_INVALID, "model or prefix is NULL"));
+  if (hipSetDevice(model->device) != hipSuccess) return fail(Status::err(JET_E_DEVICE, "hipSetDevice failed"));
+  void *scratch = noalloc_scratch(model->device);
+  if (model->scratch_status != hipSuccess || !scratch)
+    return fail(Status::err(JET_E_DEVICE, std::string("no scratch on this device: ") +
+                                              hipGetErrorString(model->scratch_status)));
+  model->arena = (char *)scratch;
+  model->arena_cap = kNoallocScratchBytes;
+  model->arena_top = model->arena_mark = 0;
+  model->arena_map.clear();
+  Status s = score(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens, out_token_logprob, out_cand_sum);
+  if (!s) (void)hipStreamSynchronize(model->st);
+  model->arena = nullptr;
+  model->arena_cap = model->arena_top = model->arena_mark = 0;
+  model->arena_map.clear();
+  if (!s) {
     drain_timers(model);
     return fail(s);
   }

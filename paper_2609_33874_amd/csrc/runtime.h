@@ -10,6 +10,7 @@
 #include "host.h"
 #include "kernels.h"
 #include "model_file.h"
+#include "noalloc.h"
 
 struct jet_model;
 struct jet_prefix;
@@ -94,6 +95,14 @@ struct jet_model {
   int rt_which = -1;
   int64_t rt_layer = 0;
   std::vector<int64_t> rt_rowmap;
+  // jet_score_candidates_noalloc: while `arena` is set, work buffers are
+  // carved from it (a fixed device scratch) instead of the growable workspace:
+  // buffer name -> (offset, bytes); entries at or past `arena_mark` are
+  // dropped at every scoring wave
+  char *arena = nullptr;
+  size_t arena_cap = 0, arena_top = 0, arena_mark = 0;
+  std::map<std::string, std::pair<size_t, size_t>> arena_map;
+  hipError_t scratch_status = hipSuccess;  // lookup of the device's scratch at load
 };
 
 struct jet_prefix {

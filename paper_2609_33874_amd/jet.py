@@ -20,12 +20,13 @@ JET_BF16, JET_FP32, JET_BF16_SINGLE, JET_F16, JET_F16P = 0, 1, 2, 3, 4
 JET_CHOICE, JET_BINARY, JET_ORDINAL = 0, 1, 2
 JET_FLAG_KERNEL_TIMING = 1
 JET_FLAG_RECORD_ROUTES = 2
+JET_NOALLOC_SCRATCH_BYTES = 64 << 20
 KERNEL_CLASSES = ["gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "lmhead", "attn_prefix",
                   "attn_cand", "gdn", "other"]
 ERROR_NAMES = {1: "JET_E_INVALID", 2: "JET_E_CAPACITY", 3: "JET_E_OOM", 4: "JET_E_DEVICE", 5: "JET_E_IO"}
 
 # every symbol include/jet.h declares
-EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_score_candidates", "jet_decide",
+EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_score_candidates", "jet_score_candidates_noalloc", "jet_decide",
            "jet_answer_classes", "jet_evaluate", "jet_candidate_layout", "jet_stats_get", "jet_stats_reset", "jet_model_info",
            "jet_routes_get", "jet_prefix_free", "jet_model_free", "jet_last_error"]
 
@@ -73,6 +74,7 @@ def lib() -> ctypes.CDLL:
         L.jet_model_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(jet_load_opts), ctypes.POINTER(P)]
         L.jet_prefill_prefix.argtypes = [P, I32, P, P, ctypes.POINTER(P)]
         L.jet_score_candidates.argtypes = [P, P, P, P, P, P, P]
+        L.jet_score_candidates_noalloc.argtypes = [P, P, P, P, P, P, P]
         L.jet_decide.argtypes = [I32, I32, P, P, P, P, P]
         L.jet_answer_classes.argtypes = [I32, P, P, P, P]
         L.jet_evaluate.argtypes = [I32, P, P, P, P, P, P, P, P]
@@ -136,7 +138,7 @@ def jet_prefill_prefix(model, prefix_offsets, prefix_tokens):
 
 
 def jet_score_candidates(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens,
-                         out_token_logprob=True, out_cand_sum=None):
+                         out_token_logprob=True, out_cand_sum=None, _entry="jet_score_candidates"):
     """Returns (token log-probs or None, candidate sums). Pass torch tensors as
     outputs to have the library write them in place (host or device)."""
     qo, k1 = _ptr(q_cand_offsets, np.int64)
@@ -156,8 +158,16 @@ def jet_score_candidates(model, prefix, q_cand_offsets, cand_tok_offsets, cand_t
         raise TypeError("out_cand_sum must be a contiguous float32 array")
     if isinstance(out_token_logprob, np.ndarray) and k4 is not out_token_logprob:
         raise TypeError("out_token_logprob must be a contiguous float32 array")
-    _check(lib().jet_score_candidates(model, prefix, qo, co, ct, ot, os_))
+    _check(getattr(lib(), _entry)(model, prefix, qo, co, ct, ot, os_))
     return out_token_logprob, out_cand_sum
+
+
+def jet_score_candidates_noalloc(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens,
+                                 out_token_logprob=True, out_cand_sum=None):
+    """jet_score_candidates with every work buffer in the library's fixed
+    per-device scratch (no device allocation); same arguments and results."""
+    return jet_score_candidates(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens,
+                                out_token_logprob, out_cand_sum, _entry="jet_score_candidates_noalloc")
 
 
 def jet_decide(mode: int, q_cand_offsets, cand_sum):
