@@ -527,12 +527,23 @@ Status plan_attention(jet_model *m, int mode, const QDesc &qd, const char *tag, 
   const int G = (int)(h.n_heads / h.n_kv_heads);
   std::vector<jetk::AttnItem> items;
   double pairs = 0;
-  // Prefix attention: 128-slot items (two query blocks per wave) where the
-  // kernel supports them. Candidate attention: 64-slot items always, so that
-  // a candidate runs the same kernel (and rounds alike) whatever batch it is
-  // in, and the few query slots a question's candidates have (often well
-  // under 64 per KV head) do not leave most of an item idle.
-  const int block = mode == 0 && jetk::attn_slots_per_item(m->kdt, m->apair) >= 128 ? 128 : 64;
+  // 128-slot items (two query blocks per wave: each staged tile and each
+  // K/V fragment read serves twice the queries) where the kernel supports
+  // them: always for the prefix, and for candidates when their questions
+  // average at least 96 query slots per KV head (few slots would leave most
+  // of a 128-slot item idle). A query's arithmetic is the same in either
+  // item size, so a candidate rounds alike whatever batch it is in.
+  int block = 64;
+  if (jetk::attn_slots_per_item(m->kdt, m->apair) >= 128) {
+    if (mode == 0) {
+      block = 128;
+    } else {
+      double slots = 0, nq = 0;
+      for (auto n : qd.nrows)
+        if (n > 0) slots += (double)G * n, nq += 1;
+      if (nq > 0 && slots >= 96.0 * nq) block = 128;
+    }
+  }
   build_items(qd, G, (int)h.n_kv_heads, mode == 0, block, &items, &pairs);
   // Longest work first: the dispatcher hands out workgroups in order, so long
   // items no longer run alone at the end (an item's result does not depend
