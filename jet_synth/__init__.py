@@ -23,6 +23,13 @@ a list of ``{name, dtype, shape, offset, nbytes}``. Matrices use the
 ``[out_features, in_features]`` convention. Norm gains, ``A_log`` and
 ``dt_bias`` are stored as f32 whatever the matrix dtype is.
 
+Block-quantized models (``dtype`` "q8"): every matrix whose last dimension
+is a multiple of 32 is stored as int8 values q [rows][cols] followed by one
+int8 exponent per block of 32 consecutive values of a row, e [rows][cols/32];
+the weight is q * 2^e (|q| <= 127). The exponent of a block is the smallest e
+with max|w| <= 127 * 2^e over the block's values w, and q = rint(w / 2^e).
+Other tensors keep bf16 (matrices) or f32 (norm gains, A_log, dt_bias).
+
 Random numbers: every tensor is split into fixed chunks of ``CHUNK`` elements;
 chunk ``j`` of tensor ``name`` is drawn from a Philox-4x64 counter-based
 stream keyed on ``(seed, crc32(name) << 32 | j)`` as standard normals in
@@ -43,6 +50,7 @@ from dataclasses import dataclass
 import numpy as np
 
 MAGIC = b"JETMDL01"
+QBLOCK = 32  # values per quantization block of a "q8" matrix
 ALIGN = 4096
 CHUNK = 1 << 22
 # Sampling seed of the paper's experimental protocol (Appendix A); reused here
@@ -122,6 +130,21 @@ MODEL_SPECS: dict[str, dict] = {
                            n_heads=4, n_kv_heads=2, head_dim=16, ffn=32,
                            vocab=512, n_experts=4, top_k=2, moe_ffn=32,
                            shared_ffn=32, max_ctx=4096),
+    # Block-quantized (int8 blocks of 32 with power-of-two scales) dense
+    # decoders: the small GQA shape, the 1.5B and the 27B shapes.
+    "small_gqa_q8": dict(arch="dense", dtype="q8", d_model=256, n_layers=2,
+                         n_heads=6, n_kv_heads=2, head_dim=128, ffn=768,
+                         vocab=3000, max_ctx=8192),
+    "dense_1p5b_q8": dict(arch="dense", dtype="q8", d_model=1536, n_layers=28,
+                          n_heads=12, n_kv_heads=2, head_dim=128, ffn=8960,
+                          vocab=151936, max_ctx=8192),
+    "dense_27b_q8": dict(arch="dense", dtype="q8", d_model=5120, n_layers=64,
+                         n_heads=40, n_kv_heads=8, head_dim=128, ffn=17408,
+                         vocab=151936, max_ctx=8192),
+    # Micro quantized decoder for oracle self-checks on the CPU.
+    "micro_q8": dict(arch="dense", dtype="q8", d_model=64, n_layers=2,
+                     n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
+                     vocab=512, max_ctx=4096),
     # Micro hybrid for oracle self-checks on the CPU: L=4, d=64.
     "micro_hybrid_fp32": dict(arch="hybrid", dtype="f32", d_model=64, n_layers=4,
                               n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
@@ -152,47 +175,55 @@ def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
     """
     s = full_spec(spec)
     d, V, F = s["d_model"], s["vocab"], s["ffn"]
-    mt = s["dtype"]
-    out = [("tok_embed", mt, (V, d), "normal")]
+    q8 = s["dtype"] == "q8"
+    out = []
+
+    def mat(name, shape, init="normal"):
+        dt = ("q8" if shape[-1] % QBLOCK == 0 else "bf16") if q8 else s["dtype"]
+        out.append((name, dt, tuple(shape), init))
+
+    mt = "bf16" if q8 else s["dtype"]
+    mat("tok_embed", (V, d))
     for i, lt in enumerate(s["layer_types"]):
         p = f"blk.{i}."
         out.append((p + "attn_norm", "f32", (d,), "ones"))
         if lt == "attn":
             hq, hkv, hd = s["n_heads"], s["n_kv_heads"], s["head_dim"]
-            out += [(p + "wq", mt, (hq * hd, d), "normal"),
-                    (p + "wk", mt, (hkv * hd, d), "normal"),
-                    (p + "wv", mt, (hkv * hd, d), "normal"),
-                    (p + "wo", mt, (d, hq * hd), "normal")]
+            mat(p + "wq", (hq * hd, d))
+            mat(p + "wk", (hkv * hd, d))
+            mat(p + "wv", (hkv * hd, d))
+            mat(p + "wo", (d, hq * hd))
         else:
             H, dk, dv, kc = s["gdn_heads"], s["gdn_dk"], s["gdn_dv"], s["conv_kernel"]
-            out += [(p + "gdn_wq", mt, (H * dk, d), "normal"),
-                    (p + "gdn_wk", mt, (H * dk, d), "normal"),
-                    (p + "gdn_wv", mt, (H * dv, d), "normal"),
-                    (p + "gdn_wz", mt, (H * dv, d), "normal"),
-                    (p + "gdn_wb", mt, (H, d), "normal"),
-                    (p + "gdn_wa", mt, (H, d), "normal"),
-                    (p + "gdn_conv", mt, (2 * H * dk + H * dv, kc), "normal"),
-                    (p + "gdn_A_log", "f32", (H,), "zeros"),
+            mat(p + "gdn_wq", (H * dk, d))
+            mat(p + "gdn_wk", (H * dk, d))
+            mat(p + "gdn_wv", (H * dv, d))
+            mat(p + "gdn_wz", (H * dv, d))
+            mat(p + "gdn_wb", (H, d))
+            mat(p + "gdn_wa", (H, d))
+            out.append((p + "gdn_conv", mt, (2 * H * dk + H * dv, kc), "normal"))
+            out += [(p + "gdn_A_log", "f32", (H,), "zeros"),
                     (p + "gdn_dt_bias", "f32", (H,), "zeros"),
-                    (p + "gdn_norm", "f32", (dv,), "ones"),
-                    (p + "gdn_wo", mt, (d, H * dv), "normal")]
+                    (p + "gdn_norm", "f32", (dv,), "ones")]
+            mat(p + "gdn_wo", (d, H * dv))
         out.append((p + "ffn_norm", "f32", (d,), "ones"))
         if s["n_experts"] == 0:
-            out += [(p + "w_gate", mt, (F, d), "normal"),
-                    (p + "w_up", mt, (F, d), "normal"),
-                    (p + "w_down", mt, (d, F), "normal")]
+            mat(p + "w_gate", (F, d))
+            mat(p + "w_up", (F, d))
+            mat(p + "w_down", (d, F))
         else:
             E, Fe, Fs = s["n_experts"], s["moe_ffn"], s["shared_ffn"]
-            out += [(p + "moe_router", mt, (E, d), "normal"),
-                    (p + "moe_gate", mt, (E, Fe, d), "normal"),
-                    (p + "moe_up", mt, (E, Fe, d), "normal"),
-                    (p + "moe_down", mt, (E, d, Fe), "normal")]
+            mat(p + "moe_router", (E, d))
+            mat(p + "moe_gate", (E, Fe, d))
+            mat(p + "moe_up", (E, Fe, d))
+            mat(p + "moe_down", (E, d, Fe))
             if Fs:
-                out += [(p + "shared_router", mt, (1, d), "normal"),
-                        (p + "shared_gate", mt, (Fs, d), "normal"),
-                        (p + "shared_up", mt, (Fs, d), "normal"),
-                        (p + "shared_down", mt, (d, Fs), "normal")]
-    out += [("final_norm", "f32", (d,), "ones"), ("lm_head", mt, (V, d), "normal")]
+                mat(p + "shared_router", (1, d))
+                mat(p + "shared_gate", (Fs, d))
+                mat(p + "shared_up", (Fs, d))
+                mat(p + "shared_down", (d, Fs))
+    out.append(("final_norm", "f32", (d,), "ones"))
+    mat("lm_head", (V, d))
     return out
 
 
@@ -215,8 +246,42 @@ def _f32_to_bf16_rne(x: np.ndarray, out: np.ndarray) -> None:
     out[:] = t
 
 
+def quantize_q8(val: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Blocks of QBLOCK float32 values -> (int8 q, int8 exponent per block):
+    the smallest e with max|w| <= 127 * 2^e, q = rint(w / 2^e)."""
+    blocks = np.asarray(val, np.float32).reshape(-1, QBLOCK)
+    amax = np.abs(blocks).max(axis=1).astype(np.float64)
+    m, x = np.frexp(amax / 127.0)          # amax / 127 = m 2^x, m in [0.5, 1)
+    e = np.where(m == 0.5, x - 1, x)       # ceil(log2(amax / 127))
+    e = np.where(amax > 0, e, 0).clip(-126, 126).astype(np.int32)
+    scale = np.ldexp(np.float32(1.0), -e).astype(np.float32)[:, None]
+    q = np.rint(blocks * scale).clip(-127, 127).astype(np.int8)   # exact power-of-two scaling
+    return q.reshape(-1), e.astype(np.int8)
+
+
+class Q8Raw:
+    """Stored int8 values and per-block exponents of a "q8" tensor (rows
+    indexable like the tensor itself, the last dimension whole)."""
+
+    def __init__(self, q: np.ndarray, e: np.ndarray):
+        self.q, self.e = q, e
+
+    @property
+    def shape(self):
+        return self.q.shape
+
+    def __getitem__(self, idx):
+        return Q8Raw(self.q[idx], self.e[idx])
+
+
 def _fill_chunk(seed: int, name: str, j: int, std: float, init: str,
-                dst: np.ndarray, dtype: str, zero: bool) -> None:
+                dst, dtype: str, zero: bool) -> None:
+    if dtype == "q8":
+        dq, de = dst
+        val = np.empty(dq.size, np.float32)
+        _fill_chunk(seed, name, j, std, init, val, "f32", zero)
+        dq[:], de[:] = quantize_q8(val)
+        return
     n = dst.size
     if init == "ones":
         val = np.ones(n, np.float32)
@@ -235,7 +300,14 @@ def _fill_chunk(seed: int, name: str, j: int, std: float, init: str,
 
 
 def _np_storage(dtype: str):
-    return np.uint16 if dtype == "bf16" else np.float32
+    return np.uint16 if dtype == "bf16" else np.int8 if dtype == "q8" else np.float32
+
+
+def tensor_nbytes(dtype: str, shape) -> int:
+    n = int(np.prod(shape))
+    if dtype == "q8":
+        return n + n // QBLOCK
+    return n * (2 if dtype == "bf16" else 4)
 
 
 def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
@@ -247,7 +319,7 @@ def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
     hdr_room = 1 << 20
     off = ALIGN * ((16 + hdr_room + ALIGN - 1) // ALIGN)
     for name, dt, shape, init in tensor_list(s):
-        nbytes = int(np.prod(shape)) * (2 if dt == "bf16" else 4)
+        nbytes = tensor_nbytes(dt, shape)
         tensors.append(dict(name=name, dtype=dt, shape=list(shape), offset=off,
                             nbytes=nbytes, init=init))
         off += ALIGN * ((nbytes + ALIGN - 1) // ALIGN)
@@ -268,6 +340,14 @@ def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
     mm = np.memmap(tmp, dtype=np.uint8, mode="r+")
     jobs = []
     for t in tensors:
+        if t["dtype"] == "q8":
+            n = int(np.prod(t["shape"]))
+            q = mm[t["offset"]:t["offset"] + n].view(np.int8)
+            e = mm[t["offset"] + n:t["offset"] + t["nbytes"]].view(np.int8)
+            for j in range(0, (n + CHUNK - 1) // CHUNK):
+                jobs.append((t["name"], j, t["init"], (q[j * CHUNK:(j + 1) * CHUNK],
+                                                       e[j * CHUNK // QBLOCK:(j + 1) * CHUNK // QBLOCK]), "q8"))
+            continue
         n = t["nbytes"] // (2 if t["dtype"] == "bf16" else 4)
         arr = mm[t["offset"]:t["offset"] + t["nbytes"]].view(_np_storage(t["dtype"]))
         for j in range(0, (n + CHUNK - 1) // CHUNK):
@@ -291,13 +371,21 @@ def read_header(path: str) -> dict:
         return json.loads(f.read(n))
 
 
-def tensor_raw(path: str, name: str, header: dict | None = None) -> np.ndarray:
-    """Memory-mapped raw storage of one tensor (uint16 bf16 bits or float32)."""
+def tensor_raw(path: str, name: str, header: dict | None = None):
+    """Memory-mapped raw storage of one tensor: uint16 bf16 bits, float32, or
+    for "q8" a Q8Raw of the int8 values and int8 block exponents."""
     h = header or read_header(path)
     for t in h["tensors"]:
         if t["name"] == name:
+            shape = tuple(t["shape"])
+            if t["dtype"] == "q8":
+                n = int(np.prod(shape))
+                q = np.memmap(path, dtype=np.int8, mode="r", offset=t["offset"], shape=shape)
+                e = np.memmap(path, dtype=np.int8, mode="r", offset=t["offset"] + n,
+                              shape=shape[:-1] + (shape[-1] // QBLOCK,))
+                return Q8Raw(q, e)
             return np.memmap(path, dtype=_np_storage(t["dtype"]), mode="r",
-                             offset=t["offset"], shape=tuple(t["shape"]))
+                             offset=t["offset"], shape=shape)
     raise KeyError(name)
 
 
@@ -386,6 +474,9 @@ WORKLOADS: dict[str, dict] = {
     # enough prefix rows that the expert segments average over 1024 rows
     "tiny_moe_long": dict(model="tiny_moe_bf16", Q=16, P=(250, 400), ids="zipf", K=4, m=(1, 12)),
     "micro_moe": dict(model="micro_moe_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
+    "small_q8": dict(model="small_gqa_q8", Q=12, P=(40, 300), ids="zipf", K=4, m=(1, 24)),
+    "dense_1p5b_q8_k4": dict(model="dense_1p5b_q8", Q=256, P=(150, 900), ids="zipf", K=4, m=(1, 24)),
+    "dense_27b_q8_k10": dict(model="dense_27b_q8", Q=64, P=(1024, 4096), ids="zipf", K=10, m=(8, 40)),
 }
 
 

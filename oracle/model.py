@@ -34,8 +34,14 @@ import numpy as np
 import jet_synth
 
 
-def upcast(raw: np.ndarray) -> np.ndarray:
-    """Exact conversion of stored weights (bf16 bits or f32) to float64."""
+def upcast(raw) -> np.ndarray:
+    """Exact conversion of stored weights to float64: bf16 bits, f32, or
+    block-quantized int8 values q with one exponent e per block of
+    consecutive values along the last dimension (weight = q * 2^e)."""
+    if isinstance(raw, jet_synth.Q8Raw):
+        q = np.asarray(raw.q, np.float64)
+        e = np.repeat(np.asarray(raw.e, np.int64), q.shape[-1] // raw.e.shape[-1], axis=-1)
+        return np.ldexp(q, e)
     raw = np.asarray(raw)
     if raw.dtype == np.uint16:
         return (raw.astype(np.uint32) << 16).view(np.float32).astype(np.float64)

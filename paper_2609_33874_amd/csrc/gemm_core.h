@@ -19,6 +19,12 @@
 //           NSTAGE - 1 K steps in flight, each step's loads interleaved with
 //           the MFMAs of the step before it (fixed by scheduling groups);
 //   LOAD 8  the LOAD 7 schedule for a plain (single-plane) A operand.
+//   LOAD 9  the LOAD 8 schedule with an int8 B operand: the stored values q
+//           of a block-quantized weight matrix (blocks of 32 along K) and one
+//           fp16 scale per (row, block), a power of two; a stage holds the A
+//           tile, the B tile as [K chunk][row] 16-byte units and the tile's
+//           scales, and each B fragment is turned into fp16 q * scale in
+//           registers (exact) before its MFMAs.
 // Rows beyond M / N load a clamped valid row; their outputs are discarded.
 #pragma once
 
@@ -42,16 +48,22 @@ struct GCfg {
   // LOAD 7 (pair-aware): A holds (hi, lo) planes and both are staged, B once
   static constexpr bool PAIRA = LOAD == 7;
   static constexpr bool INTERLEAVED = LOAD == 7 || LOAD == 8;  // the LOAD 7 / 8 schedule
+  static constexpr bool Q8B = LOAD == 9;                       // int8 B with per-block scales
   static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
-  static constexpr int A_PT = BM * CPR / NT, B_PT = BN * CPR / NT;  // chunks per thread per K step (per plane)
-  static constexpr int BUF = (BROW0 + BN) * CPR;                     // chunks per LDS stage
+  static constexpr int B_CH = BK / 16;                               // int8 B: 16-byte chunks per row per K step
+  static constexpr int A_PT = BM * CPR / NT;                         // chunks per thread per K step (per plane)
+  static constexpr int B_PT = Q8B ? B_CH * BN / NT : BN * CPR / NT;
+  static constexpr int BUF = Q8B ? BM * CPR + B_CH * BN + BN / 8 : (BROW0 + BN) * CPR;  // chunks per LDS stage
   static constexpr size_t LDS_BYTES = sizeof(uint4) * NSTAGE * BUF;
   static constexpr int RPI = 64 / CPR;  // tile rows per direct-load wave instruction
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8, "tile load schedule");
-  static_assert(INTERLEAVED ? NSTAGE >= 2 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8 || LOAD == 9, "tile load schedule");
+  static_assert(!Q8B || (BK == 32 && B_CH * BN % (64 * NWAVES) == 0 && BN / 8 == 4 * NWAVES && WN <= 128 &&
+                         128 % WN == 0),
+                "int8 B: one quantization block per K step, whole direct-load rounds, 4 scale chunks per wave");
+  static_assert(INTERLEAVED || Q8B ? NSTAGE >= 2 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
                 "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
 };
@@ -239,6 +251,125 @@ __device__ __forceinline__ void kk_mma(const Frag<typename C::type> (&fa)[C::MI]
     for (int j = 0; j < C::NI; ++j) mma32(acc[i][j], fa[i], fb[j]);
 }
 
+// ---------------------------------------------------------------------------
+// int8 B operand (LOAD 9)
+// ---------------------------------------------------------------------------
+
+typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+
+template <int OFF>
+__device__ __forceinline__ void ds_read8(uint2 &v, uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
+}
+template <int OFF>
+__device__ __forceinline__ void ds_read4(uint32_t &v, uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
+}
+template <int STRIDE, int N, int... I>
+__device__ __forceinline__ void ds_read8_rows(uint2 (&r)[N], uint32_t addr, std::integer_sequence<int, I...>) {
+  (ds_read8<I * STRIDE>(r[I], addr), ...);
+}
+
+// fp16 fragment of 8 int8 values q (K order) times the power-of-two scale s:
+// (0x6400 | (q + 128)) is the fp16 number 1024 + q + 128, so subtracting
+// 1152 gives q exactly, and q * s is exact for every scale the loader stores.
+__device__ __forceinline__ Frag<f16> q8_frag(uint2 raw, uint32_t sbits) {
+  const uint32_t x0 = raw.x ^ 0x80808080u, x1 = raw.y ^ 0x80808080u;
+  const _Float16 s = __builtin_bit_cast(_Float16, (uint16_t)sbits);
+  const h2v bias = {(_Float16)1152.0f, (_Float16)1152.0f}, sc = {s, s};
+  const uint32_t p[4] = {__builtin_amdgcn_perm(0x64646464u, x0, 0x04010400u),
+                         __builtin_amdgcn_perm(0x64646464u, x0, 0x04030402u),
+                         __builtin_amdgcn_perm(0x64646464u, x1, 0x04010400u),
+                         __builtin_amdgcn_perm(0x64646464u, x1, 0x04030402u)};
+  Frag<f16> f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const h2v v = (__builtin_bit_cast(h2v, p[i]) - bias) * sc;
+    f.v[2 * i] = v.x;
+    f.v[2 * i + 1] = v.y;
+  }
+  return f;
+}
+
+// Fragment reads of MFMA step kk of stage `buf`: the A rows (fp16) and the
+// wave's NI raw int8 B fragments (8 bytes each).
+template <class C>
+__device__ __forceinline__ void kk_frags_q8(uint32_t lds_addr, int buf, int kk, int lane, int wm, int wn,
+                                           Frag<f16> (&fa)[C::MI], uint2 (&rb)[C::NI]) {
+  const int c0 = (kk * 16 + (lane >> 5) * 8) / C::EPC;
+  const int ra = wm * C::WM + (lane & 31), rbw = wn * C::WN + (lane & 31);
+  const uint32_t stage = lds_addr + (uint32_t)(buf * C::BUF) * 16u;
+  const uint32_t a = stage + (uint32_t)(ra * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
+  const uint32_t b = stage + (uint32_t)(C::BM * C::CPR + kk * C::BN + rbw) * 16u + (uint32_t)((lane >> 5) * 8);
+  ds_read_rows<32 * C::CPR * 16>(fa, a, std::make_integer_sequence<int, C::MI>{});
+  ds_read8_rows<32 * 16>(rb, b, std::make_integer_sequence<int, C::NI>{});
+}
+
+// The scales of the wave's NI fragment rows for stage `buf` (NI consecutive
+// fp16 values: the stage holds [row group of 128][row % 32][(row / 32) % 4]).
+// The read and its wait are one statement: a result register of an
+// asynchronous read must not be live across compiler-scheduled code (the
+// compiler may copy it before the data has arrived).
+template <class C>
+__device__ __forceinline__ void scale_read_q8(uint32_t lds_addr, int buf, int lane, int wn, uint2 &sc) {
+  const int n = wn * C::WN + (lane & 31);
+  const int off = (n >> 7) * 128 + (n & 31) * 4 + ((wn * C::WN) >> 5) % 4;
+  const uint32_t a = lds_addr + (uint32_t)(buf * C::BUF + C::BM * C::CPR + C::B_CH * C::BN) * 16u + (uint32_t)off * 2u;
+  if constexpr (C::NI == 4) {
+    asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(sc) : "v"(a) : "memory");
+  } else {
+    static_assert(C::NI == 2, "2 or 4 fragments per wave row block");
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(sc.x) : "v"(a) : "memory");
+    sc.y = 0u;
+  }
+}
+
+template <int N, int MI, int NI>
+__device__ __forceinline__ void wait_frags_q8(Frag<f16> (&fa)[MI], uint2 (&rb)[NI]) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+#pragma unroll
+  for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(fa[i].v));
+#pragma unroll
+  for (int j = 0; j < NI; ++j) asm volatile("" : "+v"(rb[j]));
+}
+
+// Direct loads of one K step (k: first K column) of the int8 B operand:
+// A as tile_issue_direct; B rows as [chunk][row] 16-byte units; the tile's
+// scales from Bs [K / 32][NG][32][4] (fp16 bits; NG = row groups of 128),
+// four 16-byte units per wave.
+template <class C>
+__device__ __forceinline__ void tile_issue_direct_q8(const f16 *__restrict__ A, int64_t lda,
+                                                     const int8_t *__restrict__ B, int64_t ldb,
+                                                     const uint16_t *__restrict__ Bs, int NG, int M, int N, int m0,
+                                                     int n0, int k, uint4 *lds, int buf, int wave, int lane) {
+  uint4 *a = lds + buf * C::BUF, *b = a + C::BM * C::CPR, *s = b + C::B_CH * C::BN;
+  const int sub_r = lane / C::CPR, pc = lane % C::CPR;
+#pragma unroll
+  for (int i = 0; i < C::A_PT; ++i) {
+    const int blk = i * C::NWAVES + wave;
+    const int r = blk * C::RPI + sub_r;
+    const int c = pc ^ lds_swz<C>(r);
+    const int gm = min(m0 + r, M - 1);
+    __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)gm * lda + k + c * C::EPC),
+                                     (lds_void *)(a + blk * 64), 16, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < C::B_PT; ++i) {
+    const int blk = i * C::NWAVES + wave;
+    const int u = blk * 64 + lane, c = u / C::BN, r = u % C::BN;
+    const int gn = min(n0 + r, N - 1);
+    __builtin_amdgcn_global_load_lds((const void *)(B + (int64_t)gn * ldb + k + c * 16), (lds_void *)(b + blk * 64),
+                                     16, 0, 0);
+  }
+  if (lane < 4) {
+    const int u = wave * 4 + lane, gg = min((n0 >> 7) + (u >> 4), NG - 1);
+    const char *src = (const char *)Bs + ((int64_t)(k >> 5) * NG + gg) * 256 + (u & 15) * 16;
+    __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(s + wave * 4), 16, 0, 0);
+  }
+}
+
 // Register path: global -> registers.
 template <class C>
 __device__ __forceinline__ void tile_gload(const typename C::type *__restrict__ A, int64_t lda,
@@ -317,7 +448,7 @@ template <class C>
 __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A, int64_t lda,
                                           const typename C::type *__restrict__ B, int64_t ldb, int M, int N,
                                           int K, int KA, int KB, int m0, int n0, uint4 *lds,
-                                          f32x16 (&acc)[C::MI][C::NI]) {
+                                          f32x16 (&acc)[C::MI][C::NI], const uint16_t *__restrict__ Bs = nullptr) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   zero_acc<C>(acc);
@@ -491,6 +622,78 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
       wait_frags<0>(fa[0], fb[0]);
       wait_frags<0>(fa[1], fb[1]);
     }
+    __builtin_amdgcn_s_barrier();
+  } else if constexpr (C::Q8B) {
+    // The LOAD 8 schedule (see above) with an int8 B operand: B is int8
+    // [N][KB] (ldb bytes per row) with fp16 scales Bs; a stage's scales are
+    // read with the first fragments of the stage and serve both MFMA steps
+    // of its K step (one quantization block).
+    static_assert(sizeof(typename C::type) == 2, "fp16 A with int8 B");
+    constexpr int PT = C::A_PT + C::B_PT + 1, NS = C::NSTAGE, KK = C::BK / 16, NR = C::MI + C::NI;
+    constexpr int NMMA = C::MI * C::NI, R = NMMA >= PT ? NMMA / PT : 1, NG = NMMA >= PT ? PT : NMMA;
+    constexpr int PRE = NS - 1;
+    const int nk5 = KB / C::BK, ngroups = (N + 127) / 128;
+    const int8_t *Bq = reinterpret_cast<const int8_t *>(B);
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(lds_void *)lds;
+#pragma unroll
+    for (int s = 0; s < PRE; ++s)
+      tile_issue_direct_q8<C>(A, lda, Bq, ldb, Bs, ngroups, M, N, m0, n0, min(s, nk5 - 1) * C::BK, lds, s, wave,
+                              lane);
+    wait_vmcnt<(PRE - 1) * PT>();
+    __builtin_amdgcn_s_barrier();
+    static_assert(KK == 2, "two MFMA steps per K step");
+    Frag<f16> fa[2][C::MI];
+    uint2 rb[2][C::NI], sc;
+    kk_frags_q8<C>(lds_addr, 0, 0, lane, wm, wn, fa[0], rb[0]);
+    int st = 0, sl = NS - 1;  // stage of tile kt; stage of tile kt + NS - 1
+    for (int kt = 0; kt < nk5; ++kt) {
+      const int kn = min(kt + PRE, nk5 - 1) * C::BK;
+      const int snext = st + 1 == NS ? 0 : st + 1;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int cur = kk & 1, nx = cur ^ 1;
+        if (kk == 0) {
+          // this step's fragments (read at the stage boundary), then the
+          // stage's scales, read and waited for at once
+          wait_frags_q8<0>(fa[cur], rb[cur]);
+          scale_read_q8<C>(lds_addr, st, lane, wn, sc);
+        } else {
+          // own loads of tile kt + 1 have landed; after the barrier every
+          // wave's have, and no wave reads stage kt any more
+          wait_vmcnt<(NS - 2) * PT>();
+          wait_frags_q8<0>(fa[cur], rb[cur]);
+          __builtin_amdgcn_s_barrier();
+          kk_frags_q8<C>(lds_addr, snext, 0, lane, wm, wn, fa[nx], rb[nx]);
+        }
+        Frag<f16> fb[C::NI];
+#pragma unroll
+        for (int j = 0; j < C::NI; ++j) {
+          const uint32_t w = (j >> 1) ? sc.y : sc.x;
+          fb[j] = q8_frag(rb[cur][j], (j & 1) ? w >> 16 : w & 0xffffu);
+        }
+        if (kk == 0) kk_frags_q8<C>(lds_addr, st, 1, lane, wm, wn, fa[nx], rb[nx]);
+        if (kk == 0) {
+          __builtin_amdgcn_sched_barrier(0);
+          kk_mma<C>(fa[cur], fb, acc);
+          tile_issue_direct_q8<C>(A, lda, Bq, ldb, Bs, ngroups, M, N, m0, n0, kn, lds, sl, wave, lane);
+#pragma unroll
+          for (int i = 0; i < PT; ++i) {
+            if (i < NG) __builtin_amdgcn_sched_group_barrier(0x008, R, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);              // VMEM read
+          }
+          if constexpr (NMMA > R * NG) __builtin_amdgcn_sched_group_barrier(0x008, NMMA - R * NG, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        } else {
+          kk_mma<C>(fa[cur], fb, acc);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      st = snext;
+      sl = sl + 1 == NS ? 0 : sl + 1;
+    }
+    wait_vmcnt<0>();
+    wait_frags_q8<0>(fa[0], rb[0]);
+    wait_frags_q8<0>(fa[1], rb[1]);
     __builtin_amdgcn_s_barrier();
   }
 }

@@ -32,6 +32,8 @@ struct GemmArgs {
   // with tile_group -1 do nothing (null: one B for all tiles)
   const int *tile_group = nullptr;
   int64_t group_stride = 0;
+  // int8 B (LOAD 9 configurations): fp16 scales [K / 32][ceil(N / 128)][32][4]
+  const uint16_t *Bs = nullptr;
 };
 
 // (hi, lo) split of v stored at p[0] and p[ps] (lo only with pair).
@@ -170,7 +172,7 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
     B += (int64_t)grp * g.group_stride;
   }
   f32x16 acc[C::MI][C::NI];
-  gemm_tile<C>(g.A, g.lda, B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc);
+  gemm_tile<C>(g.A, g.lda, B, g.ldb, g.M, g.N, g.K, g.KA, g.KB, m0, n0, lds, acc, g.Bs);
   if (staged_epilogue<C, EPI>(g, m0, n0, acc, lds)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
@@ -361,6 +363,11 @@ using HalfM = GCfg<f16, 256, 128, 64, 64, 8, 2, 3, 4>;
 using HalfPairB = GCfg<f16, 256, 256, 64, 128, 7, 2, 3, 4>;
 using HalfPairS = GCfg<f16, 128, 128, 32, 64, 7, 2, 3, 4>;
 using LmH = GCfg<f16, 256, 256, 64, 128, 8, 2, 3, 4>;
+// int8 B operand (block-quantized weights): the LOAD 8 schedule with int8 B
+// tiles and per-block scales (three 24.5 KB stages), 256x256 tiles of 8
+// waves, or 128x128 tiles of 4 waves for problems with fewer tiles.
+using Q8B = GCfg<f16, 256, 256, 64, 128, 9, 2, 3, 4>;
+using Q8S = GCfg<f16, 128, 128, 64, 64, 9, 2, 3, 4>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
 template <class C>
@@ -458,6 +465,38 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
     }
   }
   return run_epi<CfgF>(epi, A, lda, B, ldb, M, N, K, 0, out, ldo, oscale, st);
+}
+
+template <class C, int EPI>
+static hipError_t run_gemm_q8(const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N, int K,
+                              void *out, int64_t ldo, float oscale, hipStream_t st) {
+  static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
+  if (once != hipSuccess) return once;
+  GemmArgs<f16> g{(const f16 *)A, (const f16 *)Bq, lda, K, M, N, K, K, K, out, ldo, 0, oscale, QkvRope{}};
+  g.Bs = Bs;
+  const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
+  return hipGetLastError();
+}
+
+template <class C>
+static hipError_t run_q8_epi(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
+                             int K, void *out, int64_t ldo, float oscale, hipStream_t st) {
+  switch (epi) {
+    case EPI_STORE_F32: return run_gemm_q8<C, 0>(A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+    case EPI_RESID_ADD: return run_gemm_q8<C, 1>(A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+    case EPI_SWIGLU: return run_gemm_q8<C, 2>(A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+    default: return run_gemm_q8<C, 3>(A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+  }
+}
+
+hipError_t launch_gemm_q8(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
+                          int K, void *out, int64_t ldo, float oscale, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % 32 != 0) return hipErrorInvalidValue;
+  const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+  if (big_tiles >= 512) return run_q8_epi<Q8B>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+  return run_q8_epi<Q8S>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
 }
 
 template <class C, int EPI>

@@ -39,6 +39,14 @@ hipError_t launch_gemm_qkv_rope(int dtype, const void *A, int64_t lda, const voi
 // out[M x N] as [hi (N/2) | lo (N/2)]. Every product is multiplied by oscale
 // before the epilogue (the inverse of a power-of-two weight scale).
 int gemm_k_step(int dtype);
+// fp16 A [M][K] times an int8 B operand: Bq [N][K] int8 (K bytes per row)
+// holding the values q of a block-quantized matrix, Bs the fp16 bits of the
+// scale of each (row, block of 32 K columns), a power of two, laid out as
+// [K / 32][ceil(N / 128)][32][4] (row n = 128 g + 32 j + r at [.][g][r][j]);
+// B = q * scale exactly in fp16. Epilogues as launch_gemm (no pairs).
+// K must be a multiple of 32.
+hipError_t launch_gemm_q8(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
+                          int K, void *out, int64_t ldo, float oscale, hipStream_t st);
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
                        int N, int K, int pair, void *out, int64_t ldo, float oscale, hipStream_t st);
 

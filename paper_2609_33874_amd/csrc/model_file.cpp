@@ -155,9 +155,10 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
   if (!arch || arch->kind != JVal::STR || !dt || dt->kind != JVal::STR)
     return Status::err(JET_E_IO, path + ": header lacks arch/dtype");
   if (arch->str != "dense" && arch->str != "hybrid") return Status::err(JET_E_IO, "unknown arch " + arch->str);
-  if (dt->str != "bf16" && dt->str != "f32") return Status::err(JET_E_IO, "unknown dtype " + dt->str);
+  if (dt->str != "bf16" && dt->str != "f32" && dt->str != "q8") return Status::err(JET_E_IO, "unknown dtype " + dt->str);
   h->hybrid = arch->str == "hybrid";
-  h->bf16 = dt->str == "bf16";
+  h->q8 = dt->str == "q8";
+  h->bf16 = dt->str == "bf16" || h->q8;
   bool ok = get_int(root, "d_model", &h->d) && get_int(root, "n_layers", &h->n_layers) &&
             get_int(root, "n_heads", &h->n_heads) && get_int(root, "n_kv_heads", &h->n_kv_heads) &&
             get_int(root, "head_dim", &h->head_dim) && get_int(root, "ffn", &h->ffn) &&
@@ -190,10 +191,11 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
     TensorInfo ti;
     const JVal *nm = t.get("name"), *tdt = t.get("dtype"), *sh = t.get("shape");
     if (!nm || nm->kind != JVal::STR || !tdt || tdt->kind != JVal::STR || !sh || sh->kind != JVal::ARR ||
-        (tdt->str != "bf16" && tdt->str != "f32"))
+        (tdt->str != "bf16" && tdt->str != "f32" && tdt->str != "q8"))
       return Status::err(JET_E_IO, path + ": bad tensor entry");
     ti.name = nm->str;
     ti.bf16 = tdt->str == "bf16";
+    ti.q8 = tdt->str == "q8";
     int64_t numel = 1;
     for (auto &s : sh->arr) {
       int64_t dim = 0;
@@ -204,7 +206,9 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
     }
     if (!get_int(t, "offset", &ti.offset) || !get_int(t, "nbytes", &ti.nbytes))
       return Status::err(JET_E_IO, path + ": tensor lacks offset/nbytes");
-    if (ti.nbytes != numel * (ti.bf16 ? 2 : 4))
+    if (ti.q8 && (ti.shape.empty() || ti.shape.back() % 32 != 0))
+      return Status::err(JET_E_IO, path + ": q8 tensor " + ti.name + " needs a last dimension multiple of 32");
+    if (ti.nbytes != (ti.q8 ? numel + numel / 32 : numel * (ti.bf16 ? 2 : 4)))
       return Status::err(JET_E_IO, path + ": tensor " + ti.name + " size mismatch");
     h->tensors[ti.name] = ti;
   }

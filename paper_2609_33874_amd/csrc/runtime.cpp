@@ -176,12 +176,125 @@ struct Loader {
   std::vector<char> host;
   unsigned long long *inexact = nullptr;  // device counter of inexact fp16 conversions
 
+  TensorInfo cur;  // the tensor last read, as the caller sees it
+
+  // A tensor's bytes into `host`. Block-quantized (q8) tensors arrive as the
+  // bf16 bits of their weights q * 2^e, which bf16 holds exactly (8
+  // significant bits, fp32's exponent range).
   Status read(const std::string &name, const TensorInfo **ti) {
     auto it = m->h.tensors.find(name);
     if (it == m->h.tensors.end()) return Status::err(JET_E_IO, "model file lacks tensor " + name);
-    *ti = &it->second;
+    cur = it->second;
+    *ti = &cur;
     host.resize((size_t)it->second.nbytes);
-    return read_tensor_bytes(m->path, it->second, host.data());
+    TRY(read_tensor_bytes(m->path, it->second, host.data()));
+    if (!cur.q8) return Status::ok();
+    const int64_t n = cur.numel();
+    std::vector<char> raw;
+    raw.swap(host);
+    host.resize((size_t)n * 2);
+    const int8_t *q = reinterpret_cast<const int8_t *>(raw.data()), *e = q + n;
+    uint16_t *dst = reinterpret_cast<uint16_t *>(host.data());
+    for (int64_t i = 0; i < n; ++i) {
+      const float w = std::ldexp((float)q[i], (int)e[i / 32]);
+      uint32_t u;
+      std::memcpy(&u, &w, 4);
+      dst[i] = (uint16_t)(u >> 16);  // exact: the low 16 bits are zero
+    }
+    cur.q8 = false;
+    cur.bf16 = true;
+    cur.nbytes = n * 2;
+    return Status::ok();
+  }
+
+  // Block-quantized weight rows kept as int8 for the fused GEMM path.
+  struct Q8Rows {
+    std::vector<int8_t> q, e;  // [rows][cols], [rows][cols / 32]
+    int64_t rows = 0, cols = 0;
+  };
+  Status q8_read(const std::string &name, Q8Rows *w) {
+    auto it = m->h.tensors.find(name);
+    if (it == m->h.tensors.end()) return Status::err(JET_E_IO, "model file lacks tensor " + name);
+    const TensorInfo &t = it->second;
+    if (!t.q8 || t.shape.size() != 2) return Status::err(JET_E_IO, name + ": expected a q8 matrix");
+    std::vector<char> raw((size_t)t.nbytes);
+    TRY(read_tensor_bytes(m->path, t, raw.data()));
+    w->rows = t.shape[0];
+    w->cols = t.shape[1];
+    const int64_t n = w->rows * w->cols;
+    w->q.assign(reinterpret_cast<const int8_t *>(raw.data()), reinterpret_cast<const int8_t *>(raw.data()) + n);
+    w->e.assign(reinterpret_cast<const int8_t *>(raw.data()) + n, reinterpret_cast<const int8_t *>(raw.data()) + n + n / 32);
+    return Status::ok();
+  }
+  // Rows of several matrices stacked; with interleave, gate/up style: blocks
+  // of 32 rows of the first then 32 rows of the second.
+  static Q8Rows q8_stack(const std::vector<Q8Rows> &parts, bool interleave) {
+    Q8Rows out;
+    out.cols = parts[0].cols;
+    const int64_t eb = out.cols / 32;
+    for (auto &p : parts) out.rows += p.rows;
+    out.q.resize((size_t)(out.rows * out.cols));
+    out.e.resize((size_t)(out.rows * eb));
+    auto put = [&](int64_t dst_row, const Q8Rows &p, int64_t src_row, int64_t nrows) {
+      std::memcpy(&out.q[(size_t)(dst_row * out.cols)], &p.q[(size_t)(src_row * out.cols)], (size_t)(nrows * out.cols));
+      std::memcpy(&out.e[(size_t)(dst_row * eb)], &p.e[(size_t)(src_row * eb)], (size_t)(nrows * eb));
+    };
+    int64_t r = 0;
+    if (interleave) {
+      for (int64_t b = 0; b < parts[0].rows / 32; ++b)
+        for (auto &p : parts) {
+          put(r, p, b * 32, 32);
+          r += 32;
+        }
+    } else {
+      for (auto &p : parts) {
+        put(r, p, 0, p.rows);
+        r += p.rows;
+      }
+    }
+    return out;
+  }
+  // int8 values to the device as they are; the scale of each (row, block) as
+  // fp16 bits of 2^(e + k), k a power-of-two scale of the whole matrix that
+  // puts its largest weight in [2^14, 2^15) (as the fp16 conversion does):
+  // q * 2^(e + k) is then exact in fp16 for e + k >= -24; blocks below that
+  // (far below the matrix's largest weight) round and are counted.
+  Status put_q8(const Q8Rows &w, void **q_dev, uint16_t **s_dev, float *inv_scale) {
+    const int64_t N = w.rows, K = w.cols, KB = K / 32, NG = (N + 127) / 128;
+    int top = -1000;  // exponent of the largest weight: max over blocks of e + bit length of max|q| - 1
+    for (int64_t r = 0; r < N; ++r)
+      for (int64_t b = 0; b < KB; ++b) {
+        int mq = 0;
+        for (int64_t i = 0; i < 32; ++i) mq = std::max(mq, std::abs((int)w.q[(size_t)(r * K + b * 32 + i)]));
+        if (mq == 0) continue;
+        int bl = 0;
+        while ((1 << bl) <= mq) ++bl;
+        top = std::max(top, (int)w.e[(size_t)(r * KB + b)] + bl - 1);
+      }
+    const int k = top == -1000 ? 0 : 14 - top;
+    *inv_scale = std::ldexp(1.0f, -k);
+    std::vector<uint16_t> sc((size_t)(KB * NG * 128), 0);
+    int64_t inexact = 0;
+    for (int64_t r = 0; r < N; ++r)
+      for (int64_t b = 0; b < KB; ++b) {
+        const int ek = (int)w.e[(size_t)(r * KB + b)] + k;
+        if (ek > 15) return Status::err(JET_E_INVALID, "q8 block scale beyond fp16 range");
+        uint16_t bits = 0;
+        if (ek >= -14) bits = (uint16_t)((ek + 15) << 10);
+        else if (ek >= -24) bits = (uint16_t)(1u << (ek + 24));
+        else
+          for (int64_t i = 0; i < 32; ++i) inexact += w.q[(size_t)(r * K + b * 32 + i)] != 0;
+        const int64_t g = r / 128, j = (r / 32) % 4, rr = r % 32;
+        sc[(size_t)(((b * NG + g) * 32 + rr) * 4 + j)] = bits;
+      }
+    m->f16_inexact += inexact;
+    TRY(dmalloc(m, w.q.size(), q_dev));
+    m->weight_allocs.push_back(*q_dev);
+    HIPC(hipMemcpy(*q_dev, w.q.data(), w.q.size(), hipMemcpyHostToDevice));
+    TRY(dmalloc(m, sc.size() * 2, (void **)s_dev));
+    m->weight_allocs.push_back(*s_dev);
+    HIPC(hipMemcpy(*s_dev, sc.data(), sc.size() * 2, hipMemcpyHostToDevice));
+    return Status::ok();
   }
 
   // Uploads host bytes of `n` elements stored as bf16 (src_bf16) or f32 into a
@@ -343,6 +456,14 @@ Status check_shapes(const ModelHeader &h, int dtype) {
   if (h.d % bk || (h.n_heads * h.head_dim) % bk || h.ffn % bk)
     return Status::err(JET_E_INVALID, "d_model, n_heads*head_dim and ffn must be multiples of " + std::to_string(bk));
   if (h.ffn % 32) return Status::err(JET_E_INVALID, "ffn must be a multiple of 32");
+  if (h.q8) {
+    if (h.hybrid || h.n_experts)
+      return Status::err(JET_E_INVALID, "block-quantized (q8) models must be dense decoders without experts");
+    if (dtype != JET_F16 && dtype != JET_FP32)
+      return Status::err(JET_E_INVALID, "block-quantized (q8) models run in the JET_F16 and JET_FP32 modes");
+    if (h.d % 128 || (h.n_heads * h.head_dim) % 32 || h.ffn % 64)
+      return Status::err(JET_E_INVALID, "q8 models need d_model a multiple of 128 and ffn of 64");
+  }
   if (h.n_experts) {
     if (h.n_experts > jetk::kMoeMaxExperts || h.top_k < 1 || h.top_k > h.n_experts ||
         h.top_k > jetk::kMoeMaxTopK)
@@ -382,6 +503,10 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   m->scratch_status = noalloc_scratch_init(m->device);
   if (m->scratch_status != hipSuccess) (void)hipGetLastError();
   Loader L{m, {}};
+  // block-quantized models in the fp16 mode keep the projection and FFN
+  // weights as int8 (dequantized in the GEMM's operand path); every other
+  // matrix, and every matrix in the fp32 mode, is dequantized here
+  const bool q8_gemm = h.q8 && m->kdt == 2;
   if (m->kdt == 2) {
     TRY(dmalloc(m, sizeof(unsigned long long), (void **)&L.inexact));
     m->weight_allocs.push_back(L.inexact);
@@ -397,7 +522,15 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
     ly.gdn = h.layer_is_gdn[(size_t)i] != 0;
     TRY(L.vec_f32(p + "attn_norm", &ly.attn_norm, h.d));
     TRY(L.vec_f32(p + "ffn_norm", &ly.ffn_norm, h.d));
-    if (!ly.gdn) {
+    if (!ly.gdn && q8_gemm) {
+      Loader::Q8Rows wq, wk, wv, wo;
+      TRY(L.q8_read(p + "wq", &wq));
+      TRY(L.q8_read(p + "wk", &wk));
+      TRY(L.q8_read(p + "wv", &wv));
+      TRY(L.put_q8(Loader::q8_stack({wq, wk, wv}, false), &ly.w_qkv, &ly.s_qkv, &ly.is_qkv));
+      TRY(L.q8_read(p + "wo", &wo));
+      TRY(L.put_q8(wo, &ly.w_o, &ly.s_o, &ly.is_o));
+    } else if (!ly.gdn) {
       TRY(L.concat({p + "wq", p + "wk", p + "wv"}, h.d, 0, &ly.w_qkv, nullptr, &ly.is_qkv));
       TRY(L.matrix(p + "wo", &ly.w_o, &ly.is_o));
     } else {
@@ -421,6 +554,13 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
         TRY(L.gate_up(p + "shared_gate", p + "shared_up", h.shared_ffn, h.d, &ly.w_sgu, &ly.is_sgu));
         TRY(L.matrix(p + "shared_down", &ly.w_sdown, &ly.is_sdown));
       }
+    } else if (q8_gemm) {
+      Loader::Q8Rows wg, wu, wd;
+      TRY(L.q8_read(p + "w_gate", &wg));
+      TRY(L.q8_read(p + "w_up", &wu));
+      TRY(L.put_q8(Loader::q8_stack({wg, wu}, true), &ly.w_gu, &ly.s_gu, &ly.is_gu));
+      TRY(L.q8_read(p + "w_down", &wd));
+      TRY(L.put_q8(wd, &ly.w_down, &ly.s_down, &ly.is_down));
     } else {
       TRY(L.gate_up(p + "w_gate", p + "w_up", h.ffn, h.d, &ly.w_gu, &ly.is_gu));
       TRY(L.matrix(p + "w_down", &ly.w_down, &ly.is_down));
@@ -445,7 +585,7 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
   if (L.inexact) {
     unsigned long long n = 0;
     HIPC(hipMemcpy(&n, L.inexact, sizeof(n), hipMemcpyDeviceToHost));
-    m->f16_inexact = (int64_t)n;
+    m->f16_inexact += (int64_t)n;
   }
   return Status::ok();
 }
@@ -457,12 +597,19 @@ Status load_model(jet_model *m, const char *path, const jet_load_opts *o) {
 double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (double)N * (double)K; }
 
 // A holds activations ([hi | lo] pairs when pair, lda counts both planes).
+// Bs: block scales of an int8 B (block-quantized weights, fp16 mode), else NULL.
 Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, int pair, const void *B, int64_t ldb,
-                int64_t M, int64_t N, int64_t K, void *out, int64_t ldo, float oscale) {
+                int64_t M, int64_t N, int64_t K, void *out, int64_t ldo, float oscale, const uint16_t *Bs = nullptr) {
   const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 * m->np : N) *
                            (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
                            (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
-  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * (pair ? 2 : 1) + N * K) * (double)m->esz + out_bytes);
+  const double b_bytes = Bs ? (double)(N * K) * (1.0 + 2.0 / 32.0) : (double)(N * K) * (double)m->esz;
+  KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * (pair ? 2 : 1)) * (double)m->esz + b_bytes + out_bytes);
+  if (Bs) {
+    if (pair || ldb != K) return Status::err(JET_E_INVALID, "int8 weights: no pair operands, dense rows");
+    LAUNCH(jetk::launch_gemm_q8(epi, A, lda, B, Bs, (int)M, (int)N, (int)K, out, ldo, oscale, m->st));
+    return Status::ok();
+  }
   LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, pair, out, ldo, oscale, m->st));
   return Status::ok();
 }
@@ -743,9 +890,9 @@ Status ffn(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   }
   if (h.n_experts) return moe_ffn(m, ly, b, R);
   TRY(run_gemm(m, JET_K_GEMM_GATEUP, jetk::EPI_SWIGLU, b.xn, m->np * h.d, m->pair, ly.w_gu, h.d, R, 2 * h.ffn, h.d,
-               b.act, m->np * h.ffn, ly.is_gu));
+               b.act, m->np * h.ffn, ly.is_gu, ly.s_gu));
   TRY(run_gemm(m, JET_K_GEMM_DOWN, jetk::EPI_RESID_ADD, b.act, m->np * h.ffn, m->pair, ly.w_down, h.ffn, R, h.d,
-               h.ffn, b.resid, h.d, ly.is_down));
+               h.ffn, b.resid, h.d, ly.is_down, ly.s_down));
   return Status::ok();
 }
 
@@ -760,7 +907,7 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
     LAUNCH(jetk::launch_rmsnorm(m->kdt, m->apair, b.resid, nullptr, ly.attn_norm, (int)R, (int)h.d,
                                 (float)h.rms_eps, b.xn, m->st));
   }
-  if (jetk::gemm_qkv_rope_ok(m->kdt, m->apair, (int)R, (int)nqkv, (int)h.head_dim)) {
+  if (!ly.s_qkv && jetk::gemm_qkv_rope_ok(m->kdt, m->apair, (int)R, (int)nqkv, (int)h.head_dim)) {
     // projection, RoPE and the K/V scatter in one kernel
     const double out_bytes = (double)R * (double)nqkv * (double)m->esz * m->anp;
     KTimer t(m, JET_K_GEMM_QKV, gemm_flops(R, nqkv, h.d),
@@ -772,7 +919,7 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
     return Status::ok();
   }
   TRY(run_gemm(m, JET_K_GEMM_QKV, jetk::EPI_STORE_F32, b.xn, m->anp * h.d, m->apair, ly.w_qkv, h.d, R, nqkv, h.d,
-               b.qkv, nqkv, ly.is_qkv));
+               b.qkv, nqkv, ly.is_qkv, ly.s_qkv));
   KTimer t(m, JET_K_OTHER, 0, 0);
   LAUNCH(jetk::launch_rope_scatter(m->kdt, m->apair, b.qkv, d_pos, m->rope_cos, m->rope_sin, (int)R, (int)h.n_heads,
                                    (int)h.n_kv_heads, (int)h.head_dim, b.q, R * h.n_heads * h.head_dim, kc, vc,
@@ -783,7 +930,7 @@ Status attn_in(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, cons
 Status attn_out(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R) {
   const ModelHeader &h = m->h;
   return run_gemm(m, JET_K_GEMM_O, jetk::EPI_RESID_ADD, b.att, m->anp * h.n_heads * h.head_dim, m->apair, ly.w_o,
-                  h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d, ly.is_o);
+                  h.n_heads * h.head_dim, R, h.d, h.n_heads * h.head_dim, b.resid, h.d, ly.is_o, ly.s_o);
 }
 
 // Per-wave tables of the delta-rule layers (built on the host, uploaded once).

@@ -27,6 +27,9 @@ struct Layer {
   // inverse weight scales of w_qkv / w_in, w_o, w_gu, w_down (fp16 mode: the
   // stored matrices are the file's values times a power of two; else 1)
   float is_qkv = 1.0f, is_o = 1.0f, is_gu = 1.0f, is_down = 1.0f;
+  // block-quantized model in the fp16 mode: w_qkv, w_o, w_gu and w_down hold
+  // int8 values [N][K] and these their fp16 block scales (see launch_gemm_q8)
+  uint16_t *s_qkv = nullptr, *s_o = nullptr, *s_gu = nullptr, *s_down = nullptr;
   // gated delta-rule layers
   void *w_in = nullptr;    // [n_in][d]: q, k, v (conv channels), z, b, a, zero pad
   int64_t n_in = 0;

@@ -218,6 +218,36 @@ def test_zero_weights_give_uniform_vocabulary(model_dir):
 # network blocks: closed forms and special cases
 # --------------------------------------------------------------------------
 
+def test_q8_weights_against_the_bf16_twin(model_dir):
+    """Block-quantized storage: the oracle's dequantized weights of a q8 model
+    lie within half a quantization step (plus bf16 rounding) of the bf16
+    model drawn from the same seed, every block's scale is tight (its largest
+    |q| is at least 64) and all-zero q8 weights give exactly -ln|V|."""
+    pq = jet_synth.ensure_model("micro_q8", cache_dir=model_dir)
+    pb = os.path.join(model_dir, "micro_q8_bf16twin.jetm")
+    if not os.path.exists(pb):
+        jet_synth.write_model(pb, _spec("micro_q8", dtype="bf16"))
+    mq, mb = om.Model(pq), om.Model(pb)
+    checked = 0
+    for t in mq.h["tensors"]:
+        if t["dtype"] != "q8":
+            continue
+        raw = jet_synth.tensor_raw(pq, t["name"], mq.h)
+        wq, wb = mq.w(t["name"]), mb.w(t["name"])
+        step = np.ldexp(1.0, np.repeat(np.asarray(raw.e, np.int64), 32, axis=-1))
+        assert np.all(np.abs(wq - wb) <= 0.5 * step + np.abs(wb) * 2.0 ** -8), t["name"]
+        qmax = np.abs(np.asarray(raw.q, np.int32)).reshape(-1, 32).max(axis=1)
+        assert np.all(qmax >= 64) and np.all(qmax <= 127)
+        checked += 1
+    assert checked >= 5
+    pz = os.path.join(model_dir, "micro_q8_zero.jetm")
+    if not os.path.exists(pz):
+        jet_synth.write_model(pz, _spec("micro_q8"), zero=True)
+    wl = jet_synth.make_workload("micro_hybrid", vocab=512, Q=2, P=(3, 9), K=3, m=(1, 4))
+    tok, sums = oracle.score_unshared(pz, wl)
+    np.testing.assert_allclose(tok, -math.log(512), rtol=0, atol=1e-12)
+
+
 def test_rope_identity_and_relative_position():
     rng = np.random.default_rng(2)
     x = rng.normal(size=(1, 3, 32))
