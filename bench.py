@@ -285,6 +285,51 @@ def prefix_reuse(steps: int, unshared_steps: int) -> dict:
             "speedup": round(ms_un / ms_sh, 3)}
 
 
+def reasoning_trace(steps: int, tau: float = 0.8, seed: int = 7) -> dict:
+    """Optional reasoning (Section 3.4) on the dense 1.5B choice workload: a
+    trace of `steps` sampled tokens per question (all 256 questions decode
+    together, one row each per step) frozen into the retained prefix, then
+    one scoring pass on the extended prefix. A decode step reads every
+    weight matrix once and every question's cached K/V once; those bytes over
+    the step time give its HBM rate."""
+    import jet_synth
+    import torch
+    r = Runner(REUSE_WORKLOAD, "f16", timing=False)
+    J, wl = r.J, r.wl
+    Q = wl.n_questions
+    try:
+        inp = r.inputs(wl)
+        p = J.jet_prefill_prefix(r.model, wl.prefix_offsets, inp[0])
+        toks = torch.empty(Q * steps, dtype=torch.int32, device=r.dev)
+        J.jet_generate_trace(r.model, p, Q, 2, tau, seed + 1)  # warm-up (workspace growth)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        J.jet_generate_trace(r.model, p, Q, steps, tau, seed, out=toks)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        log(f"reasoning trace: {steps} steps in {dt:.3f}s")
+        # one scoring pass on the extended prefixes
+        J.jet_score_candidates(r.model, p, wl.q_cand_offsets, wl.cand_tok_offsets, inp[1], inp[2], inp[3])
+        finite = bool(torch.isfinite(inp[3]).all().item())
+        J.jet_prefix_free(p)
+    finally:
+        r.free()
+    sp = jet_synth.full_spec(jet_synth.WORKLOADS[REUSE_WORKLOAD]["model"])
+    d, L, hd, F, V = sp["d_model"], sp["n_layers"], sp["head_dim"], sp["ffn"], sp["vocab"]
+    Hq, Hkv = sp["n_heads"], sp["n_kv_heads"]
+    w_bytes = 2.0 * (L * ((Hq + 2 * Hkv) * hd * d + d * Hq * hd + 3 * d * F) + V * d)
+    T = float(wl.prefix_offsets[-1]) + 2 * Q  # after the warm-up trace
+    kv_bytes = 2.0 * L * 2 * Hkv * hd * (T + Q * (steps + 1) / 2.0)  # mean over the steps
+    step_s = dt / steps
+    gbs = (w_bytes + kv_bytes) / step_s / 1e9
+    return {"workload": REUSE_WORKLOAD, "dtype": "f16", "questions": Q, "steps": steps, "temperature": tau,
+            "ms_per_step": round(1e3 * step_s, 3), "tokens_per_s": round(Q * steps / dt, 1),
+            "hbm_bytes_per_step": round(w_bytes + kv_bytes), "hbm_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "scores_finite_after_trace": finite,
+            "note": "per step: the LM head over the last rows, Gumbel-max sampling, one row per question through "
+                    "every layer (its K/V appended to the question's cache); includes the one cache relayout"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -304,6 +349,9 @@ def main() -> int:
                     help="shared steps of the dense 1.5B choice workload for its prefix-reuse speedup "
                          "(with 2 unshared steps), run after the timed workload when that is another "
                          "workload; 0 = skip")
+    ap.add_argument("--trace-steps", type=int, default=16,
+                    help="reasoning-trace decode steps on the dense 1.5B choice workload after the timed "
+                         "workload (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with HIP events")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -417,6 +465,8 @@ def main() -> int:
     r.free()
     if wname != REUSE_WORKLOAD and args.reuse_steps > 0:
         result["prefix_reuse"] = prefix_reuse(args.reuse_steps, 2)
+    if args.trace_steps > 0:
+        result["reasoning_trace"] = reasoning_trace(args.trace_steps)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the CPU")
         P0 = len(wl.prefix(0))

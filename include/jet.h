@@ -162,6 +162,38 @@ int jet_prefill_prefix(jet_model *model, int32_t n_q, const int64_t *prefix_offs
                        const int32_t *prefix_tokens, jet_prefix **out);
 
 /*
+ * jet_generate_trace - optional reasoning (Section 3.4; Figure 1): sample a
+ * trace of n_steps tokens once per question and freeze it into the question's
+ * retained prefix, so that later jet_score_candidates calls score every
+ * candidate conditional on x_q || trace_q.
+ *   prefix: made by jet_prefill_prefix from this model (or extended by an
+ *     earlier call); extended in place: afterwards it describes prefixes of
+ *     P_q + n_steps tokens (the retained attention caches are laid out again
+ *     once per call, with room for the trace after each question).
+ *   n_steps: tokens per question (>= 0; 0 changes nothing).
+ *   temperature: >= 0 and finite. Token t of question q is
+ *     argmax_v (z_v / temperature + G(seed, q, t, v)) over the full
+ *     vocabulary, z the logits of the model's next-token distribution at
+ *     that point; temperature 0 takes argmax_v z_v. Equal keys go to the
+ *     lowest token id. G is Gumbel noise, -log(-log U), with U from output
+ *     1 + (q << 38 | t << 18 | v) of a SplitMix64 stream seeded with `seed`
+ *     (top 53 bits, mapped to the open interval (0, 1)); q is the question's
+ *     index in the prefix, t = 0 .. n_steps - 1 within this call. The paper
+ *     fixes no sampler; this Gumbel-max form draws from softmax(z /
+ *     temperature) and needs no probabilities materialised.
+ *   seed: any 64-bit value.
+ *   out_tokens: host or device, int32[n_q * n_steps] (question-major), may be
+ *     NULL.
+ * Limits: n_steps < 2^20, n_q < 2^26, vocab <= 2^18; P_q + n_steps <= max_ctx.
+ * Errors: JET_E_INVALID (arguments, a prefix of another model; the prefix is
+ *   unchanged), JET_E_CAPACITY (max_ctx; unchanged), JET_E_OOM (before any
+ *   change: unchanged), JET_E_DEVICE (the prefix is then in an unspecified
+ *   state and may only be freed).
+ */
+int jet_generate_trace(jet_model *model, jet_prefix *prefix, int32_t n_steps, float temperature, uint64_t seed,
+                       int32_t *out_tokens);
+
+/*
  * jet_score_candidates - teacher-forced log-likelihood of every candidate
  * (Section 3.1 Eq. 1-2, Section 3.2 Eq. 3).
  *   q_cand_offsets: host, int64[n_q + 1] (n_q of the prefix); candidate j

@@ -161,6 +161,15 @@ template <class C, int EPI>
 __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> g) {
   using T = typename C::type;
   extern __shared__ uint4 lds[];
+  if (gridDim.y > 1) {
+    // split K (plain operands, fp32 store): workgroup row y takes K columns
+    // [y Kc, (y + 1) Kc) and writes its partial sums to slice y of out
+    const int kc = g.K / (int)gridDim.y;
+    g.A += (int64_t)blockIdx.y * kc;
+    g.B += (int64_t)blockIdx.y * kc;
+    g.K = g.KA = g.KB = kc;
+    g.out = (float *)g.out + (int64_t)blockIdx.y * g.M * g.ldo;
+  }
   const int nt_m = (g.M + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
   int tm, tn;
   tile_coords(nt_m, nt_n, &tm, &tn);
@@ -401,6 +410,43 @@ static hipError_t run_epi(int epi, const void *A, int64_t lda, const void *B, in
 }
 
 int gemm_k_step(int dtype) { return dtype == 1 ? CfgF::BK : BigB::BK; }
+
+// Fixed-order sum of the split-K partials: out (+)= sum over s of part[s].
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restrict__ part, int S, int M, int N,
+                                                            float *__restrict__ out, int64_t ldo, int add) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)M * N) return;
+  const int r = (int)(i / N), c = (int)(i % N);
+  float v = 0.0f;
+  for (int s = 0; s < S; ++s) v += part[((int64_t)s * M + r) * N + c];
+  float *o = out + (int64_t)r * ldo + c;
+  *o = add ? *o + v : v;
+}
+
+int gemm_splitk_ways(int dtype, int pair, int M, int N, int K) {
+  if (dtype != 2 || pair) return 1;
+  const int tiles = ((M + HalfS::BM - 1) / HalfS::BM) * ((N + HalfS::BN - 1) / HalfS::BN);
+  int s = 1;
+  while (s < 16 && tiles * s < 256 && K % (2 * s * HalfS::BK) == 0 && K / (2 * s) >= 512) s *= 2;
+  return s;
+}
+
+hipError_t launch_gemm_splitk(int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+                              int S, float *part, void *out, int64_t ldo, float oscale, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (S < 2 || K % (S * HalfS::BK) || (epi != EPI_STORE_F32 && epi != EPI_RESID_ADD)) return hipErrorInvalidValue;
+  static const hipError_t once = allow_lds<HalfS>((const void *)gemm_kernel<HalfS, 0>);
+  if (once != hipSuccess) return once;
+  GemmArgs<f16> g{(const f16 *)A, (const f16 *)B, lda, ldb, M, N, K, K, K, part, N, 0, oscale, QkvRope{}};
+  const int tiles = ((M + HalfS::BM - 1) / HalfS::BM) * ((N + HalfS::BN - 1) / HalfS::BN);
+  hipLaunchKernelGGL((gemm_kernel<HalfS, 0>), dim3(tiles, S), dim3(HalfS::NT), HalfS::LDS_BYTES, st, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t n = (int64_t)M * N;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S, M, N,
+                     (float *)out, ldo, epi == EPI_RESID_ADD ? 1 : 0);
+  return hipGetLastError();
+}
 
 // Workgroups of gemm_kernel<C, EPI> the device holds at once (0 if unknown).
 template <class C, int EPI>

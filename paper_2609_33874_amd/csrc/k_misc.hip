@@ -386,4 +386,142 @@ hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// reasoning trace: cache layout, K/V append, sampling
+// ---------------------------------------------------------------------------
+
+// Question q's rows [offs[q], offs[q+1]) of every block of an [nblk][S_old]
+// row cache go to rows offs[q] + q extra + i of the [nblk][S_new] cache.
+__global__ __launch_bounds__(256) void kv_relayout_kernel(const uint4 *__restrict__ src, uint4 *__restrict__ dst,
+                                                          const int64_t *__restrict__ offs, int64_t S_old,
+                                                          int64_t S_new, int64_t row_chunks, int extra) {
+  const int q = blockIdx.x, blk = blockIdx.y;
+  const int64_t r0 = offs[q], n = (offs[q + 1] - r0) * row_chunks;
+  const uint4 *s = src + ((int64_t)blk * S_old + r0) * row_chunks;
+  uint4 *d = dst + ((int64_t)blk * S_new + r0 + (int64_t)q * extra) * row_chunks;
+  for (int64_t c = threadIdx.x; c < n; c += 256) d[c] = s[c];
+}
+
+hipError_t launch_kv_relayout(const void *src, void *dst, const int64_t *offs, int n_q, int nblk, int64_t S_old,
+                              int64_t S_new, int64_t row_bytes, int extra, hipStream_t st) {
+  if (n_q <= 0 || nblk <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kv_relayout_kernel, dim3(n_q, nblk), dim3(256), 0, st, (const uint4 *)src, (uint4 *)dst, offs,
+                     S_old, S_new, row_bytes / 16, extra);
+  return hipGetLastError();
+}
+
+// Row r of every block of tmp [nblk][R] goes to row slot[r] of the same block
+// of cache [nblk][S].
+__global__ __launch_bounds__(64) void kv_append_kernel(const uint4 *__restrict__ tmp, uint4 *__restrict__ cache,
+                                                       const int32_t *__restrict__ slot, int R, int64_t S,
+                                                       int64_t row_chunks) {
+  const int r = blockIdx.x, blk = blockIdx.y;
+  const uint4 *s = tmp + ((int64_t)blk * R + r) * row_chunks;
+  uint4 *d = cache + ((int64_t)blk * S + slot[r]) * row_chunks;
+  for (int64_t c = threadIdx.x; c < row_chunks; c += 64) d[c] = s[c];
+}
+
+hipError_t launch_kv_append(const void *tmp, void *cache, const int32_t *slot, int R, int nblk, int64_t S,
+                            int64_t row_bytes, hipStream_t st) {
+  if (R <= 0 || nblk <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kv_append_kernel, dim3(R, nblk), dim3(64), 0, st, (const uint4 *)tmp, (uint4 *)cache, slot, R,
+                     S, row_bytes / 16);
+  return hipGetLastError();
+}
+
+// SplitMix64 (Steele, Lea and Flood, 2014): output i + 1 of the generator
+// seeded with `seed`, i.e. the mix of seed + (i + 1) * golden gamma.
+__device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, uint64_t i) {
+  uint64_t z = seed + (i + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Gumbel noise of (question q, step t, token v): -log(-log U), U the top 53
+// bits of the counter's output mapped to the open interval (0, 1).
+__device__ __forceinline__ double gumbel_at(uint64_t seed, int q, int t, int v) {
+  const uint64_t i = ((uint64_t)q << 38) | ((uint64_t)t << 18) | (uint64_t)v;
+  const double u = ((double)(splitmix64_at(seed, i) >> 11) + 0.5) * 0x1p-53;
+  return -log(-log(u));
+}
+
+// Row r, slice y of the vocabulary (gridDim.y slices): the slice's largest
+// key_v = z_v / tau + G_v (tau > 0) or z_v (tau = 0) and its token, the
+// lowest v among equal keys, v = -1 if no key is a number.
+constexpr int kSampleSplit = 32;
+
+__global__ __launch_bounds__(256) void sample_part_kernel(const float *__restrict__ logits, int64_t ldl, int V,
+                                                          double tau, uint64_t seed, int q0, int t,
+                                                          double *__restrict__ pk, int *__restrict__ pv) {
+  __shared__ double bk[256];
+  __shared__ int bv[256];
+  const int r = blockIdx.x, y = blockIdx.y, tid = threadIdx.x;
+  const int per = (V + kSampleSplit - 1) / kSampleSplit, v0 = y * per, v1 = min(V, v0 + per);
+  const float *z = logits + (int64_t)r * ldl;
+  double best = 0.0;
+  int arg = -1;
+  for (int v = v0 + tid; v < v1; v += 256) {
+    const double key = tau > 0.0 ? (double)z[v] / tau + gumbel_at(seed, q0 + r, t, v) : (double)z[v];
+    if (key == key && (arg < 0 || key > best)) {  // v ascends: equal keys keep the lower v
+      best = key;
+      arg = v;
+    }
+  }
+  bk[tid] = best;
+  bv[tid] = arg;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) {
+      const int va = bv[tid], vb = bv[tid + o];
+      const double ka = bk[tid], kb = bk[tid + o];
+      if (vb >= 0 && (va < 0 || kb > ka || (kb == ka && vb < va))) {
+        bk[tid] = kb;
+        bv[tid] = vb;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    pk[(int64_t)r * kSampleSplit + y] = bk[0];
+    pv[(int64_t)r * kSampleSplit + y] = bv[0];
+  }
+}
+
+// The row's token: the best of its slices (slices in vocabulary order, so
+// the first of equal keys has the lowest v).
+__global__ __launch_bounds__(64) void sample_pick_kernel(const double *__restrict__ pk, const int *__restrict__ pv,
+                                                         int R, int32_t *__restrict__ tokens, int64_t ld_tok) {
+  const int r = blockIdx.x * 64 + threadIdx.x;
+  if (r >= R) return;
+  double best = 0.0;
+  int arg = -1;
+  for (int y = 0; y < kSampleSplit; ++y) {
+    const int v = pv[(int64_t)r * kSampleSplit + y];
+    const double k = pk[(int64_t)r * kSampleSplit + y];
+    if (v >= 0 && (arg < 0 || k > best)) {
+      best = k;
+      arg = v;
+    }
+  }
+  tokens[(int64_t)r * ld_tok] = arg;
+}
+
+int sample_scratch_bytes(int R) { return R * kSampleSplit * (int)(sizeof(double) + sizeof(int)); }
+
+hipError_t launch_sample(const float *logits, int64_t ldl, int R, int V, double tau, uint64_t seed, int q0, int t,
+                         void *scratch, int32_t *tokens, int64_t ld_tok, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  double *pk = (double *)scratch;
+  int *pv = (int *)(pk + (int64_t)R * kSampleSplit);
+  hipLaunchKernelGGL(sample_part_kernel, dim3(R, kSampleSplit), dim3(256), 0, st, logits, ldl, V, tau, seed, q0, t,
+                     pk, pv);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sample_pick_kernel, dim3((R + 63) / 64), dim3(64), 0, st, pk, pv, R, tokens, ld_tok);
+  return hipGetLastError();
+}
+
 }  // namespace jetk

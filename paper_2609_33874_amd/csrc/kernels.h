@@ -25,6 +25,13 @@ struct QkvRope {
   void *k_cache, *v_cache;  // [planes][Hkv][S][128]
   int64_t kv_ps, S, slot0;
 };
+// Split-K for GEMMs of few rows (fp16, plain operands): the number of K
+// chunks worth running (1 = none), and the launch: S chunks of K / S columns
+// each write fp32 partial sums to part [S][M][N], then a fixed-order sum
+// stores them (EPI_STORE_F32) or adds them (EPI_RESID_ADD) to out.
+int gemm_splitk_ways(int dtype, int pair, int M, int N, int K);
+hipError_t launch_gemm_splitk(int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+                              int S, float *part, void *out, int64_t ldo, float oscale, hipStream_t st);
 // Whether launch_gemm_qkv_rope can run this problem (head_dim 128 and a tile
 // configuration whose waves cover whole heads).
 bool gemm_qkv_rope_ok(int dtype, int pair, int M, int N, int head_dim);
@@ -179,6 +186,25 @@ hipError_t launch_convert_bf16_to_f32(const uint16_t *src, int64_t n, float *dst
 hipError_t launch_convert_bf16_to_f16(const uint16_t *src, int64_t n, float scale, void *dst,
                                       unsigned long long *inexact, hipStream_t st);
 
+
+// ---- reasoning trace (decode) ----
+// Question q's rows [offs[q], offs[q + 1]) of each of nblk blocks of an
+// [nblk][S_old] cache of rows (row_bytes each, a multiple of 16) are copied
+// to rows offs[q] + q * extra + i of an [nblk][S_new] cache (room for extra
+// rows after each question).
+hipError_t launch_kv_relayout(const void *src, void *dst, const int64_t *offs, int n_q, int nblk, int64_t S_old,
+                              int64_t S_new, int64_t row_bytes, int extra, hipStream_t st);
+// Row r of each block of tmp [nblk][R] to row slot[r] of cache [nblk][S].
+hipError_t launch_kv_append(const void *tmp, void *cache, const int32_t *slot, int R, int nblk, int64_t S,
+                            int64_t row_bytes, hipStream_t st);
+// tokens[r * ld_tok] = argmax_v (z[r][v] / tau + G(seed, q0 + r, t, v)), or
+// argmax_v z[r][v] when tau = 0; lowest v among equal keys, -1 if no logit is
+// a number. G: Gumbel noise from SplitMix64 output 1 + (q << 38 | t << 18 | v)
+// of the stream seeded with seed (V < 2^18, t < 2^20, q < 2^26).
+// scratch: sample_scratch_bytes(R) bytes of device memory.
+int sample_scratch_bytes(int R);
+hipError_t launch_sample(const float *logits, int64_t ldl, int R, int V, double tau, uint64_t seed, int q0, int t,
+                         void *scratch, int32_t *tokens, int64_t ld_tok, hipStream_t st);
 
 // ---- mixture-of-experts FFN (k_moe.hip) ----
 constexpr int kMoeMaxExperts = 512;

@@ -610,6 +610,18 @@ Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, int 
     LAUNCH(jetk::launch_gemm_q8(epi, A, lda, B, Bs, (int)M, (int)N, (int)K, out, ldo, oscale, m->st));
     return Status::ok();
   }
+  // decode steps (one row per question): too few output tiles to fill the
+  // device, so K is split across workgroups and summed in a fixed order
+  if (m->splitk && (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD)) {
+    const int S = jetk::gemm_splitk_ways(m->kdt, pair, (int)M, (int)N, (int)K);
+    if (S > 1) {
+      float *part;
+      TRY(ws_t<float>(m, "splitk_part", (size_t)(S * M * N), &part));
+      LAUNCH(jetk::launch_gemm_splitk(epi, A, lda, B, ldb, (int)M, (int)N, (int)K, S, part, out, ldo, oscale,
+                                      m->st));
+      return Status::ok();
+    }
+  }
   LAUNCH(jetk::launch_gemm(m->kdt, epi, A, lda, B, ldb, (int)M, (int)N, (int)K, pair, out, ldo, oscale, m->st));
   return Status::ok();
 }
@@ -1231,6 +1243,202 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
 }
 
 // ---------------------------------------------------------------------------
+// reasoning trace (Section 3.4): sampled once per question, frozen into the
+// retained prefix
+// ---------------------------------------------------------------------------
+
+// Extends every question's prefix by n sampled tokens. Step t samples token
+// t of each question from the prefix's last row (the prefix's first-token
+// distribution at t = 0) and then runs that token through the model at
+// position P_q + t as one new row per question: its attention reads the
+// question's retained K/V (its own row included, appended first), its
+// delta-rule layers continue the question's state and convolution tail in
+// place. The caches are laid out again once, with room for the n rows after
+// each question, so the prefix stays a plain prefix of P_q + n tokens.
+Status generate(jet_model *m, jet_prefix *p, int32_t n, float tau, uint64_t seed, int32_t *out) {
+  const ModelHeader &h = m->h;
+  if (n < 0) return Status::err(JET_E_INVALID, "n_steps must be >= 0");
+  if (!(tau >= 0.0f) || !std::isfinite(tau)) return Status::err(JET_E_INVALID, "temperature must be finite and >= 0");
+  const int32_t nq = p->n_q;
+  if (n >= (1 << 20) || nq >= (1 << 26) || h.vocab > (1 << 18))
+    return Status::err(JET_E_INVALID, "trace counters: n_steps < 2^20, n_q < 2^26 and vocab <= 2^18");
+  const std::vector<int64_t> offs = p->prefix_offsets;
+  for (int32_t q = 0; q < nq; ++q)
+    if (offs[q + 1] - offs[q] + n > m->max_ctx)
+      return Status::err(JET_E_CAPACITY, "prefix " + std::to_string(q) + " plus the trace is longer than max_ctx");
+  if (n == 0) return Status::ok();
+  struct SplitK {  // split-K GEMMs for the decode steps of this call only
+    jet_model *m;
+    explicit SplitK(jet_model *mm) : m(mm) { m->splitk = true; }
+    ~SplitK() { m->splitk = false; }
+  } splitk_scope(m);
+  const bool out_dev = out && is_device_ptr(out);
+  const int64_t T = p->T, T2 = T + (int64_t)nq * n, V = h.vocab;
+  std::vector<int64_t> offs2((size_t)nq + 1);
+  for (int32_t q = 0; q <= nq; ++q) offs2[(size_t)q] = offs[(size_t)q] + (int64_t)q * n;
+  m->rt_which = -1;
+
+  // Every buffer is allocated before the prefix changes; once the caches are
+  // laid out again only a device error can stop the call (the prefix is then
+  // in an unspecified state and may only be freed).
+  const int64_t nblk = m->anp * h.n_kv_heads;
+  const int64_t row_bytes = h.head_dim * (int64_t)m->esz;
+  const int64_t R = nq;
+  std::vector<void *> fresh;  // new K then V cache of each attention layer
+  for (int64_t l = 0; l < h.n_layers; ++l) {
+    if (m->layers[(size_t)l].gdn) continue;
+    for (int kv = 0; kv < 2; ++kv) {
+      void *nb;
+      TRY(palloc(p, (size_t)(nblk * T2 * row_bytes), &nb));
+      fresh.push_back(nb);
+    }
+  }
+  int64_t *d_offs;
+  int32_t *d_tok, *d_zero_t;
+  float *logits;
+  void *kt, *vt;
+  TRY(upload(m, "gen_offs", offs, &d_offs));
+  TRY(ws_t<int32_t>(m, "gen_tok", (size_t)(R * n), &d_tok));
+  TRY(ws_t<float>(m, "gen_logits", (size_t)(R * V), &logits));
+  TRY(ws(m, "gen_k", (size_t)(nblk * R * row_bytes), &kt));
+  TRY(ws(m, "gen_v", (size_t)(nblk * R * row_bytes), &vt));
+  void *samp;
+  TRY(ws(m, "gen_sample", (size_t)jetk::sample_scratch_bytes((int)R), &samp));
+  TRY(upload(m, "gen_zero_t", std::vector<int32_t>((size_t)R, 0), &d_zero_t));
+  // attention caches laid out again with n free rows after each question
+  size_t fi = 0;
+  for (int64_t l = 0; l < h.n_layers; ++l) {
+    if (m->layers[(size_t)l].gdn) continue;
+    for (int kv = 0; kv < 2; ++kv) {
+      void *&buf = kv ? p->vcache[(size_t)l] : p->kcache[(size_t)l];
+      void *nb = fresh[fi++];
+      {
+        KTimer t(m, JET_K_OTHER, 0, 0);
+        LAUNCH(jetk::launch_kv_relayout(buf, nb, d_offs, nq, (int)nblk, T, T2, row_bytes, n, m->st));
+      }
+      // the old buffer goes back to the model's pool (later work on the
+      // stream that reuses it runs after the copy)
+      for (size_t i = 0; i < p->allocs.size(); ++i)
+        if (p->allocs[i].first == buf) {
+          m->pool.push_back({p->allocs[i].second, buf});
+          p->bytes -= p->allocs[i].second;
+          p->allocs.erase(p->allocs.begin() + (std::ptrdiff_t)i);
+          break;
+        }
+      buf = nb;
+    }
+  }
+
+  const int64_t gH = h.gdn_heads;
+  for (int32_t t = 0; t < n; ++t) {
+    // token t of every question from the current last rows
+    TRY(run_gemm(m, JET_K_LMHEAD, jetk::EPI_STORE_F32, p->f_last, m->np * h.d, m->pair, m->lm_head, h.d, R, V, h.d,
+                 logits, V, m->is_lm));
+    {
+      KTimer tm(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_sample(logits, V, (int)R, (int)V, (double)tau, seed, 0, t, samp, d_tok + t, n, m->st));
+    }
+    // ... and through the model at positions P_q + t
+    std::vector<int32_t> pos((size_t)R), idx((size_t)R), slot((size_t)R);
+    QDesc qd;
+    for (int32_t q = 0; q < nq; ++q) {
+      const int64_t P = offs[(size_t)q + 1] - offs[(size_t)q];
+      pos[(size_t)q] = (int32_t)(P + t);
+      idx[(size_t)q] = q * n + t;
+      slot[(size_t)q] = (int32_t)(offs2[(size_t)q] + P + t);
+      qd.qrow0.push_back(q);
+      qd.nrows.push_back(1);
+      qd.pre_slot0.push_back(offs2[(size_t)q]);
+      qd.pre_len.push_back((int32_t)(P + t + 1));
+      qd.suf_row0.push_back(0);
+      qd.suf_len.push_back(0);
+    }
+    int32_t *d_pos, *d_idx, *d_slot;
+    TRY(upload(m, "gen_pos", pos, &d_pos));
+    TRY(upload(m, "gen_idx", idx, &d_idx));
+    TRY(upload(m, "gen_slot", slot, &d_slot));
+    AttnPlan plan;
+    TRY(plan_attention(m, 1, qd, "gen_at_", &plan));
+    GdnPlan gp;
+    if (h.hybrid) {
+      // the convolution tail of question q is a ring of its last 3 input
+      // rows: before step t, row j back sits in slot (t + 3 - j) % 3, and
+      // the step's row replaces the oldest (slot t % 3) once it is read
+      std::vector<int32_t> hist((size_t)R * 3), tslot((size_t)R);
+      std::vector<jetk::GdnSeq> seqs;
+      for (int32_t q = 0; q < nq; ++q) {
+        for (int j = 1; j <= 3; ++j) hist[(size_t)(q * 3 + j - 1)] = -2 - (q * 3 + (t + 3 - j) % 3);
+        tslot[(size_t)q] = q * 3 + t % 3;
+        seqs.push_back({q, 1, q, q});
+      }
+      TRY(upload(m, "gen_ghist", hist, &gp.hist));
+      TRY(upload(m, "gen_gtslot", tslot, &gp.tail_slot));
+      TRY(upload(m, "gen_gseqs", seqs, &gp.seqs));
+      gp.nseq = (int)seqs.size();
+      gp.tok_heads = (double)R * (double)gH;
+    }
+    WaveBufs b;
+    TRY(wave_bufs(m, R, &b));
+    {
+      KTimer tm(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_embed(m->edt, m->embed, d_tok, d_idx, (int)R, (int)h.d, b.resid, m->st));
+    }
+    for (int64_t l = 0; l < h.n_layers; ++l) {
+      const Layer &ly = m->layers[(size_t)l];
+      if (ly.gdn) {
+        TRY(gdn_layer(m, ly, b, R, gp, p->conv_tail[(size_t)l], p->S_pre[(size_t)l], p->S_pre[(size_t)l]));
+        TRY(ffn(m, ly, b, R));
+        continue;
+      }
+      TRY(attn_in(m, ly, b, R, d_pos, kt, vt, R, 0));
+      {
+        KTimer tm(m, JET_K_OTHER, 0, 0);
+        LAUNCH(jetk::launch_kv_append(kt, p->kcache[(size_t)l], d_slot, (int)R, (int)nblk, T2, row_bytes, m->st));
+        LAUNCH(jetk::launch_kv_append(vt, p->vcache[(size_t)l], d_slot, (int)R, (int)nblk, T2, row_bytes, m->st));
+      }
+      TRY(run_attention(m, plan, b.q, R, b.att, p->kcache[(size_t)l], p->vcache[(size_t)l], T2, nullptr, nullptr, 0,
+                        nullptr, d_zero_t));
+      TRY(attn_out(m, ly, b, R));
+      TRY(ffn(m, ly, b, R));
+    }
+    KTimer tm(m, JET_K_OTHER, 0, 0);
+    LAUNCH(jetk::launch_rmsnorm(m->kdt, m->pair, b.resid, nullptr, m->final_norm, (int)R, (int)h.d, (float)h.rms_eps,
+                                p->f_last, m->st));
+  }
+  // convolution tails back to the order the scoring path reads (oldest first)
+  if (h.hybrid && n % 3) {
+    const int64_t gC = 2 * gH * h.gdn_dk + gH * h.gdn_dv;
+    std::vector<int32_t> rot((size_t)nq * 3);
+    for (int32_t q = 0; q < nq; ++q)
+      for (int s2 = 0; s2 < 3; ++s2) rot[(size_t)(q * 3 + s2)] = q * 3 + (n + s2) % 3;
+    int32_t *d_rot;
+    float *tmp;
+    TRY(upload(m, "gen_rot", rot, &d_rot));
+    TRY(ws_t<float>(m, "gen_tail", (size_t)(nq * 3 * gC), &tmp));
+    for (int64_t l = 0; l < h.n_layers; ++l) {
+      if (!m->layers[(size_t)l].gdn) continue;
+      KTimer tm(m, JET_K_OTHER, 0, 0);
+      LAUNCH(jetk::launch_gather_rows(p->conv_tail[(size_t)l], gC * 4, d_rot, nq * 3, tmp, m->st));
+      HIPC(hipMemcpyAsync(p->conv_tail[(size_t)l], tmp, (size_t)(nq * 3 * gC) * 4, hipMemcpyDeviceToDevice, m->st));
+    }
+  }
+  TRY(run_lmhead(m, p->f_last, nq, p->lse_last));
+  std::vector<int32_t> toks((size_t)(R * n));
+  HIPC(hipMemcpyAsync(toks.data(), d_tok, toks.size() * 4, hipMemcpyDeviceToHost, m->st));
+  TRY(sync(m));
+  for (int32_t v : toks)
+    if (v < 0) return Status::err(JET_E_DEVICE, "sampling met no finite logit");
+  p->prefix_offsets = offs2;
+  p->T = T2;
+  m->stats.prefix_tokens += R * n;
+  if (out) {
+    if (out_dev) HIPC(hipMemcpy(out, toks.data(), toks.size() * 4, hipMemcpyHostToDevice));
+    else std::memcpy(out, toks.data(), toks.size() * 4);
+  }
+  return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
 // candidate scoring
 // ---------------------------------------------------------------------------
 
@@ -1536,6 +1744,21 @@ extern "C" int jet_prefill_prefix(jet_model *model, int32_t n_q, const int64_t *
     return fail(s);
   }
   *out = p;
+  return JET_OK;
+}
+
+extern "C" int jet_generate_trace(jet_model *model, jet_prefix *prefix, int32_t n_steps, float temperature,
+                                  uint64_t seed, int32_t *out_tokens) {
+  clear_error();
+  if (!model || !prefix) return fail(Status::err(JET_E_INVALID, "model or prefix is NULL"));
+  if (prefix->m != model) return fail(Status::err(JET_E_INVALID, "prefix was not made from this model"));
+  if (hipSetDevice(model->device) != hipSuccess) return fail(Status::err(JET_E_DEVICE, "hipSetDevice failed"));
+  Status s = generate(model, prefix, n_steps, temperature, seed, out_tokens);
+  if (!s) {
+    (void)hipStreamSynchronize(model->st);
+    drain_timers(model);
+    return fail(s);
+  }
   return JET_OK;
 }
 

@@ -106,6 +106,7 @@ struct jet_model {
   size_t arena_cap = 0, arena_top = 0, arena_mark = 0;
   std::map<std::string, std::pair<size_t, size_t>> arena_map;
   hipError_t scratch_status = hipSuccess;  // lookup of the device's scratch at load
+  bool splitk = false;  // run_gemm may split K (decode steps of jet_generate_trace)
 };
 
 struct jet_prefix {

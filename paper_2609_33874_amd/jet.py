@@ -26,7 +26,8 @@ KERNEL_CLASSES = ["gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "lmhead", "a
 ERROR_NAMES = {1: "JET_E_INVALID", 2: "JET_E_CAPACITY", 3: "JET_E_OOM", 4: "JET_E_DEVICE", 5: "JET_E_IO"}
 
 # every symbol include/jet.h declares
-EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_score_candidates", "jet_score_candidates_noalloc", "jet_decide",
+EXPORTS = ["jet_model_load", "jet_prefill_prefix", "jet_generate_trace", "jet_score_candidates",
+           "jet_score_candidates_noalloc", "jet_decide",
            "jet_answer_classes", "jet_evaluate", "jet_candidate_layout", "jet_stats_get", "jet_stats_reset", "jet_model_info",
            "jet_routes_get", "jet_prefix_free", "jet_model_free", "jet_last_error"]
 
@@ -73,6 +74,7 @@ def lib() -> ctypes.CDLL:
         P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         L.jet_model_load.argtypes = [ctypes.c_char_p, ctypes.POINTER(jet_load_opts), ctypes.POINTER(P)]
         L.jet_prefill_prefix.argtypes = [P, I32, P, P, ctypes.POINTER(P)]
+        L.jet_generate_trace.argtypes = [P, P, I32, ctypes.c_float, ctypes.c_uint64, P]
         L.jet_score_candidates.argtypes = [P, P, P, P, P, P, P]
         L.jet_score_candidates_noalloc.argtypes = [P, P, P, P, P, P, P]
         L.jet_decide.argtypes = [I32, I32, P, P, P, P, P]
@@ -135,6 +137,21 @@ def jet_prefill_prefix(model, prefix_offsets, prefix_tokens):
     h = ctypes.c_void_p()
     _check(lib().jet_prefill_prefix(model, n_q, po, pt, ctypes.byref(h)))
     return h
+
+
+def jet_generate_trace(model, prefix, n_q: int, n_steps: int, temperature: float = 0.0, seed: int = 0, out=None):
+    """Extends every question of `prefix` by n_steps sampled tokens (in place).
+    Returns the tokens as int32 [n_q, n_steps] (host), or writes them into
+    `out` (a contiguous int32 tensor or array of n_q * n_steps, host or device)
+    and returns it."""
+    if out is None:
+        out = np.empty((n_q, max(int(n_steps), 0)), np.int32)
+    ot, keep = _ptr(out, np.int32)
+    if isinstance(out, np.ndarray) and keep is not out:
+        raise TypeError("out must be a contiguous int32 array")
+    _check(lib().jet_generate_trace(model, prefix, int(n_steps), float(temperature),
+                                    ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ot))
+    return out
 
 
 def jet_score_candidates(model, prefix, q_cand_offsets, cand_tok_offsets, cand_tokens,

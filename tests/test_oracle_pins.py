@@ -681,3 +681,78 @@ def test_duplicates_and_causality(pin_dense_path):
     np.testing.assert_allclose(tok[8:11], tok[0:3], atol=1e-12)   # y2 shares its first 3 tokens
     assert abs(tok[11] - tok[3]) > 1e-6
     np.testing.assert_allclose(tok[12:14], tok[0:2], atol=1e-12)  # the 2-token prefix of y
+
+
+# --------------------------------------------------------------------------
+# Section 3.4: reasoning traces (Gumbel-max sampling, the reading used here)
+# --------------------------------------------------------------------------
+
+from oracle import generate as og  # noqa: E402
+
+
+def test_splitmix64_reference_outputs():
+    """The first outputs of SplitMix64 seeded with 0 are the generator's
+    published reference values."""
+    got = [int(x) for x in og.splitmix64_at(0, np.arange(3))]
+    assert got == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def test_counter_uniforms_are_uniform_and_keyed():
+    u = og.uniform_at(7, 3, 2, np.arange(200_000))
+    assert 0.0 < u.min() and u.max() < 1.0
+    assert abs(u.mean() - 0.5) < 4 * math.sqrt(1 / 12 / len(u))
+    assert abs(u.var() - 1 / 12) < 2e-3
+    # every coordinate of the counter changes the draw
+    base = og.uniform_at(7, 3, 2, 5)
+    for other in (og.uniform_at(8, 3, 2, 5), og.uniform_at(7, 4, 2, 5), og.uniform_at(7, 3, 3, 5),
+                  og.uniform_at(7, 3, 2, 6)):
+        assert other != base
+
+
+def test_gumbel_max_draws_from_tempered_softmax():
+    """argmax(z / tau + G) over fresh counters has the frequencies of
+    softmax(z / tau) (the Gumbel-max property), within 5 standard errors."""
+    z = np.array([0.3, 1.2, -0.5, 0.9, 0.0])
+    tau, n = 0.7, 40_000
+    counts = np.zeros(len(z))
+    for t in range(n):
+        counts[og.first_argmax(og.sample_keys(z, tau, 99, 1, t))] += 1
+    p = scipy.special.softmax(z / tau)
+    se = np.sqrt(p * (1 - p) / n)
+    assert np.all(np.abs(counts / n - p) < 5 * se), (counts / n, p)
+
+
+def test_greedy_keys_and_ties():
+    z = np.array([1.0, 3.0, 3.0, -2.0])
+    np.testing.assert_array_equal(og.sample_keys(z, 0.0, 5, 0, 0), z)
+    assert og.first_argmax(og.sample_keys(z, 0.0, 5, 0, 0)) == 1      # lowest index among equal maxima
+
+
+def test_greedy_trace_is_the_scorer_argmax(pin_hybrid_path):
+    """Each greedy trace token is the most likely next token by the pinned
+    scorer: scoring every vocabulary entry as a one-token candidate after the
+    trace so far (Eq. 2) puts its maximum on the generated token."""
+    model = oracle.Model(pin_hybrid_path)
+    V = model.h["vocab"]
+    x = np.array([3, 17, 250, 9, 400, 44], np.int32)
+    toks, steps = og.generate_trace(model, x, 0, 3, 0.0, 1)
+    seq = list(x)
+    for t in range(3):
+        wl = jet_synth.from_lists([np.asarray(seq, np.int32)], [[np.array([v], np.int32) for v in range(V)]])
+        _, s = oracle.score_unshared(model, wl)
+        assert int(np.argmax(s)) == int(toks[t])
+        assert steps[t]["choice"] == int(toks[t]) and steps[t]["key"] == steps[t]["max_key"]
+        seq.append(int(toks[t]))
+
+
+def test_forced_trace_reports_the_gap(pin_dense_path):
+    model = oracle.Model(pin_dense_path)
+    x = np.array([5, 9, 2, 77], np.int32)
+    toks, _ = og.generate_trace(model, x, 2, 4, 0.9, 7)
+    again, st = og.generate_trace(model, x, 2, 4, 0.9, 7, forced=toks)
+    np.testing.assert_array_equal(again, toks)
+    assert all(s["key"] == s["max_key"] for s in st)
+    other = toks.copy()
+    other[1] = (toks[1] + 1) % model.h["vocab"]
+    _, st2 = og.generate_trace(model, x, 2, 4, 0.9, 7, forced=other)
+    assert st2[1]["key"] < st2[1]["max_key"]
