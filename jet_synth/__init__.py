@@ -29,6 +29,10 @@ int8 exponent per block of 32 consecutive values of a row, e [rows][cols/32];
 the weight is q * 2^e (|q| <= 127). The exponent of a block is the smallest e
 with max|w| <= 127 * 2^e over the block's values w, and q = rint(w / 2^e).
 Other tensors keep bf16 (matrices) or f32 (norm gains, A_log, dt_bias).
+``dtype`` "q4" is the same with 4-bit values: q in -8..7 (two's complement),
+two per byte, value 2i of a row in the low nibble of byte i, then the int8
+block exponents; the exponent of a block is the smallest e with
+max|w| <= 7 * 2^e.
 
 Random numbers: every tensor is split into fixed chunks of ``CHUNK`` elements;
 chunk ``j`` of tensor ``name`` is drawn from a Philox-4x64 counter-based
@@ -50,7 +54,7 @@ from dataclasses import dataclass
 import numpy as np
 
 MAGIC = b"JETMDL01"
-QBLOCK = 32  # values per quantization block of a "q8" matrix
+QBLOCK = 32  # values per quantization block of a "q8" / "q4" matrix
 ALIGN = 4096
 CHUNK = 1 << 22
 # Sampling seed of the paper's experimental protocol (Appendix A); reused here
@@ -135,7 +139,13 @@ MODEL_SPECS: dict[str, dict] = {
     "small_gqa_q8": dict(arch="dense", dtype="q8", d_model=256, n_layers=2,
                          n_heads=6, n_kv_heads=2, head_dim=128, ffn=768,
                          vocab=3000, max_ctx=8192),
+    "small_gqa_q4": dict(arch="dense", dtype="q4", d_model=256, n_layers=2,
+                         n_heads=6, n_kv_heads=2, head_dim=128, ffn=768,
+                         vocab=3000, max_ctx=8192),
     "dense_1p5b_q8": dict(arch="dense", dtype="q8", d_model=1536, n_layers=28,
+                          n_heads=12, n_kv_heads=2, head_dim=128, ffn=8960,
+                          vocab=151936, max_ctx=8192),
+    "dense_1p5b_q4": dict(arch="dense", dtype="q4", d_model=1536, n_layers=28,
                           n_heads=12, n_kv_heads=2, head_dim=128, ffn=8960,
                           vocab=151936, max_ctx=8192),
     "dense_27b_q8": dict(arch="dense", dtype="q8", d_model=5120, n_layers=64,
@@ -143,6 +153,9 @@ MODEL_SPECS: dict[str, dict] = {
                          vocab=151936, max_ctx=8192),
     # Micro quantized decoder for oracle self-checks on the CPU.
     "micro_q8": dict(arch="dense", dtype="q8", d_model=64, n_layers=2,
+                     n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
+                     vocab=512, max_ctx=4096),
+    "micro_q4": dict(arch="dense", dtype="q4", d_model=64, n_layers=2,
                      n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
                      vocab=512, max_ctx=4096),
     # Micro hybrid for oracle self-checks on the CPU: L=4, d=64.
@@ -175,11 +188,11 @@ def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
     """
     s = full_spec(spec)
     d, V, F = s["d_model"], s["vocab"], s["ffn"]
-    q8 = s["dtype"] == "q8"
+    q8 = s["dtype"] in ("q8", "q4")
     out = []
 
     def mat(name, shape, init="normal"):
-        dt = ("q8" if shape[-1] % QBLOCK == 0 else "bf16") if q8 else s["dtype"]
+        dt = (s["dtype"] if shape[-1] % QBLOCK == 0 else "bf16") if q8 else s["dtype"]
         out.append((name, dt, tuple(shape), init))
 
     mt = "bf16" if q8 else s["dtype"]
@@ -259,6 +272,54 @@ def quantize_q8(val: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
     return q.reshape(-1), e.astype(np.int8)
 
 
+def quantize_q4(val: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Blocks of QBLOCK float32 values -> (packed int4 bytes, int8 exponent
+    per block): the smallest e with max|w| <= 7 * 2^e, q = rint(w / 2^e),
+    value 2i in the low nibble of byte i."""
+    blocks = np.asarray(val, np.float32).reshape(-1, QBLOCK)
+    amax = np.abs(blocks).max(axis=1).astype(np.float64)
+    m, x = np.frexp(amax / 7.0)
+    e = np.where(m == 0.5, x - 1, x)       # ceil(log2(amax / 7))
+    e = np.where(amax > 0, e, 0).clip(-126, 126).astype(np.int32)
+    scale = np.ldexp(np.float32(1.0), -e).astype(np.float32)[:, None]
+    q = np.rint(blocks * scale).clip(-8, 7).astype(np.int8).reshape(-1)
+    u = (q.astype(np.uint8) & np.uint8(0x0F))
+    packed = (u[0::2] | (u[1::2] << np.uint8(4))).astype(np.uint8)
+    return packed, e.astype(np.int8)
+
+
+def unpack_q4(packed: np.ndarray) -> np.ndarray:
+    """Packed int4 bytes [..., n / 2] -> int8 values [..., n]."""
+    b = np.asarray(packed, np.uint8)
+    lo = (b & np.uint8(0x0F)).astype(np.int8)
+    hi = (b >> np.uint8(4)).astype(np.int8)
+    lo = np.where(lo > 7, lo - 16, lo).astype(np.int8)
+    hi = np.where(hi > 7, hi - 16, hi).astype(np.int8)
+    out = np.empty(b.shape[:-1] + (2 * b.shape[-1],), np.int8)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out
+
+
+class Q4Raw:
+    """Stored packed int4 values and per-block exponents of a "q4" tensor
+    (rows indexable like the tensor itself, the last dimension whole)."""
+
+    def __init__(self, p: np.ndarray, e: np.ndarray):
+        self.p, self.e = p, e
+
+    @property
+    def shape(self):
+        return self.p.shape[:-1] + (2 * self.p.shape[-1],)
+
+    @property
+    def q(self):
+        return unpack_q4(self.p)
+
+    def __getitem__(self, idx):
+        return Q4Raw(self.p[idx], self.e[idx])
+
+
 class Q8Raw:
     """Stored int8 values and per-block exponents of a "q8" tensor (rows
     indexable like the tensor itself, the last dimension whole)."""
@@ -281,6 +342,12 @@ def _fill_chunk(seed: int, name: str, j: int, std: float, init: str,
         val = np.empty(dq.size, np.float32)
         _fill_chunk(seed, name, j, std, init, val, "f32", zero)
         dq[:], de[:] = quantize_q8(val)
+        return
+    if dtype == "q4":
+        dp, de = dst
+        val = np.empty(2 * dp.size, np.float32)
+        _fill_chunk(seed, name, j, std, init, val, "f32", zero)
+        dp[:], de[:] = quantize_q4(val)
         return
     n = dst.size
     if init == "ones":
@@ -307,6 +374,8 @@ def tensor_nbytes(dtype: str, shape) -> int:
     n = int(np.prod(shape))
     if dtype == "q8":
         return n + n // QBLOCK
+    if dtype == "q4":
+        return n // 2 + n // QBLOCK
     return n * (2 if dtype == "bf16" else 4)
 
 
@@ -348,6 +417,14 @@ def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
                 jobs.append((t["name"], j, t["init"], (q[j * CHUNK:(j + 1) * CHUNK],
                                                        e[j * CHUNK // QBLOCK:(j + 1) * CHUNK // QBLOCK]), "q8"))
             continue
+        if t["dtype"] == "q4":
+            n = int(np.prod(t["shape"]))
+            pk = mm[t["offset"]:t["offset"] + n // 2]
+            e = mm[t["offset"] + n // 2:t["offset"] + t["nbytes"]].view(np.int8)
+            for j in range(0, (n + CHUNK - 1) // CHUNK):
+                jobs.append((t["name"], j, t["init"], (pk[j * CHUNK // 2:(j + 1) * CHUNK // 2],
+                                                       e[j * CHUNK // QBLOCK:(j + 1) * CHUNK // QBLOCK]), "q4"))
+            continue
         n = t["nbytes"] // (2 if t["dtype"] == "bf16" else 4)
         arr = mm[t["offset"]:t["offset"] + t["nbytes"]].view(_np_storage(t["dtype"]))
         for j in range(0, (n + CHUNK - 1) // CHUNK):
@@ -373,7 +450,8 @@ def read_header(path: str) -> dict:
 
 def tensor_raw(path: str, name: str, header: dict | None = None):
     """Memory-mapped raw storage of one tensor: uint16 bf16 bits, float32, or
-    for "q8" a Q8Raw of the int8 values and int8 block exponents."""
+    for "q8" a Q8Raw of the int8 values and int8 block exponents, for "q4" a
+    Q4Raw of the packed int4 values and int8 block exponents."""
     h = header or read_header(path)
     for t in h["tensors"]:
         if t["name"] == name:
@@ -384,6 +462,13 @@ def tensor_raw(path: str, name: str, header: dict | None = None):
                 e = np.memmap(path, dtype=np.int8, mode="r", offset=t["offset"] + n,
                               shape=shape[:-1] + (shape[-1] // QBLOCK,))
                 return Q8Raw(q, e)
+            if t["dtype"] == "q4":
+                n = int(np.prod(shape))
+                pk = np.memmap(path, dtype=np.uint8, mode="r", offset=t["offset"],
+                               shape=shape[:-1] + (shape[-1] // 2,))
+                e = np.memmap(path, dtype=np.int8, mode="r", offset=t["offset"] + n // 2,
+                              shape=shape[:-1] + (shape[-1] // QBLOCK,))
+                return Q4Raw(pk, e)
             return np.memmap(path, dtype=_np_storage(t["dtype"]), mode="r",
                              offset=t["offset"], shape=shape)
     raise KeyError(name)
@@ -476,6 +561,8 @@ WORKLOADS: dict[str, dict] = {
     "micro_moe": dict(model="micro_moe_fp32", Q=4, P=(5, 20), ids="uniform", K=3, m=(1, 5)),
     "small_q8": dict(model="small_gqa_q8", Q=12, P=(40, 300), ids="zipf", K=4, m=(1, 24)),
     "dense_1p5b_q8_k4": dict(model="dense_1p5b_q8", Q=256, P=(150, 900), ids="zipf", K=4, m=(1, 24)),
+    "small_q4": dict(model="small_gqa_q4", Q=12, P=(40, 300), ids="zipf", K=4, m=(1, 24)),
+    "dense_1p5b_q4_k4": dict(model="dense_1p5b_q4", Q=256, P=(150, 900), ids="zipf", K=4, m=(1, 24)),
     "dense_27b_q8_k10": dict(model="dense_27b_q8", Q=64, P=(1024, 4096), ids="zipf", K=10, m=(8, 40)),
 }
 

@@ -36,9 +36,9 @@ import jet_synth
 
 def upcast(raw) -> np.ndarray:
     """Exact conversion of stored weights to float64: bf16 bits, f32, or
-    block-quantized int8 values q with one exponent e per block of
+    block-quantized int8 / int4 values q with one exponent e per block of
     consecutive values along the last dimension (weight = q * 2^e)."""
-    if isinstance(raw, jet_synth.Q8Raw):
+    if isinstance(raw, (jet_synth.Q8Raw, jet_synth.Q4Raw)):
         q = np.asarray(raw.q, np.float64)
         e = np.repeat(np.asarray(raw.e, np.int64), q.shape[-1] // raw.e.shape[-1], axis=-1)
         return np.ldexp(q, e)

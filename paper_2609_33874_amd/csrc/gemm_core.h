@@ -48,21 +48,26 @@ struct GCfg {
   // LOAD 7 (pair-aware): A holds (hi, lo) planes and both are staged, B once
   static constexpr bool PAIRA = LOAD == 7;
   static constexpr bool INTERLEAVED = LOAD == 7 || LOAD == 8;  // the LOAD 7 / 8 schedule
-  static constexpr bool Q8B = LOAD == 9;                       // int8 B with per-block scales
+  // block-quantized B with per-block scales: int8 (LOAD 9) or int4 (LOAD 10)
+  static constexpr int QBITS = LOAD == 9 ? 8 : LOAD == 10 ? 4 : 0;
+  static constexpr bool Q8B = QBITS > 0;
   static constexpr int BROW0 = PAIRA ? 2 * BM : BM;                  // first B row of a stage
-  static constexpr int B_CH = BK / 16;                               // int8 B: 16-byte chunks per row per K step
+  static constexpr int B_CH = Q8B ? BK * QBITS / 128 : BK / 16;     // quantized B: 16-byte chunks per row per K step
   static constexpr int A_PT = BM * CPR / NT;                         // chunks per thread per K step (per plane)
-  static constexpr int B_PT = Q8B ? B_CH * BN / NT : BN * CPR / NT;
+  // quantized B: B_CH * BN chunks per K step, 64 per wave (one direct load
+  // each) or, for int4 tiles of 32 per wave, one load with half the lanes
+  static constexpr int B_PT = Q8B ? (B_CH * BN >= NT ? B_CH * BN / NT : 1) : BN * CPR / NT;
   static constexpr int BUF = Q8B ? BM * CPR + B_CH * BN + BN / 8 : (BROW0 + BN) * CPR;  // chunks per LDS stage
   static constexpr size_t LDS_BYTES = sizeof(uint4) * NSTAGE * BUF;
   static constexpr int RPI = 64 / CPR;  // tile rows per direct-load wave instruction
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/thread mismatch");
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "direct loads fill whole row groups");
   static_assert(BK % 16 == 0, "K step must hold whole MFMA steps");
-  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8 || LOAD == 9, "tile load schedule");
-  static_assert(!Q8B || (BK == 32 && B_CH * BN % (64 * NWAVES) == 0 && BN / 8 == 4 * NWAVES && WN <= 128 &&
-                         128 % WN == 0),
-                "int8 B: one quantization block per K step, whole direct-load rounds, 4 scale chunks per wave");
+  static_assert(LOAD == 0 || LOAD == 2 || LOAD == 4 || LOAD == 7 || LOAD == 8 || LOAD == 9 || LOAD == 10,
+                "tile load schedule");
+  static_assert(!Q8B || (BK == 32 && (B_CH * BN % (64 * NWAVES) == 0 || B_CH * BN == 32 * NWAVES) &&
+                         BN / 8 == 4 * NWAVES && WN <= 128 && 128 % WN == 0),
+                "quantized B: one quantization block per K step, whole direct-load rounds, 4 scale chunks per wave");
   static_assert(INTERLEAVED || Q8B ? NSTAGE >= 2 : LOAD >= 4 ? NSTAGE >= 2 : LOAD == 2 ? NSTAGE >= 3 : NSTAGE == 2,
                 "pipeline depth");
   static_assert(LOAD < 4 || (BK / 16) % 2 == 0, "fragment pipelining alternates two register sets");
@@ -271,6 +276,10 @@ template <int STRIDE, int N, int... I>
 __device__ __forceinline__ void ds_read8_rows(uint2 (&r)[N], uint32_t addr, std::integer_sequence<int, I...>) {
   (ds_read8<I * STRIDE>(r[I], addr), ...);
 }
+template <int STRIDE, int N, int... I>
+__device__ __forceinline__ void ds_read4_rows(uint2 (&r)[N], uint32_t addr, std::integer_sequence<int, I...>) {
+  (ds_read4<I * STRIDE>(r[I].x, addr), ...);
+}
 
 // fp16 fragment of 8 int8 values q (K order) times the power-of-two scale s:
 // (0x6400 | (q + 128)) is the fp16 number 1024 + q + 128, so subtracting
@@ -293,6 +302,30 @@ __device__ __forceinline__ Frag<f16> q8_frag(uint2 raw, uint32_t sbits) {
   return f;
 }
 
+// fp16 fragment of 8 int4 values q (K order, two per byte, low nibble first)
+// times the power-of-two scale s: flipping each nibble's sign bit gives
+// u = q + 8 in 0..15, (0x6400 | u) is the fp16 number 1024 + u, so
+// subtracting 1032 gives q exactly, and q * s is exact.
+__device__ __forceinline__ Frag<f16> q4_frag(uint32_t raw, uint32_t sbits) {
+  const uint32_t x = raw ^ 0x88888888u;
+  const uint32_t lo = x & 0x0F0F0F0Fu, hi = (x >> 4) & 0x0F0F0F0Fu;  // values 0, 2, 4, 6 / 1, 3, 5, 7
+  const _Float16 s = __builtin_bit_cast(_Float16, (uint16_t)sbits);
+  const h2v bias = {(_Float16)1032.0f, (_Float16)1032.0f}, sc = {s, s};
+  // pair i = (value 2i, value 2i + 1) = (byte i of lo, byte i of hi); selector 0x0c gives a zero byte
+  const uint32_t p[4] = {__builtin_amdgcn_perm(hi, lo, 0x0c040c00u) | 0x64006400u,
+                         __builtin_amdgcn_perm(hi, lo, 0x0c050c01u) | 0x64006400u,
+                         __builtin_amdgcn_perm(hi, lo, 0x0c060c02u) | 0x64006400u,
+                         __builtin_amdgcn_perm(hi, lo, 0x0c070c03u) | 0x64006400u};
+  Frag<f16> f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const h2v v = (__builtin_bit_cast(h2v, p[i]) - bias) * sc;
+    f.v[2 * i] = v.x;
+    f.v[2 * i + 1] = v.y;
+  }
+  return f;
+}
+
 // Fragment reads of MFMA step kk of stage `buf`: the A rows (fp16) and the
 // wave's NI raw int8 B fragments (8 bytes each).
 template <class C>
@@ -302,9 +335,16 @@ __device__ __forceinline__ void kk_frags_q8(uint32_t lds_addr, int buf, int kk, 
   const int ra = wm * C::WM + (lane & 31), rbw = wn * C::WN + (lane & 31);
   const uint32_t stage = lds_addr + (uint32_t)(buf * C::BUF) * 16u;
   const uint32_t a = stage + (uint32_t)(ra * C::CPR + (c0 ^ lds_swz<C>(ra))) * 16u;
-  const uint32_t b = stage + (uint32_t)(C::BM * C::CPR + kk * C::BN + rbw) * 16u + (uint32_t)((lane >> 5) * 8);
   ds_read_rows<32 * C::CPR * 16>(fa, a, std::make_integer_sequence<int, C::MI>{});
-  ds_read8_rows<32 * 16>(rb, b, std::make_integer_sequence<int, C::NI>{});
+  if constexpr (C::QBITS == 8) {
+    // chunk kk of the row holds the step's 16 values; 8 bytes per lane half
+    const uint32_t b = stage + (uint32_t)(C::BM * C::CPR + kk * C::BN + rbw) * 16u + (uint32_t)((lane >> 5) * 8);
+    ds_read8_rows<32 * 16>(rb, b, std::make_integer_sequence<int, C::NI>{});
+  } else {
+    // one chunk holds the K step's 32 values (low nibble first); 4 bytes per lane half
+    const uint32_t b = stage + (uint32_t)(C::BM * C::CPR + rbw) * 16u + (uint32_t)(kk * 8 + (lane >> 5) * 4);
+    ds_read4_rows<32 * 16>(rb, b, std::make_integer_sequence<int, C::NI>{});
+  }
 }
 
 // The scales of the wave's NI fragment rows for stage `buf` (NI consecutive
@@ -355,13 +395,25 @@ __device__ __forceinline__ void tile_issue_direct_q8(const f16 *__restrict__ A, 
     __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)gm * lda + k + c * C::EPC),
                                      (lds_void *)(a + blk * 64), 16, 0, 0);
   }
+  if constexpr (C::B_CH * C::BN >= 64 * C::NWAVES) {
 #pragma unroll
-  for (int i = 0; i < C::B_PT; ++i) {
-    const int blk = i * C::NWAVES + wave;
-    const int u = blk * 64 + lane, c = u / C::BN, r = u % C::BN;
-    const int gn = min(n0 + r, N - 1);
-    __builtin_amdgcn_global_load_lds((const void *)(B + (int64_t)gn * ldb + k + c * 16), (lds_void *)(b + blk * 64),
-                                     16, 0, 0);
+    for (int i = 0; i < C::B_PT; ++i) {
+      const int blk = i * C::NWAVES + wave;
+      const int u = blk * 64 + lane, c = u / C::BN, r = u % C::BN;
+      const int gn = min(n0 + r, N - 1);
+      __builtin_amdgcn_global_load_lds((const void *)(B + (int64_t)gn * ldb + k * C::QBITS / 8 + c * 16),
+                                       (lds_void *)(b + blk * 64), 16, 0, 0);
+    }
+  } else {
+    // 32 chunks per wave: one load, lanes 0..31 (every wave issues it, so
+    // each wave's count of loads in flight stays B_PT per K step)
+    constexpr int BPW = C::B_CH * C::BN / C::NWAVES;
+    if (lane < BPW) {
+      const int u = wave * BPW + lane, c = u / C::BN, r = u % C::BN;
+      const int gn = min(n0 + r, N - 1);
+      __builtin_amdgcn_global_load_lds((const void *)(B + (int64_t)gn * ldb + k * C::QBITS / 8 + c * 16),
+                                       (lds_void *)(b + wave * BPW), 16, 0, 0);
+    }
   }
   if (lane < 4) {
     const int u = wave * 4 + lane, gg = min((n0 >> 7) + (u >> 4), NG - 1);
@@ -669,7 +721,9 @@ __device__ __forceinline__ void gemm_tile(const typename C::type *__restrict__ A
 #pragma unroll
         for (int j = 0; j < C::NI; ++j) {
           const uint32_t w = (j >> 1) ? sc.y : sc.x;
-          fb[j] = q8_frag(rb[cur][j], (j & 1) ? w >> 16 : w & 0xffffu);
+          const uint32_t sb = (j & 1) ? w >> 16 : w & 0xffffu;
+          if constexpr (C::QBITS == 8) fb[j] = q8_frag(rb[cur][j], sb);
+          else fb[j] = q4_frag(rb[cur][j].x, sb);
         }
         if (kk == 0) kk_frags_q8<C>(lds_addr, st, 1, lane, wm, wn, fa[nx], rb[nx]);
         if (kk == 0) {

@@ -377,6 +377,9 @@ using LmH = GCfg<f16, 256, 256, 64, 128, 8, 2, 3, 4>;
 // waves, or 128x128 tiles of 4 waves for problems with fewer tiles.
 using Q8B = GCfg<f16, 256, 256, 64, 128, 9, 2, 3, 4>;
 using Q8S = GCfg<f16, 128, 128, 64, 64, 9, 2, 3, 4>;
+// int4 B (packed two per byte), the same schedule
+using Q4B = GCfg<f16, 256, 256, 64, 128, 10, 2, 3, 4>;
+using Q4S = GCfg<f16, 128, 128, 64, 64, 10, 2, 3, 4>;
 
 // Kernels whose LDS exceeds the default 64 KB limit must opt in once.
 template <class C>
@@ -518,7 +521,8 @@ static hipError_t run_gemm_q8(const void *A, int64_t lda, const void *Bq, const 
                               void *out, int64_t ldo, float oscale, hipStream_t st) {
   static const hipError_t once = allow_lds<C>((const void *)gemm_kernel<C, EPI>);
   if (once != hipSuccess) return once;
-  GemmArgs<f16> g{(const f16 *)A, (const f16 *)Bq, lda, K, M, N, K, K, K, out, ldo, 0, oscale, QkvRope{}};
+  GemmArgs<f16> g{(const f16 *)A, (const f16 *)Bq, lda, (int64_t)K * C::QBITS / 8, M, N, K, K, K, out, ldo, 0,
+                  oscale, QkvRope{}};
   g.Bs = Bs;
   const int tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   hipLaunchKernelGGL((gemm_kernel<C, EPI>), dim3(tiles), dim3(C::NT), C::LDS_BYTES, st, g);
@@ -543,6 +547,15 @@ hipError_t launch_gemm_q8(int epi, const void *A, int64_t lda, const void *Bq, c
   const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
   if (big_tiles >= 512) return run_q8_epi<Q8B>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
   return run_q8_epi<Q8S>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+}
+
+hipError_t launch_gemm_q4(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
+                          int K, void *out, int64_t ldo, float oscale, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % 32 != 0) return hipErrorInvalidValue;
+  const int64_t big_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+  if (big_tiles >= 512) return run_q8_epi<Q4B>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
+  return run_q8_epi<Q4S>(epi, A, lda, Bq, Bs, M, N, K, out, ldo, oscale, st);
 }
 
 template <class C, int EPI>

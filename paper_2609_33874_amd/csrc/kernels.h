@@ -54,6 +54,10 @@ int gemm_k_step(int dtype);
 // K must be a multiple of 32.
 hipError_t launch_gemm_q8(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
                           int K, void *out, int64_t ldo, float oscale, hipStream_t st);
+// As launch_gemm_q8 with int4 values: Bq [N][K / 2] bytes, value 2i of a row
+// in the low nibble of byte i, two's complement (-8..7).
+hipError_t launch_gemm_q4(int epi, const void *A, int64_t lda, const void *Bq, const uint16_t *Bs, int M, int N,
+                          int K, void *out, int64_t ldo, float oscale, hipStream_t st);
 hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const void *B, int64_t ldb, int M,
                        int N, int K, int pair, void *out, int64_t ldo, float oscale, hipStream_t st);
 

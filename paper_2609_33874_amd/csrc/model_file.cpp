@@ -155,9 +155,11 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
   if (!arch || arch->kind != JVal::STR || !dt || dt->kind != JVal::STR)
     return Status::err(JET_E_IO, path + ": header lacks arch/dtype");
   if (arch->str != "dense" && arch->str != "hybrid") return Status::err(JET_E_IO, "unknown arch " + arch->str);
-  if (dt->str != "bf16" && dt->str != "f32" && dt->str != "q8") return Status::err(JET_E_IO, "unknown dtype " + dt->str);
+  if (dt->str != "bf16" && dt->str != "f32" && dt->str != "q8" && dt->str != "q4")
+    return Status::err(JET_E_IO, "unknown dtype " + dt->str);
   h->hybrid = arch->str == "hybrid";
-  h->q8 = dt->str == "q8";
+  h->q8 = dt->str == "q8" || dt->str == "q4";
+  h->qbits = dt->str == "q8" ? 8 : dt->str == "q4" ? 4 : 0;
   h->bf16 = dt->str == "bf16" || h->q8;
   bool ok = get_int(root, "d_model", &h->d) && get_int(root, "n_layers", &h->n_layers) &&
             get_int(root, "n_heads", &h->n_heads) && get_int(root, "n_kv_heads", &h->n_kv_heads) &&
@@ -191,11 +193,12 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
     TensorInfo ti;
     const JVal *nm = t.get("name"), *tdt = t.get("dtype"), *sh = t.get("shape");
     if (!nm || nm->kind != JVal::STR || !tdt || tdt->kind != JVal::STR || !sh || sh->kind != JVal::ARR ||
-        (tdt->str != "bf16" && tdt->str != "f32" && tdt->str != "q8"))
+        (tdt->str != "bf16" && tdt->str != "f32" && tdt->str != "q8" && tdt->str != "q4"))
       return Status::err(JET_E_IO, path + ": bad tensor entry");
     ti.name = nm->str;
     ti.bf16 = tdt->str == "bf16";
-    ti.q8 = tdt->str == "q8";
+    ti.q8 = tdt->str == "q8" || tdt->str == "q4";
+    ti.qbits = tdt->str == "q8" ? 8 : tdt->str == "q4" ? 4 : 0;
     int64_t numel = 1;
     for (auto &s : sh->arr) {
       int64_t dim = 0;
@@ -207,8 +210,11 @@ Status read_model_header(const std::string &path, ModelHeader *h) {
     if (!get_int(t, "offset", &ti.offset) || !get_int(t, "nbytes", &ti.nbytes))
       return Status::err(JET_E_IO, path + ": tensor lacks offset/nbytes");
     if (ti.q8 && (ti.shape.empty() || ti.shape.back() % 32 != 0))
-      return Status::err(JET_E_IO, path + ": q8 tensor " + ti.name + " needs a last dimension multiple of 32");
-    if (ti.nbytes != (ti.q8 ? numel + numel / 32 : numel * (ti.bf16 ? 2 : 4)))
+      return Status::err(JET_E_IO, path + ": block-quantized tensor " + ti.name +
+                                       " needs a last dimension multiple of 32");
+    if (ti.q8 && h->qbits != ti.qbits)
+      return Status::err(JET_E_IO, path + ": tensor " + ti.name + " is quantized unlike the model");
+    if (ti.nbytes != (ti.q8 ? numel * ti.qbits / 8 + numel / 32 : numel * (ti.bf16 ? 2 : 4)))
       return Status::err(JET_E_IO, path + ": tensor " + ti.name + " size mismatch");
     h->tensors[ti.name] = ti;
   }

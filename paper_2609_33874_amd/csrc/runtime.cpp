@@ -193,10 +193,10 @@ struct Loader {
     std::vector<char> raw;
     raw.swap(host);
     host.resize((size_t)n * 2);
-    const int8_t *q = reinterpret_cast<const int8_t *>(raw.data()), *e = q + n;
+    const int8_t *q = reinterpret_cast<const int8_t *>(raw.data()), *e = q + n * cur.qbits / 8;
     uint16_t *dst = reinterpret_cast<uint16_t *>(host.data());
     for (int64_t i = 0; i < n; ++i) {
-      const float w = std::ldexp((float)q[i], (int)e[i / 32]);
+      const float w = std::ldexp((float)qval(q, i, cur.qbits), (int)e[i / 32]);
       uint32_t u;
       std::memcpy(&u, &w, 4);
       dst[i] = (uint16_t)(u >> 16);  // exact: the low 16 bits are zero
@@ -209,9 +209,17 @@ struct Loader {
 
   // Block-quantized weight rows kept as int8 for the fused GEMM path.
   struct Q8Rows {
-    std::vector<int8_t> q, e;  // [rows][cols], [rows][cols / 32]
+    std::vector<int8_t> q, e;  // [rows][cols] (one value per byte), [rows][cols / 32]
     int64_t rows = 0, cols = 0;
+    int bits = 8;  // storage on the device: int8, or int4 two per byte
   };
+  // Value i of block-quantized storage (int8, or int4 two per byte, low
+  // nibble first, two's complement).
+  static int qval(const int8_t *q, int64_t i, int bits) {
+    if (bits == 8) return q[i];
+    const int b = ((const uint8_t *)q)[i >> 1], u = (i & 1) ? b >> 4 : b & 15;
+    return u >= 8 ? u - 16 : u;
+  }
   Status q8_read(const std::string &name, Q8Rows *w) {
     auto it = m->h.tensors.find(name);
     if (it == m->h.tensors.end()) return Status::err(JET_E_IO, "model file lacks tensor " + name);
@@ -221,9 +229,12 @@ struct Loader {
     TRY(read_tensor_bytes(m->path, t, raw.data()));
     w->rows = t.shape[0];
     w->cols = t.shape[1];
-    const int64_t n = w->rows * w->cols;
-    w->q.assign(reinterpret_cast<const int8_t *>(raw.data()), reinterpret_cast<const int8_t *>(raw.data()) + n);
-    w->e.assign(reinterpret_cast<const int8_t *>(raw.data()) + n, reinterpret_cast<const int8_t *>(raw.data()) + n + n / 32);
+    w->bits = t.qbits;
+    const int64_t n = w->rows * w->cols, qb = n * t.qbits / 8;
+    const int8_t *q = reinterpret_cast<const int8_t *>(raw.data());
+    w->q.resize((size_t)n);
+    for (int64_t i = 0; i < n; ++i) w->q[(size_t)i] = (int8_t)qval(q, i, t.qbits);  // one value per byte here
+    w->e.assign(q + qb, q + qb + n / 32);
     return Status::ok();
   }
   // Rows of several matrices stacked; with interleave, gate/up style: blocks
@@ -231,6 +242,7 @@ struct Loader {
   static Q8Rows q8_stack(const std::vector<Q8Rows> &parts, bool interleave) {
     Q8Rows out;
     out.cols = parts[0].cols;
+    out.bits = parts[0].bits;
     const int64_t eb = out.cols / 32;
     for (auto &p : parts) out.rows += p.rows;
     out.q.resize((size_t)(out.rows * out.cols));
@@ -288,9 +300,17 @@ struct Loader {
         sc[(size_t)(((b * NG + g) * 32 + rr) * 4 + j)] = bits;
       }
     m->f16_inexact += inexact;
-    TRY(dmalloc(m, w.q.size(), q_dev));
+    std::vector<int8_t> packed;
+    const std::vector<int8_t> *dev = &w.q;
+    if (w.bits == 4) {  // two values per byte, value 2i in the low nibble of byte i
+      packed.resize(w.q.size() / 2);
+      for (size_t i = 0; i < packed.size(); ++i)
+        packed[i] = (int8_t)((w.q[2 * i] & 15) | ((w.q[2 * i + 1] & 15) << 4));
+      dev = &packed;
+    }
+    TRY(dmalloc(m, dev->size(), q_dev));
     m->weight_allocs.push_back(*q_dev);
-    HIPC(hipMemcpy(*q_dev, w.q.data(), w.q.size(), hipMemcpyHostToDevice));
+    HIPC(hipMemcpy(*q_dev, dev->data(), dev->size(), hipMemcpyHostToDevice));
     TRY(dmalloc(m, sc.size() * 2, (void **)s_dev));
     m->weight_allocs.push_back(*s_dev);
     HIPC(hipMemcpy(*s_dev, sc.data(), sc.size() * 2, hipMemcpyHostToDevice));
@@ -458,11 +478,11 @@ Status check_shapes(const ModelHeader &h, int dtype) {
   if (h.ffn % 32) return Status::err(JET_E_INVALID, "ffn must be a multiple of 32");
   if (h.q8) {
     if (h.hybrid || h.n_experts)
-      return Status::err(JET_E_INVALID, "block-quantized (q8) models must be dense decoders without experts");
+      return Status::err(JET_E_INVALID, "block-quantized models must be dense decoders without experts");
     if (dtype != JET_F16 && dtype != JET_FP32)
-      return Status::err(JET_E_INVALID, "block-quantized (q8) models run in the JET_F16 and JET_FP32 modes");
+      return Status::err(JET_E_INVALID, "block-quantized models run in the JET_F16 and JET_FP32 modes");
     if (h.d % 128 || (h.n_heads * h.head_dim) % 32 || h.ffn % 64)
-      return Status::err(JET_E_INVALID, "q8 models need d_model a multiple of 128 and ffn of 64");
+      return Status::err(JET_E_INVALID, "block-quantized models need d_model a multiple of 128 and ffn of 64");
   }
   if (h.n_experts) {
     if (h.n_experts > jetk::kMoeMaxExperts || h.top_k < 1 || h.top_k > h.n_experts ||
@@ -603,11 +623,12 @@ Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, int 
   const double out_bytes = (double)M * (double)(epi == jetk::EPI_SWIGLU ? N / 2 * m->np : N) *
                            (epi == jetk::EPI_STORE_F32 || epi == jetk::EPI_RESID_ADD ? 4.0 : (double)m->esz) *
                            (epi == jetk::EPI_RESID_ADD ? 2.0 : 1.0);
-  const double b_bytes = Bs ? (double)(N * K) * (1.0 + 2.0 / 32.0) : (double)(N * K) * (double)m->esz;
+  const double b_bytes = Bs ? (double)(N * K) * (m->h.qbits / 8.0 + 2.0 / 32.0) : (double)(N * K) * (double)m->esz;
   KTimer t(m, cls, gemm_flops(M, N, K), (double)(M * K * (pair ? 2 : 1)) * (double)m->esz + b_bytes + out_bytes);
   if (Bs) {
     if (pair || ldb != K) return Status::err(JET_E_INVALID, "int8 weights: no pair operands, dense rows");
-    LAUNCH(jetk::launch_gemm_q8(epi, A, lda, B, Bs, (int)M, (int)N, (int)K, out, ldo, oscale, m->st));
+    if (m->h.qbits == 4) LAUNCH(jetk::launch_gemm_q4(epi, A, lda, B, Bs, (int)M, (int)N, (int)K, out, ldo, oscale, m->st));
+    else LAUNCH(jetk::launch_gemm_q8(epi, A, lda, B, Bs, (int)M, (int)N, (int)K, out, ldo, oscale, m->st));
     return Status::ok();
   }
   // decode steps (one row per question): too few output tiles to fill the

@@ -292,3 +292,29 @@ def test_dense_1p5b_q8_k4_full():
         ref_tok, ref_sum = oracle.score_unshared(path, sub)
         got_tok, got_sum = gather(wl, tok, sums, idx)
         compare(f"dense_1p5b_q8_k4/q{qs}", sub, got_tok, got_sum, ref_tok, ref_sum, J.JET_F16)
+
+
+@pytest.mark.timeout(900)
+def test_dense_1p5b_q4_k4_full():
+    """Block-quantized 1.5B-shape model (int4 blocks of 32, two per byte,
+    power-of-two scales) in the fp16 mode with the int4 GEMMs: all 256
+    questions on the GPU, the first and the longest-prefix question against
+    the oracle (run on the host here: the oracle dequantizes the stored
+    blocks)."""
+    with model_file("dense_1p5b_q4") as path:
+        wl = jet_synth.make_workload("dense_1p5b_q4_k4")
+        log(f"[fullsize] dense_1p5b_q4_k4: {wl.n_questions} questions, {int(wl.prefix_offsets[-1])} prefix tokens")
+        m = J.jet_model_load(path, dtype=J.JET_F16)
+        try:
+            tok, sums = run(m, wl)
+            info = J.jet_model_info(m)
+        finally:
+            J.jet_model_free(m)
+        log(f"[fullsize] dense_1p5b_q4_k4: weights not exact in fp16: {info['f16_inexact_weights']}")
+        properties(wl, tok, sums)
+        qs = [0, int(np.argmax(np.diff(wl.prefix_offsets)))]
+        sub = wl.subset(qs)
+        idx = [c for q in qs for c in range(int(wl.q_cand_offsets[q]), int(wl.q_cand_offsets[q + 1]))]
+        ref_tok, ref_sum = oracle.score_unshared(path, sub)
+        got_tok, got_sum = gather(wl, tok, sums, idx)
+        compare(f"dense_1p5b_q4_k4/q{qs}", sub, got_tok, got_sum, ref_tok, ref_sum, J.JET_F16)

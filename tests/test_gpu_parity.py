@@ -118,6 +118,8 @@ CASES = [
     # block-quantized weights: dequantized at load (fp32), int8 in the GEMMs (fp16)
     ("small_gqa_q8", "small_q8", J.JET_FP32),
     ("small_gqa_q8", "small_q8", J.JET_F16),
+    ("small_gqa_q4", "small_q4", J.JET_FP32),
+    ("small_gqa_q4", "small_q4", J.JET_F16),
 ]
 
 
@@ -379,17 +381,19 @@ def test_moe_routes_recorded_and_valid(dtype, model_dir):
     check_parity(wl, tok, sums, ref_tok, ref_sum, dtype)
 
 
-def test_q8_model_modes_and_int8_gemm_tiles(model_dir):
-    """Block-quantized model: the modes without an int8 GEMM path are refused;
-    a prefill long enough for 256x256 int8 tiles matches the oracle in fp16."""
-    path = jet_synth.ensure_model("small_gqa_q8", cache_dir=model_dir)
+@pytest.mark.parametrize("spec", ["small_gqa_q8", "small_gqa_q4"])
+def test_block_quantized_modes_and_gemm_tiles(spec, model_dir):
+    """Block-quantized model (int8 or int4 blocks): the modes without a
+    quantized GEMM path are refused; a prefill long enough for 256x256
+    quantized tiles matches the oracle in fp16."""
+    path = jet_synth.ensure_model(spec, cache_dir=model_dir)
     for dt in (J.JET_BF16, J.JET_F16P, J.JET_BF16_SINGLE):
         with pytest.raises(J.JetError) as e:
             J.jet_model_load(path, dtype=dt)
         assert e.value.code == J.JET_E_INVALID
     # 3 questions of ~7.9k prefix tokens: the gate/up GEMM (23.7k x 1536) has
-    # 93 x 6 tiles of 256x256 (>= 512: the 256-row int8 tiles), the others
-    # run 128x128 int8 tiles with a ragged last row tile
+    # 93 x 6 tiles of 256x256 (>= 512: the 256-row quantized tiles), the
+    # others run 128x128 tiles with a ragged last row tile
     rng = np.random.default_rng(3)
     pre = [rng.integers(0, 3000, n).astype(np.int32) for n in (7950, 7900, 7861)]
     cands = [[rng.integers(0, 3000, m).astype(np.int32) for m in (1, 5, 17)], [rng.integers(0, 3000, 9).astype(np.int32)],
@@ -398,4 +402,4 @@ def test_q8_model_modes_and_int8_gemm_tiles(model_dir):
     tok, sums, _ = run_gpu(path, wl, J.JET_F16)
     ref_tok, ref_sum = oracle.score_unshared(path, wl)
     dt, ds = check_parity(wl, tok, sums, ref_tok, ref_sum, J.JET_F16)
-    log(f"[q8] long prefill: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")
+    log(f"[{spec}] long prefill: max|d tok|={dt:.3e} max|d sum|={ds:.3e}")

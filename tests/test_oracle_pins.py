@@ -248,6 +248,47 @@ def test_q8_weights_against_the_bf16_twin(model_dir):
     np.testing.assert_allclose(tok, -math.log(512), rtol=0, atol=1e-12)
 
 
+def test_q4_packing_of_a_hand_built_block():
+    """int4 storage read by hand: byte i holds value 2i in its low nibble and
+    2i+1 in its high nibble, two's complement; the oracle's weight is
+    q * 2^e with the block's own exponent."""
+    vals = np.array([-8, 7, -1, 0, 1, -2, 3, -5] * 4, np.int8)
+    want = bytes([0x78, 0x0F, 0xE1, 0xB3] * 4)
+    packed, e = jet_synth.quantize_q4(vals.astype(np.float32) * np.float32(0.25))
+    # max|w| = 2 = 8 * 2^-2 > 7 * 2^-2: the exponent rises to -1 and the
+    # values halve (rint rounds halves to even)
+    assert int(e[0]) == -1
+    assert np.array_equal(jet_synth.unpack_q4(packed), np.rint(vals / 2.0).astype(np.int8))
+    assert np.array_equal(jet_synth.unpack_q4(np.frombuffer(want, np.uint8)), vals)
+    raw = jet_synth.Q4Raw(np.frombuffer(want, np.uint8)[None, :], np.array([[-3]], np.int8))
+    assert raw.shape == (1, 32)
+    np.testing.assert_array_equal(om.upcast(raw)[0], vals.astype(np.float64) / 8.0)
+
+
+def test_q4_weights_against_the_bf16_twin(model_dir):
+    """int4 blocks: the oracle's dequantized weights of a q4 model lie within
+    half a quantization step (plus bf16 rounding) of the bf16 model drawn from
+    the same seed, and every block's scale is tight (its largest |q| is 4..7)."""
+    pq = jet_synth.ensure_model("micro_q4", cache_dir=model_dir)
+    pb = os.path.join(model_dir, "micro_q4_bf16twin.jetm")
+    if not os.path.exists(pb):
+        jet_synth.write_model(pb, _spec("micro_q4", dtype="bf16"))
+    mq, mb = om.Model(pq), om.Model(pb)
+    checked = 0
+    for t in mq.h["tensors"]:
+        if t["dtype"] != "q4":
+            continue
+        assert t["nbytes"] == int(np.prod(t["shape"])) // 2 + int(np.prod(t["shape"])) // 32
+        raw = jet_synth.tensor_raw(pq, t["name"], mq.h)
+        wq, wb = mq.w(t["name"]), mb.w(t["name"])
+        step = np.ldexp(1.0, np.repeat(np.asarray(raw.e, np.int64), 32, axis=-1))
+        assert np.all(np.abs(wq - wb) <= 0.5 * step + np.abs(wb) * 2.0 ** -8), t["name"]
+        qmax = np.abs(np.asarray(raw.q, np.int32)).reshape(-1, 32).max(axis=1)
+        assert np.all(qmax >= 4) and np.all(qmax <= 7)
+        checked += 1
+    assert checked >= 5
+
+
 def test_rope_identity_and_relative_position():
     rng = np.random.default_rng(2)
     x = rng.normal(size=(1, 3, 32))
