@@ -91,7 +91,7 @@ typedef struct {
   int64_t max_ctx;              /* max positions per sequence; 0 = the file's value */
   int64_t prefill_token_budget; /* max prefix tokens per prefill wave; 0 = no limit.
                                    Waves hold whole questions. */
-  int64_t wave_token_budget;    /* max candidate body tokens per scoring wave;
+  int64_t wave_token_budget;    /* max scored candidate tokens per scoring wave;
                                    0 = no limit. Waves hold whole candidates. */
   int64_t max_device_bytes;     /* cap on the library's device allocations; 0 = none */
   void *hip_stream;             /* hipStream_t to run on; NULL = the null stream */
@@ -118,7 +118,7 @@ typedef struct {
   int64_t prefix_evals;      /* prefixes evaluated (questions over prefill calls) */
   int64_t cand_body_tokens;  /* candidate tokens run through the network (sum of m-1) */
   int64_t scored_tokens;     /* candidate tokens scored (sum of m) */
-  int64_t lm_rows;           /* rows through the LM head */
+  int64_t lm_rows;           /* rows through the LM head (one per scored token) */
   int64_t prefill_waves;
   int64_t score_waves;
   int64_t kernel_launches[JET_K_COUNT];
@@ -207,6 +207,9 @@ int jet_generate_trace(jet_model *model, jet_prefix *prefix, int32_t n_steps, fl
  *     candidate's earlier tokens (same CSR indexing as cand_tokens).
  *   out_cand_sum: host or device, float[N]; s_j, summed in ascending t.
  * Token y_{c,t} sits at position P + t - 1. Candidates never see each other.
+ * log p = z_y - log sum_v exp(z_v), with z_y the very fp32 logit that the
+ * LM head's vocabulary tile adds into the log-sum-exp (one LM-head row per
+ * scored token; the logits are never stored).
  * Errors: JET_E_INVALID (offsets, ids, m = 0, prefix of another model),
  *   JET_E_CAPACITY (P + m - 1 > max_ctx), JET_E_OOM, JET_E_DEVICE.
  */
@@ -228,7 +231,7 @@ int jet_score_candidates(jet_model *model, const jet_prefix *prefix,
  * partials) are carved from a fixed device array of
  * JET_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it has loaded
  * a model on, until the process ends; candidates run in waves of whole
- * candidates sized to fit it (at most the model's wave_token_budget rows).
+ * candidates sized to fit it (at most the model's wave_token_budget tokens).
  * Limits: JET_E_CAPACITY when the call's token tables and one wave holding
  * its longest candidate do not fit the scratch (large mixture-of-experts
  * models need more than it holds). The scratch is shared by every call on

@@ -263,11 +263,16 @@ __global__ __launch_bounds__(C::NT) void gemm_kernel(GemmArgs<typename C::type> 
 // (row, vocabulary split) is written. The logits stay in registers.
 // F holds R rows of K columns: the final hidden rows, or (hi, lo) pairs of
 // them when K = 2 KW (W rows are then read twice).
+// With target (one vocabulary index per row of F), the product of a row with
+// its target's W row is kept as well, zt[row] (unscaled): the very
+// accumulator the log-sum-exp takes in, written by the one lane that holds it.
 template <class C>
 __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::type *__restrict__ W,
                                                           const typename C::type *__restrict__ F, int V, int R,
                                                           int KW, int K, int tiles_per_split, float zscale,
-                                                          float *__restrict__ part_m, float *__restrict__ part_s) {
+                                                          float *__restrict__ part_m, float *__restrict__ part_s,
+                                                          const int32_t *__restrict__ target,
+                                                          float *__restrict__ zt) {
   extern __shared__ uint4 lds[];
   const int n0 = blockIdx.x * C::BN, split = blockIdx.y;
   const int ntiles = (V + C::BM - 1) / C::BM;
@@ -275,15 +280,33 @@ __global__ __launch_bounds__(C::NT) void lmhead_lse_kernel(const typename C::typ
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   float rm[C::NI], rs[C::NI];
+  int tj[C::NI];  // this lane's rows' targets (-1: none)
 #pragma unroll
   for (int j = 0; j < C::NI; ++j) {
     rm[j] = -INFINITY;
     rs[j] = 0.0f;
+    const int row = n0 + wn * C::WN + j * 32 + (lane & 31);
+    tj[j] = target && row < R ? target[row] : -1;
   }
   f32x16 acc[C::MI][C::NI];
   for (int vt = vt0; vt < vt1; ++vt) {
     const int m0 = vt * C::BM;
     gemm_tile<C>(W, KW, F, K, V, R, K, KW, K, m0, n0, lds, acc);
+    // element e of acc[i][j] is vocabulary index vb + 32 i + 8 (e / 4) + e % 4
+    const int vb = m0 + wm * C::WM + 4 * (lane >> 5);
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const int dv = tj[j] - vb;
+      if (dv >= 0 && dv < 32 * C::MI && (dv & 4) == 0) {
+        const int row = n0 + wn * C::WN + j * 32 + (lane & 31);
+        float z = 0.0f;
+#pragma unroll
+        for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) z = dv == 32 * i + 8 * (e >> 2) + (e & 3) ? acc[i][j][e] : z;
+        zt[row] = z;
+      }
+    }
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
       float mx = -INFINITY;
@@ -649,23 +672,27 @@ void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit) {
 
 template <class C>
 static hipError_t run_lmhead(const void *W, const void *F, int V, int R, int K, int pair, int tiles_per_split,
-                             float wscale, float *part_m, float *part_s, hipStream_t st) {
+                             float wscale, float *part_m, float *part_s, const int32_t *target, float *zt,
+                             hipStream_t st) {
   using T = typename C::type;
   static const hipError_t once = allow_lds<C>((const void *)lmhead_lse_kernel<C>);
   if (once != hipSuccess) return once;
   const int nsplit = ((V + C::BM - 1) / C::BM + tiles_per_split - 1) / tiles_per_split;
   dim3 grid((R + C::BN - 1) / C::BN, nsplit);
   hipLaunchKernelGGL((lmhead_lse_kernel<C>), grid, dim3(C::NT), C::LDS_BYTES, st, (const T *)W, (const T *)F, V, R,
-                     K, pair ? 2 * K : K, tiles_per_split, wscale * kLog2e, part_m, part_s);
+                     K, pair ? 2 * K : K, tiles_per_split, wscale * kLog2e, part_m, part_s, target, zt);
   return hipGetLastError();
 }
 
 hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
-                             int tiles_per_split, float wscale, float *part_m, float *part_s, hipStream_t st) {
+                             int tiles_per_split, float wscale, float *part_m, float *part_s, const int32_t *target,
+                             float *zt, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  if (dtype == 0) return run_lmhead<LmB>(W, F, V, R, K, pair, tiles_per_split, wscale, part_m, part_s, st);
-  if (dtype == 2) return run_lmhead<LmH>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, st);
-  return run_lmhead<LmF>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, st);
+  if ((target == nullptr) != (zt == nullptr)) return hipErrorInvalidValue;
+  if (dtype == 0)
+    return run_lmhead<LmB>(W, F, V, R, K, pair, tiles_per_split, wscale, part_m, part_s, target, zt, st);
+  if (dtype == 2) return run_lmhead<LmH>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, target, zt, st);
+  return run_lmhead<LmF>(W, F, V, R, K, 0, tiles_per_split, wscale, part_m, part_s, target, zt, st);
 }
 
 }  // namespace jetk

@@ -138,49 +138,30 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *__restri
 }
 
 __global__ __launch_bounds__(256) void lse_merge_kernel(const float *__restrict__ pm, const float *__restrict__ ps,
-                                                         int nsplit, int R, float *__restrict__ lse) {
+                                                         int nsplit, int R, float *__restrict__ lse,
+                                                         const float *__restrict__ zt, float wscale,
+                                                         float *__restrict__ ell) {
   const int r = blockIdx.x * 256 + threadIdx.x;
   if (r >= R) return;
   float M = -INFINITY;
   for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pm[(int64_t)s * R + r]);
   float S = 0.0f;
   for (int s = 0; s < nsplit; ++s) S += ps[(int64_t)s * R + r] * exp2f(pm[(int64_t)s * R + r] - M);
-  lse[r] = (M + log2f(S)) * kLn2;
+  const float l = (M + log2f(S)) * kLn2;
+  lse[r] = l;
+  if (zt) ell[r] = zt[r] * wscale - l;
 }
 
-// One wave per scored token: ell = <f_row, W[y]> - lse_row.
-template <typename T, bool PAIR>
-__global__ __launch_bounds__(256) void gather_logprob_kernel(const int32_t *__restrict__ tokens,
-                                                              const int32_t *__restrict__ lm_row, int n_out,
-                                                              int row_base, const T *__restrict__ f_body,
-                                                              const float *__restrict__ lse_body,
-                                                              const T *__restrict__ f_last,
-                                                              const float *__restrict__ lse_last,
-                                                              const T *__restrict__ W, int d, float wscale,
-                                                              float *__restrict__ ell) {
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (i >= n_out) return;
-  const int r = lm_row[i];
-  const T *f;
-  float lse;
-  const int64_t ld = (int64_t)d * (PAIR ? 2 : 1);
-  if (r < 0) {
-    f = f_last + (int64_t)(-r - 1) * ld;
-    lse = lse_last[-r - 1];
-  } else {
-    f = f_body + (int64_t)(r - row_base) * ld;
-    lse = lse_body[r - row_base];
-  }
-  const T *w = W + (int64_t)tokens[i] * d;
-  float acc = 0.0f;
-  for (int k = lane; k < d; k += 64) {
-    float fv = to_f<T>(f[k]);
-    if constexpr (PAIR) fv += to_f<T>(f[d + k]);
-    acc += fv * to_f<T>(w[k]);
-  }
-  acc = warp_sum(acc);
-  if (lane == 0) ell[i] = acc * wscale - lse;
+// Rows of the final hidden states in scored-token order: a candidate body
+// row, or the question's last prefix row for a candidate's first token.
+__global__ __launch_bounds__(256) void token_rows_kernel(const int32_t *__restrict__ lm_row, int row_base,
+                                                          const uint4 *__restrict__ f_body,
+                                                          const uint4 *__restrict__ f_last, int64_t row_chunks,
+                                                          uint4 *__restrict__ dst) {
+  const int i = blockIdx.x, r = lm_row[i];
+  const uint4 *s = r < 0 ? f_last + (int64_t)(-r - 1) * row_chunks : f_body + (int64_t)(r - row_base) * row_chunks;
+  uint4 *d = dst + (int64_t)i * row_chunks;
+  for (int64_t c = threadIdx.x; c < row_chunks; c += 256) d[c] = s[c];
 }
 
 __global__ __launch_bounds__(256) void segment_sum_kernel(const float *__restrict__ ell, const int64_t *__restrict__ off,
@@ -301,34 +282,21 @@ hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int3
   return hipGetLastError();
 }
 
-hipError_t launch_lse_merge(const float *pm, const float *ps, int nsplit, int R, float *lse, hipStream_t st) {
+hipError_t launch_lse_merge(const float *pm, const float *ps, int nsplit, int R, float *lse, const float *zt,
+                            float wscale, float *ell, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(lse_merge_kernel, dim3((R + 255) / 256), dim3(256), 0, st, pm, ps, nsplit, R, lse);
+  if (zt && !ell) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3((R + 255) / 256), dim3(256), 0, st, pm, ps, nsplit, R, lse, zt, wscale,
+                     ell);
   return hipGetLastError();
 }
 
-hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
-                                 int row_base, const void *f_body, const float *lse_body, const void *f_last,
-                                 const float *lse_last, const void *W, int d, float wscale, float *ell,
-                                 hipStream_t st) {
-  if (n_out <= 0) return hipSuccess;
-  dim3 grid((n_out + 3) / 4);
-  if (dtype == 0 && pair)
-    hipLaunchKernelGGL((gather_logprob_kernel<bf16, true>), grid, dim3(256), 0, st, tokens, lm_row, n_out, row_base,
-                       (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d, wscale,
-                       ell);
-  else if (dtype == 0)
-    hipLaunchKernelGGL((gather_logprob_kernel<bf16, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
-                       row_base, (const bf16 *)f_body, lse_body, (const bf16 *)f_last, lse_last, (const bf16 *)W, d,
-                       wscale, ell);
-  else if (dtype == 2)
-    hipLaunchKernelGGL((gather_logprob_kernel<f16, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
-                       row_base, (const f16 *)f_body, lse_body, (const f16 *)f_last, lse_last, (const f16 *)W, d,
-                       wscale, ell);
-  else
-    hipLaunchKernelGGL((gather_logprob_kernel<float, false>), grid, dim3(256), 0, st, tokens, lm_row, n_out,
-                       row_base, (const float *)f_body, lse_body, (const float *)f_last, lse_last,
-                       (const float *)W, d, wscale, ell);
+hipError_t launch_token_rows(const int32_t *lm_row, int n, int row_base, const void *f_body, const void *f_last,
+                             int64_t row_bytes, void *dst, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(token_rows_kernel, dim3(n), dim3(256), 0, st, lm_row, row_base, (const uint4 *)f_body,
+                     (const uint4 *)f_last, row_bytes / 16, (uint4 *)dst);
   return hipGetLastError();
 }
 

@@ -65,12 +65,17 @@ hipError_t launch_gemm(int dtype, int epi, const void *A, int64_t lda, const voi
 // lmhead_plan gives the vocabulary tiles per workgroup and the split count.
 void lmhead_plan(int dtype, int V, int R, int *tiles_per_split, int *nsplit);
 // F: [R][K] rows, or [R][2K] (hi, lo) pairs when pair. The logits are the
-// products times wscale.
+// products times wscale. target (int32[R], values in [0, V), or -1) and zt
+// (float[R]) together or both NULL: zt[r] = the product of row r with
+// W[target[r]] as accumulated for the log-sum-exp (unscaled); rows with -1
+// are not written.
 hipError_t launch_lmhead_lse(int dtype, const void *W, const void *F, int V, int R, int K, int pair,
-                             int tiles_per_split, float wscale, float *part_m, float *part_s, hipStream_t st);
-// lse[r] = ln(sum over splits) from the partials.
+                             int tiles_per_split, float wscale, float *part_m, float *part_s, const int32_t *target,
+                             float *zt, hipStream_t st);
+// lse[r] = ln(sum over splits) from the partials; with zt (else NULL),
+// also ell[r] = zt[r] * wscale - lse[r].
 hipError_t launch_lse_merge(const float *part_m, const float *part_s, int nsplit, int R, float *lse,
-                            hipStream_t st);
+                            const float *zt, float wscale, float *ell, hipStream_t st);
 
 // Attention work item: one (question, kv head, block of at most
 // attn_slots_per_item query slots).
@@ -166,13 +171,10 @@ hipError_t launch_rope_scatter(int dtype, int pair, const float *qkv, const int3
                                const float *sin_t, int R, int Hq, int Hkv, int hd, void *q_out, int64_t q_ps,
                                void *k_cache, void *v_cache, int64_t kv_ps, int64_t S, int64_t slot0,
                                hipStream_t st);
-// ell[i] = wscale * dot(f_row, W[y_i]) - lse_row for output i; the row is
-// f_body[lm_row[i] - row_base] or, when lm_row[i] < 0, f_last[-lm_row[i] - 1];
-// rows are [hi | lo] pairs when pair.
-hipError_t launch_gather_logprob(int dtype, int pair, const int32_t *tokens, const int32_t *lm_row, int n_out,
-                                 int row_base, const void *f_body, const float *lse_body, const void *f_last,
-                                 const float *lse_last, const void *W, int d, float wscale, float *ell,
-                                 hipStream_t st);
+// dst row i = f_body row lm_row[i] - row_base or, when lm_row[i] < 0,
+// f_last row -lm_row[i] - 1 (rows of row_bytes bytes, a multiple of 16).
+hipError_t launch_token_rows(const int32_t *lm_row, int n, int row_base, const void *f_body, const void *f_last,
+                             int64_t row_bytes, void *dst, hipStream_t st);
 // s[c] = sum of ell[off[c] - off[0] .. off[c+1] - off[0]) in ascending order.
 hipError_t launch_segment_sum(const float *ell, const int64_t *off, int n_cand, float *s, hipStream_t st);
 // dst row i = src row idx[i], rows of row_bytes (a multiple of 16) bytes.

@@ -648,21 +648,26 @@ Status run_gemm(jet_model *m, int cls, int epi, const void *A, int64_t lda, int 
 }
 
 // LM head + online LSE over R rows of F (compute dtype) -> lse[R] (fp32).
-Status run_lmhead(jet_model *m, const void *F, int64_t R, float *lse) {
+// With target (device int32[R]): ell[r] = log p(target[r]) = z - lse, z the
+// target's logit as the LM-head tile accumulated it for the log-sum-exp
+// (Section 3.1 Eq. 2).
+Status run_lmhead(jet_model *m, const void *F, int64_t R, float *lse, const int32_t *target = nullptr,
+                  float *ell = nullptr) {
   if (R <= 0) return Status::ok();
   const int64_t V = m->h.vocab, d = m->h.d;
   int tps = 1, nsplit = 1;
   jetk::lmhead_plan(m->kdt, (int)V, (int)R, &tps, &nsplit);
-  float *pm, *ps;
+  float *pm, *ps, *zt = nullptr;
   TRY(ws_t<float>(m, "lm_pm", (size_t)(nsplit * R), &pm));
   TRY(ws_t<float>(m, "lm_ps", (size_t)(nsplit * R), &ps));
+  if (target) TRY(ws_t<float>(m, "lm_zt", (size_t)R, &zt));
   {
     KTimer t(m, JET_K_LMHEAD, gemm_flops(R, V, d), (double)(V * d + R * d * m->np) * (double)m->esz);
     LAUNCH(jetk::launch_lmhead_lse(m->kdt, m->lm_head, F, (int)V, (int)R, (int)d, m->pair, tps, m->is_lm, pm, ps,
-                                   m->st));
+                                   target, zt, m->st));
   }
   KTimer t2(m, JET_K_OTHER, 0, 0);
-  LAUNCH(jetk::launch_lse_merge(pm, ps, nsplit, (int)R, lse, m->st));
+  LAUNCH(jetk::launch_lse_merge(pm, ps, nsplit, (int)R, lse, zt, m->is_lm, ell, m->st));
   m->stats.lm_rows += R;
   return Status::ok();
 }
@@ -1127,7 +1132,6 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     TRY(palloc(p, kv_bytes, &p->vcache[(size_t)l]));
   }
   TRY(palloc(p, (size_t)(n_q * h.d) * m->esz * m->np, &p->f_last));
-  TRY(palloc(p, (size_t)n_q * 4, (void **)&p->lse_last));
 
   const int32_t *d_tok = tokens;
   if (!tok_dev) {
@@ -1256,7 +1260,6 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
     q0 = q1;
   }
   m->rt_which = -1;
-  TRY(run_lmhead(m, p->f_last, n_q, p->lse_last));
   TRY(sync(m));
   m->stats.prefix_tokens += T;
   m->stats.prefix_evals += n_q;
@@ -1443,7 +1446,6 @@ Status generate(jet_model *m, jet_prefix *p, int32_t n, float tau, uint64_t seed
       HIPC(hipMemcpyAsync(p->conv_tail[(size_t)l], tmp, (size_t)(nq * 3 * gC) * 4, hipMemcpyDeviceToDevice, m->st));
     }
   }
-  TRY(run_lmhead(m, p->f_last, nq, p->lse_last));
   std::vector<int32_t> toks((size_t)(R * n));
   HIPC(hipMemcpyAsync(toks.data(), d_tok, toks.size() * 4, hipMemcpyDeviceToHost, m->st));
   TRY(sync(m));
@@ -1486,8 +1488,8 @@ void wave_bytes_bound(const jet_model *m, double *per_row, double *fixed) {
   jetk::lmhead_plan(m->kdt, (int)h.vocab, 1, &tps, &nsplit);
   double r = d * 4 + nqkv * 4 + d * std::max(pe, pa) + 2 * hq * pa + (double)h.ffn * pe;  // wave buffers
   r += 2.0 * (double)(h.n_kv_heads * h.head_dim) * esz * m->anp;                           // own K / V
-  r += d * esz * m->np + 4;                                                                  // final-norm rows, lse
-  r += 2.0 * nsplit * 4;                                                                     // LM-head partials
+  r += 2 * (d * esz * m->np + 8);  // final-norm rows, and again in scored-token order; lse, target logit
+  r += 2.0 * nsplit * 4;            // LM-head partials
   r += 40.0 * (double)h.n_kv_heads + 28;  // attention items and per-question tables (at most one question per row)
   double f = 64.0 * 256;                  // alignment of every buffer
   if (h.hybrid) {
@@ -1567,11 +1569,11 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
     const double room = (double)m->arena_cap - (double)m->arena_mark - fixed;
     const int64_t fit = room > per_row ? (int64_t)(room / per_row) : 0;
     int64_t longest = 0;
-    for (int64_t c = 0; c < N; ++c) longest = std::max<int64_t>(longest, cto[c + 1] - cto[c] - 1);
+    for (int64_t c = 0; c < N; ++c) longest = std::max<int64_t>(longest, cto[c + 1] - cto[c]);
     if (fit < std::max<int64_t>(longest, 1))
       return Status::err(JET_E_CAPACITY, "the scratch of " + std::to_string(m->arena_cap) +
                                              " bytes holds the call's tables and " + std::to_string(fit) +
-                                             " candidate rows per wave; the longest candidate needs " +
+                                             " candidate tokens per wave; the longest candidate has " +
                                              std::to_string(longest));
     budget = budget > 0 ? std::min(budget, fit) : fit;
   }
@@ -1580,11 +1582,12 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
   while (c0 < N) {
     if (m->arena) arena_reset(m);
     int64_t c1 = c0 + 1;
-    while (c1 < N && (budget <= 0 || row0(c1 + 1) - row0(c0) <= budget)) ++c1;
+    // a wave holds whole candidates, at most `budget` scored tokens (each
+    // token is one LM-head row; body rows are one fewer per candidate)
+    while (c1 < N && (budget <= 0 || cto[c1 + 1] - cto[c0] <= budget)) ++c1;
     const int64_t r0 = row0(c0), r1 = row0(c1), R = r1 - r0;
     const int64_t t0 = cto[c0], t1 = cto[c1];
     void *f_body = nullptr;
-    float *lse_body = nullptr;
     if (R > 0) {
       QDesc qd;
       int64_t c = c0;
@@ -1647,19 +1650,27 @@ Status score(jet_model *m, const jet_prefix *p, const int64_t *qco, const int64_
       }
       m->rt_which = -1;
       TRY(ws(m, "f_body", (size_t)(R * h.d) * m->esz * m->np, &f_body));
-      TRY(ws_t<float>(m, "lse_body", (size_t)R, &lse_body));
       {
         KTimer t(m, JET_K_OTHER, 0, 0);
         LAUNCH(jetk::launch_rmsnorm(dt, m->pair, b.resid, nullptr, m->final_norm, (int)R, (int)h.d,
                                     (float)h.rms_eps, f_body, m->st));
       }
-      TRY(run_lmhead(m, f_body, R, lse_body));
     }
+    // one LM-head row per scored token, in token order: the candidate's
+    // previous body row, or the question's last prefix row for its first
+    // token; the head's tiles keep each row's target logit
+    const int64_t nt = t1 - t0, row_bytes = h.d * m->esz * m->np;
+    void *f_tok;
+    float *lse_tok;
+    TRY(ws(m, "f_tok", (size_t)(nt * row_bytes), &f_tok));
+    TRY(ws_t<float>(m, "lse_tok", (size_t)nt, &lse_tok));
     {
       KTimer t(m, JET_K_OTHER, 0, 0);
-      LAUNCH(jetk::launch_gather_logprob(dt, m->pair, d_tok + t0, d_lm + t0, (int)(t1 - t0), (int)r0, f_body,
-                                         lse_body, p->f_last, p->lse_last, m->lm_head, (int)h.d, m->is_lm, d_ell + t0,
-                                         m->st));
+      LAUNCH(jetk::launch_token_rows(d_lm + t0, (int)nt, (int)r0, f_body, p->f_last, row_bytes, f_tok, m->st));
+    }
+    TRY(run_lmhead(m, f_tok, nt, lse_tok, d_tok + t0, d_ell + t0));
+    {
+      KTimer t(m, JET_K_OTHER, 0, 0);
       LAUNCH(jetk::launch_segment_sum(d_ell + t0, d_cto + c0, (int)(c1 - c0), d_sum + c0, m->st));
     }
     m->stats.score_waves++;
@@ -1691,7 +1702,6 @@ void free_model(jet_model *m) {
     p->S_pre.clear();
     p->conv_tail.clear();
     p->f_last = nullptr;
-    p->lse_last = nullptr;
     p->m = nullptr;
   }
   m->live.clear();

@@ -118,7 +118,6 @@ struct jet_prefix {
   std::vector<float *> S_pre;        // per layer (delta-rule only), [n_q][H][dv][dk]
   std::vector<float *> conv_tail;    // per layer (delta-rule only), [n_q][kc-1][C]
   void *f_last = nullptr;            // [n_q][planes * d] final-normed last prefix rows
-  float *lse_last = nullptr;         // [n_q]
   std::vector<std::pair<void *, size_t>> allocs;  // (buffer, allocated bytes)
   size_t bytes = 0;
 };
