@@ -231,6 +231,221 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
   }
 }
 
+// Chunked form of the same recurrence on the matrix cores (the WY / UT
+// representation of a product of generalised Householder updates). Within a
+// chunk of GC steps t = 0..GC-1 that starts from state S0, with
+// g_t = sum_{u <= t} log alpha_u and Gamma[t][s] = exp(g_t - g_s):
+//   delta_t = beta_t (v_t - alpha_t S_{t-1} k_t) is the row added at step t,
+//   S_t = alpha_t S_{t-1} + delta_t k_t^T, so unrolling the chunk gives
+//   (I + A) Delta = diag(beta) (V - diag(e^g) K S0^T),
+//     A[t][s] = beta_t Gamma[t][s] (k_t . k_s) for s < t (strictly lower),
+//   O = diag(e^g) Q S0^T + (Gamma o Q K^T)_{s <= t} Delta,
+//   S_end = e^{g_last} S0 + Delta^T diag(exp(g_last - g)) K.
+// The products run as fp16 MFMAs with fp32 accumulation; the triangular
+// solve for Delta is a forward substitution in fp32 (one thread per column of
+// Delta); the state stays in fp32 accumulators for the whole sequence and is
+// rounded to fp16 only as an operand of the next chunk's products.
+//
+// One workgroup of 4 waves per (sequence, head); wave w owns rows
+// 32w .. 32w + 31 of the state (4 MFMA tiles of 32 x 32) and the same columns
+// of the chunk's outputs. LDS rows of fp16 operands are stored in 16-byte
+// chunks whose position is XOR-swizzled by the row, so the 32 rows a fragment
+// read touches fall in distinct banks.
+constexpr int GC = 32;  // chunk length
+
+// element (r, c) of a [*][128] / [*][32] fp16 array
+__device__ __forceinline__ int sw128(int r, int c) { return r * 128 + ((((c >> 3) ^ (r & 15)) << 3) | (c & 7)); }
+__device__ __forceinline__ int sw32(int r, int c) { return r * 32 + ((((c >> 3) ^ ((r >> 2) & 3)) << 3) | (c & 7)); }
+
+// MFMA operand: row r, columns c0 .. c0 + 7 (c0 a multiple of 8)
+__device__ __forceinline__ Frag<f16> frag128(const f16 *a, int r, int c0) {
+  Frag<f16> f;
+  f.v = *reinterpret_cast<const f16x8 *>(a + sw128(r, c0));
+  return f;
+}
+__device__ __forceinline__ Frag<f16> frag32(const f16 *a, int r, int c0) {
+  Frag<f16> f;
+  f.v = *reinterpret_cast<const f16x8 *>(a + sw32(r, c0));
+  return f;
+}
+
+// x, as a value the compiler cannot see through: address arithmetic built on
+// it is redone in every chunk instead of being held in registers across the
+// chunk loop
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+__global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
+  // sh: S0 in fp16 [dv][dk]; once every wave's products with S0 are done its
+  // first 16 KB hold the solve's right-hand side r (fp32 [GC][dv])
+  __shared__ __align__(16) f16 sh[GDN_D * GDN_D];
+  __shared__ __align__(16) f16 kh[GC * GDN_D], qh[GC * GDN_D];  // K, Q rows [t][d]
+  __shared__ __align__(16) f16 kt[GDN_D * GC];                  // K~^T [d][s]
+  __shared__ __align__(16) f16 dt[GDN_D * GC];                  // Delta^T [v][s]
+  __shared__ __align__(16) f16 pm[GC * GC];                     // masked Gamma o Q K^T [t][s]
+  __shared__ __align__(16) float al[GC * GC];                   // A [t][s]
+  __shared__ float gs[GC], bs[GC];
+  float *rr = reinterpret_cast<float *>(sh);
+
+  const int H = g.H;
+  const int si = blockIdx.x / H, h = blockIdx.x % H;
+  const GdnSeq sq = g.seqs[si];
+  const int tid = threadIdx.x, l = tid & 63, lc = l & 31, lh = l >> 5;
+  // the wave index as a scalar: the MFMAs only some waves issue sit behind
+  // scalar branches (an MFMA writes its result whatever the execution mask,
+  // so masking lanes off would not skip it)
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // state rows 32 w + 8 (e / 4) + 4 lh + e % 4, columns 32 j + lc
+  f32x16 sacc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
+      sacc[j][e] = sq.init >= 0 ? g.S_init[(((int64_t)sq.init * H + h) * GDN_D + v) * GDN_D + 32 * j + lc] : 0.0f;
+    }
+
+  for (int c0 = 0; c0 < sq.len; c0 += GC) {
+    const int L = min(GC, sq.len - c0);
+    const int64_t row0 = sq.row0 + c0;
+    const int tid = opaque(threadIdx.x), l = tid & 63, lc = l & 31, lh = l >> 5;
+    __syncthreads();  // the previous chunk's readers of every buffer are done
+    // ---- stage: S0 (fp16), K and Q rows, gates; rows past L are zero
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
+        sh[sw128(v, 32 * j + lc)] = (f16)sacc[j][e];
+      }
+    float4 kr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv;
+      if (t < L) {
+        kv = *reinterpret_cast<const float4 *>(g.k + ((row0 + t) * H + h) * GDN_D + d);
+        qv = *reinterpret_cast<const float4 *>(g.q + ((row0 + t) * H + h) * GDN_D + d);
+      }
+      kr[i] = kv;
+      *reinterpret_cast<uint2 *>(kh + sw128(t, d)) = make_uint2(f2h2(kv.x, kv.y), f2h2(kv.z, kv.w));
+      *reinterpret_cast<uint2 *>(qh + sw128(t, d)) = make_uint2(f2h2(qv.x, qv.y), f2h2(qv.z, qv.w));
+    }
+    // v for this wave's output columns, in the accumulator layout
+    float vr[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
+      vr[e] = t < L ? g.v[((row0 + t) * H + h) * GDN_D + 32 * w + lc] : 0.0f;
+    }
+    if (w == 0) {
+      // log-decay prefix sums (a vanishing alpha is held at e^-80) and gates
+      float la = 0.0f, b = 0.0f;
+      if (l < L) {
+        la = fmaxf(__logf(g.alpha[(row0 + l) * H + h]), -80.0f);
+        b = g.beta[(row0 + l) * H + h];
+      }
+      if (l < GC) gs[l] = la;
+      __builtin_amdgcn_wave_barrier();
+      if (l < GC) {
+        float acc = 0.0f;
+        for (int u = 0; u <= l; ++u) acc += gs[u];
+        bs[l] = b;
+        __builtin_amdgcn_wave_barrier();
+        gs[l] = acc;
+      }
+    }
+    __syncthreads();
+    // K~^T = (K rows scaled by exp(g_last - g_s)) transposed
+    const float glast = gs[GC - 1];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
+      const float f = __expf(glast - gs[t]);
+      kt[sw32(d, t)] = (f16)(kr[i].x * f);
+      kt[sw32(d + 1, t)] = (f16)(kr[i].y * f);
+      kt[sw32(d + 2, t)] = (f16)(kr[i].z * f);
+      kt[sw32(d + 3, t)] = (f16)(kr[i].w * f);
+    }
+    // ---- products with S0 (every wave, its 32 state rows as output columns)
+    //      and K K^T (wave 0) / Q K^T (wave 1)
+    f32x16 xk, xq, xt;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) xk[e] = xq[e] = xt[e] = 0.0f;
+#pragma unroll
+    for (int d0 = 0; d0 < GDN_D; d0 += 16) {
+      const Frag<f16> fk = frag128(kh, lc, d0 + 8 * lh), fq = frag128(qh, lc, d0 + 8 * lh);
+      const Frag<f16> fs = frag128(sh, 32 * w + lc, d0 + 8 * lh);
+      mma32(xk, fk, fs);
+      mma32(xq, fq, fs);
+      if (w == 0) mma32(xt, fk, fk);
+      if (w == 1) mma32(xt, fq, fk);
+    }
+    __syncthreads();  // S0 no longer read: its space takes r
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
+      const float eg = __expf(gs[t]);
+      rr[t * GDN_D + 32 * w + lc] = bs[t] * (vr[e] - eg * xk[e]);
+      xq[e] *= eg;  // this wave's output tile starts as diag(e^g) Q S0^T
+      const int s = lc;
+      if (w == 0) al[t * GC + s] = s < t ? bs[t] * __expf(gs[t] - gs[s]) * xt[e] : 0.0f;
+      if (w == 1) pm[sw32(t, s)] = (f16)(s <= t ? __expf(gs[t] - gs[s]) * xt[e] : 0.0f);
+    }
+    __syncthreads();
+    // ---- forward substitution, one thread per column v of Delta
+    if (tid < GDN_D) {
+      float dl[GC];
+#pragma unroll
+      for (int t = 0; t < GC; ++t) {
+        float x = rr[t * GDN_D + tid];
+#pragma unroll
+        for (int s = 0; s < t; ++s) x -= al[t * GC + s] * dl[s];
+        dl[t] = x;
+      }
+#pragma unroll
+      for (int c = 0; c < GC / 8; ++c) {
+        uint4 u;
+        u.x = f2h2(dl[8 * c], dl[8 * c + 1]);
+        u.y = f2h2(dl[8 * c + 2], dl[8 * c + 3]);
+        u.z = f2h2(dl[8 * c + 4], dl[8 * c + 5]);
+        u.w = f2h2(dl[8 * c + 6], dl[8 * c + 7]);
+        *reinterpret_cast<uint4 *>(dt + sw32(tid, 8 * c)) = u;
+      }
+    }
+    __syncthreads();
+    // ---- O += (Gamma o Q K^T) Delta; S = e^{g_last} S0 + Delta^T K~
+#pragma unroll
+    for (int s0 = 0; s0 < GC; s0 += 16) mma32(xq, frag32(pm, lc, s0 + 8 * lh), frag32(dt, 32 * w + lc, s0 + 8 * lh));
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
+      if (t < L) g.o[((row0 + t) * H + h) * GDN_D + 32 * w + lc] = xq[e];
+    }
+    const float eg = __expf(glast);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[j][e] *= eg;
+#pragma unroll
+      for (int s0 = 0; s0 < GC; s0 += 16)
+        mma32(sacc[j], frag32(dt, 32 * w + lc, s0 + 8 * lh), frag32(kt, 32 * j + lc, s0 + 8 * lh));
+    }
+  }
+  if (sq.fin >= 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
+        g.S_fin[(((int64_t)sq.fin * H + h) * GDN_D + v) * GDN_D + 32 * j + lc] = sacc[j][e];
+      }
+  }
+}
+
 // y = RMSNorm(o) * w * silu(z) per head, written as the A operand of the
 // output projection ([hi | lo] pairs with PAIR).
 template <typename T, bool PAIR>
@@ -268,6 +483,13 @@ hipError_t launch_gdn_recur(const GdnRecurArgs &g, int nseq, hipStream_t st) {
   if (nseq <= 0) return hipSuccess;
   if (g.dk != GDN_D || g.dv != GDN_D) return hipErrorInvalidValue;
   hipLaunchKernelGGL(gdn_recur_kernel, dim3(nseq * g.H), dim3(128), 0, st, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_gdn_chunk(const GdnRecurArgs &g, int nseq, hipStream_t st) {
+  if (nseq <= 0) return hipSuccess;
+  if (g.dk != GDN_D || g.dv != GDN_D) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gdn_chunk_kernel, dim3(nseq * g.H), dim3(256), 0, st, g);
   return hipGetLastError();
 }
 
