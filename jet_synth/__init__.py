@@ -184,7 +184,8 @@ def full_spec(spec: dict | str) -> dict:
 def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
     """(name, storage dtype, shape, init) for every tensor, in file order.
 
-    init is "normal" (i.i.d. N(0, init_std^2)), "ones" or "zeros".
+    init is "normal" (i.i.d. N(0, init_std^2)), "ones", "zeros" or
+    "const:<value>".
     """
     s = full_spec(spec)
     d, V, F = s["d_model"], s["vocab"], s["ffn"]
@@ -215,7 +216,8 @@ def tensor_list(spec: dict) -> list[tuple[str, str, tuple, str]]:
             mat(p + "gdn_wb", (H, d))
             mat(p + "gdn_wa", (H, d))
             out.append((p + "gdn_conv", mt, (2 * H * dk + H * dv, kc), "normal"))
-            out += [(p + "gdn_A_log", "f32", (H,), "zeros"),
+            a_log = float(s.get("gdn_a_log", 0.0))  # optional constant (decay strength)
+            out += [(p + "gdn_A_log", "f32", (H,), f"const:{a_log!r}" if a_log else "zeros"),
                     (p + "gdn_dt_bias", "f32", (H,), "zeros"),
                     (p + "gdn_norm", "f32", (dv,), "ones")]
             mat(p + "gdn_wo", (d, H * dv))
@@ -354,6 +356,8 @@ def _fill_chunk(seed: int, name: str, j: int, std: float, init: str,
         val = np.ones(n, np.float32)
     elif init == "zeros" or zero:
         val = np.zeros(n, np.float32)
+    elif init.startswith("const:"):
+        val = np.full(n, float(init[6:]), np.float32)
     else:
         key = (zlib.crc32(name.encode()) << 32) | j
         g = np.random.Generator(np.random.Philox(key=[seed, key]))

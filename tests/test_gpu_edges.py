@@ -81,6 +81,26 @@ def test_hybrid_short_sequences(dtype, model_dir):
     compare(path, wl, dtype, "hybrid short")
 
 
+@pytest.mark.parametrize("a_log", [2.0, 6.0])
+@pytest.mark.parametrize("dtype", [J.JET_FP32, J.JET_F16])
+def test_hybrid_strong_decay(dtype, a_log, model_dir):
+    """Delta-rule layers with strong decay: alpha = exp(-e^A_log softplus(a +
+    dt_bias)) with softplus of order 1 lies around e^-3..e^-8 for A_log = 2
+    (the chunk's decay products span e^-100 and below) and below e^-150 for
+    A_log = 6 (0 in fp32: the state is forgotten at every step), over
+    prefixes that span several chunks of the chunked recurrence (fp16 mode)
+    with ragged tails."""
+    import os
+    path = os.path.join(model_dir, f"edge_hybrid_decay{int(a_log)}.jetm")
+    if not os.path.exists(path):
+        spec = dict(jet_synth.MODEL_SPECS["small_hybrid_bf16"])
+        spec["gdn_a_log"] = a_log
+        jet_synth.write_model(path, spec)
+    vocab = jet_synth.read_header(path)["vocab"]
+    wl = edge_workload(vocab, [1, 31, 32, 33, 95, 200], [1, 2, 7, 17], seed=14)
+    compare(path, wl, dtype, f"hybrid decay A_log={a_log}")
+
+
 def test_no_candidates(model_dir):
     path = jet_synth.ensure_model("small_gqa_bf16", cache_dir=model_dir)
     m = J.jet_model_load(path, dtype=J.JET_BF16)
