@@ -318,3 +318,37 @@ def test_dense_1p5b_q4_k4_full():
         ref_tok, ref_sum = oracle.score_unshared(path, sub)
         got_tok, got_sum = gather(wl, tok, sums, idx)
         compare(f"dense_1p5b_q4_k4/q{qs}", sub, got_tok, got_sum, ref_tok, ref_sum, J.JET_F16)
+
+
+# The pair-bf16 mode's largest deviation from the stored oracle scores on the
+# sampled questions of every dense and hybrid workload (per token, per
+# candidate), measured with these kernels: the whole-workload check below
+# spends it from the tolerances.
+BF16_DEV_TOK, BF16_DEV_SUM = 2e-4, 6e-4
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,spec", [("dense_1p5b_k4", "dense_1p5b"), ("dense_1p5b_binary", "dense_1p5b"),
+                                       ("dense_1p5b_ordinal", "dense_1p5b"), ("hybrid_4b_k4", "hybrid_4b")])
+def test_benched_mode_on_every_candidate(name, spec):
+    """The mode bench.py times on a workload (single fp16) against the
+    pair-bf16 mode on every token and candidate of the whole workload: the
+    sampled oracle comparisons above bound the pair mode's own error, so the
+    benched mode meets the tolerances on every candidate when it stays within
+    them minus that error of the pair mode."""
+    with model_file(spec) as path:
+        wl = jet_synth.make_workload(name)
+        out = {}
+        for dt in (J.JET_BF16, J.JET_F16):
+            m = J.jet_model_load(path, dtype=dt)
+            try:
+                out[dt] = run(m, wl)
+            finally:
+                J.jet_model_free(m)
+        dt_ = np.abs(out[J.JET_F16][0].astype(np.float64) - out[J.JET_BF16][0]).max()
+        ds_ = np.abs(out[J.JET_F16][1].astype(np.float64) - out[J.JET_BF16][1]).max()
+        log(f"[fullsize] {name}: fp16 against pair-bf16 over {len(wl.cand_tokens)} tokens / {wl.n_candidates} "
+            f"candidates: max|d tok|={dt_:.3e} max|d sum|={ds_:.3e}")
+        from conftest import record_parity
+        record_parity(f"whole/{name}/f16_vs_bf16pair", max_tok=dt_, max_sum=ds_)
+        assert dt_ <= TOK_TOL - BF16_DEV_TOK and ds_ <= SUM_TOL - BF16_DEV_SUM
