@@ -211,7 +211,11 @@ def dense_27b_path():
 def test_dense_27b_k10_full(dtype, dense_27b_path):
     """27B-shape dense decoder (64 layers, d=5120): all 64 questions on the
     GPU; the first question's ten candidates (3.2k-token prefix) and the
-    longest-prefix question's shortest candidate against the oracle."""
+    longest-prefix question's shortest candidate against the oracle. The
+    pair-bf16 mode is the one bench.py times here; f16p meets the tolerances
+    on these samples but not on every candidate of the workload (its longest
+    candidates reach 0.09 per candidate against pair-bf16), which is why it
+    is not the timed mode."""
     golden_parity("dense_27b_k10", dense_27b_path, dtype)
 
 
