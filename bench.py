@@ -217,7 +217,7 @@ class Runner:
         self.wname = wname
         spec = jet_synth.WORKLOADS[wname]["model"]
         t = time.perf_counter()
-        self.path = jet_synth.ensure_model(spec)
+        self.path = jet_synth.ensure_model(spec, evict=True)
         log(f"model file {self.path} ready in {time.perf_counter() - t:.1f}s")
         self.wl = jet_synth.make_workload(wname)
         self.mode = {"binary": J.JET_BINARY, "ordinal": J.JET_ORDINAL}.get(MODE_OF.get(wname, ""), J.JET_CHOICE)

@@ -484,12 +484,34 @@ def model_cache_dir() -> str:
     return d
 
 
+def make_room(path: str, spec: dict | str, min_evict: int = 8 << 30) -> None:
+    """While the disk lacks room for `spec`'s file at `path`, deletes the
+    largest other cached model files (``*.jetm`` of over `min_evict` bytes in
+    the same folder; each is written again from its seed when needed)."""
+    import shutil
+    need = sum(tensor_nbytes(dt, shape) for _, dt, shape, _ in tensor_list(spec)) + (2 << 30)
+    d = os.path.dirname(os.path.abspath(path))
+    others = sorted((os.path.join(d, f) for f in os.listdir(d) if f.endswith(".jetm")),
+                    key=os.path.getsize, reverse=True)
+    for f in others:
+        if shutil.disk_usage(d).free >= need:
+            break
+        if os.path.abspath(f) != os.path.abspath(path) and os.path.getsize(f) > min_evict:
+            print(f"[jet_synth] removing cached {os.path.basename(f)} to make room for {os.path.basename(path)}",
+                  flush=True)
+            os.remove(f)
+
+
 def ensure_model(spec_name: str, seed: int = MASTER_SEED, zero: bool = False,
-                 cache_dir: str | None = None) -> str:
-    """Path of the model file for a named spec, writing it if absent."""
+                 cache_dir: str | None = None, evict: bool = False) -> str:
+    """Path of the model file for a named spec, writing it if absent (with
+    evict, after deleting other large cached model files if the disk lacks
+    room for it)."""
     d = cache_dir or model_cache_dir()
     path = os.path.join(d, f"{spec_name}_s{seed}{'_zero' if zero else ''}.jetm")
     if not os.path.exists(path):
+        if evict:
+            make_room(path, spec_name)
         write_model(path, spec_name, seed=seed, zero=zero)
     return path
 

@@ -64,7 +64,7 @@ def model_file(spec):
     (the largest files do not all fit on the disk at once)."""
     path = os.path.join(jet_synth.model_cache_dir(), f"{spec}_s{jet_synth.MASTER_SEED}.jetm")
     existed = os.path.exists(path)
-    path = jet_synth.ensure_model(spec)
+    path = jet_synth.ensure_model(spec, evict=True)
     try:
         yield path
     finally:
