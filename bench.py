@@ -429,6 +429,12 @@ def main() -> int:
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
                         "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None}
         roofline["traffic"] = measured_traffic(dom, wname, args.dtype)
+        if not dom.startswith("attn"):
+            # (hi, lo) pair operands: two MFMA products per credited multiply
+            # (bf16 everywhere; f16p on the attention side's GEMMs)
+            pairs = args.dtype == "bf16" or (args.dtype == "f16p" and dom in ("gemm_qkv", "gemm_o"))
+            roofline["mfma_products_per_multiply"] = 2 if pairs else 1
+            roofline["executed_frac"] = round(roofline["frac"] * (2 if pairs else 1), 4)
         roofline["launches"] = n
         roofline["ms_per_launch"] = round(ms_avg, 4)
         roofline["flops_per_launch"] = stats["kernel_flops"][dom] / n
