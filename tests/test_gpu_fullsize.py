@@ -325,7 +325,7 @@ def test_dense_1p5b_q4_k4_full():
 
 
 # The pair-bf16 mode's largest deviation from the stored oracle scores on the
-# sampled questions of every dense and hybrid workload (per token, per
+# sampled questions of the 1.5B and hybrid workloads (per token, per
 # candidate), measured with these kernels: the whole-workload check below
 # spends it from the tolerances.
 BF16_DEV_TOK, BF16_DEV_SUM = 2e-4, 6e-4
