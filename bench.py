@@ -268,6 +268,30 @@ class Runner:
         self.J.jet_model_free(self.model)
 
 
+def tolerance_check(wname: str, dtype: str) -> dict:
+    """Every token and candidate of the workload in mode `dtype` against the
+    pair-bf16 mode (which the full-size tests hold to the oracle's stored
+    scores on sampled questions): the largest deviations and how many tokens
+    and candidates pass the per-token 2e-2 / per-candidate 5e-2 bounds."""
+    import numpy as np
+    out = {}
+    for dt in (dtype, "bf16"):
+        r = Runner(wname, dt, timing=False)
+        try:
+            inp = r.inputs(r.wl)
+            r.step(r.wl, inp)
+            out[dt] = (inp[2].cpu().numpy().astype(np.float64), inp[3].cpu().numpy().astype(np.float64))
+        finally:
+            r.free()
+        log(f"tolerance check: {wname} scored in {dt}")
+    dtok = np.abs(out[dtype][0] - out["bf16"][0])
+    dsum = np.abs(out[dtype][1] - out["bf16"][1])
+    return {"workload": wname, "dtype": dtype, "reference": "bf16 (pair operands)", "tokens": int(dtok.size),
+            "candidates": int(dsum.size), "max_token_dev": float(dtok.max()), "max_cand_dev": float(dsum.max()),
+            "rms_token_dev": float(np.sqrt((dtok ** 2).mean())), "tokens_over_2e-2": int((dtok > 2e-2).sum()),
+            "candidates_over_5e-2": int((dsum > 5e-2).sum())}
+
+
 def prefix_reuse(steps: int, unshared_steps: int) -> dict:
     """Shared vs unshared evaluation of the dense 1.5B choice workload with
     the same kernels (only the prefix sharing switched off)."""
@@ -358,6 +382,8 @@ def main() -> int:
                          "workload (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with HIP events")
+    ap.add_argument("--tolerance-check", action="store_true",
+                    help="only score the whole workload in --dtype and in pair-bf16 and print the deviations")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (reference for the HBM byte counters)")
     args = ap.parse_args()
@@ -367,6 +393,10 @@ def main() -> int:
         return 2
     if args.calibrate_copy:
         return calibrate_copy()
+    if args.tolerance_check:
+        dt = args.dtype or DEFAULT_DTYPE.get(args.workload, "f16")
+        print(json.dumps(tolerance_check(args.workload, dt)), flush=True)
+        return 0
 
     import torch
 
