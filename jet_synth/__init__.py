@@ -47,6 +47,8 @@ import json
 import os
 import shutil
 import struct
+import sys
+import time
 import zlib
 from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
@@ -435,8 +437,15 @@ def write_model(path: str, spec: dict | str, seed: int = MASTER_SEED,
             jobs.append((t["name"], j, t["init"], arr[j * CHUNK:(j + 1) * CHUNK], t["dtype"]))
     nthr = threads or max(1, min(32, len(os.sched_getaffinity(0))))
     std = s["init_std"]
+    # large files take minutes: report the chunks written about every 20 s on
+    # the process's own stderr (a test runner capturing output would hold it)
+    total, t_last = len(jobs), time.monotonic()
     with ThreadPoolExecutor(nthr) as ex:
-        list(ex.map(lambda a: _fill_chunk(seed, a[0], a[1], std, a[2], a[3], a[4], zero), jobs))
+        for i, _ in enumerate(ex.map(lambda a: _fill_chunk(seed, a[0], a[1], std, a[2], a[3], a[4], zero), jobs)):
+            if time.monotonic() - t_last > 20:
+                t_last = time.monotonic()
+                print(f"[jet_synth] {os.path.basename(path)}: {i + 1}/{total} chunks written", file=sys.__stderr__,
+                      flush=True)
     mm.flush()
     del mm
     os.replace(tmp, path)

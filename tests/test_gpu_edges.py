@@ -24,8 +24,7 @@ TOL = {J.JET_FP32: 1e-4, J.JET_BF16: 2e-2, J.JET_F16: 2e-2, J.JET_F16P: 2e-2}
 
 
 def log(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    print(msg, file=sys.__stderr__, flush=True)
 
 
 def edge_workload(vocab, prefix_lens, cand_lens, seed, empty_question=True):

@@ -47,8 +47,9 @@ ROUTE_TOL = 2e-2
 
 
 def log(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    # the process's own stderr: a step's line shows while the run is going,
+    # whatever pytest captures
+    print(msg, file=sys.__stderr__, flush=True)
 
 
 # the fp16 mode (what bench.py times) and the pair-bf16 mode
@@ -257,6 +258,7 @@ def forced_parity(path, wl, tok, sums, pre, cand, qs, dtype, tag, tol=(TOK_TOL, 
     idx = [c for q in qs for c in range(int(wl.q_cand_offsets[q]), int(wl.q_cand_offsets[q + 1]))]
     routes = candidate_routes(wl, pre, cand, qs)
     gaps = []
+    log(f"[fullsize] {tag}: the oracle on questions {qs} ({sub.n_candidates} candidates) under the GPU's routes")
     ref_tok, ref_sum = oracle.score_unshared(path, sub, routes=routes, route_gaps=gaps)
     g = np.concatenate(gaps)
     n_flip = int(np.count_nonzero(g < 0))

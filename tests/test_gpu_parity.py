@@ -24,8 +24,7 @@ TOL = {J.JET_FP32: (1e-4, 1e-4), J.JET_BF16: (2e-2, 5e-2), J.JET_BF16_SINGLE: (2
 
 
 def log(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    print(msg, file=sys.__stderr__, flush=True)
 
 
 def check_parity(wl, tok, sums, ref_tok, ref_sums, dtype):

@@ -25,8 +25,7 @@ pytestmark = pytest.mark.gpu
 
 
 def log(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    print(msg, file=sys.__stderr__, flush=True)
 
 
 def extended(wl, trace):
