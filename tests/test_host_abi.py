@@ -232,3 +232,29 @@ def test_moe_model_shapes():
     assert names["blk.0.moe_gate"] == (256, 512, 2048) and names["blk.0.moe_down"] == (256, 2048, 512)
     assert names["blk.39.shared_router"] == (1, 2048) and "blk.0.w_gate" not in names
     assert s["layer_types"] == ["gdn", "gdn", "gdn", "attn"] * 10
+
+
+def test_model_cache_eviction(tmp_path, monkeypatch):
+    """Writing a model file into a full cache deletes the largest other cached
+    model files of over the size threshold until the new file fits, and no
+    more; small files and the file's own path are never deleted."""
+    import collections
+    import shutil
+    files = {"big1.jetm": 900, "big2.jetm": 700, "big3.jetm": 650, "small.jetm": 100, "other.bin": 5000}
+    for name, size in files.items():
+        with open(tmp_path / name, "wb") as f:
+            f.truncate(size)
+    need = sum(jet_synth.tensor_nbytes(dt, shape) for _, dt, shape, _ in jet_synth.tensor_list("tiny_dense_fp32"))
+    Usage = collections.namedtuple("Usage", "total used free")
+    base_free = need + (2 << 30) - 1500   # room once 1500 more bytes are freed
+
+    def fake_usage(d):
+        freed = sum(s for n, s in files.items() if not (tmp_path / n).exists())
+        return Usage(0, 0, base_free + freed)
+
+    monkeypatch.setattr(shutil, "disk_usage", fake_usage)
+    target = tmp_path / "tiny.jetm"
+    jet_synth.make_room(str(target), "tiny_dense_fp32", min_evict=500)
+    left = sorted(p.name for p in tmp_path.iterdir())
+    # big1 (900) and big2 (700) free 1600 >= 1500; big3, the small file and non-model files stay
+    assert left == ["big3.jetm", "other.bin", "small.jetm"]
