@@ -242,20 +242,35 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
 //   O = diag(e^g) Q S0^T + (Gamma o Q K^T)_{s <= t} Delta,
 //   S_end = e^{g_last} S0 + Delta^T diag(exp(g_last - g)) K.
 // The products run as fp16 MFMAs with fp32 accumulation; the triangular
-// solve for Delta is a forward substitution in fp32 (one thread per column of
-// Delta); the state stays in fp32 accumulators for the whole sequence and is
-// rounded to fp16 only as an operand of the next chunk's products.
+// solve for Delta is a forward substitution in fp32; the state stays in fp32
+// accumulators for the whole sequence and is rounded to fp16 only as an
+// operand of the next chunk's products.
 //
-// One workgroup of 4 waves per (sequence, head); wave w owns rows
-// 32w .. 32w + 31 of the state (4 MFMA tiles of 32 x 32) and the same columns
-// of the chunk's outputs. LDS rows of fp16 operands are stored in 16-byte
-// chunks whose position is XOR-swizzled by the row, so the 32 rows a fragment
-// read touches fall in distinct banks.
+// One workgroup of 4 waves per (sequence, head); wave w owns columns
+// v = 32 w + lane % 32 of the state, of Delta and of the chunk's outputs.
+// Everything that is per column stays in that wave's registers:
+//   * the state is held transposed, S^T[d][v] in 4 accumulator tiles, and
+//     its registers serve directly as the operand of K S0^T and Q S0^T (the
+//     accumulator's row order, taken as the contraction order, differs from
+//     the operand's by a swap of bits 2 and 3 of d; K and Q are stored in
+//     LDS with the same swap);
+//   * the right-hand side comes out of K S0^T in the accumulator layout, in
+//     which lane half h holds rows t with (t / 4) % 2 = h, and the solve runs
+//     on those rows in place;
+//   * Delta, once solved, is in every lane of its column and is the operand
+//     of the products that follow.
+// LDS holds only what is shared across columns: K and Q rows, K~^T, the
+// masked Gamma o Q K^T and A. fp16 rows in LDS are stored in 16-byte chunks
+// whose position is XOR-swizzled by the row, so the 32 rows a fragment read
+// touches fall in distinct banks.
 constexpr int GC = 32;  // chunk length
 
 // element (r, c) of a [*][128] / [*][32] fp16 array
 __device__ __forceinline__ int sw128(int r, int c) { return r * 128 + ((((c >> 3) ^ (r & 15)) << 3) | (c & 7)); }
 __device__ __forceinline__ int sw32(int r, int c) { return r * 32 + ((((c >> 3) ^ ((r >> 2) & 3)) << 3) | (c & 7)); }
+// column d with bits 2 and 3 swapped: within each block of 16, positions
+// 0..15 hold d = 0..3, 8..11, 4..7, 12..15
+__device__ __forceinline__ int swap23(int d) { return (d & ~12) | ((d & 4) << 1) | ((d & 8) >> 1); }
 
 // MFMA operand: row r, columns c0 .. c0 + 7 (c0 a multiple of 8)
 __device__ __forceinline__ Frag<f16> frag128(const f16 *a, int r, int c0) {
@@ -268,6 +283,13 @@ __device__ __forceinline__ Frag<f16> frag32(const f16 *a, int r, int c0) {
   f.v = *reinterpret_cast<const f16x8 *>(a + sw32(r, c0));
   return f;
 }
+// MFMA operand from 8 fp32 values
+__device__ __forceinline__ Frag<f16> frag_regs(const float *x) {
+  Frag<f16> f;
+  const uint4 u = make_uint4(f2h2(x[0], x[1]), f2h2(x[2], x[3]), f2h2(x[4], x[5]), f2h2(x[6], x[7]));
+  f.v = __builtin_bit_cast(f16x8, u);
+  return f;
+}
 
 // x, as a value the compiler cannot see through: address arithmetic built on
 // it is redone in every chunk instead of being held in registers across the
@@ -278,16 +300,13 @@ __device__ __forceinline__ int opaque(int x) {
 }
 
 __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
-  // sh: S0 in fp16 [dv][dk]; once every wave's products with S0 are done its
-  // first 16 KB hold the solve's right-hand side r (fp32 [GC][dv])
-  __shared__ __align__(16) f16 sh[GDN_D * GDN_D];
-  __shared__ __align__(16) f16 kh[GC * GDN_D], qh[GC * GDN_D];  // K, Q rows [t][d]
+  __shared__ __align__(16) f16 kh[GC * GDN_D], qh[GC * GDN_D];  // K, Q rows [t][swap23(d)]
   __shared__ __align__(16) f16 kt[GDN_D * GC];                  // K~^T [d][s]
-  __shared__ __align__(16) f16 dt[GDN_D * GC];                  // Delta^T [v][s]
   __shared__ __align__(16) f16 pm[GC * GC];                     // masked Gamma o Q K^T [t][s]
-  __shared__ __align__(16) float al[GC * GC];                   // A [t][s]
+  // A by columns, each split by lane half: A[t][s] at [s][16 h + e] where
+  // lane half h, register e holds row t (t = 8 (e / 4) + 4 h + e % 4)
+  __shared__ __align__(16) float al[GC * GC];
   __shared__ float gs[GC], bs[GC];
-  float *rr = reinterpret_cast<float *>(sh);
 
   const int H = g.H;
   const int si = blockIdx.x / H, h = blockIdx.x % H;
@@ -298,64 +317,80 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
   // so masking lanes off would not skip it)
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // state rows 32 w + 8 (e / 4) + 4 lh + e % 4, columns 32 j + lc
+  // S^T[d][v], v = 32 w + lc, d = 32 j + 8 (e / 4) + 4 lh + e % 4: four
+  // consecutive d per quarter of a tile, one 16-byte piece of row v of S
   f32x16 sacc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
-      sacc[j][e] = sq.init >= 0 ? g.S_init[(((int64_t)sq.init * H + h) * GDN_D + v) * GDN_D + 32 * j + lc] : 0.0f;
+    for (int c = 0; c < 4; ++c) {
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (sq.init >= 0)
+        x = *reinterpret_cast<const float4 *>(g.S_init + (((int64_t)sq.init * H + h) * GDN_D + 32 * w + lc) * GDN_D +
+                                              32 * j + 8 * c + 4 * lh);
+      sacc[j][4 * c] = x.x;
+      sacc[j][4 * c + 1] = x.y;
+      sacc[j][4 * c + 2] = x.z;
+      sacc[j][4 * c + 3] = x.w;
     }
+  // the initial state has arrived before the loop: without this wait the
+  // compiler's wait at the top of the loop, made for both ways in, also holds
+  // each chunk until the previous chunk's output stores have completed
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
   for (int c0 = 0; c0 < sq.len; c0 += GC) {
     const int L = min(GC, sq.len - c0);
     const int64_t row0 = sq.row0 + c0;
     const int tid = opaque(threadIdx.x), l = tid & 63, lc = l & 31, lh = l >> 5;
-    __syncthreads();  // the previous chunk's readers of every buffer are done
-    // ---- stage: S0 (fp16), K and Q rows, gates; rows past L are zero
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
-        sh[sw128(v, 32 * j + lc)] = (f16)sacc[j][e];
-      }
-    float4 kr[4];
+    // every global load of the chunk is issued before the first wait, with no
+    // branch between them: rows past L read row L - 1 (in bounds, L >= 1) and
+    // are replaced by zeros once they arrive
+    float ga, gb;  // gates of step lc (read by every wave, used by wave 0)
+    {
+      const int64_t r = (row0 + min(lc, L - 1)) * H + h;
+      ga = g.alpha[r];
+      gb = g.beta[r];
+    }
+    float4 kr[4], qr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
-      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv;
-      if (t < L) {
-        kv = *reinterpret_cast<const float4 *>(g.k + ((row0 + t) * H + h) * GDN_D + d);
-        qv = *reinterpret_cast<const float4 *>(g.q + ((row0 + t) * H + h) * GDN_D + d);
-      }
-      kr[i] = kv;
-      *reinterpret_cast<uint2 *>(kh + sw128(t, d)) = make_uint2(f2h2(kv.x, kv.y), f2h2(kv.z, kv.w));
-      *reinterpret_cast<uint2 *>(qh + sw128(t, d)) = make_uint2(f2h2(qv.x, qv.y), f2h2(qv.z, qv.w));
+      const int64_t r = ((row0 + min(t, L - 1)) * H + h) * GDN_D + d;
+      kr[i] = *reinterpret_cast<const float4 *>(g.k + r);
+      qr[i] = *reinterpret_cast<const float4 *>(g.q + r);
     }
-    // v for this wave's output columns, in the accumulator layout
+    // v for this wave's columns, in the accumulator layout
     float vr[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
-      vr[e] = t < L ? g.v[((row0 + t) * H + h) * GDN_D + 32 * w + lc] : 0.0f;
+      vr[e] = g.v[((row0 + min(t, L - 1)) * H + h) * GDN_D + 32 * w + lc];
     }
+    __syncthreads();  // the previous chunk's readers of every buffer are done
+    // ---- stage: K and Q rows, gates; rows past L are zero
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
+      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (t >= L) kr[i] = qr[i] = z;
+      *reinterpret_cast<uint2 *>(kh + sw128(t, swap23(d))) = make_uint2(f2h2(kr[i].x, kr[i].y), f2h2(kr[i].z, kr[i].w));
+      *reinterpret_cast<uint2 *>(qh + sw128(t, swap23(d))) = make_uint2(f2h2(qr[i].x, qr[i].y), f2h2(qr[i].z, qr[i].w));
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (8 * (e >> 2) + 4 * lh + (e & 3) >= L) vr[e] = 0.0f;
     if (w == 0) {
-      // log-decay prefix sums (a vanishing alpha is held at e^-80) and gates
-      float la = 0.0f, b = 0.0f;
-      if (l < L) {
-        la = fmaxf(__logf(g.alpha[(row0 + l) * H + h]), -80.0f);
-        b = g.beta[(row0 + l) * H + h];
+      // log-decay prefix sums over the chunk (lanes 0..31; the loads were
+      // issued first), a vanishing alpha held at e^-80
+      float la = lc < L ? fmaxf(__logf(ga), -80.0f) : 0.0f;
+#pragma unroll
+      for (int off = 1; off < GC; off *= 2) {
+        const float y = __shfl_up(la, off, GC);
+        if (lc >= off) la += y;
       }
-      if (l < GC) gs[l] = la;
-      __builtin_amdgcn_wave_barrier();
       if (l < GC) {
-        float acc = 0.0f;
-        for (int u = 0; u <= l; ++u) acc += gs[u];
-        bs[l] = b;
-        __builtin_amdgcn_wave_barrier();
-        gs[l] = acc;
+        gs[l] = la;
+        bs[l] = l < L ? gb : 0.0f;
       }
     }
     __syncthreads();
@@ -370,56 +405,83 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
       kt[sw32(d + 2, t)] = (f16)(kr[i].z * f);
       kt[sw32(d + 3, t)] = (f16)(kr[i].w * f);
     }
-    // ---- products with S0 (every wave, its 32 state rows as output columns)
-    //      and K K^T (wave 0) / Q K^T (wave 1)
+    // ---- products with S0 (every wave, its 32 state columns from its own
+    //      registers) and K K^T (wave 0) / Q K^T (wave 1)
     f32x16 xk, xq, xt;
 #pragma unroll
     for (int e = 0; e < 16; ++e) xk[e] = xq[e] = xt[e] = 0.0f;
 #pragma unroll
     for (int d0 = 0; d0 < GDN_D; d0 += 16) {
       const Frag<f16> fk = frag128(kh, lc, d0 + 8 * lh), fq = frag128(qh, lc, d0 + 8 * lh);
-      const Frag<f16> fs = frag128(sh, 32 * w + lc, d0 + 8 * lh);
+      float sv[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sv[i] = sacc[d0 >> 5][8 * ((d0 >> 4) & 1) + i];
+      const Frag<f16> fs = frag_regs(sv);
       mma32(xk, fk, fs);
       mma32(xq, fq, fs);
       if (w == 0) mma32(xt, fk, fk);
       if (w == 1) mma32(xt, fq, fk);
     }
-    __syncthreads();  // S0 no longer read: its space takes r
+    // ---- right-hand side r (in registers), O's first term, A and the masked
+    //      Gamma o Q K^T
+    float xr[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
       const float eg = __expf(gs[t]);
-      rr[t * GDN_D + 32 * w + lc] = bs[t] * (vr[e] - eg * xk[e]);
+      xr[e] = bs[t] * (vr[e] - eg * xk[e]);
       xq[e] *= eg;  // this wave's output tile starts as diag(e^g) Q S0^T
       const int s = lc;
-      if (w == 0) al[t * GC + s] = s < t ? bs[t] * __expf(gs[t] - gs[s]) * xt[e] : 0.0f;
+      // K K^T is symmetric: this lane's (t, s) entry also serves as (s, t),
+      // so A[s][t] goes to column t of A, 32 lanes to 32 distinct banks
+      if (w == 0)
+        al[t * GC + 16 * ((s >> 2) & 1) + 4 * (s >> 3) + (s & 3)] =
+            t < s ? bs[s] * __expf(gs[s] - gs[t]) * xt[e] : 0.0f;
       if (w == 1) pm[sw32(t, s)] = (f16)(s <= t ? __expf(gs[t] - gs[s]) * xt[e] : 0.0f);
     }
     __syncthreads();
-    // ---- forward substitution, one thread per column v of Delta
-    if (tid < GDN_D) {
-      float dl[GC];
+    // ---- forward substitution for column v = 32 w + lc of Delta, in the
+    //      column-oriented order: once delta_s is final it is taken off every
+    //      later row, so the updates of one step are independent of each
+    //      other. Each lane half updates the rows it holds; a final delta_s
+    //      reaches the other half by a swap of the wave's lane halves. Every
+    //      row still takes its terms in the order s = 0, 1, ..., t - 1.
+    // Delta[s][v] reaches both lane halves; each keeps the rows it supplies
+    // as an MFMA operand, s = 16 c + 8 lh + i in dk[8 c + i]
+    float dk[16];
+    {
+      const float *ap = al + 16 * lh;  // A[t(e)][s] at ap[s * GC + e]
+      // column s of A is read one step ahead of its use; register e is
+      // updated at step s while its row on the high half, 8 (e / 4) + 4 + e % 4,
+      // is above s (a row at or above s on the low half reads A = 0)
+      float ac[16], an[16];
 #pragma unroll
-      for (int t = 0; t < GC; ++t) {
-        float x = rr[t * GDN_D + tid];
+      for (int e = 0; e < 16; ++e) ac[e] = ap[e];
 #pragma unroll
-        for (int s = 0; s < t; ++s) x -= al[t * GC + s] * dl[s];
-        dl[t] = x;
-      }
+      for (int s = 0; s < GC; ++s) {
+        if (s + 1 < GC) {
 #pragma unroll
-      for (int c = 0; c < GC / 8; ++c) {
-        uint4 u;
-        u.x = f2h2(dl[8 * c], dl[8 * c + 1]);
-        u.y = f2h2(dl[8 * c + 2], dl[8 * c + 3]);
-        u.z = f2h2(dl[8 * c + 4], dl[8 * c + 5]);
-        u.w = f2h2(dl[8 * c + 6], dl[8 * c + 7]);
-        *reinterpret_cast<uint4 *>(dt + sw32(tid, 8 * c)) = u;
+          for (int e = 0; e < 16; ++e)
+            if (8 * (e >> 2) + 4 + (e & 3) > s + 1) an[e] = ap[(s + 1) * GC + e];
+        }
+        // row s is final in half (s / 4) % 2, register 4 (s / 8) + s % 4;
+        // q[0] holds the low half's value in every lane, q[1] the high half's
+        const int es = 4 * (s >> 3) + (s & 3);
+        const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(xr[es]), __float_as_uint(xr[es]), false, false);
+        const float ds = __uint_as_float(q[(s >> 2) & 1]);
+        if (((s >> 3) & 1) == lh) dk[8 * (s >> 4) + (s & 7)] = ds;
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (8 * (e >> 2) + 4 + (e & 3) > s) xr[e] = fmaf(-ac[e], ds, xr[e]);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ac[e] = an[e];
       }
     }
-    __syncthreads();
-    // ---- O += (Gamma o Q K^T) Delta; S = e^{g_last} S0 + Delta^T K~
+    // Delta as an MFMA operand: lane half lh supplies rows 16 c + 8 lh + i
+    const Frag<f16> fd[2] = {frag_regs(dk), frag_regs(dk + 8)};
+    // ---- O += (Gamma o Q K^T) Delta; S^T = e^{g_last} S0^T + K~^T Delta
 #pragma unroll
-    for (int s0 = 0; s0 < GC; s0 += 16) mma32(xq, frag32(pm, lc, s0 + 8 * lh), frag32(dt, 32 * w + lc, s0 + 8 * lh));
+    for (int c = 0; c < 2; ++c) mma32(xq, frag32(pm, lc, 16 * c + 8 * lh), fd[c]);
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
@@ -431,18 +493,17 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) sacc[j][e] *= eg;
 #pragma unroll
-      for (int s0 = 0; s0 < GC; s0 += 16)
-        mma32(sacc[j], frag32(dt, 32 * w + lc, s0 + 8 * lh), frag32(kt, 32 * j + lc, s0 + 8 * lh));
+      for (int c = 0; c < 2; ++c) mma32(sacc[j], frag32(kt, 32 * j + lc, 16 * c + 8 * lh), fd[c]);
     }
   }
   if (sq.fin >= 0) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = 32 * w + 8 * (e >> 2) + 4 * lh + (e & 3);
-        g.S_fin[(((int64_t)sq.fin * H + h) * GDN_D + v) * GDN_D + 32 * j + lc] = sacc[j][e];
-      }
+      for (int c = 0; c < 4; ++c)
+        *reinterpret_cast<float4 *>(g.S_fin + (((int64_t)sq.fin * H + h) * GDN_D + 32 * w + lc) * GDN_D + 32 * j +
+                                    8 * c + 4 * lh) =
+            make_float4(sacc[j][4 * c], sacc[j][4 * c + 1], sacc[j][4 * c + 2], sacc[j][4 * c + 3]);
   }
 }
 
