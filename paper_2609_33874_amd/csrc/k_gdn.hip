@@ -241,9 +241,10 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
 //     A[t][s] = beta_t Gamma[t][s] (k_t . k_s) for s < t (strictly lower),
 //   O = diag(e^g) Q S0^T + (Gamma o Q K^T)_{s <= t} Delta,
 //   S_end = e^{g_last} S0 + Delta^T diag(exp(g_last - g)) K.
-// The products run as fp16 MFMAs with fp32 accumulation; the triangular
-// solve for Delta is a forward substitution in fp32; the state stays in fp32
-// accumulators for the whole sequence and is rounded to fp16 only as an
+// The products run as fp16 MFMAs (or, with PAIR, as three bf16 MFMAs over
+// (hi, lo) operand pairs) with fp32 accumulation; the triangular solve for
+// Delta is a forward substitution in fp32; the state stays in fp32
+// accumulators for the whole sequence and is rounded to 16 bits only as an
 // operand of the next chunk's products.
 //
 // One workgroup of 4 waves per (sequence, head); wave w owns columns
@@ -272,23 +273,65 @@ __device__ __forceinline__ int sw32(int r, int c) { return r * 32 + ((((c >> 3) 
 // 0..15 hold d = 0..3, 8..11, 4..7, 12..15
 __device__ __forceinline__ int swap23(int d) { return (d & ~12) | ((d & 4) << 1) | ((d & 8) >> 1); }
 
+// Operand storage: single fp16 values, or with PAIR (hi, lo) bf16 pairs whose
+// sum carries about 16 significant bits. NP parts of each array are stored
+// one after the other.
+template <bool PAIR> struct ChunkOp {
+  typedef f16 T;
+  static constexpr int NP = 1;
+};
+template <> struct ChunkOp<true> {
+  typedef bf16 T;
+  static constexpr int NP = 2;
+};
+
 // MFMA operand: row r, columns c0 .. c0 + 7 (c0 a multiple of 8)
-__device__ __forceinline__ Frag<f16> frag128(const f16 *a, int r, int c0) {
-  Frag<f16> f;
-  f.v = *reinterpret_cast<const f16x8 *>(a + sw128(r, c0));
+template <typename T> __device__ __forceinline__ Frag<T> frag128(const T *a, int r, int c0) {
+  Frag<T> f;
+  f.v = *reinterpret_cast<const typename Vec8<T>::type *>(a + sw128(r, c0));
   return f;
 }
-__device__ __forceinline__ Frag<f16> frag32(const f16 *a, int r, int c0) {
-  Frag<f16> f;
-  f.v = *reinterpret_cast<const f16x8 *>(a + sw32(r, c0));
+template <typename T> __device__ __forceinline__ Frag<T> frag32(const T *a, int r, int c0) {
+  Frag<T> f;
+  f.v = *reinterpret_cast<const typename Vec8<T>::type *>(a + sw32(r, c0));
   return f;
 }
-// MFMA operand from 8 fp32 values
-__device__ __forceinline__ Frag<f16> frag_regs(const float *x) {
-  Frag<f16> f;
-  const uint4 u = make_uint4(f2h2(x[0], x[1]), f2h2(x[2], x[3]), f2h2(x[4], x[5]), f2h2(x[6], x[7]));
-  f.v = __builtin_bit_cast(f16x8, u);
-  return f;
+// two values as NP packed words: the rounded values, and with pairs the
+// rounded remainders
+template <bool PAIR> __device__ __forceinline__ void split2(float a, float b, uint32_t *u) {
+  if constexpr (PAIR) {
+    const uint32_t hi = f2bf2(a, b);
+    u[0] = hi;
+    u[1] = f2bf2(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
+  } else {
+    u[0] = f2h2(a, b);
+  }
+}
+// MFMA operand (NP parts) from 8 fp32 values
+template <bool PAIR> __device__ __forceinline__ void frag_regs(const float *x, Frag<typename ChunkOp<PAIR>::T> *f) {
+  typedef typename ChunkOp<PAIR>::T T;
+  uint32_t u[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) split2<PAIR>(x[2 * i], x[2 * i + 1], u[i]);
+#pragma unroll
+  for (int p = 0; p < ChunkOp<PAIR>::NP; ++p)
+    f[p].v = __builtin_bit_cast(typename Vec8<T>::type, make_uint4(u[0][p], u[1][p], u[2][p], u[3][p]));
+}
+// one value into part 0 at a[i] and, with pairs, its remainder into part 1
+// at a[n + i]
+template <bool PAIR, typename T> __device__ __forceinline__ void st_parts(T *a, int n, int i, float x) {
+  const T hi = from_f<T>(x);
+  a[i] = hi;
+  if constexpr (PAIR) a[n + i] = from_f<T>(x - to_f<T>(hi));
+}
+// acc += one 16-wide step of a product; with pairs hi hi + hi lo + lo hi (the
+// lo lo term is of the order of the pairs' own rounding)
+template <bool PAIR, typename T> __device__ __forceinline__ void mmap(f32x16 &acc, const Frag<T> *a, const Frag<T> *b) {
+  mma32(acc, a[0], b[0]);
+  if constexpr (PAIR) {
+    mma32(acc, a[0], b[1]);
+    mma32(acc, a[1], b[0]);
+  }
 }
 
 // x, as a value the compiler cannot see through: address arithmetic built on
@@ -299,10 +342,13 @@ __device__ __forceinline__ int opaque(int x) {
   return x;
 }
 
-__global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
-  __shared__ __align__(16) f16 kh[GC * GDN_D], qh[GC * GDN_D];  // K, Q rows [t][swap23(d)]
-  __shared__ __align__(16) f16 kt[GDN_D * GC];                  // K~^T [d][s]
-  __shared__ __align__(16) f16 pm[GC * GC];                     // masked Gamma o Q K^T [t][s]
+template <bool PAIR> __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
+  typedef typename ChunkOp<PAIR>::T T;
+  constexpr int NP = ChunkOp<PAIR>::NP;
+  constexpr int NKQ = GC * GDN_D, NKT = GDN_D * GC, NPM = GC * GC;  // elements of one part
+  __shared__ __align__(16) T kh[NP * NKQ], qh[NP * NKQ];  // K, Q rows [t][swap23(d)]
+  __shared__ __align__(16) T kt[NP * NKT];                // K~^T [d][s]
+  __shared__ __align__(16) T pm[NP * NPM];                // masked Gamma o Q K^T [t][s]
   // A by columns, each split by lane half: A[t][s] at [s][16 h + e] where
   // lane half h, register e holds row t (t = 8 (e / 4) + 4 h + e % 4)
   __shared__ __align__(16) float al[GC * GC];
@@ -373,8 +419,16 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
       const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
       const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
       if (t >= L) kr[i] = qr[i] = z;
-      *reinterpret_cast<uint2 *>(kh + sw128(t, swap23(d))) = make_uint2(f2h2(kr[i].x, kr[i].y), f2h2(kr[i].z, kr[i].w));
-      *reinterpret_cast<uint2 *>(qh + sw128(t, swap23(d))) = make_uint2(f2h2(qr[i].x, qr[i].y), f2h2(qr[i].z, qr[i].w));
+      uint32_t ka[2], kb[2], qa[2], qb[2];
+      split2<PAIR>(kr[i].x, kr[i].y, ka);
+      split2<PAIR>(kr[i].z, kr[i].w, kb);
+      split2<PAIR>(qr[i].x, qr[i].y, qa);
+      split2<PAIR>(qr[i].z, qr[i].w, qb);
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        *reinterpret_cast<uint2 *>(kh + p * NKQ + sw128(t, swap23(d))) = make_uint2(ka[p], kb[p]);
+        *reinterpret_cast<uint2 *>(qh + p * NKQ + sw128(t, swap23(d))) = make_uint2(qa[p], qb[p]);
+      }
     }
 #pragma unroll
     for (int e = 0; e < 16; ++e)
@@ -400,10 +454,10 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + 256 * i, t = idx >> 5, d = (idx & 31) * 4;
       const float f = __expf(glast - gs[t]);
-      kt[sw32(d, t)] = (f16)(kr[i].x * f);
-      kt[sw32(d + 1, t)] = (f16)(kr[i].y * f);
-      kt[sw32(d + 2, t)] = (f16)(kr[i].z * f);
-      kt[sw32(d + 3, t)] = (f16)(kr[i].w * f);
+      st_parts<PAIR>(kt, NKT, sw32(d, t), kr[i].x * f);
+      st_parts<PAIR>(kt, NKT, sw32(d + 1, t), kr[i].y * f);
+      st_parts<PAIR>(kt, NKT, sw32(d + 2, t), kr[i].z * f);
+      st_parts<PAIR>(kt, NKT, sw32(d + 3, t), kr[i].w * f);
     }
     // ---- products with S0 (every wave, its 32 state columns from its own
     //      registers) and K K^T (wave 0) / Q K^T (wave 1)
@@ -412,15 +466,20 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
     for (int e = 0; e < 16; ++e) xk[e] = xq[e] = xt[e] = 0.0f;
 #pragma unroll
     for (int d0 = 0; d0 < GDN_D; d0 += 16) {
-      const Frag<f16> fk = frag128(kh, lc, d0 + 8 * lh), fq = frag128(qh, lc, d0 + 8 * lh);
+      Frag<T> fk[NP], fq[NP], fs[NP];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        fk[p] = frag128(kh + p * NKQ, lc, d0 + 8 * lh);
+        fq[p] = frag128(qh + p * NKQ, lc, d0 + 8 * lh);
+      }
       float sv[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) sv[i] = sacc[d0 >> 5][8 * ((d0 >> 4) & 1) + i];
-      const Frag<f16> fs = frag_regs(sv);
-      mma32(xk, fk, fs);
-      mma32(xq, fq, fs);
-      if (w == 0) mma32(xt, fk, fk);
-      if (w == 1) mma32(xt, fq, fk);
+      frag_regs<PAIR>(sv, fs);
+      mmap<PAIR>(xk, fk, fs);
+      mmap<PAIR>(xq, fq, fs);
+      if (w == 0) mmap<PAIR>(xt, fk, fk);
+      if (w == 1) mmap<PAIR>(xt, fq, fk);
     }
     // ---- right-hand side r (in registers), O's first term, A and the masked
     //      Gamma o Q K^T
@@ -437,7 +496,7 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
       if (w == 0)
         al[t * GC + 16 * ((s >> 2) & 1) + 4 * (s >> 3) + (s & 3)] =
             t < s ? bs[s] * __expf(gs[s] - gs[t]) * xt[e] : 0.0f;
-      if (w == 1) pm[sw32(t, s)] = (f16)(s <= t ? __expf(gs[t] - gs[s]) * xt[e] : 0.0f);
+      if (w == 1) st_parts<PAIR>(pm, NPM, sw32(t, s), s <= t ? __expf(gs[t] - gs[s]) * xt[e] : 0.0f);
     }
     __syncthreads();
     // ---- forward substitution for column v = 32 w + lc of Delta, in the
@@ -478,10 +537,17 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
       }
     }
     // Delta as an MFMA operand: lane half lh supplies rows 16 c + 8 lh + i
-    const Frag<f16> fd[2] = {frag_regs(dk), frag_regs(dk + 8)};
+    Frag<T> fd[2][NP];
+    frag_regs<PAIR>(dk, fd[0]);
+    frag_regs<PAIR>(dk + 8, fd[1]);
     // ---- O += (Gamma o Q K^T) Delta; S^T = e^{g_last} S0^T + K~^T Delta
 #pragma unroll
-    for (int c = 0; c < 2; ++c) mma32(xq, frag32(pm, lc, 16 * c + 8 * lh), fd[c]);
+    for (int c = 0; c < 2; ++c) {
+      Frag<T> fp[NP];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) fp[p] = frag32(pm + p * NPM, lc, 16 * c + 8 * lh);
+      mmap<PAIR>(xq, fp, fd[c]);
+    }
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int t = 8 * (e >> 2) + 4 * lh + (e & 3);
@@ -493,7 +559,12 @@ __global__ __launch_bounds__(256, 2) void gdn_chunk_kernel(GdnRecurArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) sacc[j][e] *= eg;
 #pragma unroll
-      for (int c = 0; c < 2; ++c) mma32(sacc[j], frag32(kt, 32 * j + lc, 16 * c + 8 * lh), fd[c]);
+      for (int c = 0; c < 2; ++c) {
+        Frag<T> fk[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) fk[p] = frag32(kt + p * NKT, 32 * j + lc, 16 * c + 8 * lh);
+        mmap<PAIR>(sacc[j], fk, fd[c]);
+      }
     }
   }
   if (sq.fin >= 0) {
@@ -547,10 +618,13 @@ hipError_t launch_gdn_recur(const GdnRecurArgs &g, int nseq, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_gdn_chunk(const GdnRecurArgs &g, int nseq, hipStream_t st) {
+hipError_t launch_gdn_chunk(const GdnRecurArgs &g, int nseq, int pair, hipStream_t st) {
   if (nseq <= 0) return hipSuccess;
   if (g.dk != GDN_D || g.dv != GDN_D) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gdn_chunk_kernel, dim3(nseq * g.H), dim3(256), 0, st, g);
+  if (pair)
+    hipLaunchKernelGGL(gdn_chunk_kernel<true>, dim3(nseq * g.H), dim3(256), 0, st, g);
+  else
+    hipLaunchKernelGGL(gdn_chunk_kernel<false>, dim3(nseq * g.H), dim3(256), 0, st, g);
   return hipGetLastError();
 }
 

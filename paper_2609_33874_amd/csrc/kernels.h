@@ -154,8 +154,9 @@ struct GdnRecurArgs {
 };
 hipError_t launch_gdn_recur(const GdnRecurArgs &g, int nseq, hipStream_t st);
 // The same recurrence in chunks of 32 steps on the matrix cores (fp16
-// operands, fp32 accumulation and state): for long sequences (prefill).
-hipError_t launch_gdn_chunk(const GdnRecurArgs &g, int nseq, hipStream_t st);
+// operands, or (hi, lo) bf16 operand pairs with pair != 0; fp32 accumulation
+// and state): for long sequences (prefill).
+hipError_t launch_gdn_chunk(const GdnRecurArgs &g, int nseq, int pair, hipStream_t st);
 // y [R][H dv] (T; [hi | lo] pairs with pair) = RMSNorm(o) * w * silu(z), z at column zoff of x.
 hipError_t launch_gdn_out(int dtype, int pair, const float *o, const float *x, int64_t ldx, int zoff, const float *w,
                           float eps, int H, int dv, int R, void *y, hipStream_t st);

@@ -1017,7 +1017,7 @@ Status gdn_layer(jet_model *m, const Layer &ly, const WaveBufs &b, int64_t R, co
                          (double)gp.nseq * (double)H * (double)(dk * dv) * 4.0;
     KTimer t(m, JET_K_GDN, flops, bytes);
     jetk::GdnRecurArgs g{gp.seqs, gq, gk, gv, ga, gb, (int)H, (int)dk, (int)dv, S_init, S_fin, go};
-    if (gp.chunked) LAUNCH(jetk::launch_gdn_chunk(g, gp.nseq, m->st));
+    if (gp.chunked) LAUNCH(jetk::launch_gdn_chunk(g, gp.nseq, m->pair, m->st));
     else LAUNCH(jetk::launch_gdn_recur(g, gp.nseq, m->st));
   }
   {
@@ -1180,12 +1180,12 @@ Status prefill(jet_model *m, int32_t n_q, const int64_t *offs, const int32_t *to
         }
         seqs.push_back({(int32_t)base, (int32_t)P, -1, q});
       }
-      // prefixes in the 16-bit single-operand modes run the chunked form
-      // (fp16 operands), longest first (no round of the launch waits on one
-      // long sequence); models with routed experts keep the fp32 stepwise
-      // recurrence: a top-k routing decision turns its rounding into a
-      // different expert for rows near a tie
-      gp.chunked = m->kdt != 1 && !m->pair && !h.n_experts;
+      // prefixes in the 16-bit modes run the chunked form (fp16 operands, or
+      // bf16 pairs in the pair mode), longest first (no round of the launch
+      // waits on one long sequence); models with routed experts keep the fp32
+      // stepwise recurrence: a top-k routing decision turns its rounding into
+      // a different expert for rows near a tie
+      gp.chunked = m->kdt != 1 && !h.n_experts;
       if (gp.chunked)
         std::stable_sort(seqs.begin(), seqs.end(),
                          [](const jetk::GdnSeq &a, const jetk::GdnSeq &b) { return a.len > b.len; });

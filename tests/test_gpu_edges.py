@@ -81,14 +81,14 @@ def test_hybrid_short_sequences(dtype, model_dir):
 
 
 @pytest.mark.parametrize("a_log", [2.0, 6.0])
-@pytest.mark.parametrize("dtype", [J.JET_FP32, J.JET_F16])
+@pytest.mark.parametrize("dtype", [J.JET_FP32, J.JET_F16, J.JET_BF16])
 def test_hybrid_strong_decay(dtype, a_log, model_dir):
     """Delta-rule layers with strong decay: alpha = exp(-e^A_log softplus(a +
     dt_bias)) with softplus of order 1 lies around e^-3..e^-8 for A_log = 2
     (the chunk's decay products span e^-100 and below) and below e^-150 for
     A_log = 6 (0 in fp32: the state is forgotten at every step), over
-    prefixes that span several chunks of the chunked recurrence (fp16 mode)
-    with ragged tails."""
+    prefixes that span several chunks of the chunked recurrence (fp16 and
+    bf16-pair modes) with ragged tails."""
     import os
     path = os.path.join(model_dir, f"edge_hybrid_decay{int(a_log)}.jetm")
     if not os.path.exists(path):

@@ -52,7 +52,7 @@ def log(msg):
     print(msg, file=sys.__stderr__, flush=True)
 
 
-# the fp16 mode (what bench.py times) and the pair-bf16 mode
+# the fp16 mode (what bench.py times on the 1.5B workloads) and the pair-bf16 mode
 DTYPES = [pytest.param(J.JET_F16, id="f16"), pytest.param(J.JET_BF16, id="bf16pair")]
 # the 64-layer model: fp16 with attention-side pairs (what bench.py times
 # there), and the pair-bf16 mode
@@ -335,13 +335,14 @@ BF16_DEV_TOK, BF16_DEV_SUM = 2e-4, 6e-4
 
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("name,spec", [("dense_1p5b_k4", "dense_1p5b"), ("dense_1p5b_binary", "dense_1p5b"),
-                                       ("dense_1p5b_ordinal", "dense_1p5b"), ("hybrid_4b_k4", "hybrid_4b")])
+                                       ("dense_1p5b_ordinal", "dense_1p5b")])
 def test_benched_mode_on_every_candidate(name, spec):
-    """The mode bench.py times on a workload (single fp16) against the
-    pair-bf16 mode on every token and candidate of the whole workload: the
-    sampled oracle comparisons above bound the pair mode's own error, so the
-    benched mode meets the tolerances on every candidate when it stays within
-    them minus that error of the pair mode."""
+    """The mode bench.py times on a workload where that is single fp16 (the
+    1.5B workloads; the 27B and hybrid workloads are timed in the pair-bf16
+    mode itself) against the pair-bf16 mode on every token and candidate of
+    the whole workload: the sampled oracle comparisons above bound the pair
+    mode's own error, so the benched mode meets the tolerances on every
+    candidate when it stays within them minus that error of the pair mode."""
     with model_file(spec) as path:
         wl = jet_synth.make_workload(name)
         out = {}
