@@ -213,7 +213,7 @@ def unshared_workload(wl):
 class Runner:
     """One model on cuda:0 and the timed step of the hot path."""
 
-    def __init__(self, wname: str, dtype: str, timing: bool):
+    def __init__(self, wname: str, dtype: str, timing: bool, record_routes: bool = False):
         import torch
         import jet_synth
         from paper_2609_33874_amd import jet as J
@@ -227,8 +227,8 @@ class Runner:
         self.mode = {"binary": J.JET_BINARY, "ordinal": J.JET_ORDINAL}.get(MODE_OF.get(wname, ""), J.JET_CHOICE)
         self.dev = torch.device("cuda:0")
         stream = torch.cuda.current_stream(self.dev)
-        flags = J.JET_FLAG_KERNEL_TIMING if timing else 0
-        jdt = {"f16": J.JET_F16, "f16p": J.JET_F16P, "bf16": J.JET_BF16}[dtype]
+        flags = (J.JET_FLAG_KERNEL_TIMING if timing else 0) | (J.JET_FLAG_RECORD_ROUTES if record_routes else 0)
+        jdt = {"f16": J.JET_F16, "f16p": J.JET_F16P, "bf16": J.JET_BF16, "fp32": J.JET_FP32}[dtype]
         t = time.perf_counter()
         self.model = J.jet_model_load(self.path, dtype=jdt, device=0, hip_stream=stream.cuda_stream, flags=flags)
         self.load_s = time.perf_counter() - t
@@ -273,23 +273,39 @@ class Runner:
 
 def tolerance_check(wname: str, dtype: str) -> dict:
     """Every token and candidate of the workload in mode `dtype` against the
-    pair-bf16 mode (which the full-size tests hold to the oracle's stored
-    scores on sampled questions): the largest deviations and how many tokens
-    and candidates pass the per-token 2e-2 / per-candidate 5e-2 bounds."""
+    pair-bf16 mode, or on models with routed experts (which have no pair
+    mode) the fp32 mode, both held by the full-size tests to the oracle's
+    stored scores on sampled questions: the largest deviations and how many
+    tokens and candidates pass the per-token 2e-2 / per-candidate 5e-2
+    bounds."""
     import numpy as np
-    out = {}
-    for dt in (dtype, "bf16"):
-        r = Runner(wname, dt, timing=False)
+    import jet_synth
+    spec = jet_synth.MODEL_SPECS[jet_synth.WORKLOADS[wname]["model"]]
+    moe = bool(spec.get("n_experts"))
+    ref = "fp32" if moe else "bf16"
+    out, routes = {}, {}
+    for dt in (dtype, ref):
+        r = Runner(wname, dt, timing=False, record_routes=moe)
         try:
             inp = r.inputs(r.wl)
             r.step(r.wl, inp)
             out[dt] = (inp[2].cpu().numpy().astype(np.float64), inp[3].cpu().numpy().astype(np.float64))
+            if moe:
+                routes[dt] = np.sort(r.J.jet_routes_get(r.model, 0), axis=2)  # [layer, prefix row, top_k]
         finally:
             r.free()
         log(f"tolerance check: {wname} scored in {dt}")
-    dtok = np.abs(out[dtype][0] - out["bf16"][0])
-    dsum = np.abs(out[dtype][1] - out["bf16"][1])
-    return {"workload": wname, "dtype": dtype, "reference": "bf16 (pair operands)", "tokens": int(dtok.size),
+    dtok = np.abs(out[dtype][0] - out[ref][0])
+    dsum = np.abs(out[dtype][1] - out[ref][1])
+    extra = {}
+    if moe:
+        # expert sets of the prefill that differ between the two modes
+        diff = np.any(routes[dtype] != routes[ref], axis=2)
+        extra = {"prefix_rows": int(diff.shape[1]), "route_sets_differing": round(float(diff.mean()), 4),
+                 "route_sets_differing_by_layer": [round(float(x), 3) for x in diff.mean(axis=1)],
+                 "prefix_rows_with_a_differing_set": round(float(diff.any(axis=0).mean()), 4)}
+    return {"workload": wname, "dtype": dtype, "reference": {"bf16": "bf16 (pair operands)", "fp32": "fp32"}[ref],
+            **extra, "tokens": int(dtok.size),
             "candidates": int(dsum.size), "max_token_dev": float(dtok.max()), "max_cand_dev": float(dsum.max()),
             "rms_token_dev": float(np.sqrt((dtok ** 2).mean())), "tokens_over_2e-2": int((dtok > 2e-2).sum()),
             "candidates_over_5e-2": int((dsum > 5e-2).sum())}
