@@ -512,6 +512,12 @@ def main() -> int:
         "roofline": roofline, "kernels": kernels,
         "evaluate_ms": round(eval_ms, 3),
     }
+    import jet_synth
+    if jet_synth.MODEL_SPECS[jet_synth.WORKLOADS[wname]["model"]].get("n_experts"):
+        # routed experts: scores hold to the oracle only under the same expert
+        # choices (near-tie router logits swap experts between any two modes)
+        result["parity_bound"] = ("under the GPU's expert choices only (the oracle run on the GPU's routes); "
+                                  "unforced, routing near-ties make the error unbounded")
 
     if args.unshared_steps > 0:
         un = unshared_workload(wl)
