@@ -258,15 +258,16 @@ __global__ __launch_bounds__(128) void gdn_recur_kernel(GdnRecurArgs g) {
 //   * the right-hand side comes out of K S0^T in the accumulator layout, in
 //     which lane half h holds rows t with (t / 4) % 2 = h, and the solve runs
 //     on those rows in place;
-//   * Delta, once solved, is in every lane of its column and is the operand
-//     of the products that follow.
+//   * each row of Delta, once solved, reaches both lane halves of its
+//     column, which keep the rows they supply as the operand of the products
+//     that follow.
 // LDS holds only what is shared across columns: K and Q rows, K~^T, the
-// masked Gamma o Q K^T and A. fp16 rows in LDS are stored in 16-byte chunks
+// masked Gamma o Q K^T and A. 16-bit rows in LDS are stored in 16-byte chunks
 // whose position is XOR-swizzled by the row, so the 32 rows a fragment read
 // touches fall in distinct banks.
 constexpr int GC = 32;  // chunk length
 
-// element (r, c) of a [*][128] / [*][32] fp16 array
+// element (r, c) of a [*][128] / [*][32] array of 16-bit values
 __device__ __forceinline__ int sw128(int r, int c) { return r * 128 + ((((c >> 3) ^ (r & 15)) << 3) | (c & 7)); }
 __device__ __forceinline__ int sw32(int r, int c) { return r * 32 + ((((c >> 3) ^ ((r >> 2) & 3)) << 3) | (c & 7)); }
 // column d with bits 2 and 3 swapped: within each block of 16, positions
