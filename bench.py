@@ -273,11 +273,11 @@ class Runner:
 
 def tolerance_check(wname: str, dtype: str) -> dict:
     """Every token and candidate of the workload in mode `dtype` against the
-    pair-bf16 mode, or on models with routed experts (which have no pair
-    mode) the fp32 mode, both held by the full-size tests to the oracle's
-    stored scores on sampled questions: the largest deviations and how many
-    tokens and candidates pass the per-token 2e-2 / per-candidate 5e-2
-    bounds."""
+    pair-bf16 mode (held by the full-size tests to the oracle's stored scores
+    on sampled questions), or, on models with routed experts (no pair mode),
+    against the fp32 mode with the share of prefill expert sets the two
+    modes choose differently: the largest deviations and how many tokens and
+    candidates pass the per-token 2e-2 / per-candidate 5e-2 bounds."""
     import numpy as np
     import jet_synth
     spec = jet_synth.MODEL_SPECS[jet_synth.WORKLOADS[wname]["model"]]
