@@ -44,6 +44,13 @@ TOK_TOL, SUM_TOL = 2e-2, 5e-2
 # N(0, 0.02^2) weights (spread ~0.02 sqrt(d)), and a 16-bit path's activations
 # drift by ~1e-3 relative over tens of layers, so its logits by ~1e-3.
 ROUTE_TOL = 2e-2
+# The pair-bf16 mode's deviation from the stored oracle scores, per token and
+# per candidate, held on the sampled questions of each workload: about three
+# times what these kernels measure (1.5B 6.3e-5 / 1.3e-4, hybrid 1.4e-4 /
+# 4.9e-4, 27B 3.4e-4 / 1.7e-3), far inside the 16-bit tolerances, so that a
+# lost term of a pair product (about 2e-3 of a product) shows.
+PAIR_DEV = {"dense_1p5b_k4": (2e-4, 6e-4), "dense_1p5b_binary": (2e-4, 6e-4), "dense_1p5b_ordinal": (2e-4, 6e-4),
+            "hybrid_4b_k4": (4e-4, 1.5e-3), "dense_27b_k10": (1e-3, 5e-3)}
 
 
 def log(msg):
@@ -106,7 +113,7 @@ def gather(wl, tok, sums, idx):
     return t.astype(np.float64), sums[idx].astype(np.float64)
 
 
-def compare(tag, sub, got_tok, got_sum, ref_tok, ref_sum, dtype):
+def compare(tag, sub, got_tok, got_sum, ref_tok, ref_sum, dtype, pair_dev=None):
     dt = np.abs(got_tok - ref_tok).max()
     ds = np.abs(got_sum - ref_sum).max()
     log(f"[fullsize] {tag} dtype {dtype}: {sub.n_candidates} candidates, {len(ref_tok)} tokens: "
@@ -114,6 +121,8 @@ def compare(tag, sub, got_tok, got_sum, ref_tok, ref_sum, dtype):
     from conftest import record_parity
     record_parity(f"fullsize/{tag}/dtype{dtype}", max_tok=dt, max_sum=ds)
     assert dt <= TOK_TOL and ds <= SUM_TOL
+    if dtype == J.JET_BF16 and pair_dev is not None:
+        assert dt <= pair_dev[0] and ds <= pair_dev[1], (tag, dt, ds, pair_dev)
     # identical argmax wherever the oracle's margin exceeds 0.1 nats
     for q in range(sub.n_questions):
         a, b = int(sub.q_cand_offsets[q]), int(sub.q_cand_offsets[q + 1])
@@ -156,7 +165,8 @@ def golden_parity(name, path, dtype, check_decisions=None):
         sub, idx = case_subset(wl, case)
         got_tok, got_sum = gather(wl, tok, sums, idx)
         ref_tok, ref_sum = np.array(case["token_logprob"]), np.array(case["cand_sum"])
-        compare(f"{name}/{case['label']}/q{case['questions']}", sub, got_tok, got_sum, ref_tok, ref_sum, dtype)
+        compare(f"{name}/{case['label']}/q{case['questions']}", sub, got_tok, got_sum, ref_tok, ref_sum, dtype,
+                pair_dev=PAIR_DEV.get(name))
         if check_decisions:
             check_decisions(sub, got_sum, ref_sum)
     return wl, tok, sums
@@ -326,11 +336,10 @@ def test_dense_1p5b_q4_k4_full():
         compare(f"dense_1p5b_q4_k4/q{qs}", sub, got_tok, got_sum, ref_tok, ref_sum, J.JET_F16)
 
 
-# The pair-bf16 mode's largest deviation from the stored oracle scores on the
-# sampled questions of the 1.5B and hybrid workloads (per token, per
-# candidate), measured with these kernels: the whole-workload check below
-# spends it from the tolerances.
-BF16_DEV_TOK, BF16_DEV_SUM = 2e-4, 6e-4
+# The whole-workload check below spends the pair-bf16 mode's own error on
+# the 1.5B workloads (its bound in PAIR_DEV, held on their sampled
+# questions) from the tolerances.
+BF16_DEV_TOK, BF16_DEV_SUM = PAIR_DEV["dense_1p5b_k4"]
 
 
 @pytest.mark.timeout(900)
