@@ -76,6 +76,7 @@ CASES = [
     ("small_gqa_bf16", "small", J.JET_F16, 0.8),
     ("small_hybrid_bf16", "small_hybrid", J.JET_FP32, 0.8),
     ("small_hybrid_bf16", "small_hybrid", J.JET_F16, 0.0),
+    ("small_hybrid_bf16", "small_hybrid", J.JET_BF16, 0.8),
     ("small_gqa_bf16", "small", J.JET_BF16, 1.0),
     ("small_moe_bf16", "small_moe", J.JET_FP32, 0.8),
 ]
